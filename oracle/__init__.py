@@ -1,0 +1,164 @@
+"""CPU oracle for the HSTU jagged-attention path -- TEST INFRASTRUCTURE ONLY.
+
+Only ``tests/``, ``__graft_entry__.smoke()`` and the benchmark's CPU
+baseline may import this package.  The product path never routes
+through it.
+
+The arithmetic lives in ``hstu_oracle.c`` (plain fp64 loops); this module
+compiles it with gcc and marshals numpy arrays through ctypes.  Every
+float input is widened to float64 before the call, so the oracle sees
+exactly the stored (fp32 or bf16) values.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_SRC = os.path.join(_HERE, "hstu_oracle.c")
+_LIB = os.path.join(_HERE, "libhstu_oracle.so")
+_lib = None
+
+
+def build(force: bool = True) -> str:
+    """Compile the oracle with gcc (never hipcc)."""
+    if force or not os.path.exists(_LIB):
+        tmp = _LIB + ".tmp%d" % os.getpid()
+        cmd = ["gcc", "-O2", "-fopenmp", "-fPIC", "-shared", "-std=c99",
+               "-Wall", "-o", tmp, _SRC, "-lm"]
+        subprocess.run(cmd, check=True)
+        os.replace(tmp, _LIB)
+    return _LIB
+
+
+def _load():
+    global _lib
+    if _lib is None:
+        if not os.path.exists(_LIB):
+            build(force=True)
+        lib = ctypes.CDLL(_LIB)
+        P = ctypes.c_void_p
+        i32, i64, f64 = ctypes.c_int32, ctypes.c_int64, ctypes.c_double
+        lib.oracle_time_bucket.argtypes = [i64, i32]
+        lib.oracle_time_bucket.restype = i32
+        lib.oracle_complete_cumsum.argtypes = [i32, P, P]
+        lib.oracle_time_bucketize.argtypes = [i32, P, P, i32, P, P]
+        lib.oracle_attn_fwd.argtypes = [i32, P, i32, i32, i32, i32, P, P, P, P,
+                                        i32, P, P, P, P]
+        lib.oracle_attn_bwd.argtypes = [i32, P, i32, i32, i32, i32, P, P, P, P,
+                                        i32, P, P, P, P, P, P, P, P, P]
+        lib.oracle_ln_gate.argtypes = [i64, i32, P, P, P, P, f64, P, P, P]
+        lib.oracle_num_threads.restype = i32
+        _lib = lib
+    return _lib
+
+
+def _p(a):
+    return None if a is None else a.ctypes.data_as(ctypes.c_void_p)
+
+
+def _i64(a):
+    return None if a is None else np.ascontiguousarray(a, dtype=np.int64)
+
+
+def _f64(a):
+    return None if a is None else np.ascontiguousarray(a, dtype=np.float64)
+
+
+def num_threads() -> int:
+    return int(_load().oracle_num_threads())
+
+
+def time_bucket(dt: int, num_buckets: int) -> int:
+    return int(_load().oracle_time_bucket(int(dt), int(num_buckets)))
+
+
+def complete_cumsum(x) -> np.ndarray:
+    x = _i64(x)
+    out = np.empty(len(x) + 1, dtype=np.int64)
+    _load().oracle_complete_cumsum(len(x), _p(x), _p(out))
+    return out
+
+
+def time_bucketize(seq_offsets, timestamps, num_buckets):
+    """Returns (pair_offsets [B+1], buckets uint8 [sum L_b^2])."""
+    offs, ts = _i64(seq_offsets), _i64(timestamps)
+    lens = np.diff(offs)
+    pair_offsets = complete_cumsum(lens * lens)
+    out = np.zeros(int(pair_offsets[-1]), dtype=np.uint8)
+    _load().oracle_time_bucketize(len(lens), _p(offs), _p(ts), int(num_buckets),
+                                  _p(pair_offsets), _p(out))
+    return pair_offsets, out
+
+
+def _check(offs, ts, nt, N, rp, T):
+    """Data preconditions of the definition: offsets start at 0 and do not
+    decrease, every L_b <= N (so every signed offset has a rab_pos entry),
+    0 <= n_t <= L_b, timestamps in [0, 2^62)."""
+    lens = np.diff(offs)
+    if offs[0] != 0 or offs[-1] != T or (lens < 0).any():
+        raise ValueError("bad seq_offsets")
+    if len(lens) and lens.max() > N:
+        raise ValueError("sequence longer than max_seq_len")
+    if len(rp) != 2 * N - 1:
+        raise ValueError("rab_pos must have 2N-1 entries")
+    if nt is not None and ((nt < 0).any() or (nt > lens).any()):
+        raise ValueError("num_targets out of range")
+    if len(ts) != T or (T and (ts.min() < 0 or ts.max() >= (1 << 62))):
+        raise ValueError("timestamps out of range")
+
+
+def attn_fwd(seq_offsets, max_seq_len, timestamps, rab_pos, rab_time, q, k, v,
+             num_targets=None):
+    """O [T, h, d_v] = (1/N) sum_j SiLU(q_i.k_j + rab(i,j)) v_j over kept pairs."""
+    offs, ts, nt = _i64(seq_offsets), _i64(timestamps), _i64(num_targets)
+    q, k, v = _f64(q), _f64(k), _f64(v)
+    rp, rt = _f64(rab_pos), _f64(rab_time)
+    T, H, dqk = q.shape
+    dv = v.shape[2]
+    _check(offs, ts, nt, int(max_seq_len), rp, T)
+    out = np.empty((T, H, dv), dtype=np.float64)
+    _load().oracle_attn_fwd(len(offs) - 1, _p(offs), int(max_seq_len), H, dqk, dv,
+                            _p(ts), _p(nt), _p(rp), _p(rt), len(rt),
+                            _p(q), _p(k), _p(v), _p(out))
+    return out
+
+
+def attn_bwd(seq_offsets, max_seq_len, timestamps, rab_pos, rab_time, q, k, v,
+             d_out, num_targets=None):
+    """Returns (dq, dk, dv, d_rab_pos, d_rab_time) for the loss <O, d_out>."""
+    offs, ts, nt = _i64(seq_offsets), _i64(timestamps), _i64(num_targets)
+    q, k, v, do = _f64(q), _f64(k), _f64(v), _f64(d_out)
+    rp, rt = _f64(rab_pos), _f64(rab_time)
+    T, H, dqk = q.shape
+    dvd = v.shape[2]
+    _check(offs, ts, nt, int(max_seq_len), rp, T)
+    dq = np.empty_like(q)
+    dk = np.empty_like(k)
+    dv = np.empty_like(v)
+    drp = np.empty_like(rp)
+    drt = np.empty_like(rt)
+    _load().oracle_attn_bwd(len(offs) - 1, _p(offs), int(max_seq_len), H, dqk, dvd,
+                            _p(ts), _p(nt), _p(rp), _p(rt), len(rt),
+                            _p(q), _p(k), _p(v), _p(do), _p(dq), _p(dk), _p(dv),
+                            _p(drp), _p(drt))
+    return dq, dk, dv, drp, drt
+
+
+def ln_gate(x, u, gamma=None, beta=None, eps=1e-5):
+    """Y = LayerNorm(x) * u per row; returns (y, mean, rstd)."""
+    x = _f64(x)
+    T = x.shape[0]
+    x = x.reshape(T, -1)
+    D = x.shape[1]
+    u = _f64(u).reshape(T, D)
+    g, b = _f64(gamma), _f64(beta)
+    y = np.empty((T, D), dtype=np.float64)
+    mean = np.empty(T, dtype=np.float64)
+    rstd = np.empty(T, dtype=np.float64)
+    _load().oracle_ln_gate(T, D, _p(x), _p(u), _p(g), _p(b), float(eps), _p(y),
+                           _p(mean), _p(rstd))
+    return y, mean, rstd

@@ -1,0 +1,441 @@
+"""Pins for the CPU oracle (no GPU needed).
+
+The paper prints no kernel-level numbers, so the oracle is pinned by
+brute force on tiny inputs (matrix-form NumPy, tests/dense_ref.py),
+closed forms, invariants the method implies, and finite differences.
+Each test names the passage or property it rests on."""
+import math
+
+import numpy as np
+import pytest
+
+from paper_2402_17152_amd import inputs
+from tests import dense_ref
+
+
+def _small(seed=0, lengths=(7, 13, 1, 20), h=2, d=8, N=24, nt=None, dtype="f32",
+           num_buckets=128, spread=600.0):
+    rng = np.random.default_rng(seed)
+    lengths = np.asarray(lengths, dtype=np.int64)
+    offs = np.concatenate([[0], np.cumsum(lengths)])
+    T = int(offs[-1])
+    ts = np.empty(T, dtype=np.int64)
+    for b in range(len(lengths)):
+        s, e = offs[b], offs[b + 1]
+        ts[s:e] = 1_700_000_000 + np.cumsum(np.floor(rng.exponential(spread, e - s))).astype(np.int64)
+    q = rng.standard_normal((T, h, d)) * 0.7
+    k = rng.standard_normal((T, h, d)) * 0.7
+    v = rng.standard_normal((T, h, d))
+    do = rng.standard_normal((T, h, d))
+    rp = rng.standard_normal(2 * N - 1) * 0.3
+    rt = rng.standard_normal(num_buckets) * 0.3
+    ntv = None if nt is None else np.asarray(nt, dtype=np.int64)
+    return dict(offs=offs, ts=ts, q=q, k=k, v=v, do=do, rp=rp, rt=rt, N=N, nt=ntv)
+
+
+def _fwd(o, c, **over):
+    c = dict(c, **over)
+    return o.attn_fwd(c["offs"], c["N"], c["ts"], c["rp"], c["rt"], c["q"], c["k"], c["v"],
+                      num_targets=c["nt"])
+
+
+def _bwd(o, c, **over):
+    c = dict(c, **over)
+    return o.attn_bwd(c["offs"], c["N"], c["ts"], c["rp"], c["rt"], c["q"], c["k"], c["v"],
+                      c["do"], num_targets=c["nt"])
+
+
+# ---------------------------------------------------------------- buckets
+
+def _ref_bucket(dt, nb):
+    return min(nb - 1, max(abs(int(dt)), 1).bit_length() - 1)
+
+
+def test_bucket_powers_of_two(oracle_mod):
+    """Time-bucket function (notation table, rab^{p,t}): floor(log2) is exact
+    at and around every power of two up to 2^61 (Python big-int bit_length
+    as the independent reference), both signs, and the clamp at B_t - 1."""
+    vals = [0, 1, -1]
+    for kk in range(1, 62):
+        for dlt in (-1, 0, 1):
+            vals += [(1 << kk) + dlt, -((1 << kk) + dlt)]
+    for nb in (128, 61, 20, 1):
+        for x in vals:
+            assert oracle_mod.time_bucket(x, nb) == _ref_bucket(x, nb), (x, nb)
+
+
+def test_bucketize_random_bit_exact(oracle_mod):
+    """Standalone bucketisation equals bit_length on random int64 deltas
+    in [0, 2^62) (10^6 pairs)."""
+    rng = np.random.default_rng(5)
+    L = 1000
+    mags = rng.integers(0, 62, size=L)
+    ts = np.array([int(rng.integers(0, 1 << int(m))) if m > 0 else 0 for m in mags], dtype=np.int64)
+    offs = np.array([0, L], dtype=np.int64)
+    po, bk = oracle_mod.time_bucketize(offs, ts, 128)
+    assert po.tolist() == [0, L * L]
+    m = bk.reshape(L, L)
+    tsl = [int(x) for x in ts]
+    sample = rng.integers(0, L, size=(20000, 2))
+    for i, j in sample:
+        assert m[i, j] == _ref_bucket(tsl[i] - tsl[j], 128)
+    # full check vectorised with numpy on magnitudes < 2^53 would round; use exact ints
+    d = np.abs(ts[:, None] - ts[None, :]).astype(np.uint64)
+    d = np.maximum(d, 1)
+    ref = np.zeros_like(d, dtype=np.int64)
+    x = d.copy()
+    while True:
+        nz = x > 1
+        if not nz.any():
+            break
+        ref += nz
+        x = np.where(nz, x >> np.uint64(1), x)
+    assert np.array_equal(m.astype(np.int64), np.minimum(ref, 127))
+
+
+def test_bucketize_jagged_layout(oracle_mod):
+    """Each sequence's L x L square sits at pair_offsets[b], row-major,
+    entry (i, j) = bucket(t_i - t_j); empty sequences take no space."""
+    offs = np.array([0, 3, 3, 7], dtype=np.int64)
+    ts = np.array([10, 11, 15, 0, 1, 3, 1000], dtype=np.int64)
+    po, bk = oracle_mod.time_bucketize(offs, ts, 128)
+    assert po.tolist() == [0, 9, 9, 25]
+    for b in range(3):
+        s, e = offs[b], offs[b + 1]
+        L = e - s
+        sq = bk[po[b]:po[b + 1]].reshape(L, L)
+        for i in range(L):
+            for j in range(L):
+                assert sq[i, j] == _ref_bucket(ts[s + i] - ts[s + j], 128)
+
+
+def test_complete_cumsum(oracle_mod):
+    rng = np.random.default_rng(1)
+    for n in (0, 1, 5, 1000):
+        x = rng.integers(0, 1 << 40, size=n)
+        out = oracle_mod.complete_cumsum(x)
+        assert out[0] == 0 and np.array_equal(out[1:], np.cumsum(x))
+
+
+# ------------------------------------------------------- brute force
+
+@pytest.mark.parametrize("case", [
+    dict(),
+    dict(lengths=(5, 9, 16), nt=(2, 0, 5)),
+    dict(lengths=(11, 4), nt=(11, 4), h=1),          # every token a candidate
+    dict(lengths=(17, 3, 0, 9), num_buckets=6, spread=5000.0),   # clamp binds
+    dict(lengths=(24,), h=3, d=5),
+])
+def test_matches_dense_brute_force(oracle_mod, case):
+    """Whole forward and backward equal the matrix-form brute force built
+    from Eq. 2 with the Algorithm 1 mask, to fp64 rounding."""
+    c = _small(**case)
+    O = _fwd(oracle_mod, c)
+    Od, g = dense_ref.jagged_dense(c["offs"], c["ts"], c["rp"], c["rt"], c["N"], c["q"], c["k"],
+                                   c["v"], num_targets=c["nt"], d_out=c["do"])
+    np.testing.assert_allclose(O, Od, rtol=1e-12, atol=1e-14)
+    got = _bwd(oracle_mod, c)
+    for a, b in zip(got, g):
+        np.testing.assert_allclose(a, b, rtol=1e-11, atol=1e-13)
+
+
+def test_jagged_equals_padded_masked(oracle_mod):
+    """Fully raggified attention (Sec. 3.2; kernel appendix) equals the
+    padded computation with padding keys masked: pad every sequence to N,
+    run dense attention with a key-padding mask, compare valid rows."""
+    c = _small(lengths=(7, 13, 1, 20), N=24)
+    O = _fwd(oracle_mod, c)
+    N = c["N"]
+    H, d = c["q"].shape[1], c["q"].shape[2]
+    offs = c["offs"]
+    for b in range(len(offs) - 1):
+        s, e = offs[b], offs[b + 1]
+        L = e - s
+        qp = np.zeros((N, H, d)); kp = np.zeros((N, H, d)); vp = np.zeros((N, H, d))
+        tp = np.zeros(N, dtype=np.int64)
+        qp[:L], kp[:L], vp[:L], tp[:L] = c["q"][s:e], c["k"][s:e], c["v"][s:e], c["ts"][s:e]
+        tp[L:] = tp[L - 1] if L else 0
+        keymask = np.arange(N) < L
+        M = np.tril(np.ones((N, N), dtype=bool)) & keymask[None, :]
+        bias = c["rp"][dense_ref.position_index(N, 0, N)] + c["rt"][dense_ref.bucket_matrix(tp, len(c["rt"]))]
+        for a in range(H):
+            S = qp[:, a] @ kp[:, a].T + bias
+            A = np.where(M, dense_ref.silu(S) / N, 0.0)
+            np.testing.assert_allclose(O[s:e, a], (A @ vp[:, a])[:L], rtol=1e-12, atol=1e-14)
+
+
+# ------------------------------------------------------- invariants
+
+def test_causality(oracle_mod):
+    """Perturbing q, k, v or t at positions > i leaves rows <= i unchanged
+    (bitwise): the mask is causal (Algorithm 1, lower-triangular)."""
+    c = _small(lengths=(30,), h=2, N=32)
+    O = _fwd(oracle_mod, c)
+    rng = np.random.default_rng(3)
+    for cut in (0, 9, 28):
+        c2 = {kk: (vv.copy() if isinstance(vv, np.ndarray) else vv) for kk, vv in c.items()}
+        for name in ("q", "k", "v"):
+            c2[name][cut + 1:] += rng.standard_normal(c2[name][cut + 1:].shape)
+        c2["ts"][cut + 1:] += rng.integers(1, 10**6, size=30 - cut - 1)
+        c2["ts"][cut + 1:] = np.maximum.accumulate(c2["ts"][cut + 1:])
+        O2 = _fwd(oracle_mod, c2)
+        assert np.array_equal(O[:cut + 1], O2[:cut + 1])
+        assert not np.array_equal(O[cut + 1:], O2[cut + 1:])
+
+
+def test_single_token_closed_form(oracle_mod):
+    """L = 1: O = SiLU(q.k + rab_pos[N-1] + rab_time[0]) v / N (Eq. 2 with
+    the only pair being the diagonal, dt = 0 -> bucket 0)."""
+    c = _small(lengths=(1, 1, 1), h=2, d=4, N=8)
+    O = _fwd(oracle_mod, c)
+    for t in range(3):
+        for a in range(2):
+            s = float(np.dot(c["q"][t, a], c["k"][t, a])) + c["rp"][7] + c["rt"][0]
+            sil = s / (1.0 + math.exp(-s))
+            np.testing.assert_allclose(O[t, a], sil * c["v"][t, a] / 8, rtol=1e-14)
+
+
+def test_silu_closed_forms(oracle_mod):
+    """SiLU through the whole path with L = 1, N = 1, v = 1: SiLU(0) = 0,
+    SiLU(x) - SiLU(-x) = x, SiLU'(0) = 1/2, min SiLU = -0.278464542761074
+    at x = -1.27846454276107 (root of 1 + x(1 - sigma(x)) = 0)."""
+    def run(s, grad=False):
+        c = dict(offs=np.array([0, 1]), ts=np.array([5]), q=np.zeros((1, 1, 1)),
+                 k=np.zeros((1, 1, 1)), v=np.ones((1, 1, 1)), do=np.ones((1, 1, 1)),
+                 rp=np.array([s]), rt=np.array([0.0]), N=1, nt=None)
+        if grad:
+            return _bwd(oracle_mod, c)[4][0]
+        return float(_fwd(oracle_mod, c)[0, 0, 0])
+    assert run(0.0) == 0.0
+    for x in (0.3, 1.7, 5.0, 12.0):
+        assert abs(run(x) - run(-x) - x) < 1e-14 * max(1, x)
+    assert abs(run(0.0, grad=True) - 0.5) < 1e-15
+    xm = -1.27846454276107
+    assert abs(run(xm) - (-0.278464542761074)) < 1e-12
+    assert abs(run(xm, grad=True)) < 1e-12
+
+
+def test_prefix_sum_closed_form(oracle_mod):
+    """Q = 0, rab_pos = c1, rab_time = c2: O_i = SiLU(c1+c2)/N * sum_{j<=i} V_j
+    (a scaled prefix sum; Eq. 2 with a constant score).  Target-aware: a
+    candidate gets SiLU(c)/N * (sum_{j<n_h} V_j + V_i)."""
+    c = _small(lengths=(9, 14), nt=(0, 5), h=2, d=3, N=16)
+    c1, c2 = 0.37, -1.1
+    c["q"] = np.zeros_like(c["q"])
+    c["rp"] = np.full_like(c["rp"], c1)
+    c["rt"] = np.full_like(c["rt"], c2)
+    O = _fwd(oracle_mod, c)
+    sc = (c1 + c2) / (1 + math.exp(-(c1 + c2))) / 16
+    v = c["v"]
+    np.testing.assert_allclose(O[0:9], sc * np.cumsum(v[0:9], axis=0), rtol=1e-13)
+    nh = 9
+    hist = v[9:9 + nh]
+    np.testing.assert_allclose(O[9:18], sc * np.cumsum(hist, axis=0), rtol=1e-13)
+    for t in range(nh, 14):
+        np.testing.assert_allclose(O[9 + t], sc * (hist.sum(axis=0) + v[9 + t]), rtol=1e-13)
+
+
+def test_mfalcon_equivalence(oracle_mod):
+    """Algorithm 1 / M-FALCON appendix: a candidate's output in the
+    target-aware pass over prefix ++ candidates equals the last row of a
+    plain causal pass over prefix ++ [candidate] (candidate at position n_h)."""
+    nh, nt = 11, 6
+    c = _small(lengths=(nh + nt,), nt=(nt,), h=2, d=6, N=20)
+    O = _fwd(oracle_mod, c)
+    for m in range(nt):
+        idx = list(range(nh)) + [nh + m]
+        c1 = dict(c, offs=np.array([0, nh + 1]), nt=None, ts=c["ts"][idx],
+                  q=c["q"][idx], k=c["k"][idx], v=c["v"][idx])
+        O1 = _fwd(oracle_mod, c1)
+        np.testing.assert_allclose(O[nh + m], O1[nh], rtol=1e-13, atol=1e-15)
+        np.testing.assert_array_equal(O[:nh], O1[:nh])
+
+
+def test_time_shift_invariance(oracle_mod):
+    """Only timestamp differences enter rab (notation table): shifting a
+    sequence's timestamps by a constant changes nothing, bitwise."""
+    c = _small()
+    O = _fwd(oracle_mod, c)
+    g = _bwd(oracle_mod, c)
+    ts2 = c["ts"].copy()
+    ts2[7:20] += 123456789
+    ts2[0:7] -= 1_000_000_000
+    O2 = _fwd(oracle_mod, c, ts=ts2)
+    g2 = _bwd(oracle_mod, c, ts=ts2)
+    assert np.array_equal(O, O2)
+    for a, b in zip(g, g2):
+        assert np.array_equal(a, b)
+
+
+def test_rab_time_locality(oracle_mod):
+    """Changing rab_time[b] moves O only through pairs in bucket b: rows
+    with no kept pair in bucket b stay bitwise unchanged."""
+    c = _small(lengths=(25,), spread=3000.0, N=32)
+    O = _fwd(oracle_mod, c)
+    bm = dense_ref.bucket_matrix(c["ts"], 128)
+    M = dense_ref.mask_alg1(25, 0)
+    target = int(np.bincount(bm[M]).argmax())
+    rt2 = c["rt"].copy()
+    rt2[target] += 0.5
+    O2 = _fwd(oracle_mod, c, rt=rt2)
+    rows_hit = (M & (bm == target)).any(axis=1)
+    assert rows_hit.any() and not rows_hit.all()
+    assert np.array_equal(O[~rows_hit], O2[~rows_hit])
+    assert not np.array_equal(O[rows_hit], O2[rows_hit])
+
+
+def test_head_sharing(oracle_mod):
+    """rab is shared across heads (notation table: rab in R^{1 x N x N}):
+    d-rab for h heads equals the sum of the h single-head d-rabs."""
+    c = _small(h=3, d=4)
+    full = _bwd(oracle_mod, c)
+    acc_p = np.zeros_like(c["rp"])
+    acc_t = np.zeros_like(c["rt"])
+    for a in range(3):
+        sl = slice(a, a + 1)
+        g = _bwd(oracle_mod, c, q=c["q"][:, sl], k=c["k"][:, sl], v=c["v"][:, sl], do=c["do"][:, sl])
+        acc_p += g[3]
+        acc_t += g[4]
+        np.testing.assert_allclose(full[0][:, sl], g[0], rtol=1e-14, atol=1e-16)
+    np.testing.assert_allclose(full[3], acc_p, rtol=1e-12, atol=1e-15)
+    np.testing.assert_allclose(full[4], acc_t, rtol=1e-12, atol=1e-15)
+
+
+def test_drab_conservation(oracle_mod):
+    """Every kept pair adds its dS once to each table, so both tables sum to
+    the same total; offsets j > i never occur (rab_pos entries above N-1 get
+    exactly zero gradient) and unpopulated buckets stay exactly zero."""
+    c = _small(lengths=(7, 13, 1, 20), nt=(0, 4, 0, 3))
+    _, _, _, drp, drt = _bwd(oracle_mod, c)
+    N = c["N"]
+    assert np.all(drp[N:] == 0.0)
+    assert abs(drp.sum() - drt.sum()) < 1e-12 * np.abs(drp).sum()
+    used = set()
+    for b in range(4):
+        s, e = c["offs"][b], c["offs"][b + 1]
+        L = e - s
+        M = dense_ref.mask_alg1(L, int(c["nt"][b]))
+        used |= set(dense_ref.bucket_matrix(c["ts"][s:e], 128)[M].tolist())
+    unused = np.array([bb not in used for bb in range(128)])
+    assert np.all(drt[unused] == 0.0)
+    assert np.all(drt[~unused] != 0.0)
+
+
+def _loss(o, c, G, **over):
+    return float(np.sum(_fwd(o, c, **over) * G))
+
+
+def test_backward_finite_differences(oracle_mod):
+    """Backward (kernel appendix: recomputation of attention and bias)
+    against central differences of <O, G> in fp64, step 1e-6, on 50 random
+    coordinates per tensor and on every populated bias entry."""
+    c = _small(lengths=(9, 14, 5), nt=(0, 3, 0), h=2, d=4, N=16)
+    G = c["do"]
+    dq, dk, dv, drp, drt = _bwd(oracle_mod, c)
+    rng = np.random.default_rng(11)
+    eps = 1e-6
+
+    def fd(name, idx):
+        a = c[name].copy(); a[idx] += eps
+        b = c[name].copy(); b[idx] -= eps
+        return (_loss(oracle_mod, c, G, **{name: a}) - _loss(oracle_mod, c, G, **{name: b})) / (2 * eps)
+
+    for name, grad in (("q", dq), ("k", dk), ("v", dv)):
+        scale = np.sqrt(np.mean(grad ** 2))
+        flat = rng.choice(grad.size, size=50, replace=False)
+        for f in flat:
+            idx = np.unravel_index(f, grad.shape)
+            assert abs(fd(name, idx) - grad[idx]) <= 1e-6 * scale + 1e-9 * abs(grad[idx]), (name, idx)
+    for name, grad in (("rp", drp), ("rt", drt)):
+        scale = np.sqrt(np.mean(grad[grad != 0] ** 2))
+        for f in np.nonzero(grad)[0]:
+            assert abs(fd(name, (f,)) - grad[f]) <= 1e-6 * scale, (name, f)
+
+
+def test_linearity_and_normaliser(oracle_mod):
+    """O is linear in V (Eq. 2), and N * O does not depend on N once
+    rab_pos is re-centred so every signed offset keeps its value."""
+    c = _small()
+    v2 = np.random.default_rng(4).standard_normal(c["v"].shape)
+    O1 = _fwd(oracle_mod, c)
+    O2 = _fwd(oracle_mod, c, v=v2)
+    O3 = _fwd(oracle_mod, c, v=2.5 * c["v"] - 0.75 * v2)
+    np.testing.assert_allclose(O3, 2.5 * O1 - 0.75 * O2, rtol=1e-12, atol=1e-14)
+    N, N2 = c["N"], 40
+    rp2 = np.zeros(2 * N2 - 1)
+    rp2[N2 - 1 - (N - 1): N2 - 1 + N] = c["rp"]
+    O4 = _fwd(oracle_mod, c, N=N2, rp=rp2)
+    np.testing.assert_allclose(N2 * O4, N * O1, rtol=1e-12, atol=1e-14)
+
+
+def test_epilogue_layernorm(oracle_mod):
+    """Eq. 3 Norm(AV) (.) U with Norm = layer norm over the token's h*d_v
+    features: with gamma = 1, beta = 0, U = 1 each row has mean 0 and
+    variance var/(var+eps); Y is linear in U; affine and gate agree with
+    the textbook formula."""
+    rng = np.random.default_rng(8)
+    x = rng.standard_normal((37, 64)) * 3 + 1
+    u = np.ones_like(x)
+    y, mu, rs = oracle_mod.ln_gate(x, u, eps=1e-5)
+    var = x.var(axis=1)
+    np.testing.assert_allclose(y.mean(axis=1), 0, atol=1e-13)
+    np.testing.assert_allclose(y.var(axis=1), var / (var + 1e-5), rtol=1e-12)
+    np.testing.assert_allclose(mu, x.mean(axis=1), rtol=1e-13)
+    np.testing.assert_allclose(rs, 1 / np.sqrt(var + 1e-5), rtol=1e-13)
+    g, b = rng.standard_normal(64), rng.standard_normal(64)
+    u1, u2 = rng.standard_normal(x.shape), rng.standard_normal(x.shape)
+    ya = oracle_mod.ln_gate(x, u1, g, b)[0]
+    yb = oracle_mod.ln_gate(x, u2, g, b)[0]
+    yc = oracle_mod.ln_gate(x, 2 * u1 + 3 * u2, g, b)[0]
+    np.testing.assert_allclose(yc, 2 * ya + 3 * yb, rtol=1e-12, atol=1e-12)
+    ref = ((x - x.mean(1, keepdims=True)) / np.sqrt(var[:, None] + 1e-5) * g + b) * u1
+    np.testing.assert_allclose(ya, ref, rtol=1e-12, atol=1e-13)
+
+
+def test_empty_and_full_candidate_sequences(oracle_mod):
+    """L_b = 0 contributes nothing; n_t = L_b means each token sees only
+    itself at position 0 (diagonal of the Algorithm 1 mask)."""
+    c = _small(lengths=(0, 6, 0), nt=(0, 6, 0), h=1, d=3, N=8)
+    O = _fwd(oracle_mod, c)
+    for t in range(6):
+        s = float(c["q"][t, 0] @ c["k"][t, 0]) + c["rp"][7] + c["rt"][0]
+        np.testing.assert_allclose(O[t, 0], s / (1 + math.exp(-s)) / 8 * c["v"][t, 0], rtol=1e-14)
+
+
+def test_oracle_rejects_bad_data(oracle_mod):
+    """The definition needs L_b <= N and 0 <= n_t <= L_b; the oracle refuses
+    inputs outside it instead of reading past the bias table."""
+    c = _small(lengths=(30,), N=24)
+    with pytest.raises(ValueError):
+        _fwd(oracle_mod, c)
+    c = _small(lengths=(5,), nt=(6,))
+    with pytest.raises(ValueError):
+        _bwd(oracle_mod, c)
+
+
+def test_generator_matches_workloads():
+    """Seeded generator: token totals of the five workloads, determinism."""
+    want = {0: 318, 1: 11268, 2: 60383, 3: 48118, 4: 49152}
+    for i, T in want.items():
+        if i in (2, 3, 4):
+            # only lengths are checked for the large shapes (cheap path)
+            rng = np.random.default_rng(i)
+            L = inputs._lengths(inputs.WORKLOADS[i], rng)
+            assert int(L.sum()) == T
+        else:
+            b1 = inputs.make_batch(i)
+            b2 = inputs.make_batch(i)
+            assert b1.total_tokens == T
+            for kk in b1.store:
+                assert np.array_equal(b1.store[kk], b2.store[kk])
+            assert np.array_equal(b1.timestamps, b2.timestamps)
+
+
+def test_bf16_rounding():
+    """fp32 -> bf16 is round-to-nearest-even (checked on exact ties)."""
+    x = np.array([1.0, 1.0 + 2**-8, 1.0 + 3 * 2**-8, -1.0 - 2**-8, 3.0e38], dtype=np.float32)
+    got = inputs.bf16_bits_to_f64(inputs.f32_to_bf16_bits(x))
+    assert got[0] == 1.0
+    assert got[1] == 1.0          # tie -> even (mantissa 0)
+    assert got[2] == 1.0 + 2**-6  # tie -> even (rounds up)
+    assert got[3] == -1.0
