@@ -1,0 +1,197 @@
+/*
+ * hstu.h -- C ABI of libhstu: the HSTU layer's jagged pointwise attention
+ * for AMD Instinct MI355X (gfx950).
+ *
+ * Operation (Zhai et al., "Actions Speak Louder than Words", ICML 2024):
+ *   Eq. 2  A(X)V(X) = SiLU(Q K^T + rab^{p,t}) V, with the pointwise
+ *          aggregation of Sec. 3.1 normalised by the constant N
+ *          (= max_seq_len) instead of a softmax, no 1/sqrt(d) scaling;
+ *   rab^{p,t} (notation table) is shared by all heads:
+ *          rab(i,j) = rab_pos[(N-1) + p(j) - p(i)] + rab_time[bkt(t_i - t_j)],
+ *          bkt(x) = min(B_t - 1, floor(log2(max(|x|, 1))));
+ *   mask   causal with the diagonal; with n_t = num_targets[b] > 0 the
+ *          last n_t tokens of a sequence are candidates that see the
+ *          n_h = L_b - n_t history tokens and themselves only, and all sit
+ *          at position p = n_h (Algorithm 1, M-FALCON mask);
+ *   Eq. 3  Y_pre = LayerNorm(A V) (.) U, layer norm over the h*d_v
+ *          features of a token, biased variance, optional affine;
+ *   backward: recomputes attention and bias (appendix on the fused
+ *          kernels) and produces dQ, dK, dV and the gradients of both
+ *          bias tables, summed over heads and sequences.
+ *
+ * Conventions
+ *   Memory   every pointer is DEVICE memory owned by the caller unless a
+ *            comment says "host".  The library keeps no pointer after a
+ *            call returns and allocates no device memory; scratch space
+ *            comes from the caller's workspace (hstu_workspace_bytes).
+ *            Outputs must not alias inputs.
+ *   Layout   jagged, token-major: sequence b owns tokens
+ *            [seq_offsets[b], seq_offsets[b+1]).  Q/K/V/U rows: row r of X
+ *            starts at X + r * x_stride (in elements); inside a row the
+ *            layout is [h][d] contiguous, so Q/K/V/U may be strided views
+ *            of one fused projection output [U | V | Q | K] (notation
+ *            table, entry Split).  Outputs are dense [T][h][d].
+ *            Every Q/K/V/U/O/dO pointer is 16-byte aligned and every
+ *            stride a multiple of 16 bytes.
+ *   Streams  all work is enqueued on hip_stream (a hipStream_t, NULL =
+ *            the null stream) and the call returns before it completes.
+ *            Only hstu_validate synchronises.
+ *   Errors   host-side argument checks run before any launch; on failure
+ *            the call returns a non-zero hstu_status_t, sets
+ *            hstu_last_error() and enqueues nothing.  A failed launch
+ *            returns HSTU_ERR_HIP.  Device-data preconditions
+ *            (offsets monotone from 0 to T, L_b <= N, 0 <= n_t <= L_b,
+ *            timestamps in [0, 2^62)) are not checked by the hot calls;
+ *            breaking them is undefined.  hstu_validate checks them.
+ *   Precision HSTU_F32: fp32 storage and arithmetic.  HSTU_BF16: bf16
+ *            storage, fp32 accumulation; the attention weights and dS are
+ *            rounded to bf16 (nearest-even) before the second contraction.
+ *            Bias tables and their gradients are fp32; offsets and
+ *            timestamps int64.
+ *   Determinism  hstu_attn_fwd, hstu_layer_fwd, hstu_time_bucketize and
+ *            hstu_complete_cumsum are bitwise deterministic.
+ *            hstu_attn_bwd accumulates dQ and the bias gradients with
+ *            atomics, so their last bits may vary between runs.
+ */
+#ifndef HSTU_H_
+#define HSTU_H_
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define HSTU_ABI_VERSION 1
+
+typedef enum {
+  HSTU_OK = 0,
+  HSTU_ERR_INVALID_ARGUMENT = 1, /* null pointer, bad size or stride      */
+  HSTU_ERR_UNSUPPORTED = 2,      /* a shape this build has no kernel for  */
+  HSTU_ERR_WORKSPACE = 3,        /* workspace missing or too small        */
+  HSTU_ERR_HIP = 4,              /* a HIP runtime call failed             */
+  HSTU_ERR_DATA = 5              /* hstu_validate found bad device data   */
+} hstu_status_t;
+
+typedef enum { HSTU_F32 = 0, HSTU_BF16 = 1 } hstu_dtype_t;
+
+/* Host-side shape of one jagged batch; nothing is read back from the
+ * device to fill it. */
+typedef struct {
+  int32_t num_seqs;         /* B >= 1                                           */
+  int64_t total_tokens;     /* T == seq_offsets[B] (0 allowed)                  */
+  int32_t max_seq_len;      /* N >= 1: normaliser 1/N; rab_pos has 2N-1 entries;
+                               every L_b <= N.  Supported: N <= 65536          */
+  int32_t num_heads;        /* h in [1, 64]                                     */
+  int32_t d_qk, d_v;        /* head sizes, each in {32, 64, 128}                */
+  int32_t num_time_buckets; /* B_t in [1, 256]                                  */
+  hstu_dtype_t dtype;       /* storage of Q, K, V, U, O, Y, dO, dQ, dK, dV      */
+} hstu_problem_t;
+
+/* Device arrays describing the jagged structure and the bias tables. */
+typedef struct {
+  const int64_t* seq_offsets; /* [B+1]: 0 = o_0 <= o_1 <= ... <= o_B = T        */
+  const int64_t* timestamps;  /* [T]: each in [0, 2^62)                         */
+  const int64_t* num_targets; /* [B] or NULL (all 0): 0 <= n_t,b <= L_b         */
+  const float* rab_pos;       /* [2N-1]: entry (N-1)+p(j)-p(i)                  */
+  const float* rab_time;      /* [B_t]: entry bkt(t_i - t_j)                    */
+} hstu_jagged_t;
+
+/* Bytes of device workspace the attention calls need for problem p (host
+ * pointer).  0 only if p is invalid.  One workspace of this size serves
+ * every call below for the same shape; it may be reused between calls
+ * on one stream but not by calls that overlap. */
+size_t hstu_workspace_bytes(const hstu_problem_t* p);
+
+/* Eq. 2 forward: out[t][a][:] = (1/N) sum_{j kept} SiLU(q.k + rab) v_j.
+ * q, k: rows of h*d_qk elements at q_stride / k_stride; v: h*d_v at
+ * v_stride; out: dense [T][h][d_v], overwritten (rows of empty sequences
+ * do not exist; every token row is written). */
+hstu_status_t hstu_attn_fwd(const hstu_problem_t* p, const hstu_jagged_t* j,
+                            const void* q, int64_t q_stride,
+                            const void* k, int64_t k_stride,
+                            const void* v, int64_t v_stride,
+                            void* out, void* ws, size_t ws_bytes,
+                            void* hip_stream);
+
+/* Backward of hstu_attn_fwd for the loss <out, d_out>.
+ * d_out: dense [T][h][d_v].  dq, dk: dense [T][h][d_qk]; dv: dense
+ * [T][h][d_v]; d_rab_pos [2N-1] and d_rab_time [B_t] (fp32, summed over
+ * heads and sequences).  Every output is overwritten; the bias
+ * gradients are cleared on the stream first. */
+hstu_status_t hstu_attn_bwd(const hstu_problem_t* p, const hstu_jagged_t* j,
+                            const void* q, int64_t q_stride,
+                            const void* k, int64_t k_stride,
+                            const void* v, int64_t v_stride,
+                            const void* d_out,
+                            void* dq, void* dk, void* dv,
+                            float* d_rab_pos, float* d_rab_time,
+                            void* ws, size_t ws_bytes, void* hip_stream);
+
+/* Eq. 2 then the Eq. 3 gate: attn_out = hstu_attn_fwd(...) written dense
+ * [T][D] with D = h*d_v (kept for the backward), then per token
+ * y = ((x - mean) * rstd * ln_weight + ln_bias) (.) u with
+ * rstd = 1/sqrt(var + ln_eps), biased variance over the D features.
+ * ln_weight, ln_bias: fp32 [D] or NULL (identity).  u: rows of D elements
+ * at u_stride.  ln_mean, ln_rstd: fp32 [T] or NULL.  D <= 4096. */
+hstu_status_t hstu_layer_fwd(const hstu_problem_t* p, const hstu_jagged_t* j,
+                             const void* q, int64_t q_stride,
+                             const void* k, int64_t k_stride,
+                             const void* v, int64_t v_stride,
+                             const void* u, int64_t u_stride,
+                             const float* ln_weight, const float* ln_bias,
+                             float ln_eps, void* attn_out, void* y,
+                             float* ln_mean, float* ln_rstd,
+                             void* ws, size_t ws_bytes, void* hip_stream);
+
+/* Standalone timestamp bucketisation (notation table, rab^{p,t}): for
+ * each sequence b writes its L_b x L_b matrix of bkt(t_i - t_j),
+ * row-major (entry (i, j) at pair_offsets[b] + i*L_b + j), as uint8.
+ * pair_offsets [B+1] is the exclusive prefix sum of L_b^2
+ * (hstu_pair_offsets computes it); total_pairs = pair_offsets[B] (host
+ * value).  num_time_buckets in [1, 256]. */
+hstu_status_t hstu_time_bucketize(int32_t num_seqs, int64_t total_tokens,
+                                  int32_t num_time_buckets,
+                                  const int64_t* seq_offsets,
+                                  const int64_t* timestamps,
+                                  const int64_t* pair_offsets,
+                                  int64_t total_pairs, uint8_t* buckets,
+                                  void* hip_stream);
+
+/* out[0] = 0, out[i+1] = out[i] + in[i] for i < n (int64, exact): turns
+ * per-sequence lengths into the offsets of the jagged layout. */
+hstu_status_t hstu_complete_cumsum(int32_t n, const int64_t* in, int64_t* out,
+                                   void* hip_stream);
+
+/* pair_offsets[0] = 0, pair_offsets[b+1] = pair_offsets[b] + L_b^2 with
+ * L_b = seq_offsets[b+1] - seq_offsets[b]: the layout of
+ * hstu_time_bucketize's output. */
+hstu_status_t hstu_pair_offsets(int32_t num_seqs, const int64_t* seq_offsets,
+                                int64_t* pair_offsets, void* hip_stream);
+
+/* Synchronously copies the jagged metadata to the host and checks the
+ * device-data preconditions listed above; HSTU_ERR_DATA on a violation. */
+hstu_status_t hstu_validate(const hstu_problem_t* p, const hstu_jagged_t* j,
+                            void* hip_stream);
+
+/* Message of the last failed call on this thread (host string, valid
+ * until the next call on this thread); "" after a success. */
+const char* hstu_last_error(void);
+
+int32_t hstu_abi_version(void);
+
+/* Kernel timing for measurement: while enabled, every main kernel launch
+ * is bracketed by HIP events on its stream.  hstu_timing_read
+ * synchronises those events and returns, for the kernel family `name`
+ * ("attn_fwd", "attn_bwd", "ln_gate", "bucketize"), the summed
+ * milliseconds and launch count since the last reset. */
+hstu_status_t hstu_timing_enable(int32_t on);
+hstu_status_t hstu_timing_read(const char* name, double* total_ms,
+                               int64_t* launches);
+hstu_status_t hstu_timing_reset(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* HSTU_H_ */

@@ -1,0 +1,469 @@
+// libhstu C ABI: argument validation, workspace layout, kernel dispatch.
+// See include/hstu.h for the contract of every entry point.
+#include "hstu.h"
+
+#include <hip/hip_runtime.h>
+
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <map>
+#include <mutex>
+#include <string>
+#include <vector>
+
+#include "kernels.h"
+
+namespace {
+
+using namespace hstu;
+
+thread_local std::string g_err;
+
+hstu_status_t fail(hstu_status_t st, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof(buf), fmt, ap);
+  va_end(ap);
+  g_err = buf;
+  return st;
+}
+
+hstu_status_t ok() {
+  g_err.clear();
+  return HSTU_OK;
+}
+
+hstu_status_t hip_fail(hipError_t e, const char* what) {
+  return fail(HSTU_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+// ---- kernel timing ----------------------------------------------------
+
+struct Pending {
+  std::string name;
+  hipEvent_t start, stop;
+};
+std::mutex g_tmu;
+bool g_timing = false;
+std::vector<Pending> g_pending;
+std::map<std::string, std::pair<double, int64_t>> g_acc;
+
+struct TimedScope {
+  bool on = false;
+  Pending p;
+  hipStream_t s;
+  TimedScope(const char* name, hipStream_t stream) : s(stream) {
+    std::lock_guard<std::mutex> lk(g_tmu);
+    if (!g_timing) return;
+    p.name = name;
+    if (hipEventCreate(&p.start) != hipSuccess) return;
+    if (hipEventCreate(&p.stop) != hipSuccess) {
+      (void)hipEventDestroy(p.start);
+      return;
+    }
+    on = hipEventRecord(p.start, s) == hipSuccess;
+  }
+  ~TimedScope() {
+    if (!on) return;
+    (void)hipEventRecord(p.stop, s);
+    std::lock_guard<std::mutex> lk(g_tmu);
+    g_pending.push_back(p);
+  }
+};
+
+// ---- validation helpers -------------------------------------------------
+
+bool is_head_dim(int d) { return d == 32 || d == 64 || d == 128; }
+
+hstu_status_t check_problem(const hstu_problem_t* p) {
+  if (!p) return fail(HSTU_ERR_INVALID_ARGUMENT, "problem is NULL");
+  if (p->num_seqs < 1) return fail(HSTU_ERR_INVALID_ARGUMENT, "num_seqs must be >= 1 (got %d)", p->num_seqs);
+  if (p->total_tokens < 0) return fail(HSTU_ERR_INVALID_ARGUMENT, "total_tokens must be >= 0");
+  if (p->total_tokens > (int64_t)1 << 40)
+    return fail(HSTU_ERR_UNSUPPORTED, "total_tokens above 2^40 is not supported");
+  if (p->max_seq_len < 1 || p->max_seq_len > 65536)
+    return fail(HSTU_ERR_UNSUPPORTED, "max_seq_len must be in [1, 65536] (got %d)", p->max_seq_len);
+  if (p->num_heads < 1 || p->num_heads > 64)
+    return fail(HSTU_ERR_UNSUPPORTED, "num_heads must be in [1, 64] (got %d)", p->num_heads);
+  if (!is_head_dim(p->d_qk) || !is_head_dim(p->d_v))
+    return fail(HSTU_ERR_UNSUPPORTED, "d_qk and d_v must be 32, 64 or 128 (got %d, %d)", p->d_qk, p->d_v);
+  if (p->num_time_buckets < 1 || p->num_time_buckets > 256)
+    return fail(HSTU_ERR_UNSUPPORTED, "num_time_buckets must be in [1, 256] (got %d)", p->num_time_buckets);
+  if (p->dtype != HSTU_F32 && p->dtype != HSTU_BF16)
+    return fail(HSTU_ERR_INVALID_ARGUMENT, "unknown dtype %d", (int)p->dtype);
+  return HSTU_OK;
+}
+
+hstu_status_t check_jagged(const hstu_jagged_t* j) {
+  if (!j) return fail(HSTU_ERR_INVALID_ARGUMENT, "jagged descriptor is NULL");
+  if (!j->seq_offsets) return fail(HSTU_ERR_INVALID_ARGUMENT, "seq_offsets is NULL");
+  if (!j->timestamps) return fail(HSTU_ERR_INVALID_ARGUMENT, "timestamps is NULL");
+  if (!j->rab_pos) return fail(HSTU_ERR_INVALID_ARGUMENT, "rab_pos is NULL");
+  if (!j->rab_time) return fail(HSTU_ERR_INVALID_ARGUMENT, "rab_time is NULL");
+  return HSTU_OK;
+}
+
+size_t elem_size(const hstu_problem_t* p) { return p->dtype == HSTU_BF16 ? 2 : 4; }
+
+hstu_status_t check_rows(const hstu_problem_t* p, const char* name, const void* ptr,
+                         int64_t stride, int64_t width) {
+  if (!ptr) return fail(HSTU_ERR_INVALID_ARGUMENT, "%s is NULL", name);
+  if ((uintptr_t)ptr % 16) return fail(HSTU_ERR_INVALID_ARGUMENT, "%s is not 16-byte aligned", name);
+  if (stride < width)
+    return fail(HSTU_ERR_INVALID_ARGUMENT, "%s_stride %lld is smaller than a row (%lld)", name,
+                (long long)stride, (long long)width);
+  if ((stride * (int64_t)elem_size(p)) % 16)
+    return fail(HSTU_ERR_INVALID_ARGUMENT, "%s_stride must be a multiple of 16 bytes", name);
+  return HSTU_OK;
+}
+
+hstu_status_t check_dense(const char* name, const void* ptr, size_t align) {
+  if (!ptr) return fail(HSTU_ERR_INVALID_ARGUMENT, "%s is NULL", name);
+  if ((uintptr_t)ptr % align)
+    return fail(HSTU_ERR_INVALID_ARGUMENT, "%s is not %zu-byte aligned", name, align);
+  return HSTU_OK;
+}
+
+// ---- workspace layout ---------------------------------------------------
+
+constexpr size_t kAlign = 256;
+size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
+
+struct Layout {
+  size_t counts;    // int32 [2]: forward and backward item counts
+  size_t fwd_items;
+  size_t bwd_items;
+  size_t dq_acc;    // fp32 [T][h][d_qk] (bf16 problems)
+  size_t total;
+  int64_t max_fwd, max_bwd;
+};
+
+Layout layout(const hstu_problem_t* p) {
+  Layout l;
+  l.max_fwd = max_work_items(p->total_tokens, p->num_seqs, kFwdBM);
+  l.max_bwd = max_work_items(p->total_tokens, p->num_seqs, kBwdBN);
+  size_t off = 0;
+  l.counts = off;
+  off = align_up(off + 2 * sizeof(int32_t));
+  l.fwd_items = off;
+  off = align_up(off + sizeof(WorkItem) * (size_t)l.max_fwd);
+  l.bwd_items = off;
+  off = align_up(off + sizeof(WorkItem) * (size_t)l.max_bwd);
+  l.dq_acc = off;
+  if (p->dtype == HSTU_BF16)
+    off = align_up(off + sizeof(float) * (size_t)p->total_tokens * p->num_heads * p->d_qk);
+  l.total = off;
+  return l;
+}
+
+hstu_status_t check_ws(const hstu_problem_t* p, void* ws, size_t ws_bytes, Layout* l) {
+  *l = layout(p);
+  if (!ws) return fail(HSTU_ERR_WORKSPACE, "workspace is NULL (need %zu bytes)", l->total);
+  if ((uintptr_t)ws % kAlign) return fail(HSTU_ERR_WORKSPACE, "workspace must be 256-byte aligned");
+  if (ws_bytes < l->total)
+    return fail(HSTU_ERR_WORKSPACE, "workspace too small: %zu < %zu bytes", ws_bytes, l->total);
+  return HSTU_OK;
+}
+
+JaggedArgs make_args(const hstu_problem_t* p, const hstu_jagged_t* j) {
+  JaggedArgs a;
+  a.seq_offsets = j->seq_offsets;
+  a.timestamps = j->timestamps;
+  a.num_targets = j->num_targets;
+  a.rab_pos = j->rab_pos;
+  a.rab_time = j->rab_time;
+  a.num_seqs = p->num_seqs;
+  a.max_seq_len = p->max_seq_len;
+  a.num_heads = p->num_heads;
+  a.num_buckets = p->num_time_buckets;
+  a.total_tokens = p->total_tokens;
+  return a;
+}
+
+#define HSTU_TRY(expr)                 \
+  do {                                 \
+    hstu_status_t st_ = (expr);        \
+    if (st_ != HSTU_OK) return st_;    \
+  } while (0)
+
+#define HSTU_HIP(expr, what)                  \
+  do {                                        \
+    hipError_t e_ = (expr);                   \
+    if (e_ != hipSuccess) return hip_fail(e_, what); \
+  } while (0)
+
+hstu_status_t attn_fwd_impl(const hstu_problem_t* p, const hstu_jagged_t* j, const Tensors& t,
+                            void* out, void* ws, size_t ws_bytes, hipStream_t s) {
+  HSTU_TRY(check_problem(p));
+  HSTU_TRY(check_jagged(j));
+  const int64_t T = p->total_tokens;
+  const int H = p->num_heads;
+  HSTU_TRY(check_rows(p, "q", t.q, t.q_stride, (int64_t)H * p->d_qk));
+  HSTU_TRY(check_rows(p, "k", t.k, t.k_stride, (int64_t)H * p->d_qk));
+  HSTU_TRY(check_rows(p, "v", t.v, t.v_stride, (int64_t)H * p->d_v));
+  HSTU_TRY(check_dense("out", out, 16));
+  Layout l;
+  HSTU_TRY(check_ws(p, ws, ws_bytes, &l));
+  if (T == 0) return ok();
+  JaggedArgs ja = make_args(p, j);
+  char* w = (char*)ws;
+  if (p->dtype == HSTU_F32) {
+    TimedScope ts("attn_fwd", s);
+    HSTU_HIP(launch_attn_fwd_f32(ja, t, p->d_qk, p->d_v, out, s), "attn_fwd_f32 launch");
+    return ok();
+  }
+  int32_t* counts = (int32_t*)(w + l.counts);
+  WorkItem* items = (WorkItem*)(w + l.fwd_items);
+  HSTU_HIP(launch_schedule(ja, 0, items, counts, s), "schedule launch");
+  TimedScope ts("attn_fwd", s);
+  HSTU_HIP(launch_attn_fwd_bf16(ja, t, p->d_qk, p->d_v, out, items, counts, l.max_fwd, s),
+           "attn_fwd launch");
+  return ok();
+}
+
+}  // namespace
+
+extern "C" {
+
+int32_t hstu_abi_version(void) { return HSTU_ABI_VERSION; }
+
+const char* hstu_last_error(void) { return g_err.c_str(); }
+
+size_t hstu_workspace_bytes(const hstu_problem_t* p) {
+  try {
+    if (check_problem(p) != HSTU_OK) return 0;
+    return layout(p).total;
+  } catch (...) {
+    return 0;
+  }
+}
+
+hstu_status_t hstu_attn_fwd(const hstu_problem_t* p, const hstu_jagged_t* j, const void* q,
+                            int64_t q_stride, const void* k, int64_t k_stride, const void* v,
+                            int64_t v_stride, void* out, void* ws, size_t ws_bytes,
+                            void* hip_stream) {
+  try {
+    Tensors t{q, q_stride, k, k_stride, v, v_stride};
+    return attn_fwd_impl(p, j, t, out, ws, ws_bytes, (hipStream_t)hip_stream);
+  } catch (...) {
+    return fail(HSTU_ERR_INVALID_ARGUMENT, "internal error");
+  }
+}
+
+hstu_status_t hstu_attn_bwd(const hstu_problem_t* p, const hstu_jagged_t* j, const void* q,
+                            int64_t q_stride, const void* k, int64_t k_stride, const void* v,
+                            int64_t v_stride, const void* d_out, void* dq, void* dk, void* dv,
+                            float* d_rab_pos, float* d_rab_time, void* ws, size_t ws_bytes,
+                            void* hip_stream) {
+  try {
+    hipStream_t s = (hipStream_t)hip_stream;
+    HSTU_TRY(check_problem(p));
+    HSTU_TRY(check_jagged(j));
+    const int64_t T = p->total_tokens;
+    const int H = p->num_heads;
+    Tensors t{q, q_stride, k, k_stride, v, v_stride};
+    HSTU_TRY(check_rows(p, "q", q, q_stride, (int64_t)H * p->d_qk));
+    HSTU_TRY(check_rows(p, "k", k, k_stride, (int64_t)H * p->d_qk));
+    HSTU_TRY(check_rows(p, "v", v, v_stride, (int64_t)H * p->d_v));
+    HSTU_TRY(check_dense("d_out", d_out, 16));
+    HSTU_TRY(check_dense("dq", dq, 16));
+    HSTU_TRY(check_dense("dk", dk, 16));
+    HSTU_TRY(check_dense("dv", dv, 16));
+    HSTU_TRY(check_dense("d_rab_pos", d_rab_pos, 4));
+    HSTU_TRY(check_dense("d_rab_time", d_rab_time, 4));
+    Layout l;
+    HSTU_TRY(check_ws(p, ws, ws_bytes, &l));
+    const int N = p->max_seq_len;
+    HSTU_HIP(launch_fill_f32(d_rab_pos, 2 * (int64_t)N - 1, 0.0f, s), "fill launch");
+    HSTU_HIP(launch_fill_f32(d_rab_time, p->num_time_buckets, 0.0f, s), "fill launch");
+    if (T == 0) return ok();
+    JaggedArgs ja = make_args(p, j);
+    char* w = (char*)ws;
+    if (p->dtype == HSTU_F32) {
+      TimedScope ts("attn_bwd", s);
+      HSTU_HIP(launch_attn_bwd_f32(ja, t, p->d_qk, p->d_v, d_out, dq, dk, dv, d_rab_pos,
+                                   d_rab_time, s),
+               "attn_bwd_f32 launch");
+      return ok();
+    }
+    int32_t* counts = (int32_t*)(w + l.counts);
+    WorkItem* items = (WorkItem*)(w + l.bwd_items);
+    float* dq_acc = (float*)(w + l.dq_acc);
+    const int64_t ndq = T * H * p->d_qk;
+    HSTU_HIP(launch_fill_f32(dq_acc, ndq, 0.0f, s), "fill launch");
+    HSTU_HIP(launch_schedule(ja, 1, items, counts + 1, s), "schedule launch");
+    {
+      TimedScope ts("attn_bwd", s);
+      HSTU_HIP(launch_attn_bwd_bf16(ja, t, p->d_qk, p->d_v, d_out, dq_acc, dk, dv, d_rab_pos,
+                                    d_rab_time, items, counts + 1, l.max_bwd, s),
+               "attn_bwd launch");
+    }
+    HSTU_HIP(launch_dq_convert_bf16(dq_acc, dq, ndq, 1.0f / (float)N, s), "dq convert launch");
+    return ok();
+  } catch (...) {
+    return fail(HSTU_ERR_INVALID_ARGUMENT, "internal error");
+  }
+}
+
+hstu_status_t hstu_layer_fwd(const hstu_problem_t* p, const hstu_jagged_t* j, const void* q,
+                             int64_t q_stride, const void* k, int64_t k_stride, const void* v,
+                             int64_t v_stride, const void* u, int64_t u_stride,
+                             const float* ln_weight, const float* ln_bias, float ln_eps,
+                             void* attn_out, void* y, float* ln_mean, float* ln_rstd, void* ws,
+                             size_t ws_bytes, void* hip_stream) {
+  try {
+    hipStream_t s = (hipStream_t)hip_stream;
+    HSTU_TRY(check_problem(p));
+    const int64_t D = (int64_t)p->num_heads * p->d_v;
+    if (D > 4096) return fail(HSTU_ERR_UNSUPPORTED, "h*d_v must be <= 4096 (got %lld)", (long long)D);
+    HSTU_TRY(check_rows(p, "u", u, u_stride, D));
+    HSTU_TRY(check_dense("y", y, 16));
+    if (!(ln_eps >= 0.0f)) return fail(HSTU_ERR_INVALID_ARGUMENT, "ln_eps must be >= 0");
+    Tensors t{q, q_stride, k, k_stride, v, v_stride};
+    HSTU_TRY(attn_fwd_impl(p, j, t, attn_out, ws, ws_bytes, s));
+    if (p->total_tokens == 0) return ok();
+    TimedScope ts("ln_gate", s);
+    HSTU_HIP(launch_ln_gate(p->dtype == HSTU_BF16, p->total_tokens, (int32_t)D, attn_out, u,
+                            u_stride, ln_weight, ln_bias, ln_eps, y, ln_mean, ln_rstd, s),
+             "ln_gate launch");
+    return ok();
+  } catch (...) {
+    return fail(HSTU_ERR_INVALID_ARGUMENT, "internal error");
+  }
+}
+
+hstu_status_t hstu_time_bucketize(int32_t num_seqs, int64_t total_tokens, int32_t num_time_buckets,
+                                  const int64_t* seq_offsets, const int64_t* timestamps,
+                                  const int64_t* pair_offsets, int64_t total_pairs,
+                                  uint8_t* buckets, void* hip_stream) {
+  try {
+    if (num_seqs < 1) return fail(HSTU_ERR_INVALID_ARGUMENT, "num_seqs must be >= 1");
+    if (total_tokens < 0 || total_pairs < 0)
+      return fail(HSTU_ERR_INVALID_ARGUMENT, "negative size");
+    if (num_time_buckets < 1 || num_time_buckets > 256)
+      return fail(HSTU_ERR_UNSUPPORTED, "num_time_buckets must be in [1, 256]");
+    if (!seq_offsets || !pair_offsets) return fail(HSTU_ERR_INVALID_ARGUMENT, "offsets are NULL");
+    if (total_pairs > 0) {
+      if (!timestamps) return fail(HSTU_ERR_INVALID_ARGUMENT, "timestamps is NULL");
+      HSTU_TRY(check_dense("buckets", buckets, 16));
+    }
+    TimedScope ts("bucketize", (hipStream_t)hip_stream);
+    HSTU_HIP(launch_bucketize(num_seqs, num_time_buckets, seq_offsets, timestamps, pair_offsets,
+                              total_pairs, buckets, (hipStream_t)hip_stream),
+             "bucketize launch");
+    return ok();
+  } catch (...) {
+    return fail(HSTU_ERR_INVALID_ARGUMENT, "internal error");
+  }
+}
+
+hstu_status_t hstu_complete_cumsum(int32_t n, const int64_t* in, int64_t* out, void* hip_stream) {
+  try {
+    if (n < 0) return fail(HSTU_ERR_INVALID_ARGUMENT, "n must be >= 0");
+    if (!out || (n > 0 && !in)) return fail(HSTU_ERR_INVALID_ARGUMENT, "NULL pointer");
+    HSTU_HIP(launch_complete_cumsum(n, in, out, 0, (hipStream_t)hip_stream), "cumsum launch");
+    return ok();
+  } catch (...) {
+    return fail(HSTU_ERR_INVALID_ARGUMENT, "internal error");
+  }
+}
+
+hstu_status_t hstu_pair_offsets(int32_t num_seqs, const int64_t* seq_offsets, int64_t* pair_offsets,
+                                void* hip_stream) {
+  try {
+    if (num_seqs < 1) return fail(HSTU_ERR_INVALID_ARGUMENT, "num_seqs must be >= 1");
+    if (!seq_offsets || !pair_offsets) return fail(HSTU_ERR_INVALID_ARGUMENT, "NULL pointer");
+    HSTU_HIP(launch_complete_cumsum(num_seqs, seq_offsets, pair_offsets, 1, (hipStream_t)hip_stream),
+             "pair offsets launch");
+    return ok();
+  } catch (...) {
+    return fail(HSTU_ERR_INVALID_ARGUMENT, "internal error");
+  }
+}
+
+hstu_status_t hstu_validate(const hstu_problem_t* p, const hstu_jagged_t* j, void* hip_stream) {
+  try {
+    HSTU_TRY(check_problem(p));
+    HSTU_TRY(check_jagged(j));
+    hipStream_t s = (hipStream_t)hip_stream;
+    const int B = p->num_seqs;
+    const int64_t T = p->total_tokens;
+    std::vector<int64_t> offs(B + 1), nt(B, 0), ts((size_t)T);
+    HSTU_HIP(hipMemcpyAsync(offs.data(), j->seq_offsets, sizeof(int64_t) * (B + 1),
+                            hipMemcpyDeviceToHost, s), "copy offsets");
+    if (j->num_targets)
+      HSTU_HIP(hipMemcpyAsync(nt.data(), j->num_targets, sizeof(int64_t) * B, hipMemcpyDeviceToHost, s),
+               "copy num_targets");
+    if (T > 0)
+      HSTU_HIP(hipMemcpyAsync(ts.data(), j->timestamps, sizeof(int64_t) * T, hipMemcpyDeviceToHost, s),
+               "copy timestamps");
+    HSTU_HIP(hipStreamSynchronize(s), "synchronize");
+    if (offs[0] != 0) return fail(HSTU_ERR_DATA, "seq_offsets[0] = %lld, expected 0", (long long)offs[0]);
+    if (offs[B] != T)
+      return fail(HSTU_ERR_DATA, "seq_offsets[B] = %lld, expected total_tokens %lld",
+                  (long long)offs[B], (long long)T);
+    for (int b = 0; b < B; b++) {
+      const int64_t L = offs[b + 1] - offs[b];
+      if (L < 0) return fail(HSTU_ERR_DATA, "seq_offsets decreases at b = %d", b);
+      if (L > p->max_seq_len)
+        return fail(HSTU_ERR_DATA, "sequence %d has length %lld > max_seq_len %d", b, (long long)L,
+                    p->max_seq_len);
+      if (nt[b] < 0 || nt[b] > L)
+        return fail(HSTU_ERR_DATA, "num_targets[%d] = %lld outside [0, %lld]", b, (long long)nt[b],
+                    (long long)L);
+    }
+    for (int64_t i = 0; i < T; i++)
+      if (ts[i] < 0 || ts[i] >= ((int64_t)1 << 62))
+        return fail(HSTU_ERR_DATA, "timestamps[%lld] = %lld outside [0, 2^62)", (long long)i,
+                    (long long)ts[i]);
+    return ok();
+  } catch (...) {
+    return fail(HSTU_ERR_INVALID_ARGUMENT, "internal error");
+  }
+}
+
+hstu_status_t hstu_timing_enable(int32_t on) {
+  std::lock_guard<std::mutex> lk(g_tmu);
+  g_timing = on != 0;
+  return ok();
+}
+
+hstu_status_t hstu_timing_reset(void) {
+  std::lock_guard<std::mutex> lk(g_tmu);
+  for (auto& p : g_pending) {
+    (void)hipEventSynchronize(p.stop);
+    (void)hipEventDestroy(p.start);
+    (void)hipEventDestroy(p.stop);
+  }
+  g_pending.clear();
+  g_acc.clear();
+  return ok();
+}
+
+hstu_status_t hstu_timing_read(const char* name, double* total_ms, int64_t* launches) {
+  if (!name || !total_ms || !launches) return fail(HSTU_ERR_INVALID_ARGUMENT, "NULL pointer");
+  std::lock_guard<std::mutex> lk(g_tmu);
+  for (auto& p : g_pending) {
+    hipError_t e = hipEventSynchronize(p.stop);
+    float ms = 0.0f;
+    if (e == hipSuccess) e = hipEventElapsedTime(&ms, p.start, p.stop);
+    (void)hipEventDestroy(p.start);
+    (void)hipEventDestroy(p.stop);
+    if (e != hipSuccess) {
+      g_pending.clear();
+      return hip_fail(e, "timing events");
+    }
+    auto& a = g_acc[p.name];
+    a.first += ms;
+    a.second += 1;
+  }
+  g_pending.clear();
+  auto it = g_acc.find(name);
+  *total_ms = it == g_acc.end() ? 0.0 : it->second.first;
+  *launches = it == g_acc.end() ? 0 : it->second.second;
+  return ok();
+}
+
+}  // extern "C"

@@ -1,0 +1,89 @@
+// Device helpers shared by the libhstu kernels (gfx950 / CDNA4).
+//
+// Definitions restated from the paper (Zhai et al., ICML 2024):
+//  - mask: causal with the diagonal; candidates (the last n_t tokens of a
+//    sequence) see the history and themselves only (Algorithm 1);
+//  - bias position: every candidate sits at position n_h = L - n_t;
+//  - time bucket: min(B_t - 1, floor(log2(max(|t_i - t_j|, 1))))
+//    (notation table, entry rab^{p,t});
+//  - phi2 = SiLU (Eq. 2).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace hstu {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+
+constexpr float kLog2e = 1.4426950408889634f;
+
+// One work item of the jagged tile scheduler: (sequence, block index).
+struct WorkItem {
+  int32_t seq;
+  int32_t blk;
+};
+
+__device__ __forceinline__ bool pair_valid(int i, int j, int n_h) {
+  return j <= i && (j < n_h || j == i);
+}
+
+__device__ __forceinline__ int bias_pos(int x, int n_h) { return x < n_h ? x : n_h; }
+
+// floor(log2(max(|dt|, 1))) clamped to nb-1, exact integer arithmetic.
+__device__ __forceinline__ int time_bucket64(int64_t dt, int nb) {
+  uint64_t a = dt < 0 ? (uint64_t)0 - (uint64_t)dt : (uint64_t)dt;
+  a = a < 1 ? 1 : a;
+  int b = 63 - __clzll((long long)a);
+  return b < nb - 1 ? b : nb - 1;
+}
+
+// sigma(x) with one exp2 and one reciprocal (both hardware transcendentals).
+__device__ __forceinline__ float sigmoid_fast(float x) {
+  float e = __builtin_amdgcn_exp2f(-x * kLog2e);
+  return __builtin_amdgcn_rcpf(1.0f + e);
+}
+
+__device__ __forceinline__ f32x16 mfma32x32x16(bf16x8 a, bf16x8 b, f32x16 c) {
+  return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
+}
+
+__device__ __forceinline__ bf16x8 as_bf16x8(u32x4 v) { return __builtin_bit_cast(bf16x8, v); }
+
+__device__ __forceinline__ u32x4 zero_u32x4() {
+  u32x4 z = {0u, 0u, 0u, 0u};
+  return z;
+}
+
+// Packs two floats into two bf16 (round to nearest even) in one dword.
+__device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
+  bf16x2 r;
+  r[0] = (__bf16)lo;
+  r[1] = (__bf16)hi;
+  return __builtin_bit_cast(uint32_t, r);
+}
+
+__device__ __forceinline__ float bf16_bits_to_f32(uint16_t b) {
+  return __uint_as_float(((uint32_t)b) << 16);
+}
+
+__device__ __forceinline__ uint16_t f32_to_bf16_bits(float x) {
+  return __builtin_bit_cast(uint16_t, (__bf16)x);
+}
+
+// Position of row index `r` (0..31) inside a 32-wide LDS strip whose
+// contraction order matches the 32x32 MFMA accumulator layout: an
+// accumulator lane holds rows 8*g + 4*half + m (g = 0..3, m = 0..3) and
+// feeds them as the k-operand of the next contraction in the order
+// (step = g/2, half, g%2, m).  Storing row r at swap_bits23(r) lets the
+// other operand be read with one 16-byte LDS load.
+__device__ __forceinline__ int swap_bits23(int r) {
+  return (r & ~12) | ((r & 4) << 1) | ((r & 8) >> 1);
+}
+
+}  // namespace hstu

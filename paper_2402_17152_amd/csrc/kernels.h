@@ -1,0 +1,84 @@
+// Host-side launchers of the libhstu kernels (internal to the library).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+#include "common.h"
+
+namespace hstu {
+
+// Everything an attention kernel needs to know about the jagged batch.
+struct JaggedArgs {
+  const int64_t* seq_offsets;
+  const int64_t* timestamps;
+  const int64_t* num_targets;  // may be null
+  const float* rab_pos;
+  const float* rab_time;
+  int32_t num_seqs;
+  int32_t max_seq_len;  // N
+  int32_t num_heads;
+  int32_t num_buckets;
+  int64_t total_tokens;
+};
+
+struct Tensors {
+  const void* q;
+  int64_t q_stride;
+  const void* k;
+  int64_t k_stride;
+  const void* v;
+  int64_t v_stride;
+};
+
+// Tile sizes of the bf16 MFMA kernels.
+constexpr int kFwdBM = 128;  // query rows per forward workgroup
+constexpr int kFwdBN = 32;   // keys per forward step
+constexpr int kBwdBN = 128;  // keys owned by a backward workgroup
+constexpr int kBwdBM = 32;   // query rows per backward step
+constexpr int kBwdMaxLdsPos = 16384;  // bias-position gradient kept in LDS up to this N
+
+// Upper bound on the number of (sequence, block) work items for blocks of
+// `blk` tokens: sum_b ceil(L_b / blk) <= ceil(T / blk) + B.
+inline int64_t max_work_items(int64_t T, int32_t B, int blk) {
+  return (T + blk - 1) / blk + B;
+}
+
+// Scheduler: builds the work list (longest first) into `items` and
+// its length into `count`.  mode 0: forward (seq, q-block of kFwdBM rows);
+// mode 1: backward (seq, k-block of kBwdBN keys).
+hipError_t launch_schedule(const JaggedArgs& ja, int mode, WorkItem* items, int32_t* count,
+                           hipStream_t s);
+
+hipError_t launch_fill_f32(float* p, int64_t n, float value, hipStream_t s);
+hipError_t launch_complete_cumsum(int32_t n, const int64_t* in, int64_t* out, int square_of_diff,
+                                  hipStream_t s);
+hipError_t launch_bucketize(int32_t num_seqs, int32_t num_buckets, const int64_t* seq_offsets,
+                            const int64_t* timestamps, const int64_t* pair_offsets,
+                            int64_t total_pairs, uint8_t* out, hipStream_t s);
+
+// bf16 MFMA attention.
+hipError_t launch_attn_fwd_bf16(const JaggedArgs& ja, const Tensors& t, int dqk, int dv, void* out,
+                                const WorkItem* items, const int32_t* count, int64_t max_items,
+                                hipStream_t s);
+hipError_t launch_attn_bwd_bf16(const JaggedArgs& ja, const Tensors& t, int dqk, int dv,
+                                const void* d_out, float* dq_acc, void* dk, void* dv_out,
+                                float* d_rab_pos, float* d_rab_time, const WorkItem* items,
+                                const int32_t* count, int64_t max_items, hipStream_t s);
+hipError_t launch_dq_convert_bf16(const float* acc, void* dq, int64_t n, float scale,
+                                  hipStream_t s);
+
+// fp32 SIMT attention.
+hipError_t launch_attn_fwd_f32(const JaggedArgs& ja, const Tensors& t, int dqk, int dv, void* out,
+                               hipStream_t s);
+hipError_t launch_attn_bwd_f32(const JaggedArgs& ja, const Tensors& t, int dqk, int dv,
+                               const void* d_out, void* dq, void* dk, void* dv_out,
+                               float* d_rab_pos, float* d_rab_time, hipStream_t s);
+
+// LayerNorm(x) (.) u per token over D features.
+hipError_t launch_ln_gate(int is_bf16, int64_t T, int32_t D, const void* x, const void* u,
+                          int64_t u_stride, const float* w, const float* b, float eps, void* y,
+                          float* mean, float* rstd, hipStream_t s);
+
+}  // namespace hstu

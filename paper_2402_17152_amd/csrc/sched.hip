@@ -1,0 +1,192 @@
+// Jagged tile scheduler and small utility kernels.
+//
+// The scheduler turns the jagged batch into a list of (sequence, block)
+// work items for the attention kernels -- the "fully raggified" grouped
+// computation of the paper (Sec. 3.2; appendix on the fused kernels):
+// no padding, causally empty tiles never become work.  Items are written
+// longest-first (counting sort by tile count) so that the hardware
+// dispatcher, which hands out workgroups in index order, starts the
+// longest items first.
+#include "kernels.h"
+
+namespace hstu {
+
+namespace {
+
+constexpr int kSchedThreads = 1024;
+
+__device__ __forceinline__ int ceil_div(int a, int b) { return (a + b - 1) / b; }
+
+// Forward item (q-block qb): number of key tiles of kFwdBN the forward
+// kernel visits.  Key tiles made only of candidates that lie before the
+// block's first row are fully masked and skipped.
+__device__ __forceinline__ int fwd_weight(int L, int n_h, int qb) {
+  int i0 = qb * kFwdBM;
+  int rows_end = min(i0 + kFwdBM, L);
+  int kend = ceil_div(rows_end, kFwdBN);
+  int skipped = max(0, i0 / kFwdBN - ceil_div(n_h, kFwdBN));
+  return kend - skipped;
+}
+
+// Backward item (k-block kb): number of query steps of kBwdBM rows.
+__device__ __forceinline__ int bwd_weight(int L, int n_h, int kb) {
+  int j0 = kb * kBwdBN;
+  int i_end = j0 >= n_h ? min(j0 + kBwdBN, L) : L;
+  return ceil_div(i_end - j0, kBwdBM);
+}
+
+__global__ __launch_bounds__(kSchedThreads) void schedule_kernel(JaggedArgs ja, int mode,
+                                                                 WorkItem* items,
+                                                                 int32_t* count) {
+  extern __shared__ int s_bins[];  // [nbins]
+  __shared__ int s_scan[kSchedThreads];
+  const int tid = threadIdx.x;
+  const int blk = mode == 0 ? kFwdBM : kBwdBN;
+  const int maxw = mode == 0 ? ceil_div(ja.max_seq_len, kFwdBN) : ceil_div(ja.max_seq_len, kBwdBM);
+  const int nbins = maxw + 1;
+  for (int i = tid; i < nbins; i += kSchedThreads) s_bins[i] = 0;
+  __syncthreads();
+
+  // Pass 1: histogram of item weights (bin index = maxw - weight, so that
+  // an ascending scan orders items by descending weight).
+  for (int b = tid; b < ja.num_seqs; b += kSchedThreads) {
+    int L = (int)(ja.seq_offsets[b + 1] - ja.seq_offsets[b]);
+    int n_h = L - (ja.num_targets ? (int)ja.num_targets[b] : 0);
+    int nblk = ceil_div(L, blk);
+    for (int x = 0; x < nblk; x++) {
+      int w = mode == 0 ? fwd_weight(L, n_h, x) : bwd_weight(L, n_h, x);
+      w = min(max(w, 0), maxw);
+      atomicAdd(&s_bins[maxw - w], 1);
+    }
+  }
+  __syncthreads();
+
+  // Exclusive scan of the bins: each thread owns a contiguous run.
+  const int per = ceil_div(nbins, kSchedThreads);
+  const int lo = tid * per, hi = min(lo + per, nbins);
+  int local = 0;
+  for (int i = lo; i < hi; i++) local += s_bins[i];
+  s_scan[tid] = local;
+  __syncthreads();
+  for (int off = 1; off < kSchedThreads; off <<= 1) {
+    int v = tid >= off ? s_scan[tid - off] : 0;
+    __syncthreads();
+    s_scan[tid] += v;
+    __syncthreads();
+  }
+  int run = s_scan[tid] - local;
+  for (int i = lo; i < hi; i++) {
+    int c = s_bins[i];
+    s_bins[i] = run;
+    run += c;
+  }
+  if (tid == kSchedThreads - 1) *count = s_scan[tid];
+  __syncthreads();
+
+  // Pass 2: scatter the items to their sorted positions.
+  for (int b = tid; b < ja.num_seqs; b += kSchedThreads) {
+    int L = (int)(ja.seq_offsets[b + 1] - ja.seq_offsets[b]);
+    int n_h = L - (ja.num_targets ? (int)ja.num_targets[b] : 0);
+    int nblk = ceil_div(L, blk);
+    for (int x = 0; x < nblk; x++) {
+      int w = mode == 0 ? fwd_weight(L, n_h, x) : bwd_weight(L, n_h, x);
+      w = min(max(w, 0), maxw);
+      int pos = atomicAdd(&s_bins[maxw - w], 1);
+      WorkItem it;
+      it.seq = b;
+      it.blk = x;
+      items[pos] = it;
+    }
+  }
+}
+
+__global__ void fill_f32_kernel(float* p, int64_t n, float value) {
+  int64_t stride = (int64_t)gridDim.x * blockDim.x;
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += stride) p[i] = value;
+}
+
+// out[0] = 0, out[i+1] = out[i] + x_i; x_i = in[i], or (in[i+1]-in[i])^2
+// when square_of_diff (pair offsets of the bucket matrices).
+__global__ __launch_bounds__(kSchedThreads) void cumsum_kernel(int32_t n, const int64_t* in,
+                                                               int64_t* out, int square_of_diff) {
+  __shared__ int64_t s[kSchedThreads];
+  const int tid = threadIdx.x;
+  int64_t carry = 0;
+  if (tid == 0) out[0] = 0;
+  for (int32_t base = 0; base < n; base += kSchedThreads) {
+    int32_t i = base + tid;
+    int64_t x = 0;
+    if (i < n) {
+      if (square_of_diff) {
+        int64_t d = in[i + 1] - in[i];
+        x = d * d;
+      } else {
+        x = in[i];
+      }
+    }
+    s[tid] = x;
+    __syncthreads();
+    for (int off = 1; off < kSchedThreads; off <<= 1) {
+      int64_t v = tid >= off ? s[tid - off] : 0;
+      __syncthreads();
+      s[tid] += v;
+      __syncthreads();
+    }
+    if (i < n) out[i + 1] = carry + s[tid];
+    int64_t total = s[kSchedThreads - 1];
+    __syncthreads();
+    carry += total;
+  }
+}
+
+__global__ void dq_convert_kernel(const float* __restrict__ acc, uint16_t* __restrict__ dq,
+                                  int64_t n4, float scale) {
+  int64_t stride = (int64_t)gridDim.x * blockDim.x;
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n4; i += stride) {
+    f32x4 a = reinterpret_cast<const f32x4*>(acc)[i];
+    uint32_t lo = pack_bf16x2(a[0] * scale, a[1] * scale);
+    uint32_t hi = pack_bf16x2(a[2] * scale, a[3] * scale);
+    reinterpret_cast<uint2*>(dq)[i] = make_uint2(lo, hi);
+  }
+}
+
+int grid_for(int64_t n, int threads) {
+  int64_t g = (n + threads - 1) / threads;
+  if (g > 65536) g = 65536;
+  return (int)(g < 1 ? 1 : g);
+}
+
+}  // namespace
+
+hipError_t launch_schedule(const JaggedArgs& ja, int mode, WorkItem* items, int32_t* count,
+                           hipStream_t s) {
+  int maxw = mode == 0 ? (ja.max_seq_len + kFwdBN - 1) / kFwdBN
+                       : (ja.max_seq_len + kBwdBM - 1) / kBwdBM;
+  size_t lds = sizeof(int) * (size_t)(maxw + 1);
+  hipLaunchKernelGGL(schedule_kernel, dim3(1), dim3(kSchedThreads), lds, s, ja, mode, items, count);
+  return hipGetLastError();
+}
+
+hipError_t launch_fill_f32(float* p, int64_t n, float value, hipStream_t s) {
+  if (n <= 0) return hipSuccess;
+  hipLaunchKernelGGL(fill_f32_kernel, dim3(grid_for(n, 256)), dim3(256), 0, s, p, n, value);
+  return hipGetLastError();
+}
+
+hipError_t launch_complete_cumsum(int32_t n, const int64_t* in, int64_t* out, int square_of_diff,
+                                  hipStream_t s) {
+  hipLaunchKernelGGL(cumsum_kernel, dim3(1), dim3(kSchedThreads), 0, s, n, in, out,
+                     square_of_diff);
+  return hipGetLastError();
+}
+
+hipError_t launch_dq_convert_bf16(const float* acc, void* dq, int64_t n, float scale,
+                                  hipStream_t s) {
+  if (n <= 0) return hipSuccess;
+  int64_t n4 = n / 4;  // n is a multiple of 32 (d_qk)
+  hipLaunchKernelGGL(dq_convert_kernel, dim3(grid_for(n4, 256)), dim3(256), 0, s, acc,
+                     (uint16_t*)dq, n4, scale);
+  return hipGetLastError();
+}
+
+}  // namespace hstu

@@ -1,0 +1,272 @@
+"""ctypes binding of libhstu (include/hstu.h), argument marshalling only.
+
+Each C entry point has a Python function of the same name that takes
+torch tensors (device memory) and passes their data pointers, strides and
+the current HIP stream.  Every step of the computation runs in the HIP
+kernels of libhstu.so; if the library is missing or fails to load, import
+of this module raises.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Optional
+
+import torch
+
+_PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_PKG, "libhstu.so")
+
+HSTU_F32, HSTU_BF16 = 0, 1
+STATUS = {0: "HSTU_OK", 1: "HSTU_ERR_INVALID_ARGUMENT", 2: "HSTU_ERR_UNSUPPORTED",
+          3: "HSTU_ERR_WORKSPACE", 4: "HSTU_ERR_HIP", 5: "HSTU_ERR_DATA"}
+
+EXPORTED = ("hstu_workspace_bytes", "hstu_attn_fwd", "hstu_attn_bwd", "hstu_layer_fwd",
+            "hstu_time_bucketize", "hstu_complete_cumsum", "hstu_pair_offsets", "hstu_validate",
+            "hstu_last_error", "hstu_abi_version", "hstu_timing_enable", "hstu_timing_read",
+            "hstu_timing_reset")
+
+
+class Problem(ctypes.Structure):
+    _fields_ = [("num_seqs", ctypes.c_int32), ("total_tokens", ctypes.c_int64),
+                ("max_seq_len", ctypes.c_int32), ("num_heads", ctypes.c_int32),
+                ("d_qk", ctypes.c_int32), ("d_v", ctypes.c_int32),
+                ("num_time_buckets", ctypes.c_int32), ("dtype", ctypes.c_int32)]
+
+
+class Jagged(ctypes.Structure):
+    _fields_ = [("seq_offsets", ctypes.c_void_p), ("timestamps", ctypes.c_void_p),
+                ("num_targets", ctypes.c_void_p), ("rab_pos", ctypes.c_void_p),
+                ("rab_time", ctypes.c_void_p)]
+
+
+class HstuError(RuntimeError):
+    def __init__(self, status: int, message: str):
+        super().__init__(f"{STATUS.get(status, status)}: {message}")
+        self.status = status
+
+
+def _load():
+    if not os.path.exists(LIB_PATH):
+        raise ImportError(f"{LIB_PATH} is missing: build it with __graft_entry__.build()")
+    lib = ctypes.CDLL(LIB_PATH)
+    P, i32, i64, sz, f32 = (ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64, ctypes.c_size_t,
+                            ctypes.c_float)
+    PP, PJ = ctypes.POINTER(Problem), ctypes.POINTER(Jagged)
+    sig = {
+        "hstu_workspace_bytes": (sz, [PP]),
+        "hstu_attn_fwd": (i32, [PP, PJ, P, i64, P, i64, P, i64, P, P, sz, P]),
+        "hstu_attn_bwd": (i32, [PP, PJ, P, i64, P, i64, P, i64, P, P, P, P, P, P, P, sz, P]),
+        "hstu_layer_fwd": (i32, [PP, PJ, P, i64, P, i64, P, i64, P, i64, P, P, f32, P, P, P, P,
+                                 P, sz, P]),
+        "hstu_time_bucketize": (i32, [i32, i64, i32, P, P, P, i64, P, P]),
+        "hstu_complete_cumsum": (i32, [i32, P, P, P]),
+        "hstu_pair_offsets": (i32, [i32, P, P, P]),
+        "hstu_validate": (i32, [PP, PJ, P]),
+        "hstu_last_error": (ctypes.c_char_p, []),
+        "hstu_abi_version": (i32, []),
+        "hstu_timing_enable": (i32, [i32]),
+        "hstu_timing_read": (i32, [ctypes.c_char_p, ctypes.POINTER(ctypes.c_double),
+                                   ctypes.POINTER(ctypes.c_int64)]),
+        "hstu_timing_reset": (i32, []),
+    }
+    for name, (res, args) in sig.items():
+        fn = getattr(lib, name)
+        fn.restype = res
+        fn.argtypes = args
+    return lib
+
+
+lib = _load()
+
+
+def _check(status: int):
+    if status != 0:
+        raise HstuError(status, lib.hstu_last_error().decode())
+
+
+def _ptr(t: Optional[torch.Tensor]):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def _stream(stream=None):
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    return ctypes.c_void_p(stream.cuda_stream)
+
+
+def _dtype_code(t: torch.Tensor) -> int:
+    if t.dtype == torch.bfloat16:
+        return HSTU_BF16
+    if t.dtype == torch.float32:
+        return HSTU_F32
+    raise TypeError(f"unsupported dtype {t.dtype}")
+
+
+def _row_stride(t: torch.Tensor) -> int:
+    """Row stride in elements of a [T, h, d] (or [T, h*d]) view whose rows
+    are [h][d]-contiguous."""
+    if t.dim() == 3:
+        if t.stride(2) != 1 or t.stride(1) != t.shape[2]:
+            raise ValueError("rows must be [h][d] contiguous")
+    elif t.dim() == 2:
+        if t.stride(1) != 1:
+            raise ValueError("rows must be contiguous")
+    else:
+        raise ValueError("expected a [T, h, d] or [T, h*d] tensor")
+    return t.stride(0)
+
+
+def make_problem(num_seqs, total_tokens, max_seq_len, num_heads, d_qk, d_v, num_time_buckets,
+                 dtype) -> Problem:
+    return Problem(int(num_seqs), int(total_tokens), int(max_seq_len), int(num_heads), int(d_qk),
+                   int(d_v), int(num_time_buckets), int(dtype))
+
+
+def make_jagged(seq_offsets, timestamps, rab_pos, rab_time, num_targets=None) -> Jagged:
+    return Jagged(seq_offsets.data_ptr(), timestamps.data_ptr(),
+                  None if num_targets is None else num_targets.data_ptr(),
+                  rab_pos.data_ptr(), rab_time.data_ptr())
+
+
+def problem_for(q, v, seq_offsets, max_seq_len, rab_time) -> Problem:
+    T, H, dqk = q.shape[0], q.shape[1], q.shape[2]
+    dv = v.shape[2]
+    return make_problem(seq_offsets.numel() - 1, T, max_seq_len, H, dqk, dv, rab_time.numel(),
+                        _dtype_code(q))
+
+
+# ---------------------------------------------------------------- raw names
+
+def hstu_abi_version() -> int:
+    return int(lib.hstu_abi_version())
+
+
+def hstu_last_error() -> str:
+    return lib.hstu_last_error().decode()
+
+
+def hstu_workspace_bytes(problem: Problem) -> int:
+    return int(lib.hstu_workspace_bytes(ctypes.byref(problem)))
+
+
+def workspace(problem: Problem, device=None) -> torch.Tensor:
+    n = hstu_workspace_bytes(problem)
+    if n == 0:
+        raise HstuError(1, "invalid problem")
+    return torch.empty(n, dtype=torch.uint8, device=device or "cuda")
+
+
+def hstu_attn_fwd(q, k, v, seq_offsets, timestamps, rab_pos, rab_time, max_seq_len,
+                  num_targets=None, out=None, ws=None, stream=None):
+    """O [T, h, d_v] of Eq. 2 (see include/hstu.h)."""
+    p = problem_for(q, v, seq_offsets, max_seq_len, rab_time)
+    j = make_jagged(seq_offsets, timestamps, rab_pos, rab_time, num_targets)
+    if out is None:
+        out = torch.empty((q.shape[0], q.shape[1], v.shape[2]), dtype=q.dtype, device=q.device)
+    if ws is None:
+        ws = workspace(p, q.device)
+    _check(lib.hstu_attn_fwd(ctypes.byref(p), ctypes.byref(j), _ptr(q), _row_stride(q), _ptr(k),
+                             _row_stride(k), _ptr(v), _row_stride(v), _ptr(out), _ptr(ws),
+                             ws.numel(), _stream(stream)))
+    return out
+
+
+def hstu_attn_bwd(q, k, v, d_out, seq_offsets, timestamps, rab_pos, rab_time, max_seq_len,
+                  num_targets=None, grads=None, ws=None, stream=None):
+    """(dq, dk, dv, d_rab_pos, d_rab_time) for the loss <O, d_out>."""
+    p = problem_for(q, v, seq_offsets, max_seq_len, rab_time)
+    j = make_jagged(seq_offsets, timestamps, rab_pos, rab_time, num_targets)
+    if grads is None:
+        T, H = q.shape[0], q.shape[1]
+        grads = (torch.empty((T, H, q.shape[2]), dtype=q.dtype, device=q.device),
+                 torch.empty((T, H, k.shape[2]), dtype=q.dtype, device=q.device),
+                 torch.empty((T, H, v.shape[2]), dtype=q.dtype, device=q.device),
+                 torch.empty_like(rab_pos), torch.empty_like(rab_time))
+    dq, dk, dv, drp, drt = grads
+    if ws is None:
+        ws = workspace(p, q.device)
+    _check(lib.hstu_attn_bwd(ctypes.byref(p), ctypes.byref(j), _ptr(q), _row_stride(q), _ptr(k),
+                             _row_stride(k), _ptr(v), _row_stride(v), _ptr(d_out), _ptr(dq),
+                             _ptr(dk), _ptr(dv), _ptr(drp), _ptr(drt), _ptr(ws), ws.numel(),
+                             _stream(stream)))
+    return grads
+
+
+def hstu_layer_fwd(q, k, v, u, seq_offsets, timestamps, rab_pos, rab_time, max_seq_len,
+                   num_targets=None, ln_weight=None, ln_bias=None, ln_eps=1e-5, attn_out=None,
+                   y=None, ln_mean=None, ln_rstd=None, ws=None, stream=None):
+    """(attn_out [T, D], y [T, D], ln_mean [T], ln_rstd [T]) of Eq. 2-3."""
+    p = problem_for(q, v, seq_offsets, max_seq_len, rab_time)
+    j = make_jagged(seq_offsets, timestamps, rab_pos, rab_time, num_targets)
+    T, D = q.shape[0], q.shape[1] * v.shape[2]
+    if attn_out is None:
+        attn_out = torch.empty((T, D), dtype=q.dtype, device=q.device)
+    if y is None:
+        y = torch.empty((T, D), dtype=q.dtype, device=q.device)
+    if ln_mean is None:
+        ln_mean = torch.empty(T, dtype=torch.float32, device=q.device)
+    if ln_rstd is None:
+        ln_rstd = torch.empty(T, dtype=torch.float32, device=q.device)
+    if ws is None:
+        ws = workspace(p, q.device)
+    _check(lib.hstu_layer_fwd(ctypes.byref(p), ctypes.byref(j), _ptr(q), _row_stride(q), _ptr(k),
+                              _row_stride(k), _ptr(v), _row_stride(v), _ptr(u), _row_stride(u),
+                              _ptr(ln_weight), _ptr(ln_bias), float(ln_eps), _ptr(attn_out),
+                              _ptr(y), _ptr(ln_mean), _ptr(ln_rstd), _ptr(ws), ws.numel(),
+                              _stream(stream)))
+    return attn_out, y, ln_mean, ln_rstd
+
+
+def hstu_complete_cumsum(x: torch.Tensor, out=None, stream=None):
+    if out is None:
+        out = torch.empty(x.numel() + 1, dtype=torch.int64, device=x.device)
+    _check(lib.hstu_complete_cumsum(x.numel(), _ptr(x), _ptr(out), _stream(stream)))
+    return out
+
+
+def hstu_pair_offsets(seq_offsets: torch.Tensor, out=None, stream=None):
+    if out is None:
+        out = torch.empty_like(seq_offsets)
+    _check(lib.hstu_pair_offsets(seq_offsets.numel() - 1, _ptr(seq_offsets), _ptr(out),
+                                 _stream(stream)))
+    return out
+
+
+def hstu_time_bucketize(seq_offsets, timestamps, num_time_buckets, pair_offsets=None,
+                        total_pairs=None, out=None, stream=None):
+    """uint8 buckets, one L_b x L_b row-major matrix per sequence."""
+    if pair_offsets is None:
+        pair_offsets = hstu_pair_offsets(seq_offsets, stream=stream)
+    if total_pairs is None:
+        total_pairs = int(pair_offsets[-1].item())  # host read, synchronises
+    if out is None:
+        out = torch.empty(max(total_pairs, 1), dtype=torch.uint8, device=timestamps.device)
+    _check(lib.hstu_time_bucketize(seq_offsets.numel() - 1, timestamps.numel(),
+                                   int(num_time_buckets), _ptr(seq_offsets), _ptr(timestamps),
+                                   _ptr(pair_offsets), int(total_pairs), _ptr(out),
+                                   _stream(stream)))
+    return out[:total_pairs]
+
+
+def hstu_validate(seq_offsets, timestamps, rab_pos, rab_time, max_seq_len, num_heads, d_qk, d_v,
+                  dtype=HSTU_BF16, num_targets=None, stream=None):
+    p = make_problem(seq_offsets.numel() - 1, timestamps.numel(), max_seq_len, num_heads, d_qk,
+                     d_v, rab_time.numel(), dtype)
+    j = make_jagged(seq_offsets, timestamps, rab_pos, rab_time, num_targets)
+    _check(lib.hstu_validate(ctypes.byref(p), ctypes.byref(j), _stream(stream)))
+
+
+def hstu_timing_enable(on: bool = True):
+    _check(lib.hstu_timing_enable(1 if on else 0))
+
+
+def hstu_timing_reset():
+    _check(lib.hstu_timing_reset())
+
+
+def hstu_timing_read(name: str):
+    ms = ctypes.c_double(0.0)
+    n = ctypes.c_int64(0)
+    _check(lib.hstu_timing_read(name.encode(), ctypes.byref(ms), ctypes.byref(n)))
+    return ms.value, n.value

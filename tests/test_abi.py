@@ -1,0 +1,136 @@
+"""C ABI checks that need no GPU: the library loads, exports every entry
+point include/hstu.h declares, and rejects bad arguments on the host
+before anything is launched (every call below fails validation, so no
+device work is attempted)."""
+import ctypes
+import os
+import re
+import threading
+
+import pytest
+
+from tests.conftest import ROOT
+
+HEADER = os.path.join(ROOT, "include", "hstu.h")
+
+
+def _declared():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(hstu_[a-z_]+)\s*\(", text)))
+
+
+@pytest.fixture(scope="module")
+def hs():
+    from paper_2402_17152_amd import hstu
+    return hstu
+
+
+def test_header_symbols_exported(hs):
+    names = _declared()
+    assert len(names) >= 13
+    for n in names:
+        assert hasattr(hs.lib, n), n
+    assert sorted(hs.EXPORTED) == names
+
+
+def test_abi_version(hs):
+    assert hs.hstu_abi_version() == 1
+
+
+def _problem(hs, **kw):
+    a = dict(num_seqs=8, total_tokens=48118, max_seq_len=8192, num_heads=4, d_qk=128, d_v=128,
+             num_time_buckets=128, dtype=hs.HSTU_BF16)
+    a.update(kw)
+    return hs.make_problem(**a)
+
+
+def test_workspace_bytes(hs):
+    p = _problem(hs)
+    n = hs.hstu_workspace_bytes(p)
+    # work lists + fp32 dQ accumulator [T][h][d_qk]
+    assert n >= 48118 * 4 * 128 * 4
+    assert n % 256 == 0
+    assert hs.hstu_workspace_bytes(_problem(hs, d_qk=48)) == 0
+    assert hs.hstu_workspace_bytes(_problem(hs, num_heads=0)) == 0
+    assert hs.hstu_workspace_bytes(_problem(hs, max_seq_len=70000)) == 0
+    f = hs.hstu_workspace_bytes(_problem(hs, dtype=hs.HSTU_F32))
+    assert 0 < f < n
+
+
+FAKE = 0x10000  # 64 KiB-aligned, never dereferenced: every call fails validation first
+
+
+def _jagged(hs, **kw):
+    a = dict(seq_offsets=FAKE, timestamps=FAKE, num_targets=None, rab_pos=FAKE, rab_time=FAKE)
+    a.update(kw)
+    return hs.Jagged(**a)
+
+
+def _fwd(hs, p, j, q=FAKE, qs=512, k=FAKE, ks=512, v=FAKE, vs=512, out=FAKE, ws=FAKE, wsb=None):
+    if wsb is None:
+        wsb = 1 << 40
+    P = ctypes.c_void_p
+    return hs.lib.hstu_attn_fwd(None if p is None else ctypes.byref(p),
+                                None if j is None else ctypes.byref(j), P(q), qs, P(k), ks, P(v), vs,
+                                P(out), P(ws), wsb, None)
+
+
+@pytest.mark.parametrize("case,status,needle", [
+    (dict(p=None), 1, "problem"),
+    (dict(j=None), 1, "jagged"),
+    (dict(pkw=dict(d_qk=48)), 2, "d_qk"),
+    (dict(pkw=dict(num_heads=65)), 2, "num_heads"),
+    (dict(pkw=dict(num_time_buckets=300)), 2, "num_time_buckets"),
+    (dict(pkw=dict(num_seqs=0)), 1, "num_seqs"),
+    (dict(jkw=dict(rab_pos=None)), 1, "rab_pos"),
+    (dict(jkw=dict(timestamps=None)), 1, "timestamps"),
+    (dict(q=None), 1, "q is NULL"),
+    (dict(q=FAKE + 8), 1, "aligned"),
+    (dict(qs=256), 1, "q_stride"),
+    (dict(vs=516), 1, "multiple of 16"),
+    (dict(ws=None), 3, "workspace"),
+    (dict(wsb=100), 3, "too small"),
+])
+def test_fwd_argument_errors(hs, case, status, needle):
+    p = None if "p" in case else _problem(hs, **case.get("pkw", {}))
+    j = None if "j" in case else _jagged(hs, **case.get("jkw", {}))
+    kw = {k: v for k, v in case.items() if k in ("q", "qs", "k", "ks", "v", "vs", "out", "ws", "wsb")}
+    st = _fwd(hs, p, j, **kw)
+    assert st == status
+    assert needle in hs.hstu_last_error()
+
+
+def test_error_message_is_thread_local(hs):
+    st = _fwd(hs, _problem(hs, d_qk=48), _jagged(hs))
+    assert st == 2
+    seen = []
+
+    def other():
+        seen.append(hs.hstu_last_error())
+
+    th = threading.Thread(target=other)
+    th.start()
+    th.join()
+    assert seen == [""]
+    assert "d_qk" in hs.hstu_last_error()
+
+
+def test_other_entry_points_validate(hs):
+    P = ctypes.c_void_p
+    assert hs.lib.hstu_complete_cumsum(-1, P(FAKE), P(FAKE), None) == 1
+    assert hs.lib.hstu_pair_offsets(0, P(FAKE), P(FAKE), None) == 1
+    assert hs.lib.hstu_time_bucketize(1, 10, 300, P(FAKE), P(FAKE), P(FAKE), 100, P(FAKE), None) == 2
+    assert hs.lib.hstu_time_bucketize(1, 10, 128, P(FAKE), P(FAKE), P(FAKE), 100, P(FAKE + 1), None) == 1
+    assert hs.lib.hstu_validate(None, None, None) == 1
+    p = _problem(hs, num_heads=64, d_v=128)   # D = 8192 > 4096 for the epilogue
+    j = _jagged(hs)
+    st = hs.lib.hstu_layer_fwd(ctypes.byref(p), ctypes.byref(j), P(FAKE), 8192, P(FAKE), 8192,
+                               P(FAKE), 8192, P(FAKE), 8192, None, None, 1e-5, P(FAKE), P(FAKE),
+                               None, None, P(FAKE), 1 << 40, None)
+    assert st == 2 and "4096" in hs.hstu_last_error()
+    p = _problem(hs)
+    st = hs.lib.hstu_attn_bwd(ctypes.byref(p), ctypes.byref(j), P(FAKE), 512, P(FAKE), 512,
+                              P(FAKE), 512, P(FAKE), P(FAKE), P(FAKE), None, P(FAKE), P(FAKE),
+                              P(FAKE), 1 << 40, None)
+    assert st == 1 and "dv" in hs.hstu_last_error()
