@@ -1,0 +1,232 @@
+#!/usr/bin/env python3
+"""Benchmark of the HSTU jagged-attention hot path on one MI355X.
+
+One step = one pass of the whole path over the batch (inputs resident in
+HBM): hstu_layer_fwd (work-list scheduling, fused attention forward with
+the in-register bias and time bucketisation, LayerNorm(A V) (.) U
+epilogue) then hstu_attn_bwd (recomputing backward with dQ/dK/dV and the
+bias-table gradients).  Default workload: the 8192-long shape (B=8
+sequences of length U[4096, 8192], h=4, d_qk=d_v=128, N=8192, bf16).
+
+Prints one JSON line: tokens/s (whole job), the per-kernel breakdown,
+the roofline position of the dominant kernel measured live with HIP
+events on its own stream, and the CPU oracle timed on a bounded sample
+of the same workload.
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+PEAK_BF16_TFLOPS = 2516.6   # MI355X dense bf16 MFMA: 256 CU x 2.4 GHz x 4096 flop/clk
+PEAK_FP32_TFLOPS = 157.3    # MI355X fp32 vector
+PEAK_HBM_GBS = 8000.0       # MI355X HBM3E
+METRIC = "HSTU jagged attn fwd+bwd tokens/s & TFLOP/s at N=8192; % bf16 MFMA peak"
+
+
+def parse():
+    ap = argparse.ArgumentParser(description=__doc__)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=30)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default="long", help="tiny|medium|training|long|target")
+    ap.add_argument("--no-cpu-baseline", action="store_true",
+                    help="skip the oracle timing (profiling runs)")
+    ap.add_argument("--no-kernel-timing", action="store_true")
+    return ap.parse_args()
+
+
+def source_hash(*names) -> str:
+    h = hashlib.sha256()
+    for n in names:
+        with open(os.path.join(ROOT, "paper_2402_17152_amd", "csrc", n), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
+
+
+def counters_traffic(kernel: str, workload: str, src: str):
+    """HBM bytes per launch from a committed rocprofv3 counter summary, if
+    it was taken on the current kernel source; else None."""
+    path = os.path.join(ROOT, "profiles", f"{kernel}_{workload}_traffic.json")
+    if not os.path.exists(path):
+        return None
+    with open(path) as f:
+        rec = json.load(f)
+    if rec.get("source_hash") != src:
+        return None
+    return rec.get("hbm_bytes_per_launch")
+
+
+def cpu_baseline(batch, flops_full):
+    """The oracle, untuned, on the shortest sequences of the batch (one
+    OpenMP task per sequence x head, as many sequences as there are
+    threads per head), scaled to whole-workload tokens/s by FLOPs."""
+    import numpy as np
+
+    import oracle
+    from paper_2402_17152_amd import inputs
+
+    threads = oracle.num_threads()
+    h = batch.spec.num_heads
+    k = max(1, min(len(batch.lengths), threads // h))
+    seqs = [int(x) for x in np.argsort(batch.lengths, kind="stable")[:k]]
+    sub = inputs.sub_batch(batch, seqs)
+    f_fwd, f_bwd = inputs.flops(sub)
+    N = batch.spec.max_seq_len
+    args = (sub.seq_offsets, N, sub.timestamps, sub.rab_pos, sub.rab_time, sub.f64("q"),
+            sub.f64("k"), sub.f64("v"))
+    t0 = time.perf_counter()
+    oracle.attn_fwd(*args, num_targets=sub.num_targets)
+    if batch.spec.backward:
+        oracle.attn_bwd(*args, sub.f64("do"), num_targets=sub.num_targets)
+    dt = time.perf_counter() - t0
+    f_sample = f_fwd + (f_bwd if batch.spec.backward else 0)
+    equiv_s = dt * flops_full / f_sample
+    return {
+        "value": batch.total_tokens / equiv_s,
+        "unit": "tokens/s",
+        "cores": min(threads, k * h),
+        "kind": "oracle",
+        "sample": (f"fp64 oracle fwd{'+bwd' if batch.spec.backward else ''} on the {k} shortest "
+                   f"sequences (lengths {[int(batch.lengths[s]) for s in seqs]}, all {h} heads): "
+                   f"{f_sample:.3e} FLOP in {dt:.2f} s = {f_sample / dt / 1e9:.2f} GFLOP/s, "
+                   f"scaled to the whole workload by FLOPs"),
+        "gflops": f_sample / dt / 1e9,
+        "seconds": dt,
+    }
+
+
+def main():
+    args = parse()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py: this build runs on exactly one GPU (the path shards by sequence and "
+              "needs no collective until the bias-gradient all-reduce, which is not built); "
+              f"--gpus {args.gpus} is not supported", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+
+    from paper_2402_17152_amd import hstu, inputs
+
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    torch.cuda.set_device(0)
+    batch = inputs.make_batch(args.workload)
+    spec = batch.spec
+    d = inputs.to_device(batch)
+    T = batch.total_tokens
+    N = spec.max_seq_len
+    f_fwd, f_bwd = inputs.flops(batch)
+    flops_step = f_fwd + (f_bwd if spec.backward else 0)
+    p = hstu.problem_for(d["q"], d["v"], d["seq_offsets"], N, d["rab_time"])
+    ws = hstu.workspace(p)
+    D = spec.num_heads * spec.d_v
+    dt = d["q"].dtype
+    attn_out = torch.empty((T, D), dtype=dt, device="cuda")
+    y = torch.empty((T, D), dtype=dt, device="cuda")
+    mean = torch.empty(T, dtype=torch.float32, device="cuda")
+    rstd = torch.empty(T, dtype=torch.float32, device="cuda")
+    grads = (torch.empty_like(d["q"]), torch.empty_like(d["k"]), torch.empty_like(d["v"]),
+             torch.empty_like(d["rab_pos"]), torch.empty_like(d["rab_time"]))
+    stream = torch.cuda.current_stream()
+
+    def step():
+        hstu.hstu_layer_fwd(d["q"], d["k"], d["v"], d["u"], d["seq_offsets"], d["timestamps"],
+                            d["rab_pos"], d["rab_time"], N, num_targets=d["num_targets"],
+                            attn_out=attn_out, y=y, ln_mean=mean, ln_rstd=rstd, ws=ws,
+                            stream=stream)
+        if spec.backward:
+            hstu.hstu_attn_bwd(d["q"], d["k"], d["v"], d["do"], d["seq_offsets"],
+                               d["timestamps"], d["rab_pos"], d["rab_time"], N,
+                               num_targets=d["num_targets"], grads=grads, ws=ws, stream=stream)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    hstu.hstu_timing_reset()
+    if not args.no_kernel_timing:
+        hstu.hstu_timing_enable(True)
+    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    t_wall = time.perf_counter()
+    ev0.record(stream)
+    for _ in range(args.steps):
+        step()
+    ev1.record(stream)
+    torch.cuda.synchronize()
+    t_wall = time.perf_counter() - t_wall
+    hstu.hstu_timing_enable(False)
+    ms = ev0.elapsed_time(ev1) / args.steps
+
+    kernels = {}
+    for name in ("attn_fwd", "ln_gate", "attn_bwd"):
+        tot, n = hstu.hstu_timing_read(name)
+        if n:
+            kernels[name] = {"avg_ms": tot / n, "launches": n}
+    # Algorithmic work per launch: FLOPs of the contractions for attention,
+    # bytes read + written for the epilogue.
+    ln_bytes = T * D * 3 * (2 if spec.dtype == "bf16" else 4) + 8 * T
+    if "attn_fwd" in kernels:
+        kernels["attn_fwd"]["tflops"] = f_fwd / (kernels["attn_fwd"]["avg_ms"] * 1e-3) / 1e12
+    if "attn_bwd" in kernels:
+        kernels["attn_bwd"]["tflops"] = f_bwd / (kernels["attn_bwd"]["avg_ms"] * 1e-3) / 1e12
+    if "ln_gate" in kernels:
+        kernels["ln_gate"]["gbs"] = ln_bytes / (kernels["ln_gate"]["avg_ms"] * 1e-3) / 1e9
+
+    peak = PEAK_BF16_TFLOPS if spec.dtype == "bf16" else PEAK_FP32_TFLOPS
+    dom = "attn_bwd" if spec.backward else "attn_fwd"
+    roofline = None
+    if dom in kernels:
+        src = source_hash("attn_bwd.hip" if dom == "attn_bwd" else "attn_fwd.hip", "common.h")
+        ach = kernels[dom]["tflops"]
+        roofline = {"bound": "mfma", "kernel": dom, "achieved": ach, "peak": peak,
+                    "unit": "TFLOP/s", "frac": ach / peak,
+                    "traffic": counters_traffic(dom, args.workload, src),
+                    "flop_per_launch": f_bwd if dom == "attn_bwd" else f_fwd,
+                    "source_hash": src}
+
+    tflops = flops_step / (ms * 1e-3) / 1e12
+    rec = {
+        "metric": METRIC,
+        "value": T / (ms * 1e-3),
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": spec.dtype,
+        "data": "synthetic (seeded generator; no dataset)",
+        "config": {
+            "workload": f"{spec.name}: B={len(batch.lengths)} jagged sequences, T={T}, "
+                        f"h={spec.num_heads}, d_qk={spec.d_qk}, d_v={spec.d_v}, N={N}, "
+                        f"{'target-aware' if spec.target_aware else 'causal'}; step = layer fwd "
+                        f"(attention + LayerNorm gate){' + attention bwd with bias gradients' if spec.backward else ''}",
+            "num_seqs": len(batch.lengths),
+            "total_tokens": T,
+            "max_seq_len": N,
+            "parallelism": "single GPU",
+        },
+        "tflops": tflops,
+        "pct_bf16_peak": 100.0 * tflops / PEAK_BF16_TFLOPS,
+        "flop_per_step": flops_step,
+        "wall_s_timed": t_wall,
+        "kernels": kernels,
+        "roofline": roofline,
+        "cpu_baseline": None,
+    }
+    if not args.no_cpu_baseline:
+        rec["cpu_baseline"] = cpu_baseline(batch, flops_step)
+    print(json.dumps(rec), flush=True)
+
+
+if __name__ == "__main__":
+    main()

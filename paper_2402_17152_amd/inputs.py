@@ -223,3 +223,37 @@ def flops(batch: Batch):
     s = batch.spec
     p = causal_pairs(batch) * s.num_heads
     return 2 * p * (s.d_qk + s.d_v), 2 * p * (3 * s.d_qk + 2 * s.d_v)
+
+
+def sub_batch(batch: Batch, seqs) -> Batch:
+    """The sequences ``seqs`` of a batch as a batch of their own (same N,
+    tables and values)."""
+    offs = batch.seq_offsets
+    seqs = [int(b) for b in seqs]
+    rows = (np.concatenate([np.arange(offs[b], offs[b + 1]) for b in seqs])
+            if seqs else np.zeros(0, np.int64))
+    lens = np.array([offs[b + 1] - offs[b] for b in seqs], dtype=np.int64)
+    new_offs = np.concatenate([[0], np.cumsum(lens)]).astype(np.int64)
+    store = {k: v[rows] for k, v in batch.store.items()}
+    nt = None if batch.num_targets is None else batch.num_targets[seqs]
+    return Batch(batch.spec, lens, new_offs, batch.timestamps[rows], nt, batch.rab_pos,
+                 batch.rab_time, store)
+
+
+def to_device(batch: Batch, device="cuda") -> dict:
+    """Copies a batch to device memory as torch tensors (bf16 bit patterns
+    are reinterpreted, not converted)."""
+    import torch
+
+    def t(a):
+        if a.dtype == np.uint16:
+            return torch.from_numpy(a.view(np.int16).copy()).view(torch.bfloat16).to(device)
+        return torch.from_numpy(np.ascontiguousarray(a)).to(device)
+
+    d = {n: t(a) for n, a in batch.store.items()}
+    d["seq_offsets"] = t(batch.seq_offsets)
+    d["timestamps"] = t(batch.timestamps)
+    d["rab_pos"] = t(batch.rab_pos)
+    d["rab_time"] = t(batch.rab_time)
+    d["num_targets"] = None if batch.num_targets is None else t(batch.num_targets)
+    return d

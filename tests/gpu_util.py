@@ -7,23 +7,8 @@ import torch
 from paper_2402_17152_amd import inputs
 
 
-def to_dev(batch: inputs.Batch, name: str) -> torch.Tensor:
-    a = batch.store[name]
-    if a.dtype == np.uint16:
-        t = torch.from_numpy(a.view(np.int16).copy()).view(torch.bfloat16)
-    else:
-        t = torch.from_numpy(np.ascontiguousarray(a))
-    return t.cuda()
-
-
 def dev_inputs(batch: inputs.Batch):
-    d = {n: to_dev(batch, n) for n in batch.store}
-    d["seq_offsets"] = torch.from_numpy(batch.seq_offsets).cuda()
-    d["timestamps"] = torch.from_numpy(batch.timestamps).cuda()
-    d["rab_pos"] = torch.from_numpy(batch.rab_pos).cuda()
-    d["rab_time"] = torch.from_numpy(batch.rab_time).cuda()
-    d["num_targets"] = None if batch.num_targets is None else torch.from_numpy(batch.num_targets).cuda()
-    return d
+    return inputs.to_device(batch)
 
 
 def to_f64(t: torch.Tensor) -> np.ndarray:
@@ -88,17 +73,9 @@ def oracle_bwd(oracle, batch):
 
 
 def sub_batch(batch: inputs.Batch, seqs) -> inputs.Batch:
-    """The sequences `seqs` of a batch as a batch of their own (same N,
-    tables and values): sequences are independent, so every per-token
-    output of the sub-batch equals the full batch's rows."""
-    offs = batch.seq_offsets
-    rows = np.concatenate([np.arange(offs[b], offs[b + 1]) for b in seqs]) if len(seqs) else np.zeros(0, np.int64)
-    lens = np.array([offs[b + 1] - offs[b] for b in seqs], dtype=np.int64)
-    new_offs = np.concatenate([[0], np.cumsum(lens)]).astype(np.int64)
-    store = {k: v[rows] for k, v in batch.store.items()}
-    nt = None if batch.num_targets is None else batch.num_targets[list(seqs)]
-    return inputs.Batch(batch.spec, lens, new_offs, batch.timestamps[rows], nt, batch.rab_pos,
-                        batch.rab_time, store)
+    """Sequences are independent, so every per-token output of the
+    sub-batch equals the full batch's rows."""
+    return inputs.sub_batch(batch, seqs)
 
 
 def token_rows(batch: inputs.Batch, seqs):
