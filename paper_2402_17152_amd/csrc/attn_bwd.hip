@@ -3,29 +3,43 @@
 // Gradients of <O, dO> for O = (1/N) SiLU(Q K^T + rab) V (Eq. 2).  As the
 // paper's kernel appendix describes, attention and the relative bias are
 // recomputed rather than stored, and the bias gradients are accumulated
-// in on-chip shared memory before they reach HBM.  Pointwise aggregation
-// means no row statistics are needed: with S = Q K^T + rab,
+// on chip before they reach HBM.  Pointwise aggregation means no row
+// statistics are needed: with S = Q K^T + rab,
 //   P  = SiLU(S) (masked),            dV = (1/N) P^T dO
 //   dP = dO V^T,  dS = dP SiLU'(S) (masked)
 //   dK = (1/N) dS^T Q,  dQ = (1/N) dS K
 //   d rab_pos[(N-1)+p(j)-p(i)] += dS/N,  d rab_time[bkt] += dS/N.
 //
 // Workgroup = 4 waves = one (sequence, 128-key block, head) work item.
-// Wave w owns keys j0 + 32w .. +31 and keeps their K, V (as MFMA
-// operands) and dK, dV accumulators in registers for the whole item.  It
-// walks query steps of 32 rows: Q and dO of the step are staged in LDS
-// both row-major (operand of S and dP) and transposed in the
-// accumulator-matched order (operand of dK and dV).  dS is written to LDS
-// so all four waves can form the step's dQ = dS K block, which is added
-// to an fp32 workspace with hardware float atomics (converted to bf16 by
-// a separate pass).  Bias-position gradients are summed in an LDS array
-// indexed by p(i) - p(j) and time-bucket gradients in an LDS histogram;
-// each workgroup flushes them with one atomic per touched entry.
+// Wave w owns keys j0 + 32w .. +31: their K and V sit in registers as
+// MFMA operands and their dK, dV accumulate in registers for the whole
+// item.  The workgroup walks query steps of 32 rows; each step's Q and dO
+// rows are staged row-major in LDS (prefetched into registers during the
+// previous step).  Per step and wave, on v_mfma_f32_32x32x16_bf16:
+//   S  = Q K^T (accumulator seeded with the bias), dP = dO V^T;
+//   dV += P^T dO and dK += dS^T Q straight from the accumulator registers,
+//         the Q / dO operand fetched with transposing LDS reads in the
+//         accumulator's row order;
+//   dS -> LDS tile; then the whole workgroup forms dQ(step) = dS K
+//         (added to an fp32 workspace with float atomics).
+// Bias gradients:
+//   time table: per wave and step the slot range of the tile is bounded
+//         from timestamp extremes; each slot's dS is summed in registers,
+//         reduced across the wave and added to a per-wave LDS row (one
+//         slot in far-from-diagonal tiles);
+//   position table: after the step, threads own the 159 diagonals of the
+//         32 x 128 dS tile and add their sums to an LDS array indexed by
+//         p(i) - p(j) -- no atomics, one read-modify-write per diagonal.
+// Both are flushed with one global atomic per touched entry at the end.
+#include "bias.h"
 #include "kernels.h"
 
 namespace hstu {
 
 namespace {
+
+constexpr int64_t kI64Max = 0x7fffffffffffffffll;
+constexpr int64_t kI64Min = -kI64Max - 1;
 
 template <int DQK, int DV>
 __global__ __launch_bounds__(256, 1) void attn_bwd_bf16_kernel(
@@ -34,23 +48,25 @@ __global__ __launch_bounds__(256, 1) void attn_bwd_bf16_kernel(
     float* __restrict__ d_rab_time, const WorkItem* __restrict__ items,
     const int32_t* __restrict__ count, int pos_in_lds) {
   constexpr int BN = kBwdBN, BM = kBwdBM;
-  constexpr int Q_LD = DQK + 8, DO_LD = DV + 8;  // row-major tiles
-  constexpr int QT_LD = BM + 8, DOT_LD = BM + 8;  // transposed tiles
+  constexpr int Q_LD = DQK + 8, DO_LD = DV + 8;  // row-major step tiles
   constexpr int DS_LD = BN + 8, KT_LD = BN + 8;
-  constexpr int NWIN = BM + BN;
+  constexpr int NWIN = BM + BN;                   // reversed rab_pos window
+  constexpr int QCH = BM * DQK / 8, OCH = BM * DV / 8;
+  constexpr int QPT = (QCH + 255) / 256, OPT = (OCH + 255) / 256;
   static_assert(BN == 128 && BM == 32, "4 waves x 32 keys, 32-row query steps");
 
   __shared__ __align__(16) uint16_t sQ[BM * Q_LD];
-  __shared__ __align__(16) uint16_t sQT[DQK * QT_LD];
   __shared__ __align__(16) uint16_t sdO[BM * DO_LD];
-  __shared__ __align__(16) uint16_t sdOT[DV * DOT_LD];
   __shared__ __align__(16) uint16_t sdS[BM * DS_LD];
   __shared__ __align__(16) uint16_t sKT[DQK * KT_LD];
-  __shared__ int64_t sTi[BM];
-  __shared__ float sPos[NWIN];
-  __shared__ float sTime[256];
-  __shared__ float sHist[256];
-  extern __shared__ float sPosAcc[];  // [N] when pos_in_lds
+  __shared__ __align__(16) uint32_t sTr[BM];   // step row timestamps, rebased
+  __shared__ int64_t sTr64[BM];                // step row timestamps
+  __shared__ float sWin[NWIN];
+  __shared__ float sTab[64];                   // rab_time by slot
+  __shared__ float sTacc[4][64];               // per-wave time-gradient sums by slot
+  __shared__ int64_t sRange[2];                // extremes of the step's row timestamps
+  __shared__ int64_t sRed[2][4];
+  extern __shared__ float sPosAcc[];           // [N] when pos_in_lds
 
   if ((int)blockIdx.x >= *count) return;
   const WorkItem it = items[blockIdx.x];
@@ -67,12 +83,55 @@ __global__ __launch_bounds__(256, 1) void attn_bwd_bf16_kernel(
   const int my_j = jw0 + col;
   const bool key_ok = my_j < L;
   const int pj = bias_pos(my_j, n_h);
-  const int64_t tj = key_ok ? ja.timestamps[o + my_j] : 0;
   const float invN = 1.0f / (float)N;
+  const int64_t* __restrict__ ts = ja.timestamps + o;
 
   const uint16_t* __restrict__ qg = (const uint16_t*)t.q;
   const uint16_t* __restrict__ kg = (const uint16_t*)t.k;
   const uint16_t* __restrict__ vg = (const uint16_t*)t.v;
+
+  // Timestamp extremes over the tokens this item touches, [j0, L).
+  int64_t tlo = kI64Max, thi = kI64Min;
+  for (int x = j0 + tid; x < L; x += 256) {
+    const int64_t v = ts[x];
+    tlo = v < tlo ? v : tlo;
+    thi = v > thi ? v : thi;
+  }
+  tlo = wave_min_i64(tlo);
+  thi = wave_max_i64(thi);
+  if (lane == 0) {
+    sRed[0][wave] = tlo;
+    sRed[1][wave] = thi;
+  }
+  for (int x = tid; x < 64; x += 256) sTab[x] = ja.rab_time[min(63 - x, NB - 1)];
+  for (int x = tid; x < 4 * 64; x += 256) (&sTacc[0][0])[x] = 0.0f;
+  const int R = L - j0;  // p(i) - p(j) of kept pairs lies in [0, R)
+  if (pos_in_lds)
+    for (int x = tid; x < R; x += 256) sPosAcc[x] = 0.0f;
+  // K^T of the 128-key block (operand of dQ = dS K).
+  constexpr int KCH = BN * DQK / 8;
+  for (int c = tid; c < KCH; c += 256) {
+    const int r = c / (DQK / 8), cc = (c % (DQK / 8)) * 8;
+    const int j = j0 + r;
+    u32x4 v = j < L ? *reinterpret_cast<const u32x4*>(kg + (o + j) * t.k_stride + head * DQK + cc)
+                    : zero_u32x4();
+#pragma unroll
+    for (int e = 0; e < 8; e++) sKT[(cc + e) * KT_LD + r] = (uint16_t)(v[e >> 1] >> (16 * (e & 1)));
+  }
+  __syncthreads();
+  tlo = sRed[0][0];
+  thi = sRed[1][0];
+#pragma unroll
+  for (int w = 1; w < 4; w++) {
+    tlo = sRed[0][w] < tlo ? sRed[0][w] : tlo;
+    thi = sRed[1][w] > thi ? sRed[1][w] : thi;
+  }
+  const bool fast = (thi - tlo) < ((int64_t)1 << 31);
+  const int64_t tbase = tlo;
+  const int64_t tj64 = key_ok ? ts[my_j] : tbase;
+  const uint32_t tjr = (uint32_t)(tj64 - tbase);
+  const int64_t klo = wave_min_i64(key_ok ? tj64 : kI64Max);
+  const int64_t khi = wave_max_i64(key_ok ? tj64 : kI64Min);
 
   // K, V of the wave's keys as B operands (lane = key, 8 features per step).
   u32x4 kf[DQK / 16], vf[DV / 16];
@@ -87,24 +146,6 @@ __global__ __launch_bounds__(256, 1) void attn_bwd_bf16_kernel(
                                                      16 * s + 8 * half)
                    : zero_u32x4();
 
-  // K^T of the whole 128-key block (operand of dQ = dS K).
-  constexpr int KCH = BN * DQK / 8;
-  for (int c = tid; c < KCH; c += 256) {
-    const int r = c / (DQK / 8), cc = (c % (DQK / 8)) * 8;
-    const int j = j0 + r;
-    u32x4 v = j < L ? *reinterpret_cast<const u32x4*>(kg + (o + j) * t.k_stride + head * DQK + cc)
-                    : zero_u32x4();
-#pragma unroll
-    for (int e = 0; e < 8; e++) sKT[(cc + e) * KT_LD + r] = (uint16_t)(v[e >> 1] >> (16 * (e & 1)));
-  }
-  for (int x = tid; x < NB; x += 256) {
-    sTime[x] = ja.rab_time[x];
-    sHist[x] = 0.0f;
-  }
-  const int R = L - j0;  // p(i) - p(j) of kept pairs lies in [0, R)
-  if (pos_in_lds)
-    for (int x = tid; x < R; x += 256) sPosAcc[x] = 0.0f;
-
   f32x16 dkacc[DQK / 32], dvacc[DV / 32];
 #pragma unroll
   for (int nb = 0; nb < DQK / 32; nb++)
@@ -115,66 +156,118 @@ __global__ __launch_bounds__(256, 1) void attn_bwd_bf16_kernel(
 #pragma unroll
     for (int q = 0; q < 16; q++) dvacc[nb][q] = 0.0f;
 
+  // Lane addressing of the transposing reads (see lds_read_tr16): lane
+  // 16g + r reads row 4*(g/2) + r/4 (+ 8 for the second half of the
+  // k-group) and columns 16*(g%2) + 4*(r%4) .. +3 of a 32-column block.
+  const int tr_row = 4 * (lane >> 5) + ((lane & 15) >> 2);
+  const int tr_col = 16 * ((lane >> 4) & 1) + 4 * (lane & 3);
+
+  // Staging registers for the next step.
+  u32x4 pq[QPT], po[OPT];
+  int64_t pt = 0;
+  float pw = 0.0f;
+  auto prefetch = [&](int i0) {
+#pragma unroll
+    for (int k = 0; k < QPT; k++) {
+      const int c = tid + 256 * k;
+      if (c < QCH) {
+        const int r = c / (DQK / 8), cc = (c % (DQK / 8)) * 8, i = i0 + r;
+        pq[k] = i < L ? *reinterpret_cast<const u32x4*>(qg + (o + i) * t.q_stride + head * DQK + cc)
+                      : zero_u32x4();
+      }
+    }
+#pragma unroll
+    for (int k = 0; k < OPT; k++) {
+      const int c = tid + 256 * k;
+      if (c < OCH) {
+        const int r = c / (DV / 8), cc = (c % (DV / 8)) * 8, i = i0 + r;
+        po[k] = i < L ? *reinterpret_cast<const u32x4*>(dO + ((o + i) * H + head) * DV + cc)
+                      : zero_u32x4();
+      }
+    }
+    if (tid < BM) pt = (i0 + tid < L) ? ts[i0 + tid] : tbase;
+    if (tid < NWIN) {
+      // rab_pos entries reachable from (query step, key block), reversed.
+      const int pos_base = (N - 1) + min(j0, n_h) - min(i0 + BM - 1, n_h);
+      const int g = pos_base + (NWIN - 1 - tid);
+      pw = (g >= 0 && g <= 2 * N - 2) ? ja.rab_pos[g] : 0.0f;
+    }
+  };
+
   // Candidate keys see only themselves; otherwise every later row sees them.
   const int i_end = j0 >= n_h ? min(j0 + BN, L) : L;
+  prefetch(j0);
 
   for (int i0 = j0; i0 < i_end; i0 += BM) {
-    __syncthreads();  // previous step's tiles consumed
-    constexpr int QCH = BM * DQK / 8;
-    for (int c = tid; c < QCH; c += 256) {
-      const int r = c / (DQK / 8), cc = (c % (DQK / 8)) * 8;
-      const int i = i0 + r;
-      u32x4 v = i < L ? *reinterpret_cast<const u32x4*>(qg + (o + i) * t.q_stride + head * DQK + cc)
-                      : zero_u32x4();
-      *reinterpret_cast<u32x4*>(sQ + r * Q_LD + cc) = v;
-      const int pos = swap_bits23(r);
+    __syncthreads();  // previous step's LDS tiles consumed
 #pragma unroll
-      for (int e = 0; e < 8; e++)
-        sQT[(cc + e) * QT_LD + pos] = (uint16_t)(v[e >> 1] >> (16 * (e & 1)));
+    for (int k = 0; k < QPT; k++) {
+      const int c = tid + 256 * k;
+      if (c < QCH) *reinterpret_cast<u32x4*>(sQ + (c / (DQK / 8)) * Q_LD + (c % (DQK / 8)) * 8) = pq[k];
     }
-    constexpr int OCH = BM * DV / 8;
-    for (int c = tid; c < OCH; c += 256) {
-      const int r = c / (DV / 8), cc = (c % (DV / 8)) * 8;
-      const int i = i0 + r;
-      u32x4 v = i < L ? *reinterpret_cast<const u32x4*>(dO + ((o + i) * H + head) * DV + cc)
-                      : zero_u32x4();
-      *reinterpret_cast<u32x4*>(sdO + r * DO_LD + cc) = v;
-      const int pos = swap_bits23(r);
 #pragma unroll
-      for (int e = 0; e < 8; e++)
-        sdOT[(cc + e) * DOT_LD + pos] = (uint16_t)(v[e >> 1] >> (16 * (e & 1)));
+    for (int k = 0; k < OPT; k++) {
+      const int c = tid + 256 * k;
+      if (c < OCH) *reinterpret_cast<u32x4*>(sdO + (c / (DV / 8)) * DO_LD + (c % (DV / 8)) * 8) = po[k];
     }
-    if (tid < BM) sTi[tid] = (i0 + tid < L) ? ja.timestamps[o + i0 + tid] : 0;
-    // rab_pos entries reachable from (query step, key block).
-    const int pos_base = (N - 1) + min(j0, n_h) - min(i0 + BM - 1, n_h);
-    for (int x = tid; x < NWIN; x += 256) {
-      const int g = pos_base + x;
-      sPos[x] = (g >= 0 && g <= 2 * N - 2) ? ja.rab_pos[g] : 0.0f;
+    if (tid < BM) {
+      sTr64[tid] = pt;
+      sTr[tid] = (uint32_t)(pt - tbase);
+    }
+    if (tid < NWIN) sWin[tid] = pw;
+    if (wave == 0) {
+      const bool okr = lane < BM && i0 + lane < L;
+      const int64_t rlo = wave_min_i64(okr ? pt : kI64Max);
+      const int64_t rhi = wave_max_i64(okr ? pt : kI64Min);
+      if (lane == 0) {
+        sRange[0] = rlo;
+        sRange[1] = rhi;
+      }
     }
     __syncthreads();
+    if (i0 + BM < i_end) prefetch(i0 + BM);
 
     // Does any kept pair fall in (rows i0..i0+31) x (this wave's keys)?
-    bool active = jw0 < L && jw0 <= i0 + BM - 1;
+    const int imax = min(i0 + BM - 1, L - 1);
+    bool active = jw0 < L && jw0 <= imax;
     if (jw0 >= n_h && jw0 != i0) active = false;  // candidate keys: diagonal block only
 
     float ds[16];
     if (active) {
       // Accumulator lane holds (i = i0 + 8g + 4*half + m, j = my_j).
+      const bool full = (jw0 + 31 <= i0) && (i0 + BM - 1 < L) && (i0 + BM - 1 < n_h);
       f32x16 sacc, pacc;
-      uint32_t vmask = 0;
+      int slot[16];
+      uint32_t vmask = 0xffffu;
+      if (full) {
+        const int yb = (NWIN - 32 - 32 * wave - col) + 4 * half;
 #pragma unroll
-      for (int q = 0; q < 16; q++) {
-        const int il = 8 * (q >> 2) + 4 * half + (q & 3);
-        const int i = i0 + il;
-        float bias = 0.0f;
-        if (key_ok && i < L && pair_valid(i, my_j, n_h)) {
-          const int widx = (N - 1) + pj - bias_pos(i, n_h) - pos_base;
-          bias = sPos[widx] + sTime[time_bucket64(sTi[il] - tj, NB)];
-          vmask |= 1u << q;
+        for (int q = 0; q < 16; q++) {
+          const int il = 8 * (q >> 2) + 4 * half + (q & 3);
+          slot[q] = fast ? slot32(sTr[il], tjr) : slot64(sTr64[il] - tj64);
+          sacc[q] = sWin[yb + 8 * (q >> 2) + (q & 3)] + sTab[slot[q]];
         }
-        sacc[q] = bias;
-        pacc[q] = 0.0f;
+      } else {
+        vmask = 0;
+        const int pos_base = (N - 1) + min(j0, n_h) - min(i0 + BM - 1, n_h);
+#pragma unroll
+        for (int q = 0; q < 16; q++) {
+          const int il = 8 * (q >> 2) + 4 * half + (q & 3);
+          const int i = i0 + il;
+          float b = 0.0f;
+          int s = 0;
+          if (key_ok && i < L && pair_valid(i, my_j, n_h)) {
+            const int x = (N - 1) + pj - bias_pos(i, n_h) - pos_base;
+            s = fast ? slot32(sTr[il], tjr) : slot64(sTr64[il] - tj64);
+            b = sWin[NWIN - 1 - x] + sTab[s];
+            vmask |= 1u << q;
+          }
+          slot[q] = s;
+          sacc[q] = b;
+        }
       }
+#pragma unroll
+      for (int q = 0; q < 16; q++) pacc[q] = 0.0f;
 #pragma unroll
       for (int s = 0; s < DQK / 16; s++) {
         u32x4 a = *reinterpret_cast<const u32x4*>(sQ + col * Q_LD + 16 * s + 8 * half);
@@ -204,29 +297,38 @@ __global__ __launch_bounds__(256, 1) void attn_bwd_bf16_kernel(
           pa[e] = pack_bf16x2(p[8 * st + 2 * e], p[8 * st + 2 * e + 1]);
           da[e] = pack_bf16x2(ds[8 * st + 2 * e], ds[8 * st + 2 * e + 1]);
         }
+        const int row = 16 * st + tr_row;
 #pragma unroll
         for (int nb = 0; nb < DV / 32; nb++) {
-          u32x4 b = *reinterpret_cast<const u32x4*>(sdOT + (32 * nb + col) * DOT_LD + 16 * st + 8 * half);
+          const uint16_t* base = sdO + row * DO_LD + 32 * nb + tr_col;
+          const uint2 lo = lds_read_tr16(base), hi = lds_read_tr16(base + 8 * DO_LD);
+          u32x4 b = {lo.x, lo.y, hi.x, hi.y};
           dvacc[nb] = mfma32x32x16(as_bf16x8(pa), as_bf16x8(b), dvacc[nb]);
         }
 #pragma unroll
         for (int nb = 0; nb < DQK / 32; nb++) {
-          u32x4 b = *reinterpret_cast<const u32x4*>(sQT + (32 * nb + col) * QT_LD + 16 * st + 8 * half);
+          const uint16_t* base = sQ + row * Q_LD + 32 * nb + tr_col;
+          const uint2 lo = lds_read_tr16(base), hi = lds_read_tr16(base + 8 * Q_LD);
+          u32x4 b = {lo.x, lo.y, hi.x, hi.y};
           dkacc[nb] = mfma32x32x16(as_bf16x8(da), as_bf16x8(b), dkacc[nb]);
         }
       }
-      // Bias gradients: position by p(i) - p(j), time by bucket.
+      // Time-table gradient: sum dS per slot over the slots this tile spans.
+      int s_lo, s_hi;
+      slot_range(sRange[0], sRange[1], klo, khi, s_lo, s_hi);
+      if (s_lo == s_hi) {
+        float sum = 0.0f;
 #pragma unroll
-      for (int q = 0; q < 16; q++) {
-        if ((vmask >> q) & 1u) {
-          const int il = 8 * (q >> 2) + 4 * half + (q & 3);
-          const int i = i0 + il;
-          const int kpos = bias_pos(i, n_h) - pj;
-          if (pos_in_lds)
-            atomicAdd(&sPosAcc[kpos], ds[q]);
-          else
-            unsafeAtomicAdd(&d_rab_pos[(N - 1) - kpos], ds[q] * invN);
-          atomicAdd(&sHist[time_bucket64(sTi[il] - tj, NB)], ds[q]);
+        for (int q = 0; q < 16; q++) sum += ds[q];
+        sum = wave_sum_f32(sum);
+        if (lane == 0) sTacc[wave][s_lo] += sum;
+      } else {
+        for (int s = s_lo; s <= s_hi; s++) {
+          float sum = 0.0f;
+#pragma unroll
+          for (int q = 0; q < 16; q++) sum += slot[q] == s ? ds[q] : 0.0f;
+          sum = wave_sum_f32(sum);
+          if (lane == 0) sTacc[wave][s] += sum;
         }
       }
     } else {
@@ -242,24 +344,63 @@ __global__ __launch_bounds__(256, 1) void attn_bwd_bf16_kernel(
     __syncthreads();
 
     // dQ(step rows) += dS K: each wave one 32-wide d block over a share of keys.
-    constexpr int NBLK = DQK / 32;
-    constexpr int KSPLIT = 4 / NBLK;
-    constexpr int STEPS = (BN / 16) / KSPLIT;
-    const int nbq = wave % NBLK, ks = wave / NBLK;
-    f32x16 qacc;
+    {
+      constexpr int NBLK = DQK / 32;
+      constexpr int KSPLIT = 4 / NBLK;
+      constexpr int STEPS = (BN / 16) / KSPLIT;
+      const int nbq = wave % NBLK, ks = wave / NBLK;
+      f32x16 qacc;
 #pragma unroll
-    for (int q = 0; q < 16; q++) qacc[q] = 0.0f;
+      for (int q = 0; q < 16; q++) qacc[q] = 0.0f;
 #pragma unroll
-    for (int st = 0; st < STEPS; st++) {
-      const int kk = (ks * STEPS + st) * 16 + 8 * half;
-      u32x4 a = *reinterpret_cast<const u32x4*>(sdS + col * DS_LD + kk);
-      u32x4 b = *reinterpret_cast<const u32x4*>(sKT + (32 * nbq + col) * KT_LD + kk);
-      qacc = mfma32x32x16(as_bf16x8(a), as_bf16x8(b), qacc);
+      for (int st = 0; st < STEPS; st++) {
+        const int kk = (ks * STEPS + st) * 16 + 8 * half;
+        u32x4 a = *reinterpret_cast<const u32x4*>(sdS + col * DS_LD + kk);
+        u32x4 b = *reinterpret_cast<const u32x4*>(sKT + (32 * nbq + col) * KT_LD + kk);
+        qacc = mfma32x32x16(as_bf16x8(a), as_bf16x8(b), qacc);
+      }
+#pragma unroll
+      for (int q = 0; q < 16; q++) {
+        const int i = i0 + 8 * (q >> 2) + 4 * half + (q & 3);
+        if (i < L) unsafeAtomicAdd(&dq_acc[((o + i) * H + head) * DQK + 32 * nbq + col], qacc[q]);
+      }
     }
-#pragma unroll
-    for (int q = 0; q < 16; q++) {
-      const int i = i0 + 8 * (q >> 2) + 4 * half + (q & 3);
-      if (i < L) unsafeAtomicAdd(&dq_acc[((o + i) * H + head) * DQK + 32 * nbq + col], qacc[q]);
+
+    // Position-table gradient, history rows: thread tid owns diagonal
+    // i_local - j_local = tid - 127, i.e. p(i) - p(j) = i0 - j0 + tid - 127.
+    const int rh = max(0, min(BM, n_h - i0));
+    if (tid < NWIN - 1) {
+      const int dd = tid - (BN - 1);
+      const int k = i0 - j0 + dd;
+      if (k >= 0) {
+        const int ilo = max(0, dd), ihi = min(rh, BN + dd);
+        float sum = 0.0f;
+        for (int il = ilo; il < ihi; il++)
+          sum += bf16_bits_to_f32(sdS[il * DS_LD + il - dd]);
+        if (sum != 0.0f) {
+          if (pos_in_lds)
+            sPosAcc[k] += sum;
+          else
+            unsafeAtomicAdd(&d_rab_pos[(N - 1) - k], sum * invN);
+        }
+      }
+    }
+    // Candidate rows (p(i) = n_h): key j < n_h lands on n_h - j, the
+    // diagonal (j = i) on 0.
+    if (rh < BM && i0 + rh < L) {
+      __syncthreads();
+      if (tid < BN) {
+        const int j = j0 + tid;
+        float sum = 0.0f;
+        for (int il = rh; il < BM; il++) sum += bf16_bits_to_f32(sdS[il * DS_LD + tid]);
+        if (sum != 0.0f) {
+          const int k = j < n_h ? n_h - j : 0;
+          if (pos_in_lds)
+            atomicAdd(&sPosAcc[k], sum);
+          else
+            unsafeAtomicAdd(&d_rab_pos[(N - 1) - k], sum * invN);
+        }
+      }
     }
   }
 
@@ -283,9 +424,9 @@ __global__ __launch_bounds__(256, 1) void attn_bwd_bf16_kernel(
       const float v = sPosAcc[x];
       if (v != 0.0f) unsafeAtomicAdd(&d_rab_pos[(N - 1) - x], v * invN);
     }
-  for (int x = tid; x < NB; x += 256) {
-    const float v = sHist[x];
-    if (v != 0.0f) unsafeAtomicAdd(&d_rab_time[x], v * invN);
+  if (tid < 64) {
+    const float v = sTacc[0][tid] + sTacc[1][tid] + sTacc[2][tid] + sTacc[3][tid];
+    if (v != 0.0f) unsafeAtomicAdd(&d_rab_time[min(63 - tid, NB - 1)], v * invN);
   }
 }
 

@@ -13,17 +13,24 @@
 // Per 32-key tile:
 //   S^T = K_tile Q^T via v_mfma_f32_32x32x16_bf16 (accumulator seeded with
 //         the bias), so each lane holds one query row and 16 keys;
-//   P   = mask ? SiLU(S) : 0 in fp32 registers, rounded to bf16;
+//   P   = SiLU(S) in fp32 registers (masked only on diagonal, ragged and
+//         candidate tiles), rounded to bf16;
 //   O  += P V_tile, P taken straight from the accumulator registers: the
 //         contraction index is permuted to match the accumulator layout
-//         and V is stored transposed in LDS in that same order.
-// K and V^T tiles, the tile's timestamps and the slice of rab_pos it can
-// touch are staged in LDS; rab_time lives in LDS for the whole item.
+//         and V is fetched from its row-major LDS tile with transposing
+//         reads in that same order.
+// The next tile's K, V, timestamps and rab_pos slice are loaded into
+// registers while the current tile is computed.  Timestamps are rebased
+// to 32 bits when the item's span allows (see bias.h).
+#include "bias.h"
 #include "kernels.h"
 
 namespace hstu {
 
 namespace {
+
+constexpr int64_t kI64Max = 0x7fffffffffffffffll;
+constexpr int64_t kI64Min = -kI64Max - 1;
 
 template <int DQK, int DV>
 __global__ __launch_bounds__(256, 2) void attn_fwd_bf16_kernel(JaggedArgs ja, Tensors t,
@@ -32,15 +39,19 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_bf16_kernel(JaggedArgs ja, Te
                                                                const int32_t* __restrict__ count) {
   constexpr int BM = kFwdBM, BN = kFwdBN;
   constexpr int K_LD = DQK + 8;   // LDS row pitch of the K tile (bf16 elements)
-  constexpr int VT_LD = BN + 8;   // LDS row pitch of the V^T tile
+  constexpr int V_LD = DV + 8;    // LDS row pitch of the V tile
   constexpr int NWIN = BM + BN;   // rab_pos slice per tile (BM + BN - 1 used)
+  constexpr int KCH = BN * DQK / 8, VCH = BN * DV / 8;
+  constexpr int KPT = (KCH + 255) / 256, VPT = (VCH + 255) / 256;
   static_assert(BN == 32, "one 32x32 score block per wave and tile");
 
   __shared__ __align__(16) uint16_t sK[BN * K_LD];
-  __shared__ __align__(16) uint16_t sVT[DV * VT_LD];
-  __shared__ int64_t sTj[BN];
-  __shared__ float sPos[NWIN];
-  __shared__ float sTime[256];
+  __shared__ __align__(16) uint16_t sV[BN * V_LD];
+  __shared__ __align__(16) uint32_t sTj[BN];
+  __shared__ int64_t sTj64[BN];
+  __shared__ float sWin[NWIN];
+  __shared__ float sTab[64];
+  __shared__ int64_t sRed[2][4];
 
   if ((int)blockIdx.x >= *count) return;
   const WorkItem it = items[blockIdx.x];
@@ -58,12 +69,26 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_bf16_kernel(JaggedArgs ja, Te
   const int my_i = iw0 + col;
   const bool row_ok = my_i < L;
   const int wave_last = min(iw0 + 31, L - 1);
-
-  for (int x = tid; x < NB; x += 256) sTime[x] = ja.rab_time[x];
+  const int64_t* __restrict__ ts = ja.timestamps + o;
 
   const uint16_t* __restrict__ qg = (const uint16_t*)t.q;
   const uint16_t* __restrict__ kg = (const uint16_t*)t.k;
   const uint16_t* __restrict__ vg = (const uint16_t*)t.v;
+
+  // Timestamp extremes over the tokens this item touches, [0, rows_end).
+  int64_t tlo = kI64Max, thi = kI64Min;
+  for (int x = tid; x < rows_end; x += 256) {
+    const int64_t v = ts[x];
+    tlo = v < tlo ? v : tlo;
+    thi = v > thi ? v : thi;
+  }
+  tlo = wave_min_i64(tlo);
+  thi = wave_max_i64(thi);
+  if (lane == 0) {
+    sRed[0][wave] = tlo;
+    sRed[1][wave] = thi;
+  }
+  for (int x = tid; x < 64; x += 256) sTab[x] = ja.rab_time[min(63 - x, NB - 1)];
 
   // Q fragment: B operand of S^T = K Q^T (lane = query row, 8 d's per step).
   u32x4 qf[DQK / 16];
@@ -72,7 +97,18 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_bf16_kernel(JaggedArgs ja, Te
     qf[s] = row_ok ? *reinterpret_cast<const u32x4*>(qg + (o + my_i) * t.q_stride + head * DQK +
                                                      16 * s + 8 * half)
                    : zero_u32x4();
-  const int64_t ti = row_ok ? ja.timestamps[o + my_i] : 0;
+  __syncthreads();
+  tlo = sRed[0][0];
+  thi = sRed[1][0];
+#pragma unroll
+  for (int w = 1; w < 4; w++) {
+    tlo = sRed[0][w] < tlo ? sRed[0][w] : tlo;
+    thi = sRed[1][w] > thi ? sRed[1][w] : thi;
+  }
+  const bool fast = (thi - tlo) < ((int64_t)1 << 31);
+  const int64_t tbase = tlo;
+  const int64_t ti64 = row_ok ? ts[my_i] : tbase;
+  const uint32_t tir = (uint32_t)(ti64 - tbase);
   const int pi = bias_pos(my_i, n_h);
 
   f32x16 oacc[DV / 32];
@@ -83,85 +119,135 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_bf16_kernel(JaggedArgs ja, Te
 
   const int kend = (rows_end + BN - 1) / BN;
   const int nh_blk = (n_h + BN - 1) / BN;
+  // Key tiles made only of candidates that precede every row of the
+  // block are fully masked and skipped.
+  auto skipped = [&](int kb) { return kb >= nh_blk && (kb + 1) * BN <= i0; };
 
-  for (int kb = 0; kb < kend; kb++) {
+  const int tr_row = 4 * (lane >> 5) + ((lane & 15) >> 2);
+  const int tr_col = 16 * ((lane >> 4) & 1) + 4 * (lane & 3);
+
+  u32x4 pk[KPT], pv[VPT];
+  int64_t pt = 0;
+  float pw = 0.0f;
+  auto prefetch = [&](int kb) {
     const int j0 = kb * BN;
-    // Key tile of candidates entirely before this block's rows: all masked.
-    if (kb >= nh_blk && j0 + BN <= i0) continue;
+#pragma unroll
+    for (int k = 0; k < KPT; k++) {
+      const int c = tid + 256 * k;
+      if (c < KCH) {
+        const int r = c / (DQK / 8), cc = (c % (DQK / 8)) * 8, j = j0 + r;
+        pk[k] = j < L ? *reinterpret_cast<const u32x4*>(kg + (o + j) * t.k_stride + head * DQK + cc)
+                      : zero_u32x4();
+      }
+    }
+#pragma unroll
+    for (int k = 0; k < VPT; k++) {
+      const int c = tid + 256 * k;
+      if (c < VCH) {
+        const int r = c / (DV / 8), cc = (c % (DV / 8)) * 8, j = j0 + r;
+        pv[k] = j < L ? *reinterpret_cast<const u32x4*>(vg + (o + j) * t.v_stride + head * DV + cc)
+                      : zero_u32x4();
+      }
+    }
+    if (tid < BN) pt = (j0 + tid < L) ? ts[j0 + tid] : tbase;
+    if (tid < NWIN) {
+      // rab_pos entries reachable from (query block, key tile):
+      // (N-1) + p(j) - p(i), p(i) in [min(i0,n_h), min(i0+BM-1,n_h)],
+      // p(j) in [min(j0,n_h), min(j0+BN-1,n_h)].
+      const int pos_base = (N - 1) + min(j0, n_h) - min(i0 + BM - 1, n_h);
+      const int g = pos_base + tid;
+      pw = (g >= 0 && g <= 2 * N - 2) ? ja.rab_pos[g] : 0.0f;
+    }
+  };
+
+  int kb = 0;
+  while (kb < kend && skipped(kb)) kb++;
+  if (kb < kend) prefetch(kb);
+
+  while (kb < kend) {
+    const int j0 = kb * BN;
+    int kn = kb + 1;
+    while (kn < kend && skipped(kn)) kn++;
     __syncthreads();  // previous tile fully consumed
-
-    constexpr int KCH = BN * DQK / 8;
-    for (int c = tid; c < KCH; c += 256) {
-      const int r = c / (DQK / 8), cc = (c % (DQK / 8)) * 8;
-      const int j = j0 + r;
-      u32x4 v = j < L ? *reinterpret_cast<const u32x4*>(kg + (o + j) * t.k_stride + head * DQK + cc)
-                      : zero_u32x4();
-      *reinterpret_cast<u32x4*>(sK + r * K_LD + cc) = v;
-    }
-    constexpr int VCH = BN * DV / 8;
-    for (int c = tid; c < VCH; c += 256) {
-      const int r = c / (DV / 8), cc = (c % (DV / 8)) * 8;
-      const int j = j0 + r;
-      u32x4 v = j < L ? *reinterpret_cast<const u32x4*>(vg + (o + j) * t.v_stride + head * DV + cc)
-                      : zero_u32x4();
-      const int pos = swap_bits23(r);
 #pragma unroll
-      for (int e = 0; e < 8; e++)
-        sVT[(cc + e) * VT_LD + pos] = (uint16_t)(v[e >> 1] >> (16 * (e & 1)));
+    for (int k = 0; k < KPT; k++) {
+      const int c = tid + 256 * k;
+      if (c < KCH) *reinterpret_cast<u32x4*>(sK + (c / (DQK / 8)) * K_LD + (c % (DQK / 8)) * 8) = pk[k];
     }
-    if (tid < BN) sTj[tid] = (j0 + tid < L) ? ja.timestamps[o + j0 + tid] : 0;
-    // rab_pos entries reachable from this (query block, key tile):
-    // (N-1) + p(j) - p(i) with p(i) in [min(i0,n_h), min(i0+BM-1,n_h)] and
-    // p(j) in [min(j0,n_h), min(j0+BN-1,n_h)].
-    const int pos_base = (N - 1) + min(j0, n_h) - min(i0 + BM - 1, n_h);
-    for (int x = tid; x < NWIN; x += 256) {
-      const int g = pos_base + x;
-      sPos[x] = (g >= 0 && g <= 2 * N - 2) ? ja.rab_pos[g] : 0.0f;
+#pragma unroll
+    for (int k = 0; k < VPT; k++) {
+      const int c = tid + 256 * k;
+      if (c < VCH) *reinterpret_cast<u32x4*>(sV + (c / (DV / 8)) * V_LD + (c % (DV / 8)) * 8) = pv[k];
     }
+    if (tid < BN) {
+      sTj64[tid] = pt;
+      sTj[tid] = (uint32_t)(pt - tbase);
+    }
+    if (tid < NWIN) sWin[tid] = pw;
     __syncthreads();
+    if (kn < kend) prefetch(kn);
 
-    if (iw0 >= L || j0 > wave_last) continue;           // no row of this wave sees the tile
-    if (kb >= nh_blk && j0 + BN <= iw0) continue;         // candidate keys before the wave
-
-    // Bias into the accumulator; lane holds (j = j0 + 8g + 4*half + m, i = my_i).
-    f32x16 sacc;
-    uint32_t vmask = 0;
+    const bool active = iw0 < L && j0 <= wave_last && !(kb >= nh_blk && j0 + BN <= iw0);
+    if (active) {
+      // Lane holds (j = j0 + 8g + 4*half + m, i = my_i).
+      const bool full = (j0 + BN - 1 <= iw0) && (iw0 + 31 < L) && (iw0 + 31 < n_h);
+      const int pos_base = (N - 1) + min(j0, n_h) - min(i0 + BM - 1, n_h);
+      f32x16 sacc;
+      uint32_t vmask = 0xffffu;
+      if (full) {
+        // window index = j_local + (min(i0+BM-1, n_h) - i) for history rows
+        const int xb = min(i0 + BM - 1, n_h) - my_i + 4 * half;
 #pragma unroll
-    for (int q = 0; q < 16; q++) {
-      const int jl = 8 * (q >> 2) + 4 * half + (q & 3);
-      const int j = j0 + jl;
-      float bias = 0.0f;
-      if (row_ok && j < L && pair_valid(my_i, j, n_h)) {
-        const int widx = (N - 1) + bias_pos(j, n_h) - pi - pos_base;
-        bias = sPos[widx] + sTime[time_bucket64(ti - sTj[jl], NB)];
-        vmask |= 1u << q;
+        for (int q = 0; q < 16; q++) {
+          const int jl = 8 * (q >> 2) + 4 * half + (q & 3);
+          const int s = fast ? slot32(tir, sTj[jl]) : slot64(ti64 - sTj64[jl]);
+          sacc[q] = sWin[xb + 8 * (q >> 2) + (q & 3)] + sTab[s];
+        }
+      } else {
+        vmask = 0;
+#pragma unroll
+        for (int q = 0; q < 16; q++) {
+          const int jl = 8 * (q >> 2) + 4 * half + (q & 3);
+          const int j = j0 + jl;
+          float b = 0.0f;
+          if (row_ok && j < L && pair_valid(my_i, j, n_h)) {
+            const int x = (N - 1) + bias_pos(j, n_h) - pi - pos_base;
+            const int s = fast ? slot32(tir, sTj[jl]) : slot64(ti64 - sTj64[jl]);
+            b = sWin[x] + sTab[s];
+            vmask |= 1u << q;
+          }
+          sacc[q] = b;
+        }
       }
-      sacc[q] = bias;
-    }
 #pragma unroll
-    for (int s = 0; s < DQK / 16; s++) {
-      u32x4 kf = *reinterpret_cast<const u32x4*>(sK + col * K_LD + 16 * s + 8 * half);
-      sacc = mfma32x32x16(as_bf16x8(kf), as_bf16x8(qf[s]), sacc);
-    }
-    float p[16];
+      for (int s = 0; s < DQK / 16; s++) {
+        u32x4 kf = *reinterpret_cast<const u32x4*>(sK + col * K_LD + 16 * s + 8 * half);
+        sacc = mfma32x32x16(as_bf16x8(kf), as_bf16x8(qf[s]), sacc);
+      }
+      float p[16];
 #pragma unroll
-    for (int q = 0; q < 16; q++) {
-      const float x = sacc[q];
-      p[q] = ((vmask >> q) & 1u) ? x * sigmoid_fast(x) : 0.0f;
-    }
+      for (int q = 0; q < 16; q++) {
+        const float x = sacc[q];
+        p[q] = ((vmask >> q) & 1u) ? x * sigmoid_fast(x) : 0.0f;
+      }
 #pragma unroll
-    for (int st = 0; st < 2; st++) {
-      u32x4 pa;
-      pa[0] = pack_bf16x2(p[8 * st + 0], p[8 * st + 1]);
-      pa[1] = pack_bf16x2(p[8 * st + 2], p[8 * st + 3]);
-      pa[2] = pack_bf16x2(p[8 * st + 4], p[8 * st + 5]);
-      pa[3] = pack_bf16x2(p[8 * st + 6], p[8 * st + 7]);
+      for (int st = 0; st < 2; st++) {
+        u32x4 pa;
+        pa[0] = pack_bf16x2(p[8 * st + 0], p[8 * st + 1]);
+        pa[1] = pack_bf16x2(p[8 * st + 2], p[8 * st + 3]);
+        pa[2] = pack_bf16x2(p[8 * st + 4], p[8 * st + 5]);
+        pa[3] = pack_bf16x2(p[8 * st + 6], p[8 * st + 7]);
+        const int row = 16 * st + tr_row;
 #pragma unroll
-      for (int nb = 0; nb < DV / 32; nb++) {
-        u32x4 vb = *reinterpret_cast<const u32x4*>(sVT + (32 * nb + col) * VT_LD + 16 * st + 8 * half);
-        oacc[nb] = mfma32x32x16(as_bf16x8(pa), as_bf16x8(vb), oacc[nb]);
+        for (int nb = 0; nb < DV / 32; nb++) {
+          const uint16_t* base = sV + row * V_LD + 32 * nb + tr_col;
+          const uint2 lo = lds_read_tr16(base), hi = lds_read_tr16(base + 8 * V_LD);
+          u32x4 vb = {lo.x, lo.y, hi.x, hi.y};
+          oacc[nb] = mfma32x32x16(as_bf16x8(pa), as_bf16x8(vb), oacc[nb]);
+        }
       }
     }
+    kb = kn;
   }
 
   // O accumulator: lane holds (i = iw0 + 8g + 4*half + m, c = 32nb + col).
