@@ -11,9 +11,8 @@
 //   d rab_pos[(N-1)+p(j)-p(i)] += dS/N,  d rab_time[bkt] += dS/N.
 //
 // Workgroup = 4 waves = one (sequence, 128-key block, head) work item.
-// Wave w owns keys j0 + 32w .. +31: their K and V sit in registers as
-// MFMA operands and their dK, dV accumulate in registers for the whole
-// item.  The workgroup walks query steps of 32 rows; each step's Q and dO
+// Wave w owns keys j0 + 32w .. +31 and accumulates their dK, dV in
+// registers for the whole item; K and V of the block stay in LDS.  The workgroup walks query steps of 32 rows; each step's Q and dO
 // rows are staged row-major in LDS (prefetched into registers during the
 // previous step).  Per step and wave, on v_mfma_f32_32x32x16_bf16:
 //   S  = Q K^T (accumulator seeded with the bias), dP = dO V^T;
@@ -42,41 +41,60 @@ constexpr int64_t kI64Max = 0x7fffffffffffffffll;
 constexpr int64_t kI64Min = -kI64Max - 1;
 
 template <int DQK, int DV>
-__global__ __launch_bounds__(256, 1) void attn_bwd_bf16_kernel(
-    JaggedArgs ja, Tensors t, const uint16_t* __restrict__ dO, float* __restrict__ dq_acc,
-    uint16_t* __restrict__ dK, uint16_t* __restrict__ dV, float* __restrict__ d_rab_pos,
-    float* __restrict__ d_rab_time, const WorkItem* __restrict__ items,
-    const int32_t* __restrict__ count, int pos_in_lds) {
-  constexpr int BN = kBwdBN, BM = kBwdBM;
-  constexpr int Q_LD = DQK + 8, DO_LD = DV + 8;  // row-major step tiles
-  constexpr int DS_LD = BN + 8, KT_LD = BN + 8;
-  constexpr int NWIN = BM + BN;                   // reversed rab_pos window
+struct BwdShared {
+  static constexpr int BN = kBwdBN, BM = kBwdBM;
+  static constexpr int Q_LD = DQK + 8, DO_LD = DV + 8;  // row-major step tiles
+  static constexpr int DS_LD = BN + 8;
+  static constexpr int DS32_LD = BN + 1;
+  static constexpr int K_LD = DQK + 8, V_LD = DV + 8;    // the block's keys, row-major
+  static constexpr int NWIN = BM + BN;                   // reversed rab_pos window
+  __align__(16) uint16_t sQ[BM * Q_LD];
+  __align__(16) uint16_t sdO[BM * DO_LD];
+  __align__(16) uint16_t sdS[BM * DS_LD];
+  float sdS32[BM * DS32_LD];       // dS in fp32 for the bias-table gradients
+  __align__(16) uint16_t sK[BN * K_LD];
+  __align__(16) uint16_t sV[BN * V_LD];
+  __align__(16) uint32_t sTr[BM];  // step row timestamps, rebased (fast path)
+  int64_t sTr64[BM];               // step row timestamps (exact path)
+  float sWin[NWIN];
+  float sTab[64];                  // rab_time by slot
+  float sTacc[4][64];              // per-wave time-gradient sums by slot
+  int64_t sRange[2];               // extremes of the step's row timestamps
+  int64_t sRed[2][4];
+};
+
+struct BwdArgs {
+  JaggedArgs ja;
+  Tensors t;
+  const uint16_t* dO;
+  float* dq_acc;
+  uint16_t* dK;
+  uint16_t* dV;
+  float* d_rab_pos;
+  float* d_rab_time;
+  int pos_in_lds;
+};
+
+// Slot of t_i - t_j: 32-bit rebased form on the fast path, exact 64-bit otherwise.
+template <bool FAST>
+__device__ __forceinline__ int slot_of(uint32_t ri, uint32_t rj, int64_t ti, int64_t tj) {
+  if constexpr (FAST)
+    return slot32(ri, rj);
+  else
+    return slot64(ti - tj);
+}
+
+template <int DQK, int DV, bool FAST>
+__device__ __forceinline__ void bwd_item(BwdShared<DQK, DV>& sm, float* __restrict__ sPosAcc,
+                                         const BwdArgs& A, int64_t o, int L, int n_h, int j0,
+                                         int head, int64_t tbase) {
+  using S = BwdShared<DQK, DV>;
+  constexpr int BN = S::BN, BM = S::BM, Q_LD = S::Q_LD, DO_LD = S::DO_LD, DS_LD = S::DS_LD,
+                DS32_LD = S::DS32_LD, K_LD = S::K_LD, V_LD = S::V_LD, NWIN = S::NWIN;
   constexpr int QCH = BM * DQK / 8, OCH = BM * DV / 8;
   constexpr int QPT = (QCH + 255) / 256, OPT = (OCH + 255) / 256;
-  static_assert(BN == 128 && BM == 32, "4 waves x 32 keys, 32-row query steps");
-
-  __shared__ __align__(16) uint16_t sQ[BM * Q_LD];
-  __shared__ __align__(16) uint16_t sdO[BM * DO_LD];
-  __shared__ __align__(16) uint16_t sdS[BM * DS_LD];
-  __shared__ __align__(16) uint16_t sKT[DQK * KT_LD];
-  __shared__ __align__(16) uint32_t sTr[BM];   // step row timestamps, rebased
-  __shared__ int64_t sTr64[BM];                // step row timestamps
-  __shared__ float sWin[NWIN];
-  __shared__ float sTab[64];                   // rab_time by slot
-  __shared__ float sTacc[4][64];               // per-wave time-gradient sums by slot
-  __shared__ int64_t sRange[2];                // extremes of the step's row timestamps
-  __shared__ int64_t sRed[2][4];
-  extern __shared__ float sPosAcc[];           // [N] when pos_in_lds
-
-  if ((int)blockIdx.x >= *count) return;
-  const WorkItem it = items[blockIdx.x];
-  const int head = blockIdx.y;
+  const JaggedArgs& ja = A.ja;
   const int H = ja.num_heads, N = ja.max_seq_len, NB = ja.num_buckets;
-  const int64_t o = ja.seq_offsets[it.seq];
-  const int L = (int)(ja.seq_offsets[it.seq + 1] - o);
-  const int n_h = L - (ja.num_targets ? (int)ja.num_targets[it.seq] : 0);
-  const int j0 = it.blk * BN;
-
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
   const int col = lane & 31, half = lane >> 5;
   const int jw0 = j0 + 32 * wave;
@@ -85,66 +103,13 @@ __global__ __launch_bounds__(256, 1) void attn_bwd_bf16_kernel(
   const int pj = bias_pos(my_j, n_h);
   const float invN = 1.0f / (float)N;
   const int64_t* __restrict__ ts = ja.timestamps + o;
-
-  const uint16_t* __restrict__ qg = (const uint16_t*)t.q;
-  const uint16_t* __restrict__ kg = (const uint16_t*)t.k;
-  const uint16_t* __restrict__ vg = (const uint16_t*)t.v;
-
-  // Timestamp extremes over the tokens this item touches, [j0, L).
-  int64_t tlo = kI64Max, thi = kI64Min;
-  for (int x = j0 + tid; x < L; x += 256) {
-    const int64_t v = ts[x];
-    tlo = v < tlo ? v : tlo;
-    thi = v > thi ? v : thi;
-  }
-  tlo = wave_min_i64(tlo);
-  thi = wave_max_i64(thi);
-  if (lane == 0) {
-    sRed[0][wave] = tlo;
-    sRed[1][wave] = thi;
-  }
-  for (int x = tid; x < 64; x += 256) sTab[x] = ja.rab_time[min(63 - x, NB - 1)];
-  for (int x = tid; x < 4 * 64; x += 256) (&sTacc[0][0])[x] = 0.0f;
+  const uint16_t* __restrict__ qg = (const uint16_t*)A.t.q;
   const int R = L - j0;  // p(i) - p(j) of kept pairs lies in [0, R)
-  if (pos_in_lds)
-    for (int x = tid; x < R; x += 256) sPosAcc[x] = 0.0f;
-  // K^T of the 128-key block (operand of dQ = dS K).
-  constexpr int KCH = BN * DQK / 8;
-  for (int c = tid; c < KCH; c += 256) {
-    const int r = c / (DQK / 8), cc = (c % (DQK / 8)) * 8;
-    const int j = j0 + r;
-    u32x4 v = j < L ? *reinterpret_cast<const u32x4*>(kg + (o + j) * t.k_stride + head * DQK + cc)
-                    : zero_u32x4();
-#pragma unroll
-    for (int e = 0; e < 8; e++) sKT[(cc + e) * KT_LD + r] = (uint16_t)(v[e >> 1] >> (16 * (e & 1)));
-  }
-  __syncthreads();
-  tlo = sRed[0][0];
-  thi = sRed[1][0];
-#pragma unroll
-  for (int w = 1; w < 4; w++) {
-    tlo = sRed[0][w] < tlo ? sRed[0][w] : tlo;
-    thi = sRed[1][w] > thi ? sRed[1][w] : thi;
-  }
-  const bool fast = (thi - tlo) < ((int64_t)1 << 31);
-  const int64_t tbase = tlo;
+
   const int64_t tj64 = key_ok ? ts[my_j] : tbase;
   const uint32_t tjr = (uint32_t)(tj64 - tbase);
   const int64_t klo = wave_min_i64(key_ok ? tj64 : kI64Max);
   const int64_t khi = wave_max_i64(key_ok ? tj64 : kI64Min);
-
-  // K, V of the wave's keys as B operands (lane = key, 8 features per step).
-  u32x4 kf[DQK / 16], vf[DV / 16];
-#pragma unroll
-  for (int s = 0; s < DQK / 16; s++)
-    kf[s] = key_ok ? *reinterpret_cast<const u32x4*>(kg + (o + my_j) * t.k_stride + head * DQK +
-                                                     16 * s + 8 * half)
-                   : zero_u32x4();
-#pragma unroll
-  for (int s = 0; s < DV / 16; s++)
-    vf[s] = key_ok ? *reinterpret_cast<const u32x4*>(vg + (o + my_j) * t.v_stride + head * DV +
-                                                     16 * s + 8 * half)
-                   : zero_u32x4();
 
   f32x16 dkacc[DQK / 32], dvacc[DV / 32];
 #pragma unroll
@@ -172,7 +137,7 @@ __global__ __launch_bounds__(256, 1) void attn_bwd_bf16_kernel(
       const int c = tid + 256 * k;
       if (c < QCH) {
         const int r = c / (DQK / 8), cc = (c % (DQK / 8)) * 8, i = i0 + r;
-        pq[k] = i < L ? *reinterpret_cast<const u32x4*>(qg + (o + i) * t.q_stride + head * DQK + cc)
+        pq[k] = i < L ? *reinterpret_cast<const u32x4*>(qg + (o + i) * A.t.q_stride + head * DQK + cc)
                       : zero_u32x4();
       }
     }
@@ -181,7 +146,7 @@ __global__ __launch_bounds__(256, 1) void attn_bwd_bf16_kernel(
       const int c = tid + 256 * k;
       if (c < OCH) {
         const int r = c / (DV / 8), cc = (c % (DV / 8)) * 8, i = i0 + r;
-        po[k] = i < L ? *reinterpret_cast<const u32x4*>(dO + ((o + i) * H + head) * DV + cc)
+        po[k] = i < L ? *reinterpret_cast<const u32x4*>(A.dO + ((o + i) * H + head) * DV + cc)
                       : zero_u32x4();
       }
     }
@@ -203,25 +168,27 @@ __global__ __launch_bounds__(256, 1) void attn_bwd_bf16_kernel(
 #pragma unroll
     for (int k = 0; k < QPT; k++) {
       const int c = tid + 256 * k;
-      if (c < QCH) *reinterpret_cast<u32x4*>(sQ + (c / (DQK / 8)) * Q_LD + (c % (DQK / 8)) * 8) = pq[k];
+      if (c < QCH) *reinterpret_cast<u32x4*>(sm.sQ + (c / (DQK / 8)) * Q_LD + (c % (DQK / 8)) * 8) = pq[k];
     }
 #pragma unroll
     for (int k = 0; k < OPT; k++) {
       const int c = tid + 256 * k;
-      if (c < OCH) *reinterpret_cast<u32x4*>(sdO + (c / (DV / 8)) * DO_LD + (c % (DV / 8)) * 8) = po[k];
+      if (c < OCH) *reinterpret_cast<u32x4*>(sm.sdO + (c / (DV / 8)) * DO_LD + (c % (DV / 8)) * 8) = po[k];
     }
     if (tid < BM) {
-      sTr64[tid] = pt;
-      sTr[tid] = (uint32_t)(pt - tbase);
+      if constexpr (FAST)
+        sm.sTr[tid] = (uint32_t)(pt - tbase);
+      else
+        sm.sTr64[tid] = pt;
     }
-    if (tid < NWIN) sWin[tid] = pw;
+    if (tid < NWIN) sm.sWin[tid] = pw;
     if (wave == 0) {
       const bool okr = lane < BM && i0 + lane < L;
       const int64_t rlo = wave_min_i64(okr ? pt : kI64Max);
       const int64_t rhi = wave_max_i64(okr ? pt : kI64Min);
       if (lane == 0) {
-        sRange[0] = rlo;
-        sRange[1] = rhi;
+        sm.sRange[0] = rlo;
+        sm.sRange[1] = rhi;
       }
     }
     __syncthreads();
@@ -232,21 +199,33 @@ __global__ __launch_bounds__(256, 1) void attn_bwd_bf16_kernel(
     bool active = jw0 < L && jw0 <= imax;
     if (jw0 >= n_h && jw0 != i0) active = false;  // candidate keys: diagonal block only
 
-    float ds[16];
-    if (active) {
+    // dS of this wave's block as bf16 pairs: da[st][e] holds accumulator
+    // entries 8st+2e and 8st+2e+1.  The contractions run for every wave:
+    // a wave without kept pairs in this step gets an all-zero mask from
+    // the general path, so its P and dS are zero and the accumulators
+    // stay in straight-line code (no merge of the dK/dV registers).
+    u32x4 da[2];
+    {
       // Accumulator lane holds (i = i0 + 8g + 4*half + m, j = my_j).
-      const bool full = (jw0 + 31 <= i0) && (i0 + BM - 1 < L) && (i0 + BM - 1 < n_h);
+      const bool full = active && (jw0 + 31 <= i0) && (i0 + BM - 1 < L) && (i0 + BM - 1 < n_h);
       f32x16 sacc, pacc;
-      int slot[16];
       uint32_t vmask = 0xffffu;
       if (full) {
         const int yb = (NWIN - 32 - 32 * wave - col) + 4 * half;
+        int sl[16];
+        float wv[16], tv[16];
 #pragma unroll
         for (int q = 0; q < 16; q++) {
           const int il = 8 * (q >> 2) + 4 * half + (q & 3);
-          slot[q] = fast ? slot32(sTr[il], tjr) : slot64(sTr64[il] - tj64);
-          sacc[q] = sWin[yb + 8 * (q >> 2) + (q & 3)] + sTab[slot[q]];
+          sl[q] = slot_of<FAST>(sm.sTr[il], tjr, sm.sTr64[il], tj64);
         }
+#pragma unroll
+        for (int q = 0; q < 16; q++) {
+          wv[q] = sm.sWin[yb + 8 * (q >> 2) + (q & 3)];
+          tv[q] = sm.sTab[sl[q]];
+        }
+#pragma unroll
+        for (int q = 0; q < 16; q++) sacc[q] = wv[q] + tv[q];
       } else {
         vmask = 0;
         const int pos_base = (N - 1) + min(j0, n_h) - min(i0 + BM - 1, n_h);
@@ -254,92 +233,106 @@ __global__ __launch_bounds__(256, 1) void attn_bwd_bf16_kernel(
         for (int q = 0; q < 16; q++) {
           const int il = 8 * (q >> 2) + 4 * half + (q & 3);
           const int i = i0 + il;
-          float b = 0.0f;
-          int s = 0;
-          if (key_ok && i < L && pair_valid(i, my_j, n_h)) {
-            const int x = (N - 1) + pj - bias_pos(i, n_h) - pos_base;
-            s = fast ? slot32(sTr[il], tjr) : slot64(sTr64[il] - tj64);
-            b = sWin[NWIN - 1 - x] + sTab[s];
-            vmask |= 1u << q;
-          }
-          slot[q] = s;
-          sacc[q] = b;
+          const bool ok = key_ok && i < L && pair_valid(i, my_j, n_h);
+          const int x = ok ? (N - 1) + pj - bias_pos(i, n_h) - pos_base : 0;
+          const int sl = slot_of<FAST>(sm.sTr[il], tjr, sm.sTr64[il], tj64);
+          const float b = sm.sWin[NWIN - 1 - x] + sm.sTab[sl];
+          sacc[q] = ok ? b : 0.0f;
+          vmask |= (uint32_t)ok << q;
         }
       }
 #pragma unroll
       for (int q = 0; q < 16; q++) pacc[q] = 0.0f;
+      // The S and dP chains are independent: interleave them so each
+      // MFMA's accumulator dependency is covered by the other chain.
+      constexpr int SMAX = DQK > DV ? DQK / 16 : DV / 16;
 #pragma unroll
-      for (int s = 0; s < DQK / 16; s++) {
-        u32x4 a = *reinterpret_cast<const u32x4*>(sQ + col * Q_LD + 16 * s + 8 * half);
-        sacc = mfma32x32x16(as_bf16x8(a), as_bf16x8(kf[s]), sacc);
+      for (int s = 0; s < SMAX; s++) {
+        if (s < DQK / 16) {
+          u32x4 a = *reinterpret_cast<const u32x4*>(sm.sQ + col * Q_LD + 16 * s + 8 * half);
+          u32x4 b = *reinterpret_cast<const u32x4*>(sm.sK + (32 * wave + col) * K_LD + 16 * s + 8 * half);
+          sacc = mfma32x32x16(as_bf16x8(a), as_bf16x8(b), sacc);
+        }
+        if (s < DV / 16) {
+          u32x4 a = *reinterpret_cast<const u32x4*>(sm.sdO + col * DO_LD + 16 * s + 8 * half);
+          u32x4 b = *reinterpret_cast<const u32x4*>(sm.sV + (32 * wave + col) * V_LD + 16 * s + 8 * half);
+          pacc = mfma32x32x16(as_bf16x8(a), as_bf16x8(b), pacc);
+        }
       }
+      float pv[16], dsv[16], sg[16];
 #pragma unroll
-      for (int s = 0; s < DV / 16; s++) {
-        u32x4 a = *reinterpret_cast<const u32x4*>(sdO + col * DO_LD + 16 * s + 8 * half);
-        pacc = mfma32x32x16(as_bf16x8(a), as_bf16x8(vf[s]), pacc);
-      }
-      float p[16];
+      for (int q = 0; q < 16; q++) sg[q] = __builtin_amdgcn_exp2f(-sacc[q] * kLog2e);
+#pragma unroll
+      for (int q = 0; q < 16; q++) sg[q] = __builtin_amdgcn_rcpf(1.0f + sg[q]);
 #pragma unroll
       for (int q = 0; q < 16; q++) {
-        const float x = sacc[q];
-        const float sg = sigmoid_fast(x);
-        const float sl = x * sg;
+        const float sl = sacc[q] * sg[q];
         const bool ok = (vmask >> q) & 1u;
-        p[q] = ok ? sl : 0.0f;
-        ds[q] = ok ? pacc[q] * (sg + sl * (1.0f - sg)) : 0.0f;
+        pv[q] = ok ? sl : 0.0f;
+        dsv[q] = ok ? pacc[q] * (sg[q] + sl * (1.0f - sg[q])) : 0.0f;
+      }
+      // Time-table gradient: sum dS per slot over the slots this tile spans
+      // (a single slot away from the diagonal).
+      if (active) {
+        int s_lo, s_hi;
+        slot_range(sm.sRange[0], sm.sRange[1], klo, khi, s_lo, s_hi);
+        if (s_lo == s_hi) {
+          float sum = 0.0f;
+#pragma unroll
+          for (int q = 0; q < 16; q++) sum += dsv[q];
+          sum = wave_sum_f32(sum);
+          if (lane == 0) sm.sTacc[wave][s_lo] += sum;
+        } else {
+          for (int s = s_lo; s <= s_hi; s++) {
+            float sum = 0.0f;
+#pragma unroll
+            for (int q = 0; q < 16; q++) {
+              const int il = 8 * (q >> 2) + 4 * half + (q & 3);
+              const int sl = slot_of<FAST>(sm.sTr[il], tjr, sm.sTr64[il], tj64);
+              sum += sl == s ? dsv[q] : 0.0f;
+            }
+            sum = wave_sum_f32(sum);
+            if (lane == 0) sm.sTacc[wave][s] += sum;
+          }
+        }
+      }
+#pragma unroll
+      for (int q = 0; q < 16; q++) {
+        const int il = 8 * (q >> 2) + 4 * half + (q & 3);
+        sm.sdS32[il * DS32_LD + 32 * wave + col] = dsv[q];
+      }
+      u32x4 pa[2];
+#pragma unroll
+      for (int q = 0; q < 16; q += 2) {
+        pa[q >> 3][(q & 7) >> 1] = pack_bf16x2(pv[q], pv[q + 1]);
+        da[q >> 3][(q & 7) >> 1] = pack_bf16x2(dsv[q], dsv[q + 1]);
       }
       // dV += P^T dO, dK += dS^T Q  (contraction over the step's 32 rows).
 #pragma unroll
       for (int st = 0; st < 2; st++) {
-        u32x4 pa, da;
-#pragma unroll
-        for (int e = 0; e < 4; e++) {
-          pa[e] = pack_bf16x2(p[8 * st + 2 * e], p[8 * st + 2 * e + 1]);
-          da[e] = pack_bf16x2(ds[8 * st + 2 * e], ds[8 * st + 2 * e + 1]);
-        }
         const int row = 16 * st + tr_row;
 #pragma unroll
         for (int nb = 0; nb < DV / 32; nb++) {
-          const uint16_t* base = sdO + row * DO_LD + 32 * nb + tr_col;
+          const uint16_t* base = sm.sdO + row * DO_LD + 32 * nb + tr_col;
           const uint2 lo = lds_read_tr16(base), hi = lds_read_tr16(base + 8 * DO_LD);
           u32x4 b = {lo.x, lo.y, hi.x, hi.y};
-          dvacc[nb] = mfma32x32x16(as_bf16x8(pa), as_bf16x8(b), dvacc[nb]);
+          dvacc[nb] = mfma32x32x16(as_bf16x8(pa[st]), as_bf16x8(b), dvacc[nb]);
         }
 #pragma unroll
         for (int nb = 0; nb < DQK / 32; nb++) {
-          const uint16_t* base = sQ + row * Q_LD + 32 * nb + tr_col;
+          const uint16_t* base = sm.sQ + row * Q_LD + 32 * nb + tr_col;
           const uint2 lo = lds_read_tr16(base), hi = lds_read_tr16(base + 8 * Q_LD);
           u32x4 b = {lo.x, lo.y, hi.x, hi.y};
-          dkacc[nb] = mfma32x32x16(as_bf16x8(da), as_bf16x8(b), dkacc[nb]);
+          dkacc[nb] = mfma32x32x16(as_bf16x8(da[st]), as_bf16x8(b), dkacc[nb]);
         }
       }
-      // Time-table gradient: sum dS per slot over the slots this tile spans.
-      int s_lo, s_hi;
-      slot_range(sRange[0], sRange[1], klo, khi, s_lo, s_hi);
-      if (s_lo == s_hi) {
-        float sum = 0.0f;
-#pragma unroll
-        for (int q = 0; q < 16; q++) sum += ds[q];
-        sum = wave_sum_f32(sum);
-        if (lane == 0) sTacc[wave][s_lo] += sum;
-      } else {
-        for (int s = s_lo; s <= s_hi; s++) {
-          float sum = 0.0f;
-#pragma unroll
-          for (int q = 0; q < 16; q++) sum += slot[q] == s ? ds[q] : 0.0f;
-          sum = wave_sum_f32(sum);
-          if (lane == 0) sTacc[wave][s] += sum;
-        }
-      }
-    } else {
-#pragma unroll
-      for (int q = 0; q < 16; q++) ds[q] = 0.0f;
     }
     // dS tile, row-major [32 rows][128 keys] (bf16).
 #pragma unroll
     for (int q = 0; q < 16; q++) {
       const int il = 8 * (q >> 2) + 4 * half + (q & 3);
-      sdS[il * DS_LD + 32 * wave + col] = f32_to_bf16_bits(ds[q]);
+      const uint32_t w = da[q >> 3][(q & 7) >> 1];
+      sm.sdS[il * DS_LD + 32 * wave + col] = (uint16_t)((q & 1) ? (w >> 16) : (w & 0xffffu));
     }
     __syncthreads();
 
@@ -354,15 +347,18 @@ __global__ __launch_bounds__(256, 1) void attn_bwd_bf16_kernel(
       for (int q = 0; q < 16; q++) qacc[q] = 0.0f;
 #pragma unroll
       for (int st = 0; st < STEPS; st++) {
-        const int kk = (ks * STEPS + st) * 16 + 8 * half;
-        u32x4 a = *reinterpret_cast<const u32x4*>(sdS + col * DS_LD + kk);
-        u32x4 b = *reinterpret_cast<const u32x4*>(sKT + (32 * nbq + col) * KT_LD + kk);
+        const int kk = (ks * STEPS + st) * 16;
+        u32x4 a = *reinterpret_cast<const u32x4*>(sm.sdS + col * DS_LD + kk + 8 * half);
+        // B = K[kk + 8*half + e][32*nbq + col]: down the rows of the K tile.
+        const uint16_t* base = sm.sK + (kk + (tr_row & 3) + 4 * (tr_row >> 2) * 2) * K_LD + 32 * nbq + tr_col;
+        const uint2 lo = lds_read_tr16(base), hi = lds_read_tr16(base + 4 * K_LD);
+        u32x4 b = {lo.x, lo.y, hi.x, hi.y};
         qacc = mfma32x32x16(as_bf16x8(a), as_bf16x8(b), qacc);
       }
 #pragma unroll
       for (int q = 0; q < 16; q++) {
         const int i = i0 + 8 * (q >> 2) + 4 * half + (q & 3);
-        if (i < L) unsafeAtomicAdd(&dq_acc[((o + i) * H + head) * DQK + 32 * nbq + col], qacc[q]);
+        if (i < L) unsafeAtomicAdd(&A.dq_acc[((o + i) * H + head) * DQK + 32 * nbq + col], qacc[q]);
       }
     }
 
@@ -374,14 +370,22 @@ __global__ __launch_bounds__(256, 1) void attn_bwd_bf16_kernel(
       const int k = i0 - j0 + dd;
       if (k >= 0) {
         const int ilo = max(0, dd), ihi = min(rh, BN + dd);
-        float sum = 0.0f;
-        for (int il = ilo; il < ihi; il++)
-          sum += bf16_bits_to_f32(sdS[il * DS_LD + il - dd]);
+        // Rows outside [ilo, ihi) are skipped by predication; the eight
+        // partial sums keep the LDS reads independent.
+        float part[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+#pragma unroll
+        for (int il = 0; il < BM; il++) {
+          const int c = il - dd;
+          const float v = sm.sdS32[il * DS32_LD + (c < 0 ? 0 : (c > BN - 1 ? BN - 1 : c))];
+          part[il & 7] += (il >= ilo && il < ihi) ? v : 0.0f;
+        }
+        const float sum = ((part[0] + part[1]) + (part[2] + part[3])) +
+                          ((part[4] + part[5]) + (part[6] + part[7]));
         if (sum != 0.0f) {
-          if (pos_in_lds)
+          if (A.pos_in_lds)
             sPosAcc[k] += sum;
           else
-            unsafeAtomicAdd(&d_rab_pos[(N - 1) - k], sum * invN);
+            unsafeAtomicAdd(&A.d_rab_pos[(N - 1) - k], sum * invN);
         }
       }
     }
@@ -392,13 +396,13 @@ __global__ __launch_bounds__(256, 1) void attn_bwd_bf16_kernel(
       if (tid < BN) {
         const int j = j0 + tid;
         float sum = 0.0f;
-        for (int il = rh; il < BM; il++) sum += bf16_bits_to_f32(sdS[il * DS_LD + tid]);
+        for (int il = rh; il < BM; il++) sum += sm.sdS32[il * DS32_LD + tid];
         if (sum != 0.0f) {
           const int k = j < n_h ? n_h - j : 0;
-          if (pos_in_lds)
+          if (A.pos_in_lds)
             atomicAdd(&sPosAcc[k], sum);
           else
-            unsafeAtomicAdd(&d_rab_pos[(N - 1) - k], sum * invN);
+            unsafeAtomicAdd(&A.d_rab_pos[(N - 1) - k], sum * invN);
         }
       }
     }
@@ -411,23 +415,96 @@ __global__ __launch_bounds__(256, 1) void attn_bwd_bf16_kernel(
     if (j < L) {
 #pragma unroll
       for (int nb = 0; nb < DQK / 32; nb++)
-        dK[((o + j) * H + head) * DQK + 32 * nb + col] = f32_to_bf16_bits(dkacc[nb][q] * invN);
+        A.dK[((o + j) * H + head) * DQK + 32 * nb + col] = f32_to_bf16_bits(dkacc[nb][q] * invN);
 #pragma unroll
       for (int nb = 0; nb < DV / 32; nb++)
-        dV[((o + j) * H + head) * DV + 32 * nb + col] = f32_to_bf16_bits(dvacc[nb][q] * invN);
+        A.dV[((o + j) * H + head) * DV + 32 * nb + col] = f32_to_bf16_bits(dvacc[nb][q] * invN);
     }
   }
 
   __syncthreads();
-  if (pos_in_lds)
+  if (A.pos_in_lds)
     for (int x = tid; x < R; x += 256) {
       const float v = sPosAcc[x];
-      if (v != 0.0f) unsafeAtomicAdd(&d_rab_pos[(N - 1) - x], v * invN);
+      if (v != 0.0f) unsafeAtomicAdd(&A.d_rab_pos[(N - 1) - x], v * invN);
     }
   if (tid < 64) {
-    const float v = sTacc[0][tid] + sTacc[1][tid] + sTacc[2][tid] + sTacc[3][tid];
-    if (v != 0.0f) unsafeAtomicAdd(&d_rab_time[min(63 - tid, NB - 1)], v * invN);
+    const float v = sm.sTacc[0][tid] + sm.sTacc[1][tid] + sm.sTacc[2][tid] + sm.sTacc[3][tid];
+    if (v != 0.0f) unsafeAtomicAdd(&A.d_rab_time[min(63 - tid, NB - 1)], v * invN);
   }
+}
+
+template <int DQK, int DV>
+__global__ __launch_bounds__(256, 1) void attn_bwd_bf16_kernel(BwdArgs A,
+                                                               const WorkItem* __restrict__ items,
+                                                               const int32_t* __restrict__ count) {
+  using S = BwdShared<DQK, DV>;
+  constexpr int BN = S::BN, K_LD = S::K_LD, V_LD = S::V_LD;
+  __shared__ S sm;
+  extern __shared__ float sPosAcc[];  // [N] when pos_in_lds
+
+  if ((int)blockIdx.x >= *count) return;
+  const WorkItem it = items[blockIdx.x];
+  const int head = blockIdx.y;
+  const JaggedArgs& ja = A.ja;
+  const int NB = ja.num_buckets;
+  const int64_t o = ja.seq_offsets[it.seq];
+  const int L = (int)(ja.seq_offsets[it.seq + 1] - o);
+  const int n_h = L - (ja.num_targets ? (int)ja.num_targets[it.seq] : 0);
+  const int j0 = it.blk * BN;
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  const int64_t* __restrict__ ts = ja.timestamps + o;
+  const uint16_t* __restrict__ kg = (const uint16_t*)A.t.k;
+  const uint16_t* __restrict__ vg = (const uint16_t*)A.t.v;
+
+  // Timestamp extremes over the tokens this item touches, [j0, L): the
+  // 32-bit fast path applies when they span less than 2^31.
+  int64_t tlo = kI64Max, thi = kI64Min;
+  for (int x = j0 + tid; x < L; x += 256) {
+    const int64_t v = ts[x];
+    tlo = v < tlo ? v : tlo;
+    thi = v > thi ? v : thi;
+  }
+  tlo = wave_min_i64(tlo);
+  thi = wave_max_i64(thi);
+  if (lane == 0) {
+    sm.sRed[0][wave] = tlo;
+    sm.sRed[1][wave] = thi;
+  }
+  for (int x = tid; x < 64; x += 256) sm.sTab[x] = ja.rab_time[min(63 - x, NB - 1)];
+  for (int x = tid; x < 4 * 64; x += 256) (&sm.sTacc[0][0])[x] = 0.0f;
+  if (A.pos_in_lds)
+    for (int x = tid; x < L - j0; x += 256) sPosAcc[x] = 0.0f;
+  // K and V of the 128-key block, row-major: operands of S = Q K^T and
+  // dP = dO V^T (16-byte reads along a key row) and of dQ = dS K
+  // (transposing reads down the key rows).
+  constexpr int KCH = BN * DQK / 8, VCH = BN * DV / 8;
+  for (int c = tid; c < KCH; c += 256) {
+    const int r = c / (DQK / 8), cc = (c % (DQK / 8)) * 8;
+    const int j = j0 + r;
+    *reinterpret_cast<u32x4*>(sm.sK + r * K_LD + cc) =
+        j < L ? *reinterpret_cast<const u32x4*>(kg + (o + j) * A.t.k_stride + head * DQK + cc)
+              : zero_u32x4();
+  }
+  for (int c = tid; c < VCH; c += 256) {
+    const int r = c / (DV / 8), cc = (c % (DV / 8)) * 8;
+    const int j = j0 + r;
+    *reinterpret_cast<u32x4*>(sm.sV + r * V_LD + cc) =
+        j < L ? *reinterpret_cast<const u32x4*>(vg + (o + j) * A.t.v_stride + head * DV + cc)
+              : zero_u32x4();
+  }
+  __syncthreads();
+  tlo = sm.sRed[0][0];
+  thi = sm.sRed[1][0];
+#pragma unroll
+  for (int w = 1; w < 4; w++) {
+    tlo = sm.sRed[0][w] < tlo ? sm.sRed[0][w] : tlo;
+    thi = sm.sRed[1][w] > thi ? sm.sRed[1][w] : thi;
+  }
+  if (thi - tlo < ((int64_t)1 << 31))
+    bwd_item<DQK, DV, true>(sm, sPosAcc, A, o, L, n_h, j0, head, tlo);
+  else
+    bwd_item<DQK, DV, false>(sm, sPosAcc, A, o, L, n_h, j0, head, tlo);
 }
 
 template <int DQK, int DV>
@@ -435,12 +512,21 @@ hipError_t launch_bwd(const JaggedArgs& ja, const Tensors& t, const void* d_out,
                       void* dk, void* dv, float* d_rab_pos, float* d_rab_time,
                       const WorkItem* items, const int32_t* count, int64_t max_items,
                       hipStream_t s) {
-  const int pos_in_lds = ja.max_seq_len <= kBwdMaxLdsPos ? 1 : 0;
-  const size_t lds = pos_in_lds ? sizeof(float) * (size_t)ja.max_seq_len : 0;
+  BwdArgs A;
+  A.ja = ja;
+  A.t = t;
+  A.dO = (const uint16_t*)d_out;
+  A.dq_acc = dq_acc;
+  A.dK = (uint16_t*)dk;
+  A.dV = (uint16_t*)dv;
+  A.d_rab_pos = d_rab_pos;
+  A.d_rab_time = d_rab_time;
+  // The position-gradient accumulator (N floats) joins the static LDS when
+  // both fit in the 160 KiB a gfx950 workgroup may use.
+  A.pos_in_lds = sizeof(BwdShared<DQK, DV>) + sizeof(float) * (size_t)ja.max_seq_len <= kLdsBytes;
+  const size_t lds = A.pos_in_lds ? sizeof(float) * (size_t)ja.max_seq_len : 0;
   dim3 grid((unsigned)max_items, (unsigned)ja.num_heads);
-  hipLaunchKernelGGL((attn_bwd_bf16_kernel<DQK, DV>), grid, dim3(256), lds, s, ja, t,
-                     (const uint16_t*)d_out, dq_acc, (uint16_t*)dk, (uint16_t*)dv, d_rab_pos,
-                     d_rab_time, items, count, pos_in_lds);
+  hipLaunchKernelGGL((attn_bwd_bf16_kernel<DQK, DV>), grid, dim3(256), lds, s, A, items, count);
   return hipGetLastError();
 }
 

@@ -33,36 +33,40 @@ constexpr int64_t kI64Max = 0x7fffffffffffffffll;
 constexpr int64_t kI64Min = -kI64Max - 1;
 
 template <int DQK, int DV>
-__global__ __launch_bounds__(256, 2) void attn_fwd_bf16_kernel(JaggedArgs ja, Tensors t,
-                                                               uint16_t* __restrict__ out,
-                                                               const WorkItem* __restrict__ items,
-                                                               const int32_t* __restrict__ count) {
-  constexpr int BM = kFwdBM, BN = kFwdBN;
-  constexpr int K_LD = DQK + 8;   // LDS row pitch of the K tile (bf16 elements)
-  constexpr int V_LD = DV + 8;    // LDS row pitch of the V tile
-  constexpr int NWIN = BM + BN;   // rab_pos slice per tile (BM + BN - 1 used)
+struct FwdShared {
+  static constexpr int BM = kFwdBM, BN = kFwdBN;
+  static constexpr int K_LD = DQK + 8;   // LDS row pitch of the K tile (bf16 elements)
+  static constexpr int V_LD = DV + 8;    // LDS row pitch of the V tile
+  static constexpr int NWIN = BM + BN;   // rab_pos slice per tile (BM + BN - 1 used)
+  __align__(16) uint16_t sK[BN * K_LD];
+  __align__(16) uint16_t sV[BN * V_LD];
+  __align__(16) uint32_t sTj[BN];  // key timestamps, rebased (fast path)
+  int64_t sTj64[BN];               // key timestamps (exact path)
+  float sWin[NWIN];
+  float sTab[64];
+  int64_t sRed[2][4];
+};
+
+// Slot of t_i - t_j: 32-bit rebased form on the fast path, exact 64-bit otherwise.
+template <bool FAST>
+__device__ __forceinline__ int slot_of(uint32_t ri, uint32_t rj, int64_t ti, int64_t tj) {
+  if constexpr (FAST)
+    return slot32(ri, rj);
+  else
+    return slot64(ti - tj);
+}
+
+template <int DQK, int DV, bool FAST>
+__device__ __forceinline__ void fwd_item(FwdShared<DQK, DV>& sm, const JaggedArgs& ja,
+                                         const Tensors& t, uint16_t* __restrict__ out, int64_t o,
+                                         int L, int n_h, int i0, int head, int64_t tbase) {
+  using Sh = FwdShared<DQK, DV>;
+  constexpr int BM = Sh::BM, BN = Sh::BN, K_LD = Sh::K_LD, V_LD = Sh::V_LD, NWIN = Sh::NWIN;
   constexpr int KCH = BN * DQK / 8, VCH = BN * DV / 8;
   constexpr int KPT = (KCH + 255) / 256, VPT = (VCH + 255) / 256;
   static_assert(BN == 32, "one 32x32 score block per wave and tile");
-
-  __shared__ __align__(16) uint16_t sK[BN * K_LD];
-  __shared__ __align__(16) uint16_t sV[BN * V_LD];
-  __shared__ __align__(16) uint32_t sTj[BN];
-  __shared__ int64_t sTj64[BN];
-  __shared__ float sWin[NWIN];
-  __shared__ float sTab[64];
-  __shared__ int64_t sRed[2][4];
-
-  if ((int)blockIdx.x >= *count) return;
-  const WorkItem it = items[blockIdx.x];
-  const int head = blockIdx.y;
-  const int H = ja.num_heads, N = ja.max_seq_len, NB = ja.num_buckets;
-  const int64_t o = ja.seq_offsets[it.seq];
-  const int L = (int)(ja.seq_offsets[it.seq + 1] - o);
-  const int n_h = L - (ja.num_targets ? (int)ja.num_targets[it.seq] : 0);
-  const int i0 = it.blk * BM;
+  const int H = ja.num_heads, N = ja.max_seq_len;
   const int rows_end = min(i0 + BM, L);
-
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
   const int col = lane & 31, half = lane >> 5;
   const int iw0 = i0 + wave * 32;
@@ -70,25 +74,9 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_bf16_kernel(JaggedArgs ja, Te
   const bool row_ok = my_i < L;
   const int wave_last = min(iw0 + 31, L - 1);
   const int64_t* __restrict__ ts = ja.timestamps + o;
-
   const uint16_t* __restrict__ qg = (const uint16_t*)t.q;
   const uint16_t* __restrict__ kg = (const uint16_t*)t.k;
   const uint16_t* __restrict__ vg = (const uint16_t*)t.v;
-
-  // Timestamp extremes over the tokens this item touches, [0, rows_end).
-  int64_t tlo = kI64Max, thi = kI64Min;
-  for (int x = tid; x < rows_end; x += 256) {
-    const int64_t v = ts[x];
-    tlo = v < tlo ? v : tlo;
-    thi = v > thi ? v : thi;
-  }
-  tlo = wave_min_i64(tlo);
-  thi = wave_max_i64(thi);
-  if (lane == 0) {
-    sRed[0][wave] = tlo;
-    sRed[1][wave] = thi;
-  }
-  for (int x = tid; x < 64; x += 256) sTab[x] = ja.rab_time[min(63 - x, NB - 1)];
 
   // Q fragment: B operand of S^T = K Q^T (lane = query row, 8 d's per step).
   u32x4 qf[DQK / 16];
@@ -97,16 +85,6 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_bf16_kernel(JaggedArgs ja, Te
     qf[s] = row_ok ? *reinterpret_cast<const u32x4*>(qg + (o + my_i) * t.q_stride + head * DQK +
                                                      16 * s + 8 * half)
                    : zero_u32x4();
-  __syncthreads();
-  tlo = sRed[0][0];
-  thi = sRed[1][0];
-#pragma unroll
-  for (int w = 1; w < 4; w++) {
-    tlo = sRed[0][w] < tlo ? sRed[0][w] : tlo;
-    thi = sRed[1][w] > thi ? sRed[1][w] : thi;
-  }
-  const bool fast = (thi - tlo) < ((int64_t)1 << 31);
-  const int64_t tbase = tlo;
   const int64_t ti64 = row_ok ? ts[my_i] : tbase;
   const uint32_t tir = (uint32_t)(ti64 - tbase);
   const int pi = bias_pos(my_i, n_h);
@@ -172,18 +150,20 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_bf16_kernel(JaggedArgs ja, Te
 #pragma unroll
     for (int k = 0; k < KPT; k++) {
       const int c = tid + 256 * k;
-      if (c < KCH) *reinterpret_cast<u32x4*>(sK + (c / (DQK / 8)) * K_LD + (c % (DQK / 8)) * 8) = pk[k];
+      if (c < KCH) *reinterpret_cast<u32x4*>(sm.sK + (c / (DQK / 8)) * K_LD + (c % (DQK / 8)) * 8) = pk[k];
     }
 #pragma unroll
     for (int k = 0; k < VPT; k++) {
       const int c = tid + 256 * k;
-      if (c < VCH) *reinterpret_cast<u32x4*>(sV + (c / (DV / 8)) * V_LD + (c % (DV / 8)) * 8) = pv[k];
+      if (c < VCH) *reinterpret_cast<u32x4*>(sm.sV + (c / (DV / 8)) * V_LD + (c % (DV / 8)) * 8) = pv[k];
     }
     if (tid < BN) {
-      sTj64[tid] = pt;
-      sTj[tid] = (uint32_t)(pt - tbase);
+      if constexpr (FAST)
+        sm.sTj[tid] = (uint32_t)(pt - tbase);
+      else
+        sm.sTj64[tid] = pt;
     }
-    if (tid < NWIN) sWin[tid] = pw;
+    if (tid < NWIN) sm.sWin[tid] = pw;
     __syncthreads();
     if (kn < kend) prefetch(kn);
 
@@ -200,8 +180,8 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_bf16_kernel(JaggedArgs ja, Te
 #pragma unroll
         for (int q = 0; q < 16; q++) {
           const int jl = 8 * (q >> 2) + 4 * half + (q & 3);
-          const int s = fast ? slot32(tir, sTj[jl]) : slot64(ti64 - sTj64[jl]);
-          sacc[q] = sWin[xb + 8 * (q >> 2) + (q & 3)] + sTab[s];
+          const int s = slot_of<FAST>(tir, sm.sTj[jl], ti64, sm.sTj64[jl]);
+          sacc[q] = sm.sWin[xb + 8 * (q >> 2) + (q & 3)] + sm.sTab[s];
         }
       } else {
         vmask = 0;
@@ -212,8 +192,8 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_bf16_kernel(JaggedArgs ja, Te
           float b = 0.0f;
           if (row_ok && j < L && pair_valid(my_i, j, n_h)) {
             const int x = (N - 1) + bias_pos(j, n_h) - pi - pos_base;
-            const int s = fast ? slot32(tir, sTj[jl]) : slot64(ti64 - sTj64[jl]);
-            b = sWin[x] + sTab[s];
+            const int s = slot_of<FAST>(tir, sm.sTj[jl], ti64, sm.sTj64[jl]);
+            b = sm.sWin[x] + sm.sTab[s];
             vmask |= 1u << q;
           }
           sacc[q] = b;
@@ -221,7 +201,7 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_bf16_kernel(JaggedArgs ja, Te
       }
 #pragma unroll
       for (int s = 0; s < DQK / 16; s++) {
-        u32x4 kf = *reinterpret_cast<const u32x4*>(sK + col * K_LD + 16 * s + 8 * half);
+        u32x4 kf = *reinterpret_cast<const u32x4*>(sm.sK + col * K_LD + 16 * s + 8 * half);
         sacc = mfma32x32x16(as_bf16x8(kf), as_bf16x8(qf[s]), sacc);
       }
       float p[16];
@@ -240,7 +220,7 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_bf16_kernel(JaggedArgs ja, Te
         const int row = 16 * st + tr_row;
 #pragma unroll
         for (int nb = 0; nb < DV / 32; nb++) {
-          const uint16_t* base = sV + row * V_LD + 32 * nb + tr_col;
+          const uint16_t* base = sm.sV + row * V_LD + 32 * nb + tr_col;
           const uint2 lo = lds_read_tr16(base), hi = lds_read_tr16(base + 8 * V_LD);
           u32x4 vb = {lo.x, lo.y, hi.x, hi.y};
           oacc[nb] = mfma32x32x16(as_bf16x8(pa), as_bf16x8(vb), oacc[nb]);
@@ -260,6 +240,54 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_bf16_kernel(JaggedArgs ja, Te
       const int i = iw0 + 8 * (q >> 2) + 4 * half + (q & 3);
       if (i < L) og[(int64_t)i * H * DV + 32 * nb + col] = f32_to_bf16_bits(oacc[nb][q] * invN);
     }
+}
+
+template <int DQK, int DV>
+__global__ __launch_bounds__(256, 2) void attn_fwd_bf16_kernel(JaggedArgs ja, Tensors t,
+                                                               uint16_t* __restrict__ out,
+                                                               const WorkItem* __restrict__ items,
+                                                               const int32_t* __restrict__ count) {
+  using Sh = FwdShared<DQK, DV>;
+  __shared__ Sh sm;
+  if ((int)blockIdx.x >= *count) return;
+  const WorkItem it = items[blockIdx.x];
+  const int head = blockIdx.y;
+  const int NB = ja.num_buckets;
+  const int64_t o = ja.seq_offsets[it.seq];
+  const int L = (int)(ja.seq_offsets[it.seq + 1] - o);
+  const int n_h = L - (ja.num_targets ? (int)ja.num_targets[it.seq] : 0);
+  const int i0 = it.blk * Sh::BM;
+  const int rows_end = min(i0 + Sh::BM, L);
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  const int64_t* __restrict__ ts = ja.timestamps + o;
+
+  // Timestamp extremes over the tokens this item touches, [0, rows_end):
+  // the 32-bit fast path applies when they span less than 2^31.
+  int64_t tlo = kI64Max, thi = kI64Min;
+  for (int x = tid; x < rows_end; x += 256) {
+    const int64_t v = ts[x];
+    tlo = v < tlo ? v : tlo;
+    thi = v > thi ? v : thi;
+  }
+  tlo = wave_min_i64(tlo);
+  thi = wave_max_i64(thi);
+  if (lane == 0) {
+    sm.sRed[0][wave] = tlo;
+    sm.sRed[1][wave] = thi;
+  }
+  for (int x = tid; x < 64; x += 256) sm.sTab[x] = ja.rab_time[min(63 - x, NB - 1)];
+  __syncthreads();
+  tlo = sm.sRed[0][0];
+  thi = sm.sRed[1][0];
+#pragma unroll
+  for (int w = 1; w < 4; w++) {
+    tlo = sm.sRed[0][w] < tlo ? sm.sRed[0][w] : tlo;
+    thi = sm.sRed[1][w] > thi ? sm.sRed[1][w] : thi;
+  }
+  if (thi - tlo < ((int64_t)1 << 31))
+    fwd_item<DQK, DV, true>(sm, ja, t, out, o, L, n_h, i0, head, tlo);
+  else
+    fwd_item<DQK, DV, false>(sm, ja, t, out, o, L, n_h, i0, head, tlo);
 }
 
 template <int DQK, int DV>

@@ -37,7 +37,7 @@ constexpr int kFwdBM = 128;  // query rows per forward workgroup
 constexpr int kFwdBN = 32;   // keys per forward step
 constexpr int kBwdBN = 128;  // keys owned by a backward workgroup
 constexpr int kBwdBM = 32;   // query rows per backward step
-constexpr int kBwdMaxLdsPos = 16384;  // bias-position gradient kept in LDS up to this N
+constexpr size_t kLdsBytes = 160 * 1024;  // LDS a gfx950 workgroup may allocate
 
 // Upper bound on the number of (sequence, block) work items for blocks of
 // `blk` tokens: sum_b ceil(L_b / blk) <= ceil(T / blk) + B.

@@ -62,6 +62,8 @@ SMALL = [
     ((130, 77), 2, 128, 64, 160, None),
     ((250, 190, 64), 2, 128, 128, 256, (70, 190, 1)),   # target-aware, incl. all-candidate
     ((129, 128, 127), 1, 64, 64, 129, (3, 0, 127)),
+    # N too large for the backward's LDS position accumulator: global-atomic path
+    ((300, 100), 1, 128, 128, 12000, None),
 ]
 
 
@@ -71,6 +73,21 @@ def test_small_parity(hs, oracle_mod, dtype, case):
     lengths, h, dqk, dv, N, nt = SMALL[case]
     batch = inputs.make_batch(3, seed=100 + case, lengths=lengths, num_heads=h, d_qk=dqk, d_v=dv,
                               max_seq_len=N, dtype=dtype, num_targets=nt)
+    _check_fwd(hs, oracle_mod, batch)
+    _check_bwd(hs, oracle_mod, batch)
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+def test_small_parity_wide_timestamps(hs, oracle_mod, dtype):
+    """Timestamps spanning more than 2^31 (and unsorted within a sequence):
+    the exact 64-bit time-bucket path of the kernels."""
+    rng = np.random.default_rng(17)
+    lengths = (200, 77, 130)
+    T = sum(lengths)
+    ts = rng.integers(0, 1 << 60, size=T)
+    ts[200:277] = np.sort(ts[200:277])
+    batch = inputs.make_batch(3, seed=31, lengths=lengths, num_heads=2, d_qk=64, d_v=64,
+                              max_seq_len=256, dtype=dtype, timestamps=ts)
     _check_fwd(hs, oracle_mod, batch)
     _check_bwd(hs, oracle_mod, batch)
 
