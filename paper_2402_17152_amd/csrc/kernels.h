@@ -35,7 +35,7 @@ struct Tensors {
 // Tile sizes of the bf16 MFMA kernels.
 constexpr int kFwdBM = 128;  // query rows per forward workgroup
 constexpr int kFwdBN = 32;   // keys per forward step
-constexpr int kBwdBN = 128;  // keys owned by a backward workgroup
+constexpr int kBwdBN = 128;  // keys owned by a backward workgroup (8 waves x 16)
 constexpr int kBwdBM = 32;   // query rows per backward step
 constexpr size_t kLdsBytes = 160 * 1024;  // LDS a gfx950 workgroup may allocate
 
