@@ -32,7 +32,9 @@
  *            of one fused projection output [U | V | Q | K] (notation
  *            table, entry Split).  Outputs are dense [T][h][d].
  *            Every Q/K/V/U/O/dO pointer is 16-byte aligned and every
- *            stride a multiple of 16 bytes.
+ *            stride a multiple of 16 bytes; max_seq_len rows of any
+ *            input span at most 2 GiB (max_seq_len * stride * element
+ *            size <= 2^31, else HSTU_ERR_UNSUPPORTED).
  *   Streams  all work is enqueued on hip_stream (a hipStream_t, NULL =
  *            the null stream) and the call returns before it completes.
  *            Only hstu_validate synchronises.

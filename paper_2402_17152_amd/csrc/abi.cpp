@@ -116,6 +116,9 @@ hstu_status_t check_rows(const hstu_problem_t* p, const char* name, const void* 
                 (long long)stride, (long long)width);
   if ((stride * (int64_t)elem_size(p)) % 16)
     return fail(HSTU_ERR_INVALID_ARGUMENT, "%s_stride must be a multiple of 16 bytes", name);
+  // The kernels address one sequence of a tensor with 32-bit byte offsets.
+  if ((int64_t)p->max_seq_len * stride * (int64_t)elem_size(p) > ((int64_t)1 << 31))
+    return fail(HSTU_ERR_UNSUPPORTED, "max_seq_len rows of %s span more than 2 GiB", name);
   return HSTU_OK;
 }
 

@@ -80,6 +80,57 @@ __device__ __forceinline__ uint16_t f32_to_bf16_bits(float x) {
   return __builtin_bit_cast(uint16_t, (__bf16)x);
 }
 
+// Raw buffer resource over `bytes` bytes from `base` (stride 0, 32-bit
+// data format word of gfx9-family parts).  Loads whose byte offset lies at
+// or past `bytes` return zeros instead of touching memory.
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* base, uint32_t bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)bytes,
+                                           0x00020000);
+}
+
+__device__ __forceinline__ u32x4 buffer_load16(__amdgpu_buffer_rsrc_t r, uint32_t byte_off) {
+  return __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(r, byte_off, 0, 0));
+}
+
+__device__ __forceinline__ uint64_t buffer_load8(__amdgpu_buffer_rsrc_t r, uint32_t byte_off) {
+  return __builtin_bit_cast(uint64_t, __builtin_amdgcn_raw_buffer_load_b64(r, byte_off, 0, 0));
+}
+
+__device__ __forceinline__ uint32_t buffer_load4(__amdgpu_buffer_rsrc_t r, uint32_t byte_off) {
+  return __builtin_amdgcn_raw_buffer_load_b32(r, byte_off, 0, 0);
+}
+
+// LDS DMA: each of the 64 lanes loads `size` bytes at byte offset `off`
+// of the buffer and the wave writes them to LDS at lds + size * lane.
+// Completion is counted by vmcnt, like any buffer load.
+__device__ __forceinline__ void dma_to_lds16(__amdgpu_buffer_rsrc_t r, void* lds, uint32_t off) {
+  __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (__attribute__((address_space(3))) void*)lds, 16,
+                                           off, 0, 0, 0);
+}
+
+__device__ __forceinline__ void dma_to_lds4(__amdgpu_buffer_rsrc_t r, void* lds, uint32_t off) {
+  __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (__attribute__((address_space(3))) void*)lds, 4,
+                                           off, 0, 0, 0);
+}
+
+// s_waitcnt vmcnt(VM) lgkmcnt(0) (gfx9 encoding: vmcnt in bits 3:0 and
+// 15:14, expcnt in 6:4, lgkmcnt in 11:8).
+template <int VM>
+__device__ __forceinline__ void wait_vmcnt_lgkmcnt0() {
+  static_assert(VM >= 0 && VM < 64, "vmcnt is 6 bits");
+  __builtin_amdgcn_s_waitcnt((VM & 15) | ((VM >> 4) << 14) | (7 << 4));
+}
+
+// Workgroup barrier without __syncthreads' memory fence (which would wait
+// for every outstanding LDS-DMA load).  The caller waits for what must be
+// visible; the empty asm statements keep the compiler from moving memory
+// accesses across the barrier.
+__device__ __forceinline__ void barrier_no_fence() {
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
+}
+
 // Position of row index `r` (0..31) inside a 32-wide LDS strip whose
 // contraction order matches the 32x32 MFMA accumulator layout: an
 // accumulator lane holds rows 8*g + 4*half + m (g = 0..3, m = 0..3) and
