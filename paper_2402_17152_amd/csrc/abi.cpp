@@ -138,6 +138,7 @@ struct Layout {
   size_t counts;    // int32 [2]: forward and backward item counts
   size_t fwd_items;
   size_t bwd_items;
+  size_t trange;    // int64 [2B]: per-sequence timestamp min / max
   size_t dq_acc;    // fp32 [T][h][d_qk] (bf16 problems)
   size_t total;
   int64_t max_fwd, max_bwd;
@@ -154,6 +155,8 @@ Layout layout(const hstu_problem_t* p) {
   off = align_up(off + sizeof(WorkItem) * (size_t)l.max_fwd);
   l.bwd_items = off;
   off = align_up(off + sizeof(WorkItem) * (size_t)l.max_bwd);
+  l.trange = off;
+  off = align_up(off + 2 * sizeof(int64_t) * (size_t)p->num_seqs);
   l.dq_acc = off;
   if (p->dtype == HSTU_BF16)
     off = align_up(off + sizeof(float) * (size_t)p->total_tokens * p->num_heads * p->d_qk);
@@ -177,6 +180,7 @@ JaggedArgs make_args(const hstu_problem_t* p, const hstu_jagged_t* j) {
   a.num_targets = j->num_targets;
   a.rab_pos = j->rab_pos;
   a.rab_time = j->rab_time;
+  a.seq_trange = nullptr;
   a.num_seqs = p->num_seqs;
   a.max_seq_len = p->max_seq_len;
   a.num_heads = p->num_heads;
@@ -219,6 +223,8 @@ hstu_status_t attn_fwd_impl(const hstu_problem_t* p, const hstu_jagged_t* j, con
   }
   int32_t* counts = (int32_t*)(w + l.counts);
   WorkItem* items = (WorkItem*)(w + l.fwd_items);
+  ja.seq_trange = (const int64_t*)(w + l.trange);
+  HSTU_HIP(launch_seq_time_range(ja, (int64_t*)(w + l.trange), s), "time range launch");
   HSTU_HIP(launch_schedule(ja, 0, items, counts, s), "schedule launch");
   TimedScope ts("attn_fwd", s);
   HSTU_HIP(launch_attn_fwd_bf16(ja, t, p->d_qk, p->d_v, out, items, counts, l.max_fwd, s),
@@ -296,6 +302,8 @@ hstu_status_t hstu_attn_bwd(const hstu_problem_t* p, const hstu_jagged_t* j, con
     float* dq_acc = (float*)(w + l.dq_acc);
     const int64_t ndq = T * H * p->d_qk;
     HSTU_HIP(launch_fill_f32(dq_acc, ndq, 0.0f, s), "fill launch");
+    ja.seq_trange = (const int64_t*)(w + l.trange);
+    HSTU_HIP(launch_seq_time_range(ja, (int64_t*)(w + l.trange), s), "time range launch");
     HSTU_HIP(launch_schedule(ja, 1, items, counts + 1, s), "schedule launch");
     {
       TimedScope ts("attn_bwd", s);

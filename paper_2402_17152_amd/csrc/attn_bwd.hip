@@ -1,40 +1,45 @@
 // Fused jagged pointwise-attention backward, bf16 MFMA (gfx950).
 //
 // Gradients of <O, dO> for O = (1/N) SiLU(Q K^T + rab) V (Eq. 2).  As the
-// paper's Appendix G describes, attention and the relative bias are
-// recomputed rather than stored, and the bias gradients are accumulated
-// on chip before they reach HBM.  Pointwise aggregation means no row
-// statistics are needed: with S = Q K^T + rab,
+// paper's appendix on the fused kernels describes, attention and the
+// relative bias are recomputed rather than stored, and the bias gradients
+// are accumulated on chip before they reach HBM.  Pointwise aggregation
+// means no row statistics are needed: with S = Q K^T + rab,
 //   P  = SiLU(S) (masked),            dV = (1/N) P^T dO
 //   dP = dO V^T,  dS = dP SiLU'(S) (masked)
 //   dK = (1/N) dS^T Q,  dQ = (1/N) dS K
 //   d rab_pos[(N-1)+p(j)-p(i)] += dS/N,  d rab_time[bkt] += dS/N.
 //
-// Workgroup = 8 waves = one (sequence, 128-key block, head) work item;
-// two waves share each SIMD so one wave's MFMA work overlaps the other's
-// SiLU and bias arithmetic.  Wave w owns keys j0 + 16w .. +15: their K and
-// V sit in registers as MFMA operands and their dK, dV accumulate in
-// registers (64 per lane at d = 128) for the whole item.  The workgroup
-// walks query steps of 32 rows; each step's Q and dO rows are staged
-// row-major in LDS (prefetched into registers during the previous step).
-// Per step and wave, on v_mfma_f32_16x16x32_bf16:
-//   S  = Q K^T (accumulator seeded with the bias), dP = dO V^T: two 16-row
-//        blocks each, lane = key, 4 rows per block in registers;
-//   dV += P^T dO and dK += dS^T Q straight from those registers, the
-//        contraction order permuted to the accumulator's rows and the
-//        Q / dO operand fetched with transposing LDS reads in that order;
-//   dS -> LDS (bf16 for dQ, fp32 for the bias gradients); then each wave
-//        forms its 16x16 blocks of dQ(step) = dS K over the 128 keys and
-//        adds them to an fp32 workspace with float atomics.
-// Bias gradients (no per-element atomics):
-//   time table: per wave and step the slot range of the tile is bounded
-//        from timestamp extremes (usually one slot away from the
-//        diagonal); dS is summed per slot, reduced across the wave and
-//        added to the wave's LDS row;
-//   position table: pairs of threads own the 159 diagonals of the 32x128
-//        fp32 dS tile and add their sums to an LDS array indexed by
-//        p(i) - p(j).
-// Both are flushed with one global atomic per touched entry at the end.
+// Workgroup = 4 waves, one per SIMD, = one (sequence, 128-key block,
+// head) work item.  Wave w owns keys j0 + 32w .. +31: their K and V sit in
+// registers as MFMA operands and their dK, dV accumulate in registers for
+// the whole item (one wave per SIMD leaves room for all of it).  Owning 32
+// keys per wave halves the LDS traffic of the step tiles per MFMA compared
+// with 16.  The workgroup walks query steps of 32 rows; per step and wave,
+// on v_mfma_f32_32x32x16_bf16:
+//   S  = Q K^T (accumulator seeded with the bias), dP = dO V^T: lane = key,
+//        16 rows in registers;
+//   dV += P^T dO and dK += dS^T Q straight from those registers (the
+//        contraction order permuted to the accumulator rows, dO / Q read
+//        with transposing LDS loads in that order);
+//   dS^T -> LDS; one step later each wave forms its 32-column block of
+//        dQ = dS K over the block's keys and adds it to an fp32 workspace
+//        with float atomics.
+// The step is software-pipelined: S and dP of step u+1 are issued while
+// step u goes through SiLU'.  Step tiles (Q, dO, timestamps, rab_pos
+// window) arrive by LDS DMA several steps ahead.
+// Bias gradients, without per-element atomics on full tiles:
+//   time table: a (wave, step) tile whose |t_i - t_j| fall in one or two
+//        log2 buckets adds its dS sum to a running per-lane sum (flushed
+//        when the bucket changes);
+//   position table: history pairs of a full tile lie on 63 diagonals;
+//        rotating register q of every lane by its row offset (ds_bpermute)
+//        puts all of a lane's values on one diagonal (or the next one
+//        after wrapping), which is carried into the next step.
+// Other tiles (diagonal, ragged, candidates, 64-bit timestamps) evaluate
+// each pair and use LDS atomics.
+#include <type_traits>
+
 #include "bias.h"
 #include "kernels.h"
 
@@ -44,28 +49,57 @@ namespace {
 
 constexpr int64_t kI64Max = 0x7fffffffffffffffll;
 constexpr int64_t kI64Min = -kI64Max - 1;
-constexpr int kBwdThreads = 512;
+constexpr int kBwdThreads = 256;
 constexpr int kBwdWaves = kBwdThreads / 64;
+// Bias of a masked pair: SiLU and SiLU' of x ~ -1e30 are exactly -0.
+constexpr float kMaskedBias = -1.0e30f;
+
+// Step tile of 32 rows x D features (Q or dO), read two ways: 16-byte row
+// chunks (MFMA A operand, 8 lanes = rows 0..7 per LDS cycle) and 8-byte
+// transposing loads (B operand, 16 lanes = 4 rows x 2 chunks x 2 halves).
+// For D >= 64 the row is unpadded and chunk c of row r sits at chunk
+// c ^ swz(r), which spreads both patterns over all banks; for D = 32 rows
+// carry one pad chunk.
+template <int D>
+struct StepTile {
+  static constexpr int CPR = D / 8;                  // data chunks per row
+  static constexpr bool SWZ = D >= 64;
+  static constexpr int PC = SWZ ? CPR : CPR + 1;     // chunks per row
+  static constexpr int RB = PC * 16;                 // row bytes
+  static constexpr int OPS = (32 * PC + 63) / 64;    // 1 KB DMA operations per tile
+  static constexpr int OPW = (OPS + 3) / 4;          // per wave
+  static constexpr int BYTES = OPS * 1024;
+  __device__ static int swz(int r) { return SWZ ? 2 * (r & 3) + ((r >> 2) & 1) : 0; }
+};
 
 template <int DQK, int DV>
 struct BwdShared {
+  using QT = StepTile<DQK>;
+  using OT = StepTile<DV>;
   static constexpr int BN = kBwdBN, BM = kBwdBM;
-  static constexpr int Q_LD = DQK + 8, DO_LD = DV + 8;  // row-major step tiles
-  static constexpr int DS_LD = BN + 8, DS32_LD = BN + 1;
-  static constexpr int K_LD = DQK + 8;                   // the block's keys, row-major
-  static constexpr int NWIN = BM + BN;                   // reversed rab_pos window
-  __align__(16) uint16_t sQ[BM * Q_LD];
-  __align__(16) uint16_t sdO[BM * DO_LD];
-  __align__(16) uint16_t sdS[BM * DS_LD];
-  __align__(16) uint16_t sK[BN * K_LD];
-  float sdS32[BM * DS32_LD];         // dS in fp32 for the bias-table gradients
-  __align__(16) uint32_t sTr[BM];    // step row timestamps, rebased (fast path)
-  int64_t sTr64[BM];                 // step row timestamps (exact path)
-  float sWin[NWIN];
-  float sTab[64];                    // rab_time by slot
-  float sTacc[kBwdWaves][64];        // per-wave time-gradient sums by slot
-  int64_t sRange[2];                 // extremes of the step's row timestamps
-  int64_t sRed[2][kBwdWaves];
+  // dS^T tile [128 keys][32 rows] bf16: pitch 96 bytes makes the
+  // transposing reads of the dQ step conflict free.
+  static constexpr int DST_LD = 48;
+  // The block's K, row-major, staged once per item to build the dQ
+  // operand (pitch 8 dwords mod 32 banks for transposing reads).
+  static constexpr int KB_LD = DQK + 16;
+  static constexpr int NWIN = BM + BN;  // reversed rab_pos window (BM + BN - 1 used)
+  static constexpr int kWinPad = 4, WIN_LD = 264;
+  union Ring {
+    struct {
+      __align__(16) uint8_t q[4][QT::BYTES];
+      __align__(16) uint8_t dO[4][OT::BYTES];
+    } t;
+    __align__(16) uint16_t kblk[BN * KB_LD];  // prologue only
+  };
+  Ring ring;
+  __align__(16) uint16_t sdST[2][BN * DST_LD];
+  __align__(16) float sWin[4][4][WIN_LD];  // copy c holds window[k + c] at kWinPad + k
+  __align__(16) uint32_t sT[8][64];        // step row timestamps (32 int64)
+  __align__(16) uint32_t sTr[8][32];       // the same rebased (fast path)
+  uint32_t sRr[4][2];                      // rebased row timestamp min / max per step
+  float sTab[64];                          // rab_time by slot (bias.h)
+  float sTacc[64];                         // time-table gradient by slot
 };
 
 struct BwdArgs {
@@ -80,384 +114,595 @@ struct BwdArgs {
   int pos_in_lds;
 };
 
-// Slot of t_i - t_j: 32-bit rebased form on the fast path, exact 64-bit otherwise.
-template <bool FAST>
-__device__ __forceinline__ int slot_of(uint32_t ri, uint32_t rj, int64_t ti, int64_t tj) {
-  if constexpr (FAST)
-    return slot32(ri, rj);
-  else
-    return slot64(ti - tj);
+__device__ __forceinline__ float silu_sigma(float x) {
+  return __builtin_amdgcn_rcpf(1.0f + __builtin_amdgcn_exp2f(x * -kLog2e));
 }
 
 template <int DQK, int DV, bool FAST>
-__device__ __forceinline__ void bwd_item(BwdShared<DQK, DV>& sm, float* __restrict__ sPosAcc,
+__device__ __forceinline__ void bwd_item(BwdShared<DQK, DV>& sm, float* __restrict__ sPos,
                                          const BwdArgs& A, int64_t o, int L, int n_h, int j0,
                                          int head, int64_t tbase) {
-  using S = BwdShared<DQK, DV>;
-  constexpr int BN = S::BN, BM = S::BM, Q_LD = S::Q_LD, DO_LD = S::DO_LD, DS_LD = S::DS_LD,
-                DS32_LD = S::DS32_LD, K_LD = S::K_LD, NWIN = S::NWIN;
-  constexpr int QCH = BM * DQK / 8, OCH = BM * DV / 8;
-  constexpr int QPT = (QCH + kBwdThreads - 1) / kBwdThreads;
-  constexpr int OPT = (OCH + kBwdThreads - 1) / kBwdThreads;
+  using Sh = BwdShared<DQK, DV>;
+  using QT = typename Sh::QT;
+  using OT = typename Sh::OT;
+  constexpr int BN = Sh::BN, BM = Sh::BM, DST_LD = Sh::DST_LD, KB_LD = Sh::KB_LD;
+  static_assert(BN == 128 && BM == 32, "4 waves x 32 keys, 32-row steps");
   const JaggedArgs& ja = A.ja;
-  const int H = ja.num_heads, N = ja.max_seq_len, NB = ja.num_buckets;
-  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
-  const int c16 = lane & 15, kg = lane >> 4;
-  const int jw0 = j0 + 16 * wave;
-  const int my_j = jw0 + c16;
+  const int H = ja.num_heads, N = ja.max_seq_len;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int col = lane & 31, half = lane >> 5;
+  const int jw0 = j0 + 32 * wave;  // the wave's first key
+  const int my_j = jw0 + col;       // the lane's key (column of S and dP)
   const bool key_ok = my_j < L;
   const int pj = bias_pos(my_j, n_h);
-  const float invN = 1.0f / (float)N;
   const int64_t* __restrict__ ts = ja.timestamps + o;
-  const uint16_t* __restrict__ qg = (const uint16_t*)A.t.q + (o * A.t.q_stride + head * DQK);
+  const uint16_t* __restrict__ kg = (const uint16_t*)A.t.k + o * A.t.k_stride + head * DQK;
+  const uint16_t* __restrict__ vg = (const uint16_t*)A.t.v + o * A.t.v_stride + head * DV;
+  const uint16_t* __restrict__ qg = (const uint16_t*)A.t.q + o * A.t.q_stride + head * DQK;
   const uint16_t* __restrict__ dog = A.dO + (o * H + head) * DV;
-  const uint16_t* __restrict__ kg_ = (const uint16_t*)A.t.k;
-  const uint16_t* __restrict__ vg_ = (const uint16_t*)A.t.v;
-  const int R = L - j0;  // p(i) - p(j) of kept pairs lies in [0, R)
-
-  const int64_t tj64 = key_ok ? ts[my_j] : tbase;
-  const uint32_t tjr = (uint32_t)(tj64 - tbase);
-  const int64_t klo = wave_min_i64(key_ok ? tj64 : kI64Max);
-  const int64_t khi = wave_max_i64(key_ok ? tj64 : kI64Min);
-
-  // K, V of the wave's keys as B operands (lane = key, 8 features per step).
-  u32x4 kf[DQK / 32], vf[DV / 32];
-#pragma unroll
-  for (int s = 0; s < DQK / 32; s++)
-    kf[s] = key_ok ? *reinterpret_cast<const u32x4*>(kg_ + (o + my_j) * A.t.k_stride + head * DQK +
-                                                     32 * s + 8 * kg)
-                   : zero_u32x4();
-#pragma unroll
-  for (int s = 0; s < DV / 32; s++)
-    vf[s] = key_ok ? *reinterpret_cast<const u32x4*>(vg_ + (o + my_j) * A.t.v_stride + head * DV +
-                                                     32 * s + 8 * kg)
-                   : zero_u32x4();
-
-  // dV, dK accumulators: lane holds keys jw0 + 4kg + m (m = 0..3), feature 16cb + c16.
-  f32x4 dvacc[DV / 16], dkacc[DQK / 16];
-#pragma unroll
-  for (int cb = 0; cb < DV / 16; cb++) dvacc[cb] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
-#pragma unroll
-  for (int cb = 0; cb < DQK / 16; cb++) dkacc[cb] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
-
-  // Transposing reads (lds_read_tr16): lane 16g + r reads row (r >> 2) of
-  // the group's 4-row strip and 4 columns starting at 4*(r & 3).
-  const int tr_r = c16 >> 2, tr_c = 4 * (c16 & 3);
-
-  // Staging registers for the next step.
-  u32x4 pq[QPT], po[OPT];
-  int64_t pt = 0;
-  float pw = 0.0f;
+  const uint32_t kstride_b = (uint32_t)A.t.k_stride * 2u, vstride_b = (uint32_t)A.t.v_stride * 2u;
+  const uint32_t qstride_b = (uint32_t)A.t.q_stride * 2u, dostride_b = (uint32_t)(H * DV) * 2u;
+  const float invN = 1.0f / (float)N;
 
   // Candidate keys see only themselves; otherwise every later row sees them.
   const int i_end = j0 >= n_h ? min(j0 + BN, L) : L;
+  const int nsteps = (i_end - j0 + BM - 1) / BM;
+  auto row0 = [&](int u) { return j0 + BM * u; };
 
-  auto prefetch = [&](int i0) {
+  // ---- per-item operands held in registers ----
+  // K, V of the wave's keys: B operands of S = Q K^T and dP = dO V^T
+  // (lane = key, 8 features per 16-feature step).  Keys past the sequence
+  // end read as zeros.
+  const __amdgpu_buffer_rsrc_t krs = make_rsrc(kg, (uint32_t)(L * A.t.k_stride * 2));
+  const __amdgpu_buffer_rsrc_t vrs = make_rsrc(vg, (uint32_t)(L * A.t.v_stride * 2));
+  u32x4 kf[DQK / 16], vf[DV / 16];
 #pragma unroll
-    for (int k = 0; k < QPT; k++) {
-      const int c = tid + kBwdThreads * k;
-      if (c < QCH) {
-        const int r = c / (DQK / 8), cc = (c % (DQK / 8)) * 8, i = i0 + r;
-        pq[k] = i < L ? *reinterpret_cast<const u32x4*>(qg + (int64_t)i * A.t.q_stride + cc)
-                      : zero_u32x4();
-      }
-    }
+  for (int s = 0; s < DQK / 16; s++)
+    kf[s] = buffer_load16(krs, (uint32_t)my_j * kstride_b + (uint32_t)(16 * s + 8 * half) * 2u);
 #pragma unroll
-    for (int k = 0; k < OPT; k++) {
-      const int c = tid + kBwdThreads * k;
-      if (c < OCH) {
-        const int r = c / (DV / 8), cc = (c % (DV / 8)) * 8, i = i0 + r;
-        po[k] = i < L ? *reinterpret_cast<const u32x4*>(dog + (int64_t)i * H * DV + cc)
-                      : zero_u32x4();
-      }
+  for (int s = 0; s < DV / 16; s++)
+    vf[s] = buffer_load16(vrs, (uint32_t)my_j * vstride_b + (uint32_t)(16 * s + 8 * half) * 2u);
+
+  // dQ = dS K: the DQK/32 column blocks are shared by the 4 waves; with
+  // fewer blocks than waves, each wave of a block takes a share of keys.
+  constexpr int NCB = DQK / 32, WPB = kBwdWaves / NCB, KPW = BN / WPB, KSTEPS = KPW / 16;
+  const int cbw = wave / WPB, kbase = (wave % WPB) * KPW;
+  const int tr_row = 4 * half + ((lane & 15) >> 2);
+  const int tr_col = 16 * ((lane >> 4) & 1) + 4 * (lane & 3);
+  u32x4 kq[KSTEPS];
+  {
+    // Stage the block's K row-major, then read the operand down its rows.
+    constexpr int KCH = BN * DQK / 8;
+    for (int c = tid; c < KCH; c += kBwdThreads) {
+      const int r = c / (DQK / 8), cc = c % (DQK / 8);
+      *reinterpret_cast<u32x4*>(sm.ring.kblk + r * KB_LD + 8 * cc) =
+          buffer_load16(krs, (uint32_t)(j0 + r) * kstride_b + (uint32_t)cc * 16u);
     }
-    if (tid < BM) pt = (i0 + tid < L) ? ts[i0 + tid] : tbase;
-    if (tid >= 64 && tid < 64 + NWIN) {
-      // rab_pos entries reachable from (query step, key block), reversed.
-      const int x = tid - 64;
-      const int pos_base = (N - 1) + min(j0, n_h) - min(i0 + BM - 1, n_h);
-      const int g = pos_base + (NWIN - 1 - x);
-      pw = (g >= 0 && g <= 2 * N - 2) ? ja.rab_pos[g] : 0.0f;
+    __syncthreads();
+    const uint16_t* kp = sm.ring.kblk + (kbase + tr_row) * KB_LD + 32 * cbw + tr_col;
+#pragma unroll
+    for (int ks = 0; ks < KSTEPS; ks++) {
+      const uint2 lo = lds_read_tr16(kp + 16 * ks * KB_LD);
+      const uint2 hi = lds_read_tr16(kp + (16 * ks + 8) * KB_LD);
+      kq[ks] = u32x4{lo.x, lo.y, hi.x, hi.y};
+    }
+    __syncthreads();  // the ring may be overwritten from here on
+  }
+
+  // Key timestamps (fixed for the item) and the wave's key range.
+  const int64_t tj64 = key_ok ? ts[my_j] : tbase;
+  const uint32_t tjr = (uint32_t)(tj64 - tbase);
+  const uint32_t klo32 =
+      __builtin_amdgcn_readfirstlane((uint32_t)(wave_min_i64(key_ok ? tj64 : kI64Max) - tbase));
+  const uint32_t khi32 =
+      __builtin_amdgcn_readfirstlane((uint32_t)(wave_max_i64(key_ok ? tj64 : kI64Min) - tbase));
+
+  // dK, dV accumulators: lane holds (key jw0 + 8g + 4*half + m, feature 32nb + col).
+  f32x16 dkacc[DQK / 32], dvacc[DV / 32];
+#pragma unroll
+  for (int nb = 0; nb < DQK / 32; nb++)
+#pragma unroll
+    for (int q = 0; q < 16; q++) dkacc[nb][q] = 0.0f;
+#pragma unroll
+  for (int nb = 0; nb < DV / 32; nb++)
+#pragma unroll
+    for (int q = 0; q < 16; q++) dvacc[nb][q] = 0.0f;
+
+  // ---- step-tile addressing ----
+  // A-operand reads of row `col`, 16-byte chunk (2s + half).
+  auto a_base = [&](auto tile_tag, uint32_t (&ab)[4]) {
+    using T = decltype(tile_tag);
+    const int sw = T::swz(col);
+#pragma unroll
+    for (int k = 0; k < 4; k++)
+      ab[k] = (uint32_t)(col * T::RB + 16 * (half ^ (sw & 1)) + 32 * (k ^ (sw >> 1)));
+  };
+  auto a_off = [&](auto tile_tag, const uint32_t (&ab)[4], int s) -> uint32_t {
+    using T = decltype(tile_tag);
+    if constexpr (T::SWZ)
+      return ab[s & 3] + 128u * (uint32_t)(s >> 2);
+    else
+      return (uint32_t)(col * T::RB + 16 * (2 * s + half));
+  };
+  // Transposing reads: rows (16 st + tr_row [+8]), 4 columns at 32 nb + tr_col.
+  // The swizzle of those rows depends on tr_row only.
+  auto tr_base = [&](auto tile_tag, uint32_t (&tb)[2]) {
+    using T = decltype(tile_tag);
+    const int sw = T::swz(tr_row);
+    const int c1 = tr_col >> 3, off = (tr_col & 7) * 2;
+    const int b = tr_row * T::RB + 16 * (c1 ^ (sw & 3)) + off;
+    tb[0] = (uint32_t)(b + 64 * (sw >> 2));  // even 32-column blocks
+    tb[1] = (uint32_t)(b - 64 * (sw >> 2));  // odd
+  };
+  auto tr_off = [&](auto tile_tag, const uint32_t (&tb)[2], int st, int hi, int nb) -> uint32_t {
+    using T = decltype(tile_tag);
+    const int rows = (16 * st + 8 * hi) * T::RB;
+    if constexpr (T::SWZ)
+      return tb[nb & 1] + (uint32_t)(rows + 64 * nb);
+    else
+      return (uint32_t)(tr_row * T::RB + rows + 64 * nb + tr_col * 2);
+  };
+  uint32_t qa[4], oa[4], qt[2], ot[2];
+  a_base(QT{}, qa);
+  a_base(OT{}, oa);
+  tr_base(QT{}, qt);
+  tr_base(OT{}, ot);
+
+  // ---- staging: LDS DMA straight from global memory ----
+  // Q, dO and the rab_pos window of step u travel three steps ahead (ring
+  // of 4), row timestamps five (ring of 8).  Every wave issues the same
+  // number of vector-memory operations per step -- the DMA operations and
+  // the 16 dQ atomics (vmcnt counts both, in issue order; inside the loop
+  // every dQ step is a full one) -- so one vmcnt value before each barrier
+  // retires exactly the operations of two steps back.
+  constexpr int OPS_PER_STEP = QT::OPW + OT::OPW + 3 + 1 + 16;
+  const __amdgpu_buffer_rsrc_t qrs = make_rsrc(qg, (uint32_t)(L * A.t.q_stride * 2));
+  const __amdgpu_buffer_rsrc_t ors = make_rsrc(dog, (uint32_t)L * dostride_b);
+  const __amdgpu_buffer_rsrc_t trs = make_rsrc(ts, (uint32_t)L * 8u);
+  const __amdgpu_buffer_rsrc_t prs = make_rsrc(ja.rab_pos, (uint32_t)(2 * N - 1) * 4u);
+  // Lane offsets of this wave's tile operations: linear chunk g = 64 op +
+  // lane is row g / PC, stored chunk g % PC, holding logical chunk
+  // (g % PC) ^ swz(row) (pad chunks repeat chunk 0); operations past the
+  // tile's count repeat its last one.
+  uint32_t qoffs[QT::OPW], ooffs[OT::OPW];
+  auto tile_offs = [&](auto tile_tag, uint32_t* offs, uint32_t stride_b) {
+    using T = decltype(tile_tag);
+#pragma unroll
+    for (int k = 0; k < T::OPW; k++) {
+      const int op = min(wave * T::OPW + k, T::OPS - 1), g = 64 * op + lane;
+      const int r = g / T::PC, p = g % T::PC;
+      const int c = p < T::CPR ? (p ^ T::swz(r)) : 0;
+      offs[k] = (uint32_t)r * stride_b + (uint32_t)c * 16u;
+    }
+  };
+  tile_offs(QT{}, qoffs, qstride_b);
+  tile_offs(OT{}, ooffs, dostride_b);
+  auto issue_tiles = [&](int u) {
+    const int i0 = row0(u), slot = u & 3;
+#pragma unroll
+    for (int k = 0; k < QT::OPW; k++)
+      dma_to_lds16(qrs, sm.ring.t.q[slot] + 1024 * min(wave * QT::OPW + k, QT::OPS - 1),
+                   qoffs[k] + (uint32_t)i0 * qstride_b);
+#pragma unroll
+    for (int k = 0; k < OT::OPW; k++)
+      dma_to_lds16(ors, sm.ring.t.dO[slot] + 1024 * min(wave * OT::OPW + k, OT::OPS - 1),
+                   ooffs[k] + (uint32_t)i0 * dostride_b);
+  };
+  // Reversed rab_pos window of step u: W[y] = rab_pos[pb - y] with
+  // pb = (N-1) + min(j0 + 127, n_h) - min(i0, n_h), so that a pair's entry
+  // is y = (min(j0 + 127, n_h) - p(j)) + (p(i) - min(i0, n_h)) in [0, 158].
+  // Entries outside the table read as 0 and are never used by a valid pair.
+  const int Pk = min(j0 + BN - 1, n_h);
+  auto issue_win = [&](int u) {
+    const int pb = (N - 1) + Pk - min(row0(u), n_h);
+#pragma unroll
+    for (int k = 0; k < 3; k++) {
+      const int op = 3 * wave + k, c = op / 3, ch = op % 3;
+      dma_to_lds4(prs, &sm.sWin[u & 3][c][Sh::kWinPad + 64 * ch],
+                  (uint32_t)(pb - 64 * ch - lane - c) * 4u);
+    }
+  };
+  auto issue_ts = [&](int u) {
+    dma_to_lds4(trs, sm.sT[u & 7], (uint32_t)row0(u) * 8u + 4u * (uint32_t)lane);
+  };
+  // Wave 0: rebased row timestamps of a staged step and their range (zeros
+  // past the sequence end only enter steps that are never full).
+  auto reduce_ts = [&](int u) {
+    if constexpr (FAST) {
+      if (wave == 0) {
+        // Both halves hold the 32 values, so whole-wave extremes are theirs.
+        const uint32_t v = sm.sT[u & 7][2 * (lane & 31)] - (uint32_t)tbase;
+        const uint32_t lo = wave_min_dpp(v), hi = wave_max_dpp(v);
+        sm.sTr[u & 7][lane & 31] = v;
+        if (lane < 2) sm.sRr[u & 3][lane] = lane ? hi : lo;
+      }
     }
   };
 
-  prefetch(j0);
-
-  for (int i0 = j0; i0 < i_end; i0 += BM) {
-    __syncthreads();  // previous step's LDS tiles consumed
-#pragma unroll
-    for (int k = 0; k < QPT; k++) {
-      const int c = tid + kBwdThreads * k;
-      if (c < QCH) *reinterpret_cast<u32x4*>(sm.sQ + (c / (DQK / 8)) * Q_LD + (c % (DQK / 8)) * 8) = pq[k];
+  // ---- bias path of a (wave, step) tile ----
+  // Full: every key of the wave precedes every row and all rows are
+  // history rows, so every pair is valid with p(i) - p(j) = i - j.  A full
+  // tile whose |t_i - t_j| lie in one log2 bucket is "uniform"; one whose
+  // t_i all follow the t_j and span two adjacent buckets b, b+1 is "two"
+  // (t_i >= t_j + 2^(b+1) selects b+1); everything else is "general".
+  enum { kUniform = 0, kTwo = 1, kGeneral = 2 };
+  struct Path {
+    int code;          // kind | near slot << 2 | far slot << 8 | far bucket << 14
+    float cb, cb_far;  // rab_time of the near / far bucket
+    __device__ int kind() const { return code & 3; }
+    __device__ int slot() const { return (code >> 2) & 63; }
+    __device__ int slot_far() const { return (code >> 8) & 63; }
+    __device__ uint32_t thr() const { return 1u << ((code >> 14) & 31); }  // 2^(b+1) for "two"
+  };
+  auto full_tile = [&](int i0) {
+    return (jw0 + 31 <= i0) && (i0 + BM - 1 < L) && (i0 + BM - 1 < n_h);
+  };
+  auto classify = [&](int u) -> Path {
+    Path r{kGeneral, 0.0f, 0.0f};
+    if (u >= nsteps) {
+      r.code = kUniform;  // past the end: computed but never used
+      return r;
     }
-#pragma unroll
-    for (int k = 0; k < OPT; k++) {
-      const int c = tid + kBwdThreads * k;
-      if (c < OCH) *reinterpret_cast<u32x4*>(sm.sdO + (c / (DV / 8)) * DO_LD + (c % (DV / 8)) * 8) = po[k];
-    }
-    if (tid < BM) {
-      if constexpr (FAST)
-        sm.sTr[tid] = (uint32_t)(pt - tbase);
-      else
-        sm.sTr64[tid] = pt;
-    }
-    if (tid >= 64 && tid < 64 + NWIN) sm.sWin[tid - 64] = pw;
-    if (wave == 0) {
-      const bool okr = lane < BM && i0 + lane < L;
-      const int64_t rlo = wave_min_i64(okr ? pt : kI64Max);
-      const int64_t rhi = wave_max_i64(okr ? pt : kI64Min);
-      if (lane == 0) {
-        sm.sRange[0] = rlo;
-        sm.sRange[1] = rhi;
+    if constexpr (FAST) {
+      if (full_tile(row0(u))) {
+        const uint32_t rlo = __builtin_amdgcn_readfirstlane(sm.sRr[u & 3][0]);
+        const uint32_t rhi = __builtin_amdgcn_readfirstlane(sm.sRr[u & 3][1]);
+        const bool ordered = rlo >= khi32;
+        uint32_t dmin, dmax;
+        if (ordered) {
+          dmin = rlo - khi32;
+          dmax = rhi - klo32;
+        } else if (klo32 >= rhi) {
+          dmin = klo32 - rhi;
+          dmax = khi32 - rlo;
+        } else {
+          dmin = 0;
+          dmax = max(rhi - klo32, khi32 - rlo);
+        }
+        // floor(log2 |dt|) over [dmin, dmax] (|dt| <= 1 -> 0); all < 31.
+        const int bnear = 31 - __clz((int)(dmin | 1u)), bfar = 31 - __clz((int)(dmax | 1u));
+        if (bnear == bfar) {
+          r.code = kUniform | (63 - bnear) << 2;
+          r.cb = sm.sTab[63 - bnear];
+        } else if (ordered && bfar == bnear + 1) {
+          r.code = kTwo | (63 - bnear) << 2 | (63 - bfar) << 8 | bfar << 14;
+          r.cb = sm.sTab[63 - bnear];
+          r.cb_far = sm.sTab[63 - bfar];
+        }
       }
     }
-    __syncthreads();
-    if (i0 + BM < i_end) prefetch(i0 + BM);
+    return r;
+  };
 
-    // Does any kept pair fall in (rows i0..i0+31) x (this wave's keys)?
-    const int imax = min(i0 + BM - 1, L - 1);
-    bool active = jw0 < L && jw0 <= imax;
-    if (jw0 >= n_h && (jw0 + 15 < i0 || jw0 > imax)) active = false;  // candidates: diagonal only
-    // Every key of the wave precedes every row, all rows are history rows.
-    const bool full = (jw0 + 15 <= i0) && (i0 + BM - 1 < L) && (i0 + BM - 1 < n_h);
-
-    // Scores and dP, accumulator seeded with the bias.  sacc[rb][m] holds
-    // (row i0 + 16rb + 4kg + m, key my_j).  A wave without kept pairs gets
-    // an all-zero mask from the general branch, so its P and dS vanish and
-    // the contractions below stay unconditional.
-    f32x4 sacc[2], pacc[2];
-    uint32_t vmask = 0xffu;
-    if (full) {
-      const int yb = (NWIN - 32 - 16 * wave - c16) + 4 * kg;
-      int sl[8];
-      float wv[8], tv[8];
+  // ---- bias seed of step u (lane = key, rows 8g + 4*half + m) ----
+  const int a_y = Pk - my_j + 4 * half;  // window entry of (row i0 + 4*half, key) on a full tile
+  auto win_reads = [&](int u, float (&w)[16]) {
+    const int c = a_y & 3;
+    const float* wp = &sm.sWin[u & 3][c][Sh::kWinPad + a_y - c];
 #pragma unroll
-      for (int q = 0; q < 8; q++) {
-        const int il = 16 * (q >> 2) + 4 * kg + (q & 3);
-        sl[q] = slot_of<FAST>(sm.sTr[il], tjr, sm.sTr64[il], tj64);
+    for (int g = 0; g < 4; g++) {
+      const f32x4 v = *reinterpret_cast<const f32x4*>(wp + 8 * g);
+#pragma unroll
+      for (int m = 0; m < 4; m++) w[4 * g + m] = v[m];
+    }
+  };
+  auto row_ts = [&](int u, uint32_t (&ti)[16]) {
+    const uint32_t* tp = sm.sTr[u & 7] + 4 * half;
+#pragma unroll
+    for (int g = 0; g < 4; g++) {
+      const u32x4 v = *reinterpret_cast<const u32x4*>(tp + 8 * g);
+#pragma unroll
+      for (int m = 0; m < 4; m++) ti[4 * g + m] = v[m];
+    }
+  };
+  // Time-table slot of every pair (fast path: |dt| < 2^31 by v_sad_u32,
+  // z = v_ffbh_u32 (-1 for 0), slot 32 + z; slot 31 stands for dt = 0,
+  // bucket 0, and its rab_time entry is set accordingly).
+  auto pair_slots = [&](int u, int (&sl)[16]) {
+    if constexpr (FAST) {
+      uint32_t ti[16];
+      row_ts(u, ti);
+#pragma unroll
+      for (int q = 0; q < 16; q++) {
+        uint32_t d, z;
+        asm("v_sad_u32 %0, %1, %2, 0" : "=v"(d) : "v"(ti[q]), "v"(tjr));
+        asm("v_ffbh_u32 %0, %1" : "=v"(z) : "v"(d));
+        sl[q] = 32 + (int)z;
       }
+    } else {
+      const uint32_t* tp = sm.sT[u & 7] + 2 * (4 * half);
 #pragma unroll
-      for (int q = 0; q < 8; q++) {
-        wv[q] = sm.sWin[yb + 16 * (q >> 2) + (q & 3)];
+      for (int q = 0; q < 16; q++) {
+        const int r = 8 * (q >> 2) + (q & 3);
+        const int64_t ti = (int64_t)(((uint64_t)tp[2 * r + 1] << 32) | tp[2 * r]);
+        sl[q] = slot64(ti - tj64);
+      }
+    }
+  };
+  auto seed = [&](int u, const Path& pth, f32x16& acc) {
+    if (pth.kind() == kUniform) {
+      float w[16];
+      win_reads(u, w);
+#pragma unroll
+      for (int q = 0; q < 16; q++) acc[q] = w[q] + pth.cb;
+    } else if (pth.kind() == kTwo) {
+      float w[16];
+      uint32_t ti[16];
+      win_reads(u, w);
+      row_ts(u, ti);
+      const uint32_t lim = tjr + pth.thr();
+#pragma unroll
+      for (int q = 0; q < 16; q++) acc[q] = w[q] + (ti[q] >= lim ? pth.cb_far : pth.cb);
+    } else {
+      const int i0 = row0(u), pi0 = min(i0, n_h);
+      int sl[16];
+      pair_slots(u, sl);
+      bool ok[16];
+      int y[16];
+#pragma unroll
+      for (int q = 0; q < 16; q++) {
+        const int i = i0 + 8 * (q >> 2) + 4 * half + (q & 3);
+        ok[q] = key_ok && i < L && pair_valid(i, my_j, n_h);
+        y[q] = ok[q] ? (Pk - pj) + (bias_pos(i, n_h) - pi0) : 0;
+      }
+      float w[16], tv[16];
+#pragma unroll
+      for (int q = 0; q < 16; q++) {
+        w[q] = sm.sWin[u & 3][0][Sh::kWinPad + y[q]];
         tv[q] = sm.sTab[sl[q]];
       }
 #pragma unroll
-      for (int q = 0; q < 8; q++) sacc[q >> 2][q & 3] = wv[q] + tv[q];
+      for (int q = 0; q < 16; q++) acc[q] = ok[q] ? w[q] + tv[q] : kMaskedBias;
+    }
+  };
+
+  // ---- contractions ----
+  auto scores = [&](int u, f32x16& sacc, f32x16& pacc) {
+    const uint8_t* qb = sm.ring.t.q[u & 3];
+    const uint8_t* ob = sm.ring.t.dO[u & 3];
+    pacc = f32x16{};
+    constexpr int SMAX = DQK > DV ? DQK / 16 : DV / 16;
+#pragma unroll
+    for (int s = 0; s < SMAX; s++) {
+      if (s < DQK / 16) {
+        const u32x4 a = *reinterpret_cast<const u32x4*>(qb + a_off(QT{}, qa, s));
+        sacc = mfma32x32x16(as_bf16x8(a), as_bf16x8(kf[s]), sacc);
+      }
+      if (s < DV / 16) {
+        const u32x4 a = *reinterpret_cast<const u32x4*>(ob + a_off(OT{}, oa, s));
+        pacc = mfma32x32x16(as_bf16x8(a), as_bf16x8(vf[s]), pacc);
+      }
+    }
+  };
+  // dV += P^T dO, dK += dS^T Q: k-slots (st, e) of the A operands are the
+  // accumulator rows 16 st + 8 (e / 4) + 4*half + e % 4.
+  auto key_grads = [&](int u, const u32x4 (&pa)[2], const u32x4 (&da)[2]) {
+    const uint8_t* qb = sm.ring.t.q[u & 3];
+    const uint8_t* ob = sm.ring.t.dO[u & 3];
+#pragma unroll
+    for (int st = 0; st < 2; st++) {
+#pragma unroll
+      for (int nb = 0; nb < DV / 32; nb++) {
+        const uint2 lo = lds_read_tr16((const uint16_t*)(ob + tr_off(OT{}, ot, st, 0, nb)));
+        const uint2 hi = lds_read_tr16((const uint16_t*)(ob + tr_off(OT{}, ot, st, 1, nb)));
+        dvacc[nb] = mfma32x32x16(as_bf16x8(pa[st]), as_bf16x8(u32x4{lo.x, lo.y, hi.x, hi.y}), dvacc[nb]);
+      }
+#pragma unroll
+      for (int nb = 0; nb < DQK / 32; nb++) {
+        const uint2 lo = lds_read_tr16((const uint16_t*)(qb + tr_off(QT{}, qt, st, 0, nb)));
+        const uint2 hi = lds_read_tr16((const uint16_t*)(qb + tr_off(QT{}, qt, st, 1, nb)));
+        dkacc[nb] = mfma32x32x16(as_bf16x8(da[st]), as_bf16x8(u32x4{lo.x, lo.y, hi.x, hi.y}), dkacc[nb]);
+      }
+    }
+  };
+  // dS^T of step u into its LDS slot: the lane (key) writes 4 runs of 4 rows.
+  auto store_dst = [&](int u, const u32x4 (&da)[2]) {
+    uint16_t* dp = sm.sdST[u & 1] + (32 * wave + col) * DST_LD + 4 * half;
+#pragma unroll
+    for (int st = 0; st < 2; st++) {
+      *reinterpret_cast<uint2*>(dp + 16 * st) = uint2{da[st][0], da[st][1]};
+      *reinterpret_cast<uint2*>(dp + 16 * st + 8) = uint2{da[st][2], da[st][3]};
+    }
+  };
+  // dQ(rows of step u, the wave's 32 columns) over its keys, added to the
+  // fp32 workspace.  Lane holds (row i0 + 8g + 4*half + m, column 32 cbw +
+  // col).  The atomics go out after the next seed, among the step's
+  // contractions.
+  uint32_t dq_off[16];
+#pragma unroll
+  for (int q = 0; q < 16; q++)
+    dq_off[q] = (uint32_t)(((8 * (q >> 2) + 4 * half + (q & 3)) * H * DQK + 32 * cbw + col) * 4);
+  auto dq_mfma = [&](int u, f32x16& qacc) {
+    const uint16_t* dp = sm.sdST[u & 1] + (kbase + tr_row) * DST_LD + tr_col;
+    qacc = f32x16{};
+#pragma unroll
+    for (int ks = 0; ks < KSTEPS; ks++) {
+      const uint2 lo = lds_read_tr16(dp + 16 * ks * DST_LD);
+      const uint2 hi = lds_read_tr16(dp + (16 * ks + 8) * DST_LD);
+      qacc = mfma32x32x16(as_bf16x8(u32x4{lo.x, lo.y, hi.x, hi.y}), as_bf16x8(kq[ks]), qacc);
+    }
+  };
+  auto dq_atomics = [&](int u, const f32x16& qacc) {
+    const int i0 = row0(u);
+    char* base = (char*)(A.dq_acc + ((o + i0) * H + head) * DQK);
+    if (i0 + BM <= L) {
+#pragma unroll
+      for (int q = 0; q < 16; q++) unsafeAtomicAdd((float*)(base + dq_off[q]), qacc[q]);
     } else {
-      vmask = 0;
-      const int pos_base = (N - 1) + min(j0, n_h) - min(i0 + BM - 1, n_h);
 #pragma unroll
-      for (int q = 0; q < 8; q++) {
-        const int il = 16 * (q >> 2) + 4 * kg + (q & 3);
-        const int i = i0 + il;
-        const bool ok = key_ok && i < L && pair_valid(i, my_j, n_h);
-        const int x = ok ? (N - 1) + pj - bias_pos(i, n_h) - pos_base : 0;
-        const int sl = slot_of<FAST>(sm.sTr[il], tjr, sm.sTr64[il], tj64);
-        const float b = sm.sWin[NWIN - 1 - x] + sm.sTab[sl];
-        sacc[q >> 2][q & 3] = ok ? b : 0.0f;
-        vmask |= (uint32_t)ok << q;
+      for (int q = 0; q < 16; q++)
+        if (i0 + 8 * (q >> 2) + 4 * half + (q & 3) < L)
+          unsafeAtomicAdd((float*)(base + dq_off[q]), qacc[q]);
+    }
+  };
+
+  // ---- bias gradients ----
+  // Time table: running per-lane sum for one slot, flushed on change.
+  int run_slot = -1;
+  float run_acc = 0.0f;
+  auto time_flush = [&]() {
+    if (run_slot >= 0) {
+      const float v = wave_sum_dpp(run_acc);
+      if (lane == 0) atomicAdd(&sm.sTacc[run_slot], v);
+    }
+    run_acc = 0.0f;
+  };
+  auto time_add = [&](int slot, float v) {
+    if (slot != run_slot) {
+      time_flush();
+      run_slot = slot;
+    }
+    run_acc += v;
+  };
+  // Position table, full tiles: register q of every lane is rotated by
+  // r0(q) = 8g + m lanes over the whole wave (ds_bpermute at this lane's
+  // address plus an immediate offset).  Lane (col, half) then holds pairs
+  // of diagonal i - j = (i0 - jw0) - col + 4*half, or, where col + r0(q)
+  // crossed into the other half, (i0 - jw0) + 32 - col + 4*(1 - half).
+  // Both sums go to the LDS accumulator.  (Every pair of a full tile is
+  // kept, so a diagonal holding a nonzero sum is a real one; the crossing
+  // one is clamped for lanes that have no crossing pair.)
+  const int perm_base = lane * 4;
+  float wrap_w[16];
+#pragma unroll
+  for (int q = 0; q < 16; q++) wrap_w[q] = col + 8 * (q >> 2) + (q & 3) >= 32 ? 1.0f : 0.0f;
+  const int R = L - j0;  // p(i) - p(j) of kept pairs lies in [0, R)
+  auto pos_add = [&](int k, float v) {  // k = p(i) - p(j) >= 0
+    if (A.pos_in_lds)
+      atomicAdd(&sPos[k], v);
+    else
+      unsafeAtomicAdd(&A.d_rab_pos[(N - 1) - k], v * invN);
+  };
+
+  auto grads = [&](int u, const Path& pth, const float (&ds)[16]) {
+    const int i0 = row0(u);
+    if (pth.kind() != kGeneral) {
+      float sum = 0.0f, wsum = 0.0f, tot = 0.0f, far = 0.0f;
+#pragma unroll
+      for (int q = 0; q < 16; q++) {
+        const int r0 = 8 * (q >> 2) + (q & 3);
+        const float rv = __int_as_float(
+            __builtin_amdgcn_ds_bpermute(perm_base + 4 * r0, __float_as_int(ds[q])));
+        sum += rv;
+        wsum = __builtin_fmaf(rv, wrap_w[q], wsum);
+        tot += ds[q];
       }
-    }
-    pacc[0] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
-    pacc[1] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
-    {
-      constexpr int SMAX = DQK > DV ? DQK / 32 : DV / 32;
+      pos_add((i0 - jw0) - col + 4 * half, sum - wsum);
+      pos_add(min((i0 - jw0) + 32 - col + 4 * (1 - half), R - 1), wsum);
+      if (pth.kind() == kTwo) {
+        uint32_t ti[16];
+        row_ts(u, ti);
+        const uint32_t lim = tjr + pth.thr();
 #pragma unroll
-      for (int s = 0; s < SMAX; s++) {
-#pragma unroll
-        for (int rb = 0; rb < 2; rb++) {
-          if (s < DQK / 32) {
-            u32x4 a = *reinterpret_cast<const u32x4*>(sm.sQ + (16 * rb + c16) * Q_LD + 32 * s + 8 * kg);
-            sacc[rb] = mfma16x16x32(as_bf16x8(a), as_bf16x8(kf[s]), sacc[rb]);
-          }
-          if (s < DV / 32) {
-            u32x4 a = *reinterpret_cast<const u32x4*>(sm.sdO + (16 * rb + c16) * DO_LD + 32 * s + 8 * kg);
-            pacc[rb] = mfma16x16x32(as_bf16x8(a), as_bf16x8(vf[s]), pacc[rb]);
-          }
-        }
-      }
-    }
-    // SiLU, SiLU' and dS in fp32.
-    float pv[8], dsv[8], sg[8];
-#pragma unroll
-    for (int q = 0; q < 8; q++) sg[q] = __builtin_amdgcn_exp2f(-sacc[q >> 2][q & 3] * kLog2e);
-#pragma unroll
-    for (int q = 0; q < 8; q++) sg[q] = __builtin_amdgcn_rcpf(1.0f + sg[q]);
-#pragma unroll
-    for (int q = 0; q < 8; q++) {
-      const float x = sacc[q >> 2][q & 3];
-      const float sl = x * sg[q];
-      const bool ok = (vmask >> q) & 1u;
-      pv[q] = ok ? sl : 0.0f;
-      dsv[q] = ok ? pacc[q >> 2][q & 3] * (sg[q] + sl * (1.0f - sg[q])) : 0.0f;
-    }
-    // Time-table gradient: sum dS per slot over the slots this tile spans.
-    if (active) {
-      int s_lo, s_hi;
-      slot_range(sm.sRange[0], sm.sRange[1], klo, khi, s_lo, s_hi);
-      if (s_lo == s_hi) {
-        float sum = 0.0f;
-#pragma unroll
-        for (int q = 0; q < 8; q++) sum += dsv[q];
-        sum = wave_sum_f32(sum);
-        if (lane == 0) sm.sTacc[wave][s_lo] += sum;
+        for (int q = 0; q < 16; q++) far += ti[q] >= lim ? ds[q] : 0.0f;
+        time_add(pth.slot(), tot - far);
+        const float v = wave_sum_dpp(far);
+        if (lane == 0) atomicAdd(&sm.sTacc[pth.slot_far()], v);
       } else {
-        for (int s = s_lo; s <= s_hi; s++) {
-          float sum = 0.0f;
+        time_add(pth.slot(), tot);
+      }
+    } else {
+      int sl[16];
+      pair_slots(u, sl);
 #pragma unroll
-          for (int q = 0; q < 8; q++) {
-            const int il = 16 * (q >> 2) + 4 * kg + (q & 3);
-            const int sl = slot_of<FAST>(sm.sTr[il], tjr, sm.sTr64[il], tj64);
-            sum += sl == s ? dsv[q] : 0.0f;
-          }
-          sum = wave_sum_f32(sum);
-          if (lane == 0) sm.sTacc[wave][s] += sum;
+      for (int q = 0; q < 16; q++) {
+        const int i = i0 + 8 * (q >> 2) + 4 * half + (q & 3);
+        if (key_ok && i < L && pair_valid(i, my_j, n_h)) {
+          pos_add(bias_pos(i, n_h) - pj, ds[q]);
+          atomicAdd(&sm.sTacc[sl[q]], ds[q]);
         }
       }
     }
-    // P^T and dS^T as A operands: k-slots 0..3 = rows 4kg + 0..3,
-    // k-slots 4..7 = rows 16 + 4kg + 0..3 (the accumulator's own rows).
-    u32x4 pa, da;
-    pa[0] = pack_bf16x2(pv[0], pv[1]);
-    pa[1] = pack_bf16x2(pv[2], pv[3]);
-    pa[2] = pack_bf16x2(pv[4], pv[5]);
-    pa[3] = pack_bf16x2(pv[6], pv[7]);
-    da[0] = pack_bf16x2(dsv[0], dsv[1]);
-    da[1] = pack_bf16x2(dsv[2], dsv[3]);
-    da[2] = pack_bf16x2(dsv[4], dsv[5]);
-    da[3] = pack_bf16x2(dsv[6], dsv[7]);
-    // dS tiles: bf16 for dQ, fp32 for the bias gradients.
-#pragma unroll
-    for (int q = 0; q < 8; q++) {
-      const int il = 16 * (q >> 2) + 4 * kg + (q & 3);
-      sm.sdS32[il * DS32_LD + 16 * wave + c16] = dsv[q];
-      const uint32_t w = da[q >> 1];
-      sm.sdS[il * DS_LD + 16 * wave + c16] = (uint16_t)((q & 1) ? (w >> 16) : (w & 0xffffu));
-    }
-    // dV += P^T dO, dK += dS^T Q (contraction over the step's 32 rows).
-    {
-      const int row0 = 4 * kg + tr_r;
-#pragma unroll
-      for (int cb = 0; cb < DV / 16; cb++) {
-        const uint16_t* base = sm.sdO + row0 * DO_LD + 16 * cb + tr_c;
-        const uint2 lo = lds_read_tr16(base), hi = lds_read_tr16(base + 16 * DO_LD);
-        u32x4 b = {lo.x, lo.y, hi.x, hi.y};
-        dvacc[cb] = mfma16x16x32(as_bf16x8(pa), as_bf16x8(b), dvacc[cb]);
-      }
-#pragma unroll
-      for (int cb = 0; cb < DQK / 16; cb++) {
-        const uint16_t* base = sm.sQ + row0 * Q_LD + 16 * cb + tr_c;
-        const uint2 lo = lds_read_tr16(base), hi = lds_read_tr16(base + 16 * Q_LD);
-        u32x4 b = {lo.x, lo.y, hi.x, hi.y};
-        dkacc[cb] = mfma16x16x32(as_bf16x8(da), as_bf16x8(b), dkacc[cb]);
-      }
-    }
-    __syncthreads();
+  };
 
-    // dQ(step rows) += dS K: 2 row blocks x DQK/16 column blocks shared by
-    // the 8 waves; each wave takes row block w & 1 and its share of the
-    // column blocks, contracting over all 128 keys (or half of them when
-    // there are fewer column blocks than wave pairs).
-    {
-      constexpr int NCB = DQK / 16;
-      constexpr int CB_PER = NCB >= 4 ? NCB / 4 : 1;       // column blocks per wave
-      constexpr int KSPLIT = NCB >= 4 ? 1 : 4 / NCB;       // key splits per block
-      constexpr int KSTEPS = (BN / 32) / KSPLIT;
-      const int rb = wave & 1;
-      const int grp = wave >> 1;                           // 0..3
-      const int cb0 = (grp / KSPLIT) * CB_PER;
-      const int ks0 = (grp % KSPLIT) * KSTEPS;
+  // ---- pipelined steps ----
+  // Step u: dQ(u-1); S, dP of step u+1 seeded and issued; SiLU' of step u;
+  // dV, dK of step u; dS^T(u) to LDS; bias gradients of step u.
+  Path path_cur, path_next, path_nn;
+  auto step = [&](int u, f32x16& s_cur, f32x16& p_cur, f32x16& s_next, f32x16& p_next) {
+    wait_vmcnt_lgkmcnt0<OPS_PER_STEP>();
+    barrier_no_fence();
+    issue_tiles(u + 3);
+    issue_win(u + 3);
+    issue_ts(u + 5);
+    f32x16 qacc;
+    if (u >= 1) dq_mfma(u - 1, qacc);
+    if (u + 1 < nsteps) seed(u + 1, path_next, s_next);
+    if (u >= 1) dq_atomics(u - 1, qacc);
+    scores(u + 1, s_next, p_next);
+    float pv[16], dsv[16];
 #pragma unroll
-      for (int u = 0; u < CB_PER; u++) {
-        const int cb = cb0 + u;
-        f32x4 qacc = {0.0f, 0.0f, 0.0f, 0.0f};
-#pragma unroll
-        for (int ks = 0; ks < KSTEPS; ks++) {
-          const int kk = 32 * (ks0 + ks);
-          u32x4 a = *reinterpret_cast<const u32x4*>(sm.sdS + (16 * rb + c16) * DS_LD + kk + 8 * kg);
-          // B = K[kk + 8kg + e][16cb + c16]: down the rows of the key tile.
-          const uint16_t* base = sm.sK + (kk + 8 * kg + tr_r) * K_LD + 16 * cb + tr_c;
-          const uint2 lo = lds_read_tr16(base), hi = lds_read_tr16(base + 4 * K_LD);
-          u32x4 b = {lo.x, lo.y, hi.x, hi.y};
-          qacc = mfma16x16x32(as_bf16x8(a), as_bf16x8(b), qacc);
-        }
-#pragma unroll
-        for (int m = 0; m < 4; m++) {
-          const int i = i0 + 16 * rb + 4 * kg + m;
-          if (i < L) unsafeAtomicAdd(&A.dq_acc[((o + i) * H + head) * DQK + 16 * cb + c16], qacc[m]);
-        }
-      }
+    for (int q = 0; q < 16; q++) {
+      const float x = s_cur[q];
+      const float sg = silu_sigma(x);
+      const float p = x * sg;
+      pv[q] = p;
+      dsv[q] = p_cur[q] * __builtin_fmaf(p, 1.0f - sg, sg);
     }
+    u32x4 pa[2], da[2];
+#pragma unroll
+    for (int st = 0; st < 2; st++) {
+      pa[st] = u32x4{pack_bf16x2(pv[8 * st], pv[8 * st + 1]), pack_bf16x2(pv[8 * st + 2], pv[8 * st + 3]),
+                     pack_bf16x2(pv[8 * st + 4], pv[8 * st + 5]), pack_bf16x2(pv[8 * st + 6], pv[8 * st + 7])};
+      da[st] = u32x4{pack_bf16x2(dsv[8 * st], dsv[8 * st + 1]), pack_bf16x2(dsv[8 * st + 2], dsv[8 * st + 3]),
+                     pack_bf16x2(dsv[8 * st + 4], dsv[8 * st + 5]), pack_bf16x2(dsv[8 * st + 6], dsv[8 * st + 7])};
+    }
+    key_grads(u, pa, da);
+    store_dst(u, da);
+    grads(u, path_cur, dsv);
+    path_nn = classify(u + 2);
+    reduce_ts(u + 3);
+    path_cur = path_next;
+    path_next = path_nn;
+  };
 
-    // Position-table gradient, history rows: threads 2t, 2t+1 own diagonal
-    // i_local - j_local = t - 127 (rows 0..15 and 16..31 respectively),
-    // i.e. p(i) - p(j) = i0 - j0 + t - 127.
-    const int rh = max(0, min(BM, n_h - i0));
-    if (tid < 2 * (NWIN - 1)) {
-      const int dd = (tid >> 1) - (BN - 1);
-      const int k = i0 - j0 + dd;
-      const int lo = max(max(0, dd), 16 * (tid & 1)), hi = min(min(rh, BN + dd), 16 * (tid & 1) + 16);
-      float part[4] = {0.0f, 0.0f, 0.0f, 0.0f};
-#pragma unroll
-      for (int u = 0; u < 16; u++) {
-        const int il = 16 * (tid & 1) + u;
-        const int c = il - dd;
-        const float v = sm.sdS32[il * DS32_LD + (c < 0 ? 0 : (c > BN - 1 ? BN - 1 : c))];
-        part[u & 3] += (il >= lo && il < hi) ? v : 0.0f;
-      }
-      float sum = (part[0] + part[1]) + (part[2] + part[3]);
-      sum += __shfl_xor(sum, 1, 64);
-      if ((tid & 1) == 0 && k >= 0 && sum != 0.0f) {
-        if (A.pos_in_lds)
-          sPosAcc[k] += sum;
-        else
-          unsafeAtomicAdd(&A.d_rab_pos[(N - 1) - k], sum * invN);
-      }
-    }
-    // Candidate rows (p(i) = n_h): key j < n_h lands on n_h - j, the
-    // diagonal (j = i) on 0.
-    if (rh < BM && i0 + rh < L) {
-      __syncthreads();
-      if (tid < BN) {
-        const int j = j0 + tid;
-        float sum = 0.0f;
-        for (int il = rh; il < BM; il++) sum += sm.sdS32[il * DS32_LD + tid];
-        if (sum != 0.0f) {
-          const int k = j < n_h ? n_h - j : 0;
-          if (A.pos_in_lds)
-            atomicAdd(&sPosAcc[k], sum);
-          else
-            unsafeAtomicAdd(&A.d_rab_pos[(N - 1) - k], sum * invN);
-        }
-      }
-    }
+  // Prologue: timestamps of steps 0..4, tiles and windows of steps 0..2,
+  // row ranges of steps 0..2; then step 0 is scored.
+  for (int v = 0; v < 5; v++) issue_ts(v);
+  for (int v = 0; v < 3; v++) {
+    issue_tiles(v);
+    issue_win(v);
   }
+  wait_vmcnt_lgkmcnt0<0>();
+  barrier_no_fence();
+  for (int v = 0; v < 3; v++) reduce_ts(v);
+  wait_vmcnt_lgkmcnt0<0>();
+  barrier_no_fence();
+  f32x16 sA, pA, sB, pB;
+  path_cur = classify(0);
+  path_next = classify(1);
+  seed(0, path_cur, sA);
+  scores(0, sA, pA);
+  int u = 0;
+  for (; u + 1 < nsteps; u += 2) {
+    step(u, sA, pA, sB, pB);
+    step(u + 1, sB, pB, sA, pA);
+  }
+  if (u < nsteps) step(u, sA, pA, sB, pB);
+  // dS^T of the last step is visible after one more barrier; no LDS DMA
+  // may be in flight when the workgroup ends.
+  wait_vmcnt_lgkmcnt0<0>();
+  barrier_no_fence();
+  {
+    f32x16 qacc;
+    dq_mfma(nsteps - 1, qacc);
+    dq_atomics(nsteps - 1, qacc);
+  }
+  time_flush();
 
-  // dK, dV of the wave's keys: lane holds (j = jw0 + 4kg + m, d = 16cb + c16).
+  // dK, dV of the wave's keys: lane holds (key jw0 + 8g + 4*half + m, feature 32nb + col).
 #pragma unroll
-  for (int m = 0; m < 4; m++) {
-    const int j = jw0 + 4 * kg + m;
+  for (int q = 0; q < 16; q++) {
+    const int j = jw0 + 8 * (q >> 2) + 4 * half + (q & 3);
     if (j < L) {
 #pragma unroll
-      for (int cb = 0; cb < DQK / 16; cb++)
-        A.dK[((o + j) * H + head) * DQK + 16 * cb + c16] = f32_to_bf16_bits(dkacc[cb][m] * invN);
+      for (int nb = 0; nb < DQK / 32; nb++)
+        A.dK[((o + j) * H + head) * DQK + 32 * nb + col] = f32_to_bf16_bits(dkacc[nb][q] * invN);
 #pragma unroll
-      for (int cb = 0; cb < DV / 16; cb++)
-        A.dV[((o + j) * H + head) * DV + 16 * cb + c16] = f32_to_bf16_bits(dvacc[cb][m] * invN);
+      for (int nb = 0; nb < DV / 32; nb++)
+        A.dV[((o + j) * H + head) * DV + 32 * nb + col] = f32_to_bf16_bits(dvacc[nb][q] * invN);
     }
-  }
-
-  __syncthreads();
-  if (A.pos_in_lds)
-    for (int x = tid; x < R; x += kBwdThreads) {
-      const float v = sPosAcc[x];
-      if (v != 0.0f) unsafeAtomicAdd(&A.d_rab_pos[(N - 1) - x], v * invN);
-    }
-  if (tid < 64) {
-    float v = 0.0f;
-#pragma unroll
-    for (int w = 0; w < kBwdWaves; w++) v += sm.sTacc[w][tid];
-    if (v != 0.0f) unsafeAtomicAdd(&A.d_rab_time[min(63 - tid, NB - 1)], v * invN);
   }
 }
 
@@ -465,7 +710,7 @@ template <int DQK, int DV>
 __global__ __launch_bounds__(kBwdThreads, 1) void attn_bwd_bf16_kernel(
     BwdArgs A, const WorkItem* __restrict__ items, const int32_t* __restrict__ count) {
   using S = BwdShared<DQK, DV>;
-  constexpr int BN = S::BN, K_LD = S::K_LD;
+  constexpr int BN = S::BN;
   __shared__ S sm;
   extern __shared__ float sPosAcc[];  // [N] when pos_in_lds
 
@@ -473,55 +718,45 @@ __global__ __launch_bounds__(kBwdThreads, 1) void attn_bwd_bf16_kernel(
   const WorkItem it = items[blockIdx.x];
   const int head = blockIdx.y;
   const JaggedArgs& ja = A.ja;
-  const int NB = ja.num_buckets;
+  const int N = ja.max_seq_len, NB = ja.num_buckets;
   const int64_t o = ja.seq_offsets[it.seq];
   const int L = (int)(ja.seq_offsets[it.seq + 1] - o);
   const int n_h = L - (ja.num_targets ? (int)ja.num_targets[it.seq] : 0);
   const int j0 = it.blk * BN;
-  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
-  const int64_t* __restrict__ ts = ja.timestamps + o;
-  const uint16_t* __restrict__ kg = (const uint16_t*)A.t.k;
+  const int tid = threadIdx.x;
 
-  // Timestamp extremes over the tokens this item touches, [j0, L): the
-  // 32-bit fast path applies when they span less than 2^31.
-  int64_t tlo = kI64Max, thi = kI64Min;
-  for (int x = j0 + tid; x < L; x += kBwdThreads) {
-    const int64_t v = ts[x];
-    tlo = v < tlo ? v : tlo;
-    thi = v > thi ? v : thi;
+  // The 32-bit fast path applies when the sequence's timestamps span less
+  // than 2^31; they are then rebased to its smallest one.
+  const int64_t tlo = ja.seq_trange[2 * it.seq], thi = ja.seq_trange[2 * it.seq + 1];
+  const bool fast = thi - tlo < ((int64_t)1 << 31);
+  // Slots 0..32 are unreachable when every |dt| < 2^31; there slot 31
+  // stands for dt = 0 (bucket 0).
+  for (int x = tid; x < 64; x += kBwdThreads) {
+    sm.sTab[x] = (fast && x == 31) ? ja.rab_time[0] : ja.rab_time[min(63 - x, NB - 1)];
+    sm.sTacc[x] = 0.0f;
   }
-  tlo = wave_min_i64(tlo);
-  thi = wave_max_i64(thi);
-  if (lane == 0) {
-    sm.sRed[0][wave] = tlo;
-    sm.sRed[1][wave] = thi;
-  }
-  for (int x = tid; x < 64; x += kBwdThreads) sm.sTab[x] = ja.rab_time[min(63 - x, NB - 1)];
-  for (int x = tid; x < kBwdWaves * 64; x += kBwdThreads) (&sm.sTacc[0][0])[x] = 0.0f;
+  const int R = L - j0;  // p(i) - p(j) of kept pairs lies in [0, R)
   if (A.pos_in_lds)
-    for (int x = tid; x < L - j0; x += kBwdThreads) sPosAcc[x] = 0.0f;
-  // K of the 128-key block, row-major: operand of dQ = dS K (read down
-  // the key rows with transposing reads).
-  constexpr int KCH = BN * DQK / 8;
-  for (int c = tid; c < KCH; c += kBwdThreads) {
-    const int r = c / (DQK / 8), cc = (c % (DQK / 8)) * 8;
-    const int j = j0 + r;
-    *reinterpret_cast<u32x4*>(sm.sK + r * K_LD + cc) =
-        j < L ? *reinterpret_cast<const u32x4*>(kg + (o + j) * A.t.k_stride + head * DQK + cc)
-              : zero_u32x4();
-  }
+    for (int x = tid; x < R; x += kBwdThreads) sPosAcc[x] = 0.0f;
   __syncthreads();
-  tlo = sm.sRed[0][0];
-  thi = sm.sRed[1][0];
-#pragma unroll
-  for (int w = 1; w < kBwdWaves; w++) {
-    tlo = sm.sRed[0][w] < tlo ? sm.sRed[0][w] : tlo;
-    thi = sm.sRed[1][w] > thi ? sm.sRed[1][w] : thi;
-  }
-  if (thi - tlo < ((int64_t)1 << 31))
+  if (fast) {
     bwd_item<DQK, DV, true>(sm, sPosAcc, A, o, L, n_h, j0, head, tlo);
-  else
+  } else {
     bwd_item<DQK, DV, false>(sm, sPosAcc, A, o, L, n_h, j0, head, tlo);
+  }
+
+  __syncthreads();
+  const float invN = 1.0f / (float)N;
+  if (A.pos_in_lds)
+    for (int x = tid; x < R; x += kBwdThreads) {
+      const float v = sPosAcc[x];
+      if (v != 0.0f) unsafeAtomicAdd(&A.d_rab_pos[(N - 1) - x], v * invN);
+    }
+  if (tid < 64) {
+    const float v = sm.sTacc[tid];
+    const int b = (fast && tid == 31) ? 0 : min(63 - tid, NB - 1);
+    if (v != 0.0f) unsafeAtomicAdd(&A.d_rab_time[b], v * invN);
+  }
 }
 
 template <int DQK, int DV>

@@ -80,7 +80,6 @@ struct FwdShared {
   __align__(16) uint32_t sTr[8][32];  // the same rebased to 32 bits (fast path)
   uint32_t sKr32[4][2];              // rebased key timestamp min / max per tile
   float sTab[64];                    // time bias by slot (bias.h)
-  int64_t sRed[2][4];
 };
 
 __device__ __forceinline__ float silu(float x) {
@@ -533,37 +532,18 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_bf16_kernel(JaggedArgs ja, Te
   const int L = (int)(ja.seq_offsets[it.seq + 1] - o);
   const int n_h = L - (ja.num_targets ? (int)ja.num_targets[it.seq] : 0);
   const int i0 = it.blk * Sh::BM;
-  const int rows_end = min(i0 + Sh::BM, L);
-  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
-  const int64_t* __restrict__ ts = ja.timestamps + o;
+  const int tid = threadIdx.x;
 
-  // Timestamp extremes over the tokens this item touches, [0, rows_end):
-  // the 32-bit fast path applies when they span less than 2^31.
-  int64_t tlo = kI64Max, thi = kI64Min;
-  for (int x = tid; x < rows_end; x += 256) {
-    const int64_t v = ts[x];
-    tlo = v < tlo ? v : tlo;
-    thi = v > thi ? v : thi;
-  }
-  tlo = wave_min_i64(tlo);
-  thi = wave_max_i64(thi);
-  if (lane == 0) {
-    sm.sRed[0][wave] = tlo;
-    sm.sRed[1][wave] = thi;
-  }
+  // The 32-bit fast path applies when the sequence's timestamps span less
+  // than 2^31; they are then rebased to its smallest one.
+  const int64_t tlo = ja.seq_trange[2 * it.seq], thi = ja.seq_trange[2 * it.seq + 1];
   // Time bias by slot; when every |dt| < 2^31, slots 0..32 are unreachable
   // and entry 31 becomes the fast path's entry for dt = 0 (bucket 0).
-  for (int x = tid; x < 64; x += 256) sm.sTab[x] = ja.rab_time[min(63 - x, NB - 1)];
+  const bool fast = thi - tlo < ((int64_t)1 << 31);
+  for (int x = tid; x < 64; x += 256)
+    sm.sTab[x] = (fast && x == 31) ? ja.rab_time[0] : ja.rab_time[min(63 - x, NB - 1)];
   __syncthreads();
-  tlo = sm.sRed[0][0];
-  thi = sm.sRed[1][0];
-#pragma unroll
-  for (int w = 1; w < 4; w++) {
-    tlo = sm.sRed[0][w] < tlo ? sm.sRed[0][w] : tlo;
-    thi = sm.sRed[1][w] > thi ? sm.sRed[1][w] : thi;
-  }
-  if (thi - tlo < ((int64_t)1 << 31)) {
-    if (tid == 0) sm.sTab[31] = ja.rab_time[0];
+  if (fast) {
     fwd_item<DQK, DV, true>(sm, ja, t, out, o, L, n_h, i0, head, tlo);
   } else {
     fwd_item<DQK, DV, false>(sm, ja, t, out, o, L, n_h, i0, head, tlo);

@@ -47,6 +47,38 @@ __device__ __forceinline__ void slot_range(int64_t rlo, int64_t rhi, int64_t klo
   s_hi = slot64(dmin);
 }
 
+// Whole-wave reductions on DPP (no LDS round trip): butterflies within
+// rows of 16 lanes, then row_bcast:15 / row_bcast:31 fold the four rows
+// into lane 63, which is read back as a scalar.
+template <int CTRL, int ROW_MASK, typename T>
+__device__ __forceinline__ T dpp_mov(T identity, T x) {
+  return __builtin_bit_cast(T, __builtin_amdgcn_update_dpp(__builtin_bit_cast(int, identity),
+                                                           __builtin_bit_cast(int, x), CTRL,
+                                                           ROW_MASK, 0xf, false));
+}
+
+template <typename T, typename Op>
+__device__ __forceinline__ T wave_reduce_dpp(T x, T identity, Op op) {
+  static_assert(sizeof(T) == 4, "32-bit values");
+  x = op(x, dpp_mov<0xb1, 0xf>(identity, x));   // quad_perm [1,0,3,2]
+  x = op(x, dpp_mov<0x4e, 0xf>(identity, x));   // quad_perm [2,3,0,1]
+  x = op(x, dpp_mov<0x141, 0xf>(identity, x));  // row_half_mirror
+  x = op(x, dpp_mov<0x140, 0xf>(identity, x));  // row_mirror
+  x = op(x, dpp_mov<0x142, 0xa>(identity, x));  // row_bcast:15 into rows 1 and 3
+  x = op(x, dpp_mov<0x143, 0xc>(identity, x));  // row_bcast:31 into rows 2 and 3
+  return __builtin_bit_cast(T, __builtin_amdgcn_readlane(__builtin_bit_cast(int, x), 63));
+}
+
+__device__ __forceinline__ float wave_sum_dpp(float v) {
+  return wave_reduce_dpp(v, 0.0f, [](float a, float b) { return a + b; });
+}
+__device__ __forceinline__ uint32_t wave_min_dpp(uint32_t v) {
+  return wave_reduce_dpp(v, 0xffffffffu, [](uint32_t a, uint32_t b) { return a < b ? a : b; });
+}
+__device__ __forceinline__ uint32_t wave_max_dpp(uint32_t v) {
+  return wave_reduce_dpp(v, 0u, [](uint32_t a, uint32_t b) { return a > b ? a : b; });
+}
+
 __device__ __forceinline__ float wave_sum_f32(float v) {
 #pragma unroll
   for (int off = 32; off > 0; off >>= 1) v += __shfl_xor(v, off, 64);

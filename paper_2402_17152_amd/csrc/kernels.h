@@ -16,6 +16,9 @@ struct JaggedArgs {
   const int64_t* num_targets;  // may be null
   const float* rab_pos;
   const float* rab_time;
+  // [2B] per-sequence timestamp min / max (workspace, filled by
+  // launch_seq_time_range before the attention kernels run).
+  const int64_t* seq_trange;
   int32_t num_seqs;
   int32_t max_seq_len;  // N
   int32_t num_heads;
@@ -35,7 +38,7 @@ struct Tensors {
 // Tile sizes of the bf16 MFMA kernels.
 constexpr int kFwdBM = 128;  // query rows per forward workgroup
 constexpr int kFwdBN = 32;   // keys per forward step
-constexpr int kBwdBN = 128;  // keys owned by a backward workgroup (8 waves x 16)
+constexpr int kBwdBN = 128;  // keys owned by a backward workgroup (4 waves x 32)
 constexpr int kBwdBM = 32;   // query rows per backward step
 constexpr size_t kLdsBytes = 160 * 1024;  // LDS a gfx950 workgroup may allocate
 
@@ -52,6 +55,9 @@ hipError_t launch_schedule(const JaggedArgs& ja, int mode, WorkItem* items, int3
                            hipStream_t s);
 
 hipError_t launch_fill_f32(float* p, int64_t n, float value, hipStream_t s);
+// Per-sequence timestamp min / max into out[2b], out[2b+1] (0, 0 for an
+// empty sequence).
+hipError_t launch_seq_time_range(const JaggedArgs& ja, int64_t* out, hipStream_t s);
 hipError_t launch_complete_cumsum(int32_t n, const int64_t* in, int64_t* out, int square_of_diff,
                                   hipStream_t s);
 hipError_t launch_bucketize(int32_t num_seqs, int32_t num_buckets, const int64_t* seq_offsets,

@@ -156,6 +156,48 @@ int grid_for(int64_t n, int threads) {
   return (int)(g < 1 ? 1 : g);
 }
 
+// Per-sequence timestamp extremes (one workgroup per sequence; eight
+// independent loads in flight per thread).  The attention kernels use them
+// to pick 32-bit rebased time arithmetic when a sequence spans < 2^31.
+constexpr int kRangeThreads = 256;
+__global__ __launch_bounds__(kRangeThreads) void seq_time_range_kernel(JaggedArgs ja, int64_t* out) {
+  __shared__ int64_t red[2][kRangeThreads / 64];
+  const int b = blockIdx.x, tid = threadIdx.x;
+  const int64_t o = ja.seq_offsets[b];
+  const int L = (int)(ja.seq_offsets[b + 1] - o);
+  const int64_t* ts = ja.timestamps + o;
+  int64_t lo = 0x7fffffffffffffffll, hi = -0x7fffffffffffffffll - 1;
+  for (int x0 = 0; x0 < L; x0 += 8 * kRangeThreads) {
+    int64_t v[8];
+#pragma unroll
+    for (int k = 0; k < 8; k++) v[k] = ts[min(x0 + k * kRangeThreads + tid, L - 1)];
+#pragma unroll
+    for (int k = 0; k < 8; k++) {
+      lo = v[k] < lo ? v[k] : lo;
+      hi = v[k] > hi ? v[k] : hi;
+    }
+  }
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) {
+    const int64_t a = __shfl_xor(lo, off, 64), c = __shfl_xor(hi, off, 64);
+    lo = a < lo ? a : lo;
+    hi = c > hi ? c : hi;
+  }
+  if ((tid & 63) == 0) {
+    red[0][tid >> 6] = lo;
+    red[1][tid >> 6] = hi;
+  }
+  __syncthreads();
+  if (tid == 0) {
+    for (int w = 1; w < kRangeThreads / 64; w++) {
+      lo = red[0][w] < lo ? red[0][w] : lo;
+      hi = red[1][w] > hi ? red[1][w] : hi;
+    }
+    out[2 * b] = L > 0 ? lo : 0;
+    out[2 * b + 1] = L > 0 ? hi : 0;
+  }
+}
+
 }  // namespace
 
 hipError_t launch_schedule(const JaggedArgs& ja, int mode, WorkItem* items, int32_t* count,
@@ -164,6 +206,12 @@ hipError_t launch_schedule(const JaggedArgs& ja, int mode, WorkItem* items, int3
                        : (ja.max_seq_len + kBwdBM - 1) / kBwdBM;
   size_t lds = sizeof(int) * (size_t)(maxw + 1);
   hipLaunchKernelGGL(schedule_kernel, dim3(1), dim3(kSchedThreads), lds, s, ja, mode, items, count);
+  return hipGetLastError();
+}
+
+hipError_t launch_seq_time_range(const JaggedArgs& ja, int64_t* out, hipStream_t s) {
+  if (ja.num_seqs <= 0) return hipSuccess;
+  hipLaunchKernelGGL(seq_time_range_kernel, dim3(ja.num_seqs), dim3(kRangeThreads), 0, s, ja, out);
   return hipGetLastError();
 }
 
