@@ -139,7 +139,7 @@ struct Layout {
   size_t fwd_items;
   size_t bwd_items;
   size_t trange;    // int64 [2B]: per-sequence timestamp min / max
-  size_t dq_acc;    // fp32 [T][h][d_qk] (bf16 problems)
+  size_t dq_acc;    // fp32 [h][T][d_qk] (bf16 problems)
   size_t total;
   int64_t max_fwd, max_bwd;
 };
@@ -311,7 +311,8 @@ hstu_status_t hstu_attn_bwd(const hstu_problem_t* p, const hstu_jagged_t* j, con
                                     d_rab_time, items, counts + 1, l.max_bwd, s),
                "attn_bwd launch");
     }
-    HSTU_HIP(launch_dq_convert_bf16(dq_acc, dq, ndq, 1.0f / (float)N, s), "dq convert launch");
+    HSTU_HIP(launch_dq_convert_bf16(dq_acc, dq, T, H, p->d_qk, 1.0f / (float)N, s),
+             "dq convert launch");
     return ok();
   } catch (...) {
     return fail(HSTU_ERR_INVALID_ARGUMENT, "internal error");

@@ -32,12 +32,20 @@
 //   time table: a (wave, step) tile whose |t_i - t_j| fall in one or two
 //        log2 buckets adds its dS sum to a running per-lane sum (flushed
 //        when the bucket changes);
-//   position table: history pairs of a full tile lie on 63 diagonals;
-//        rotating register q of every lane by its row offset (ds_bpermute)
-//        puts all of a lane's values on one diagonal (or the next one
-//        after wrapping), which is carried into the next step.
-// Other tiles (diagonal, ragged, candidates, 64-bit timestamps) evaluate
-// each pair and use LDS atomics.
+//   position table: history pairs have p(i) - p(j) = i - j.  Rotating
+//        register q of every lane by its row offset (ds_bpermute) puts a
+//        lane's values on one diagonal, except those that crossed into
+//        the other half of the wave, which lie on the diagonal that the
+//        partner lane (other half) owns one step later and are handed to
+//        it.  Each lane then stores one sum per step, with a plain LDS
+//        store, into a ring of diagonals of its own (wave, half); a chunk
+//        of 32 diagonals is complete once the rows have moved past it and
+//        is then summed over the rings, added to the table in HBM and
+//        cleared.  Masked pairs carry dS = 0, so every tile takes this
+//        path; candidate rows (all at position n_h) add straight to HBM.
+// Tiles whose bucket is not fixed by the timestamp extremes (near the
+// diagonal, ragged, 64-bit timestamps) sum dS bucket by bucket over the
+// tile's bucket range.
 #include <type_traits>
 
 #include "bias.h"
@@ -100,6 +108,9 @@ struct BwdShared {
   uint32_t sRr[4][2];                      // rebased row timestamp min / max per step
   float sTab[64];                          // rab_time by slot (bias.h)
   float sTacc[64];                         // time-table gradient by slot
+  // Position-gradient rings, one per (wave, half): diagonal k at k % 256.
+  static constexpr int kRing = 256;
+  float sRing[kBwdWaves][2][kRing];
 };
 
 struct BwdArgs {
@@ -111,7 +122,6 @@ struct BwdArgs {
   uint16_t* dV;
   float* d_rab_pos;
   float* d_rab_time;
-  int pos_in_lds;
 };
 
 __device__ __forceinline__ float silu_sigma(float x) {
@@ -119,9 +129,8 @@ __device__ __forceinline__ float silu_sigma(float x) {
 }
 
 template <int DQK, int DV, bool FAST>
-__device__ __forceinline__ void bwd_item(BwdShared<DQK, DV>& sm, float* __restrict__ sPos,
-                                         const BwdArgs& A, int64_t o, int L, int n_h, int j0,
-                                         int head, int64_t tbase) {
+__device__ __forceinline__ void bwd_item(BwdShared<DQK, DV>& sm, const BwdArgs& A, int64_t o,
+                                         int L, int n_h, int j0, int head, int64_t tbase) {
   using Sh = BwdShared<DQK, DV>;
   using QT = typename Sh::QT;
   using OT = typename Sh::OT;
@@ -257,10 +266,10 @@ __device__ __forceinline__ void bwd_item(BwdShared<DQK, DV>& sm, float* __restri
   // every dQ step is a full one) -- so one vmcnt value before each barrier
   // retires exactly the operations of two steps back.
   constexpr int OPS_PER_STEP = QT::OPW + OT::OPW + 3 + 1 + 16;
-  const __amdgpu_buffer_rsrc_t qrs = make_rsrc(qg, (uint32_t)(L * A.t.q_stride * 2));
-  const __amdgpu_buffer_rsrc_t ors = make_rsrc(dog, (uint32_t)L * dostride_b);
-  const __amdgpu_buffer_rsrc_t trs = make_rsrc(ts, (uint32_t)L * 8u);
-  const __amdgpu_buffer_rsrc_t prs = make_rsrc(ja.rab_pos, (uint32_t)(2 * N - 1) * 4u);
+  const u32x4 qrs = rsrc_words(qg, (uint32_t)(L * A.t.q_stride * 2));
+  const u32x4 ors = rsrc_words(dog, (uint32_t)L * dostride_b);
+  const u32x4 trs = rsrc_words(ts, (uint32_t)L * 8u);
+  const u32x4 prs = rsrc_words(ja.rab_pos, (uint32_t)(2 * N - 1) * 4u);
   // Lane offsets of this wave's tile operations: linear chunk g = 64 op +
   // lane is row g / PC, stored chunk g % PC, holding logical chunk
   // (g % PC) ^ swz(row) (pad chunks repeat chunk 0); operations past the
@@ -282,11 +291,11 @@ __device__ __forceinline__ void bwd_item(BwdShared<DQK, DV>& sm, float* __restri
     const int i0 = row0(u), slot = u & 3;
 #pragma unroll
     for (int k = 0; k < QT::OPW; k++)
-      dma_to_lds16(qrs, sm.ring.t.q[slot] + 1024 * min(wave * QT::OPW + k, QT::OPS - 1),
+      dma_to_lds16_asm(qrs, sm.ring.t.q[slot] + 1024 * min(wave * QT::OPW + k, QT::OPS - 1),
                    qoffs[k] + (uint32_t)i0 * qstride_b);
 #pragma unroll
     for (int k = 0; k < OT::OPW; k++)
-      dma_to_lds16(ors, sm.ring.t.dO[slot] + 1024 * min(wave * OT::OPW + k, OT::OPS - 1),
+      dma_to_lds16_asm(ors, sm.ring.t.dO[slot] + 1024 * min(wave * OT::OPW + k, OT::OPS - 1),
                    ooffs[k] + (uint32_t)i0 * dostride_b);
   };
   // Reversed rab_pos window of step u: W[y] = rab_pos[pb - y] with
@@ -299,12 +308,12 @@ __device__ __forceinline__ void bwd_item(BwdShared<DQK, DV>& sm, float* __restri
 #pragma unroll
     for (int k = 0; k < 3; k++) {
       const int op = 3 * wave + k, c = op / 3, ch = op % 3;
-      dma_to_lds4(prs, &sm.sWin[u & 3][c][Sh::kWinPad + 64 * ch],
+      dma_to_lds4_asm(prs, &sm.sWin[u & 3][c][Sh::kWinPad + 64 * ch],
                   (uint32_t)(pb - 64 * ch - lane - c) * 4u);
     }
   };
   auto issue_ts = [&](int u) {
-    dma_to_lds4(trs, sm.sT[u & 7], (uint32_t)row0(u) * 8u + 4u * (uint32_t)lane);
+    dma_to_lds4_asm(trs, sm.sT[u & 7], (uint32_t)row0(u) * 8u + 4u * (uint32_t)lane);
   };
   // Wave 0: rebased row timestamps of a staged step and their range (zeros
   // past the sequence end only enter steps that are never full).
@@ -506,13 +515,15 @@ __device__ __forceinline__ void bwd_item(BwdShared<DQK, DV>& sm, float* __restri
     }
   };
   // dQ(rows of step u, the wave's 32 columns) over its keys, added to the
-  // fp32 workspace.  Lane holds (row i0 + 8g + 4*half + m, column 32 cbw +
-  // col).  The atomics go out after the next seed, among the step's
-  // contractions.
-  uint32_t dq_off[16];
-#pragma unroll
-  for (int q = 0; q < 16; q++)
-    dq_off[q] = (uint32_t)(((8 * (q >> 2) + 4 * half + (q & 3)) * H * DQK + 32 * cbw + col) * 4);
+  // fp32 workspace [h][T][d_qk] of the head with buffer atomics: lane holds
+  // (row i0 + 8g + 4*half + m, column 32 cbw + col); the row group goes
+  // into the lane offset and m into the immediate offset.  Rows past the
+  // sequence end fall outside the buffer and are dropped by the hardware.
+  // The atomics go out after the next seed, among the step's contractions.
+  const __amdgpu_buffer_rsrc_t dqrs =
+      make_rsrc(A.dq_acc + ((size_t)head * (size_t)ja.total_tokens + (size_t)o) * DQK,
+                (uint32_t)L * (uint32_t)DQK * 4u);
+  const uint32_t dq_lane = (uint32_t)((4 * half * DQK + 32 * cbw + col) * 4);
   auto dq_mfma = [&](int u, f32x16& qacc) {
     const uint16_t* dp = sm.sdST[u & 1] + (kbase + tr_row) * DST_LD + tr_col;
     qacc = f32x16{};
@@ -524,94 +535,131 @@ __device__ __forceinline__ void bwd_item(BwdShared<DQK, DV>& sm, float* __restri
     }
   };
   auto dq_atomics = [&](int u, const f32x16& qacc) {
-    const int i0 = row0(u);
-    char* base = (char*)(A.dq_acc + ((o + i0) * H + head) * DQK);
-    if (i0 + BM <= L) {
 #pragma unroll
-      for (int q = 0; q < 16; q++) unsafeAtomicAdd((float*)(base + dq_off[q]), qacc[q]);
-    } else {
+    for (int g = 0; g < 4; g++) {
+      const uint32_t vo = dq_lane + (uint32_t)((row0(u) + 8 * g) * DQK * 4);
 #pragma unroll
-      for (int q = 0; q < 16; q++)
-        if (i0 + 8 * (q >> 2) + 4 * half + (q & 3) < L)
-          unsafeAtomicAdd((float*)(base + dq_off[q]), qacc[q]);
+      for (int m = 0; m < 4; m++)
+        __builtin_amdgcn_raw_ptr_buffer_atomic_fadd_f32(qacc[4 * g + m], dqrs, vo + m * DQK * 4, 0, 0);
     }
   };
 
   // ---- bias gradients ----
-  // Time table: running per-lane sum for one slot, flushed on change.
-  int run_slot = -1;
-  float run_acc = 0.0f;
-  auto time_flush = [&]() {
-    if (run_slot >= 0) {
-      const float v = wave_sum_dpp(run_acc);
-      if (lane == 0) atomicAdd(&sm.sTacc[run_slot], v);
+  // Time table: running per-lane sums for up to two slots (the near and
+  // the far bucket of a tile), each flushed when its slot changes.
+  int run_slot[2] = {-1, -1};
+  float run_acc[2] = {0.0f, 0.0f};
+  auto time_flush = [&](int r) {
+    if (run_slot[r] >= 0) {
+      const float v = wave_sum_dpp(run_acc[r]);
+      if (lane == 0) atomicAdd(&sm.sTacc[run_slot[r]], v);
     }
-    run_acc = 0.0f;
+    run_acc[r] = 0.0f;
   };
-  auto time_add = [&](int slot, float v) {
-    if (slot != run_slot) {
-      time_flush();
-      run_slot = slot;
+  auto time_add = [&](int r, int slot, float v) {
+    if (slot != run_slot[r]) {
+      time_flush(r);
+      run_slot[r] = slot;
     }
-    run_acc += v;
+    run_acc[r] += v;
   };
-  // Position table, full tiles: register q of every lane is rotated by
-  // r0(q) = 8g + m lanes over the whole wave (ds_bpermute at this lane's
-  // address plus an immediate offset).  Lane (col, half) then holds pairs
-  // of diagonal i - j = (i0 - jw0) - col + 4*half, or, where col + r0(q)
-  // crossed into the other half, (i0 - jw0) + 32 - col + 4*(1 - half).
-  // Both sums go to the LDS accumulator.  (Every pair of a full tile is
-  // kept, so a diagonal holding a nonzero sum is a real one; the crossing
-  // one is clamped for lanes that have no crossing pair.)
+
+  // Position table.  Lane (col, half) reads register q = 4g + m from lane
+  // + r0, r0 = 8g + m (mod 64): the pair (row 8g + 4*half' + m, key col')
+  // then lies on diagonal D1 = (i0 - jw0) - col + 4*half if col + r0 < 32,
+  // else on D1 of the partner lane (col, 1 - half) one step later.
+  constexpr int kRing = Sh::kRing;
   const int perm_base = lane * 4;
   float wrap_w[16];
 #pragma unroll
   for (int q = 0; q < 16; q++) wrap_w[q] = col + 8 * (q >> 2) + (q & 3) >= 32 ? 1.0f : 0.0f;
-  const int R = L - j0;  // p(i) - p(j) of kept pairs lies in [0, R)
-  auto pos_add = [&](int k, float v) {  // k = p(i) - p(j) >= 0
-    if (A.pos_in_lds)
-      atomicAdd(&sPos[k], v);
-    else
-      unsafeAtomicAdd(&A.d_rab_pos[(N - 1) - k], v * invN);
+  float* const ring_mine = sm.sRing[wave][half];
+  const int d1_lane = 4 * half - col - 32 * wave;  // D1 = 32 u + d1_lane
+  float carry = 0.0f;  // partner's crossing sum of the previous step
+  auto pos_step = [&](int u, const float (&ds)[16]) {
+    float sum = 0.0f, wsum = 0.0f;
+#pragma unroll
+    for (int q = 0; q < 16; q++) {
+      const float rv = __int_as_float(__builtin_amdgcn_ds_bpermute(
+          perm_base + 4 * (8 * (q >> 2) + (q & 3)), __float_as_int(ds[q])));
+      sum += rv;
+      wsum = __builtin_fmaf(rv, wrap_w[q], wsum);
+    }
+    ring_mine[(32 * u + d1_lane) & (kRing - 1)] = (sum - wsum) + carry;
+    carry = __int_as_float(__builtin_amdgcn_ds_bpermute(perm_base ^ 128, __float_as_int(wsum)));
+  };
+  // Diagonals [32c, 32c + 31] are complete after step c + 4; one wave sums
+  // them over the rings, adds them to the table and clears them after the
+  // next barrier.
+  const int R = L - j0;  // p(i) - p(j) of kept history pairs lies in [0, R)
+  auto ring_flush = [&](int c) {
+    if (lane < 32) {
+      const int k = 32 * c + lane, sl = k & (kRing - 1);
+      float v = 0.0f;
+#pragma unroll
+      for (int w = 0; w < kBwdWaves; w++)
+#pragma unroll
+        for (int h = 0; h < 2; h++) {
+          v += sm.sRing[w][h][sl];
+          sm.sRing[w][h][sl] = 0.0f;
+        }
+      if (v != 0.0f && k < R) unsafeAtomicAdd(&A.d_rab_pos[(N - 1) - k], v * invN);
+    }
   };
 
   auto grads = [&](int u, const Path& pth, const float (&ds)[16]) {
     const int i0 = row0(u);
-    if (pth.kind() != kGeneral) {
-      float sum = 0.0f, wsum = 0.0f, tot = 0.0f, far = 0.0f;
+    if (i0 + BM - 1 >= n_h && i0 < L) {
+      // Candidate rows: position n_h for every one; straight to HBM, and
+      // out of the diagonal sums.
+      float dh[16];
 #pragma unroll
       for (int q = 0; q < 16; q++) {
-        const int r0 = 8 * (q >> 2) + (q & 3);
-        const float rv = __int_as_float(
-            __builtin_amdgcn_ds_bpermute(perm_base + 4 * r0, __float_as_int(ds[q])));
-        sum += rv;
-        wsum = __builtin_fmaf(rv, wrap_w[q], wsum);
-        tot += ds[q];
+        const int i = i0 + 8 * (q >> 2) + 4 * half + (q & 3);
+        dh[q] = i < n_h ? ds[q] : 0.0f;
+        if (i >= n_h && i < L && key_ok && pair_valid(i, my_j, n_h))
+          unsafeAtomicAdd(&A.d_rab_pos[(N - 1) - (n_h - pj)], ds[q] * invN);
       }
-      pos_add((i0 - jw0) - col + 4 * half, sum - wsum);
-      pos_add(min((i0 - jw0) + 32 - col + 4 * (1 - half), R - 1), wsum);
+      pos_step(u, dh);
+    } else {
+      pos_step(u, ds);
+    }
+    if (pth.kind() != kGeneral) {
+      float tot = 0.0f;
+#pragma unroll
+      for (int q = 0; q < 16; q++) tot += ds[q];
       if (pth.kind() == kTwo) {
         uint32_t ti[16];
         row_ts(u, ti);
         const uint32_t lim = tjr + pth.thr();
+        float far = 0.0f;
 #pragma unroll
         for (int q = 0; q < 16; q++) far += ti[q] >= lim ? ds[q] : 0.0f;
-        time_add(pth.slot(), tot - far);
-        const float v = wave_sum_dpp(far);
-        if (lane == 0) atomicAdd(&sm.sTacc[pth.slot_far()], v);
+        time_add(0, pth.slot(), tot - far);
+        time_add(1, pth.slot_far(), far);
       } else {
-        time_add(pth.slot(), tot);
+        time_add(0, pth.slot(), tot);
       }
     } else {
+      // Bucket by bucket over the slots of the tile's valid pairs.
       int sl[16];
       pair_slots(u, sl);
+      uint32_t lo = 64, hi = 0;
 #pragma unroll
       for (int q = 0; q < 16; q++) {
         const int i = i0 + 8 * (q >> 2) + 4 * half + (q & 3);
-        if (key_ok && i < L && pair_valid(i, my_j, n_h)) {
-          pos_add(bias_pos(i, n_h) - pj, ds[q]);
-          atomicAdd(&sm.sTacc[sl[q]], ds[q]);
-        }
+        if (!(key_ok && i < L && pair_valid(i, my_j, n_h))) sl[q] = 64;
+        lo = min(lo, (uint32_t)sl[q]);
+        hi = sl[q] < 64 ? max(hi, (uint32_t)sl[q]) : hi;
+      }
+      lo = wave_min_dpp(lo);
+      hi = wave_max_dpp(hi);
+      for (int b = (int)lo; b <= (int)hi; b++) {
+        float acc = 0.0f;
+#pragma unroll
+        for (int q = 0; q < 16; q++) acc += sl[q] == b ? ds[q] : 0.0f;
+        acc = wave_sum_dpp(acc);
+        if (lane == 0 && acc != 0.0f) atomicAdd(&sm.sTacc[b], acc);
       }
     }
   };
@@ -623,6 +671,7 @@ __device__ __forceinline__ void bwd_item(BwdShared<DQK, DV>& sm, float* __restri
   auto step = [&](int u, f32x16& s_cur, f32x16& p_cur, f32x16& s_next, f32x16& p_next) {
     wait_vmcnt_lgkmcnt0<OPS_PER_STEP>();
     barrier_no_fence();
+    if (u >= 5 && wave == (u & 3)) ring_flush(u - 5);
     issue_tiles(u + 3);
     issue_win(u + 3);
     issue_ts(u + 5);
@@ -689,7 +738,17 @@ __device__ __forceinline__ void bwd_item(BwdShared<DQK, DV>& sm, float* __restri
     dq_mfma(nsteps - 1, qacc);
     dq_atomics(nsteps - 1, qacc);
   }
-  time_flush();
+  time_flush(0);
+  time_flush(1);
+  // The last crossing sums belong to D1 of step nsteps; then the chunks
+  // not flushed inside the loop, max(0, nsteps - 5) .. nsteps.
+  ring_mine[(32 * nsteps + d1_lane) & (kRing - 1)] = carry;
+  wait_vmcnt_lgkmcnt0<0>();
+  barrier_no_fence();
+  {
+    const int c0 = max(0, nsteps - 5);
+    for (int c = c0 + wave; c <= nsteps; c += kBwdWaves) ring_flush(c);
+  }
 
   // dK, dV of the wave's keys: lane holds (key jw0 + 8g + 4*half + m, feature 32nb + col).
 #pragma unroll
@@ -712,7 +771,6 @@ __global__ __launch_bounds__(kBwdThreads, 1) void attn_bwd_bf16_kernel(
   using S = BwdShared<DQK, DV>;
   constexpr int BN = S::BN;
   __shared__ S sm;
-  extern __shared__ float sPosAcc[];  // [N] when pos_in_lds
 
   if ((int)blockIdx.x >= *count) return;
   const WorkItem it = items[blockIdx.x];
@@ -735,23 +793,16 @@ __global__ __launch_bounds__(kBwdThreads, 1) void attn_bwd_bf16_kernel(
     sm.sTab[x] = (fast && x == 31) ? ja.rab_time[0] : ja.rab_time[min(63 - x, NB - 1)];
     sm.sTacc[x] = 0.0f;
   }
-  const int R = L - j0;  // p(i) - p(j) of kept pairs lies in [0, R)
-  if (A.pos_in_lds)
-    for (int x = tid; x < R; x += kBwdThreads) sPosAcc[x] = 0.0f;
+  for (int x = tid; x < kBwdWaves * 2 * S::kRing; x += kBwdThreads) (&sm.sRing[0][0][0])[x] = 0.0f;
   __syncthreads();
   if (fast) {
-    bwd_item<DQK, DV, true>(sm, sPosAcc, A, o, L, n_h, j0, head, tlo);
+    bwd_item<DQK, DV, true>(sm, A, o, L, n_h, j0, head, tlo);
   } else {
-    bwd_item<DQK, DV, false>(sm, sPosAcc, A, o, L, n_h, j0, head, tlo);
+    bwd_item<DQK, DV, false>(sm, A, o, L, n_h, j0, head, tlo);
   }
 
   __syncthreads();
   const float invN = 1.0f / (float)N;
-  if (A.pos_in_lds)
-    for (int x = tid; x < R; x += kBwdThreads) {
-      const float v = sPosAcc[x];
-      if (v != 0.0f) unsafeAtomicAdd(&A.d_rab_pos[(N - 1) - x], v * invN);
-    }
   if (tid < 64) {
     const float v = sm.sTacc[tid];
     const int b = (fast && tid == 31) ? 0 : min(63 - tid, NB - 1);
@@ -773,12 +824,9 @@ hipError_t launch_bwd(const JaggedArgs& ja, const Tensors& t, const void* d_out,
   A.dV = (uint16_t*)dv;
   A.d_rab_pos = d_rab_pos;
   A.d_rab_time = d_rab_time;
-  // The position-gradient accumulator (N floats) joins the static LDS when
-  // both fit in the 160 KiB a gfx950 workgroup may use.
-  A.pos_in_lds = sizeof(BwdShared<DQK, DV>) + sizeof(float) * (size_t)ja.max_seq_len <= kLdsBytes;
-  const size_t lds = A.pos_in_lds ? sizeof(float) * (size_t)ja.max_seq_len : 0;
+  static_assert(sizeof(BwdShared<DQK, DV>) <= kLdsBytes, "LDS budget");
   dim3 grid((unsigned)max_items, (unsigned)ja.num_heads);
-  hipLaunchKernelGGL((attn_bwd_bf16_kernel<DQK, DV>), grid, dim3(kBwdThreads), lds, s, A, items,
+  hipLaunchKernelGGL((attn_bwd_bf16_kernel<DQK, DV>), grid, dim3(kBwdThreads), 0, s, A, items,
                      count);
   return hipGetLastError();
 }

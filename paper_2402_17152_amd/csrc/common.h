@@ -113,6 +113,33 @@ __device__ __forceinline__ void dma_to_lds4(__amdgpu_buffer_rsrc_t r, void* lds,
                                            off, 0, 0, 0);
 }
 
+// The same LDS DMA issued from inline assembly, on a resource given as its
+// four descriptor words.  The compiler does not see these as pending LDS
+// writes, so it does not make later LDS reads wait for every outstanding
+// vector-memory operation (it cannot tell ring slots of one array apart);
+// the caller orders the data with explicit vmcnt waits and barriers.  The
+// statement sets M0, which the kernels using it keep no value in.
+__device__ __forceinline__ u32x4 rsrc_words(const void* base, uint32_t bytes) {
+  const uint64_t a = (uint64_t)base;
+  return u32x4{(uint32_t)a, (uint32_t)(a >> 32) & 0xffffu, bytes, 0x00020000u};
+}
+
+__device__ __forceinline__ void dma_to_lds16_asm(u32x4 r, void* lds, uint32_t off) {
+  const uint32_t l = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) void*)lds;
+  asm volatile("s_mov_b32 m0, %0\n\tbuffer_load_dwordx4 %1, %2, 0 offen lds"
+               :
+               : "s"(l), "v"(off), "s"(r)
+               : "memory");
+}
+
+__device__ __forceinline__ void dma_to_lds4_asm(u32x4 r, void* lds, uint32_t off) {
+  const uint32_t l = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) void*)lds;
+  asm volatile("s_mov_b32 m0, %0\n\tbuffer_load_dword %1, %2, 0 offen lds"
+               :
+               : "s"(l), "v"(off), "s"(r)
+               : "memory");
+}
+
 // s_waitcnt vmcnt(VM) lgkmcnt(0) (gfx9 encoding: vmcnt in bits 3:0 and
 // 15:14, expcnt in 6:4, lgkmcnt in 11:8).
 template <int VM>

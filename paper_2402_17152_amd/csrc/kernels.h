@@ -72,8 +72,9 @@ hipError_t launch_attn_bwd_bf16(const JaggedArgs& ja, const Tensors& t, int dqk,
                                 const void* d_out, float* dq_acc, void* dk, void* dv_out,
                                 float* d_rab_pos, float* d_rab_time, const WorkItem* items,
                                 const int32_t* count, int64_t max_items, hipStream_t s);
-hipError_t launch_dq_convert_bf16(const float* acc, void* dq, int64_t n, float scale,
-                                  hipStream_t s);
+// fp32 head-major dQ accumulator [h][T][d] -> bf16 token-major [T][h][d], scaled.
+hipError_t launch_dq_convert_bf16(const float* acc, void* dq, int64_t T, int32_t H, int32_t d,
+                                  float scale, hipStream_t s);
 
 // fp32 SIMT attention.
 hipError_t launch_attn_fwd_f32(const JaggedArgs& ja, const Tensors& t, int dqk, int dv, void* out,

@@ -139,11 +139,17 @@ __global__ __launch_bounds__(kSchedThreads) void cumsum_kernel(int32_t n, const 
   }
 }
 
+// acc is head-major [h][T][d] (fp32), dq token-major [T][h][d] (bf16);
+// one thread per 4 features.
 __global__ void dq_convert_kernel(const float* __restrict__ acc, uint16_t* __restrict__ dq,
-                                  int64_t n4, float scale) {
+                                  int64_t T, int32_t H, int32_t d4, float scale) {
+  const int64_t n4 = T * H * d4;
   int64_t stride = (int64_t)gridDim.x * blockDim.x;
   for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n4; i += stride) {
-    f32x4 a = reinterpret_cast<const f32x4*>(acc)[i];
+    const int64_t row = i / d4;  // t * H + h
+    const int64_t c = i - row * d4;
+    const int64_t t = row / H, h = row - t * H;
+    f32x4 a = reinterpret_cast<const f32x4*>(acc)[(h * T + t) * d4 + c];
     uint32_t lo = pack_bf16x2(a[0] * scale, a[1] * scale);
     uint32_t hi = pack_bf16x2(a[2] * scale, a[3] * scale);
     reinterpret_cast<uint2*>(dq)[i] = make_uint2(lo, hi);
@@ -228,12 +234,12 @@ hipError_t launch_complete_cumsum(int32_t n, const int64_t* in, int64_t* out, in
   return hipGetLastError();
 }
 
-hipError_t launch_dq_convert_bf16(const float* acc, void* dq, int64_t n, float scale,
-                                  hipStream_t s) {
-  if (n <= 0) return hipSuccess;
-  int64_t n4 = n / 4;  // n is a multiple of 32 (d_qk)
+hipError_t launch_dq_convert_bf16(const float* acc, void* dq, int64_t T, int32_t H, int32_t d,
+                                  float scale, hipStream_t s) {
+  const int64_t n4 = T * H * (d / 4);  // d is a multiple of 32
+  if (n4 <= 0) return hipSuccess;
   hipLaunchKernelGGL(dq_convert_kernel, dim3(grid_for(n4, 256)), dim3(256), 0, s, acc,
-                     (uint16_t*)dq, n4, scale);
+                     (uint16_t*)dq, T, H, d / 4, scale);
   return hipGetLastError();
 }
 
