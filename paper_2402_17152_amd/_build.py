@@ -26,11 +26,17 @@ FLAGS = [
     "-munsafe-fp-atomics",
     "-Wall", "-Wno-unused-function",
 ]
+# Per-file extras.  The backward kernel runs one wave per SIMD, so its
+# LDS reads must be issued well ahead of their MFMAs; LLVM's ILP-first
+# machine scheduler does that, the default one serialises them.
+EXTRA = {
+    "attn_bwd.hip": ["-mllvm", "-amdgpu-sched-strategy=iterative-ilp"],
+}
 
 
 def _compile(src: str) -> str:
     obj = os.path.join(BUILD, os.path.basename(src) + ".o")
-    cmd = [HIPCC, *FLAGS, "-x", "hip", "-c", os.path.join(CSRC, src), "-o", obj]
+    cmd = [HIPCC, *FLAGS, *EXTRA.get(src, []), "-x", "hip", "-c", os.path.join(CSRC, src), "-o", obj]
     r = subprocess.run(cmd, capture_output=True, text=True)
     if r.returncode != 0:
         raise RuntimeError(f"hipcc failed for {src}:\n{r.stderr}")

@@ -260,11 +260,14 @@ __device__ __forceinline__ void bwd_item(BwdShared<DQK, DV>& sm, const BwdArgs& 
 
   // ---- staging: LDS DMA straight from global memory ----
   // Q, dO and the rab_pos window of step u travel three steps ahead (ring
-  // of 4), row timestamps five (ring of 8).  Every wave issues the same
-  // number of vector-memory operations per step -- the DMA operations and
-  // the 16 dQ atomics (vmcnt counts both, in issue order; inside the loop
-  // every dQ step is a full one) -- so one vmcnt value before each barrier
-  // retires exactly the operations of two steps back.
+  // of 4), row timestamps five (ring of 8).  vmcnt counts the DMA
+  // operations and the dQ atomics in issue order.  Every wave issues, per
+  // step, its DMA operations first and then (from step 1 on) 16 dQ
+  // atomics, and possibly a few more atomics (flushes, candidate rows);
+  // extra operations only make a vmcnt wait stricter.  Step u needs the
+  // DMA of step u - 2, which is followed by that step's atomics and all of
+  // step u - 1's operations: the wait lets those stay in flight, so the
+  // atomics get about two steps to complete.
   constexpr int OPS_PER_STEP = QT::OPW + OT::OPW + 3 + 1 + 16;
   const u32x4 qrs = rsrc_words(qg, (uint32_t)(L * A.t.q_stride * 2));
   const u32x4 ors = rsrc_words(dog, (uint32_t)L * dostride_b);
@@ -669,7 +672,10 @@ __device__ __forceinline__ void bwd_item(BwdShared<DQK, DV>& sm, const BwdArgs& 
   // dV, dK of step u; dS^T(u) to LDS; bias gradients of step u.
   Path path_cur, path_next, path_nn;
   auto step = [&](int u, f32x16& s_cur, f32x16& p_cur, f32x16& s_next, f32x16& p_next) {
-    wait_vmcnt_lgkmcnt0<OPS_PER_STEP>();
+    if (u >= 3)
+      wait_vmcnt_lgkmcnt0<OPS_PER_STEP + 16>();
+    else
+      wait_vmcnt_lgkmcnt0<OPS_PER_STEP>();
     barrier_no_fence();
     if (u >= 5 && wave == (u & 3)) ring_flush(u - 5);
     issue_tiles(u + 3);
