@@ -40,7 +40,84 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true",
                     help="skip the oracle timing (profiling runs)")
     ap.add_argument("--no-kernel-timing", action="store_true")
+    ap.add_argument("--no-aux", action="store_true",
+                    help="skip the MFMA probe, bucketize and clock measurements")
     return ap.parse_args()
+
+
+def percentile(xs, q):
+    xs = sorted(xs)
+    k = (len(xs) - 1) * q
+    lo, hi = int(k), min(int(k) + 1, len(xs) - 1)
+    return xs[lo] + (xs[hi] - xs[lo]) * (k - lo)
+
+
+def gpu_clock():
+    """The clock lines rocm-smi prints for the device (best effort)."""
+    import subprocess
+    try:
+        r = subprocess.run(["rocm-smi", "--showclocks"], capture_output=True, text=True, timeout=20)
+    except (OSError, subprocess.SubprocessError):
+        return None
+    lines = [ln.strip() for ln in r.stdout.splitlines() if "clock level" in ln]
+    return lines or None
+
+
+def aux_measurements(hstu, torch, d, batch, stream):
+    """Outside the timed region: the matrix-core rate of a kernel that only
+    issues bf16 MFMAs (the measured ceiling the attention kernels are also
+    compared against), and the standalone bucketize kernel's write rate
+    with the 256 MB last-level cache warm and flushed."""
+    out = {}
+    sink = torch.empty(256, dtype=torch.float32, device="cuda")
+    rates = []
+    for _ in range(4):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        flop = hstu.hstu_probe_mfma_bf16(20000, 2, sink, stream=stream)
+        e1.record(stream)
+        torch.cuda.synchronize()
+        rates.append(flop / (e0.elapsed_time(e1) * 1e-3) / 1e12)
+    out["mfma_probe"] = {"tflops": max(rates[1:]), "frac_of_spec": max(rates[1:]) / PEAK_BF16_TFLOPS,
+                         "kernel": "bf16 v_mfma_f32_32x32x16, 8 independent chains per wave, "
+                                   "2 waves per SIMD, every CU"}
+    po = hstu.hstu_pair_offsets(d["seq_offsets"], stream=stream)
+    total_pairs = int(po[-1].item())
+    buckets = torch.empty(total_pairs, dtype=torch.uint8, device="cuda")
+    flush = torch.empty(512 << 20, dtype=torch.uint8, device="cuda")
+    nbytes = total_pairs + 8 * batch.total_tokens
+    for mode in ("warm", "cold"):
+        ts = []
+        for _ in range(6):
+            if mode == "cold":
+                flush.zero_()
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record(stream)
+            hstu.hstu_time_bucketize(d["seq_offsets"], d["timestamps"], d["rab_time"].numel(),
+                                     pair_offsets=po, total_pairs=total_pairs, out=buckets,
+                                     stream=stream)
+            e1.record(stream)
+            torch.cuda.synchronize()
+            ts.append(e0.elapsed_time(e1))
+        ms = percentile(ts[1:], 0.5)
+        out[f"bucketize_{mode}"] = {"ms": ms, "gbs": nbytes / (ms * 1e-3) / 1e9,
+                                    "frac_hbm": nbytes / (ms * 1e-3) / 1e9 / PEAK_HBM_GBS,
+                                    "bytes": nbytes}
+    # Write-rate reference on the same buffer: the runtime's plain fill.
+    ts = []
+    for _ in range(6):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        buckets.zero_()
+        e1.record(stream)
+        torch.cuda.synchronize()
+        ts.append(e0.elapsed_time(e1))
+    ms = percentile(ts[1:], 0.5)
+    out["plain_fill_reference"] = {"ms": ms, "gbs": total_pairs / (ms * 1e-3) / 1e9,
+                                   "bytes": total_pairs}
+    del flush
+    out["gpu_clock"] = gpu_clock()
+    return out
 
 
 def source_hash(*names) -> str:
@@ -152,17 +229,18 @@ def main():
     hstu.hstu_timing_reset()
     if not args.no_kernel_timing:
         hstu.hstu_timing_enable(True)
-    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    evs = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps + 1)]
     torch.cuda.synchronize()
     t_wall = time.perf_counter()
-    ev0.record(stream)
-    for _ in range(args.steps):
+    evs[0].record(stream)
+    for k in range(args.steps):
         step()
-    ev1.record(stream)
+        evs[k + 1].record(stream)
     torch.cuda.synchronize()
     t_wall = time.perf_counter() - t_wall
     hstu.hstu_timing_enable(False)
-    ms = ev0.elapsed_time(ev1) / args.steps
+    ms = evs[0].elapsed_time(evs[-1]) / args.steps
+    per_step = [evs[k].elapsed_time(evs[k + 1]) for k in range(args.steps)]
 
     kernels = {}
     for name in ("attn_fwd", "ln_gate", "attn_bwd"):
@@ -191,6 +269,11 @@ def main():
                     "flop_per_launch": f_bwd if dom == "attn_bwd" else f_fwd,
                     "source_hash": src}
 
+    aux = None if args.no_aux else aux_measurements(hstu, torch, d, batch, stream)
+    if roofline is not None and aux is not None:
+        roofline["peak_measured"] = aux["mfma_probe"]["tflops"]
+        roofline["frac_measured"] = roofline["achieved"] / aux["mfma_probe"]["tflops"]
+
     tflops = flops_step / (ms * 1e-3) / 1e12
     rec = {
         "metric": METRIC,
@@ -200,6 +283,8 @@ def main():
         "steps": args.steps,
         "warmup": args.warmup,
         "ms_per_step": ms,
+        "ms_per_step_p10_p50_p90": [percentile(per_step, 0.1), percentile(per_step, 0.5),
+                                    percentile(per_step, 0.9)],
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
@@ -221,6 +306,7 @@ def main():
         "wall_s_timed": t_wall,
         "kernels": kernels,
         "roofline": roofline,
+        "aux": aux,
         "cpu_baseline": None,
     }
     if not args.no_cpu_baseline:

@@ -193,6 +193,16 @@ hstu_status_t hstu_timing_read(const char* name, double* total_ms,
                                int64_t* launches);
 hstu_status_t hstu_timing_reset(void);
 
+/* Matrix-core rate probe for measurement: launches on `stream` a kernel
+ * that issues only bf16 v_mfma_f32_32x32x16 instructions, `iters` x 8
+ * independent ones per wave, with `waves_per_simd` (1 or 2) waves on every
+ * SIMD of the device.  *flop receives the launch's flop count (2 per
+ * multiply-add); time the launch with events on the same stream (it is
+ * also recorded as kernel family "mfma_probe").  `sink` is device memory
+ * of at least 256 floats that the kernel may write.  iters in [1, 2^24]. */
+hstu_status_t hstu_probe_mfma_bf16(int32_t iters, int32_t waves_per_simd, float* sink,
+                                   double* flop, void* stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -362,8 +362,8 @@ hstu_status_t hstu_time_bucketize(int32_t num_seqs, int64_t total_tokens, int32_
       HSTU_TRY(check_dense("buckets", buckets, 16));
     }
     TimedScope ts("bucketize", (hipStream_t)hip_stream);
-    HSTU_HIP(launch_bucketize(num_seqs, num_time_buckets, seq_offsets, timestamps, pair_offsets,
-                              total_pairs, buckets, (hipStream_t)hip_stream),
+    HSTU_HIP(launch_bucketize(num_seqs, total_tokens, num_time_buckets, seq_offsets, timestamps,
+                              pair_offsets, total_pairs, buckets, (hipStream_t)hip_stream),
              "bucketize launch");
     return ok();
   } catch (...) {
@@ -434,6 +434,20 @@ hstu_status_t hstu_validate(const hstu_problem_t* p, const hstu_jagged_t* j, voi
   } catch (...) {
     return fail(HSTU_ERR_INVALID_ARGUMENT, "internal error");
   }
+}
+
+hstu_status_t hstu_probe_mfma_bf16(int32_t iters, int32_t waves_per_simd, float* sink,
+                                   double* flop, void* stream) {
+  if (iters < 1 || iters > (1 << 24))
+    return fail(HSTU_ERR_INVALID_ARGUMENT, "iters must be in [1, 2^24]");
+  if (waves_per_simd < 1 || waves_per_simd > 2)
+    return fail(HSTU_ERR_INVALID_ARGUMENT, "waves_per_simd must be 1 or 2");
+  if (sink == nullptr || flop == nullptr)
+    return fail(HSTU_ERR_INVALID_ARGUMENT, "sink and flop must not be null");
+  hipStream_t s = (hipStream_t)stream;
+  TimedScope ts("mfma_probe", s);
+  HSTU_HIP(launch_mfma_probe(iters, waves_per_simd, sink, flop, s), "mfma probe launch");
+  return ok();
 }
 
 hstu_status_t hstu_timing_enable(int32_t on) {

@@ -60,9 +60,10 @@ hipError_t launch_fill_f32(float* p, int64_t n, float value, hipStream_t s);
 hipError_t launch_seq_time_range(const JaggedArgs& ja, int64_t* out, hipStream_t s);
 hipError_t launch_complete_cumsum(int32_t n, const int64_t* in, int64_t* out, int square_of_diff,
                                   hipStream_t s);
-hipError_t launch_bucketize(int32_t num_seqs, int32_t num_buckets, const int64_t* seq_offsets,
-                            const int64_t* timestamps, const int64_t* pair_offsets,
-                            int64_t total_pairs, uint8_t* out, hipStream_t s);
+hipError_t launch_bucketize(int32_t num_seqs, int64_t total_tokens, int32_t num_buckets,
+                            const int64_t* seq_offsets, const int64_t* timestamps,
+                            const int64_t* pair_offsets, int64_t total_pairs, uint8_t* out,
+                            hipStream_t s);
 
 // bf16 MFMA attention.
 hipError_t launch_attn_fwd_bf16(const JaggedArgs& ja, const Tensors& t, int dqk, int dv, void* out,
@@ -82,6 +83,11 @@ hipError_t launch_attn_fwd_f32(const JaggedArgs& ja, const Tensors& t, int dqk, 
 hipError_t launch_attn_bwd_f32(const JaggedArgs& ja, const Tensors& t, int dqk, int dv,
                                const void* d_out, void* dq, void* dk, void* dv_out,
                                float* d_rab_pos, float* d_rab_time, hipStream_t s);
+
+// Matrix-core rate probe (benchmark support): `waves_per_simd` waves per
+// SIMD on every CU, each issuing iters x 8 independent bf16 32x32x16 MFMAs.
+hipError_t launch_mfma_probe(int32_t iters, int32_t waves_per_simd, float* sink, double* flop,
+                             hipStream_t s);
 
 // LayerNorm(x) (.) u per token over D features.
 hipError_t launch_ln_gate(int is_bf16, int64_t T, int32_t D, const void* x, const void* u,

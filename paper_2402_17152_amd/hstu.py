@@ -24,7 +24,7 @@ STATUS = {0: "HSTU_OK", 1: "HSTU_ERR_INVALID_ARGUMENT", 2: "HSTU_ERR_UNSUPPORTED
 EXPORTED = ("hstu_workspace_bytes", "hstu_attn_fwd", "hstu_attn_bwd", "hstu_layer_fwd",
             "hstu_time_bucketize", "hstu_complete_cumsum", "hstu_pair_offsets", "hstu_validate",
             "hstu_last_error", "hstu_abi_version", "hstu_timing_enable", "hstu_timing_read",
-            "hstu_timing_reset")
+            "hstu_timing_reset", "hstu_probe_mfma_bf16")
 
 
 class Problem(ctypes.Structure):
@@ -69,6 +69,7 @@ def _load():
         "hstu_timing_read": (i32, [ctypes.c_char_p, ctypes.POINTER(ctypes.c_double),
                                    ctypes.POINTER(ctypes.c_int64)]),
         "hstu_timing_reset": (i32, []),
+        "hstu_probe_mfma_bf16": (i32, [i32, i32, P, ctypes.POINTER(ctypes.c_double), P]),
     }
     for name, (res, args) in sig.items():
         fn = getattr(lib, name)
@@ -263,6 +264,14 @@ def hstu_timing_enable(on: bool = True):
 
 def hstu_timing_reset():
     _check(lib.hstu_timing_reset())
+
+
+def hstu_probe_mfma_bf16(iters: int, waves_per_simd: int, sink: torch.Tensor, stream=None):
+    """Launches the matrix-core rate probe; returns its flop count."""
+    flop = ctypes.c_double(0.0)
+    _check(lib.hstu_probe_mfma_bf16(int(iters), int(waves_per_simd), _ptr(sink),
+                                    ctypes.byref(flop), _stream(stream)))
+    return flop.value
 
 
 def hstu_timing_read(name: str):

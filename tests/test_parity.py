@@ -156,9 +156,10 @@ def test_workload_target_sampled(hs, oracle_mod):
 
 def test_bucketize_bit_exact(hs, oracle_mod):
     """Standalone bucketisation equals the oracle byte for byte, including
-    empty sequences, length 1, the clamp (B_t = 9) and a ragged total."""
+    empty sequences, length 1, the clamp (B_t = 9), a ragged total, rows
+    past one 4096-column slab and spans beyond 2^31 (the 64-bit path)."""
     rng = np.random.default_rng(9)
-    lens = np.array([0, 1, 17, 300, 0, 45, 1024, 3], dtype=np.int64)
+    lens = np.array([0, 1, 17, 300, 0, 45, 1024, 3, 5000, 4100], dtype=np.int64)
     offs = np.concatenate([[0], np.cumsum(lens)])
     T = int(offs[-1])
     ts = np.empty(T, dtype=np.int64)
@@ -166,6 +167,8 @@ def test_bucketize_bit_exact(hs, oracle_mod):
         s, e = offs[b], offs[b + 1]
         ts[s:e] = rng.integers(0, 1 << 40) + np.cumsum(rng.integers(0, 1 << int(rng.integers(1, 30)), e - s))
     ts[offs[6]:offs[7]] = rng.permutation(ts[offs[6]:offs[7]])   # unsorted sequence
+    # two column slabs on the 64-bit path (span ~ 2^41)
+    ts[offs[9]:offs[10]] = (1 << 50) + np.cumsum(rng.integers(0, 1 << 30, int(lens[9])))
     for nb in (128, 9):
         po_ref, bk_ref = oracle_mod.time_bucketize(offs, ts, nb)
         so = torch.from_numpy(offs).cuda()
