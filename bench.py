@@ -42,6 +42,9 @@ def parse():
     ap.add_argument("--no-kernel-timing", action="store_true")
     ap.add_argument("--no-aux", action="store_true",
                     help="skip the MFMA probe, bucketize and clock measurements")
+    ap.add_argument("--calibrate-copy", action="store_true",
+                    help="only copy 256 MiB device-to-device 3 times (the reference that "
+                         "scales rocprofv3 FETCH_SIZE / WRITE_SIZE to bytes), then exit")
     return ap.parse_args()
 
 
@@ -189,6 +192,17 @@ def main():
         sys.exit(2)
 
     import torch
+
+    if args.calibrate_copy:
+        n = 256 << 20
+        src = torch.empty(n, dtype=torch.uint8, device="cuda").fill_(1)
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        print(json.dumps({"calibration_copy_bytes": n, "copies": 3}), flush=True)
+        return
 
     from paper_2402_17152_amd import hstu, inputs
 

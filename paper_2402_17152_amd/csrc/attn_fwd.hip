@@ -31,9 +31,11 @@
 // from the timestamp ranges) the time term is one constant.  Other tiles
 // evaluate the mask and both terms per element.
 //
-// LDS staging: K tiles in a ring of 2, V tiles in a ring of 4 (V of tile t
-// is consumed one step after K), loaded from global two tiles ahead into
-// registers and stored at the end of a step; one barrier per tile.
+// LDS staging by LDS DMA (buffer loads that write LDS directly): K tiles
+// and rab_pos windows in rings of 3, issued three tiles ahead; V tiles in
+// a ring of 4, issued two ahead (V of tile t is consumed one step after
+// K); key timestamps five ahead.  One explicit vmcnt wait and one barrier
+// per tile.
 #include <type_traits>
 
 #include "bias.h"
