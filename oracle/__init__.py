@@ -51,6 +51,7 @@ def _load():
         lib.oracle_attn_bwd.argtypes = [i32, P, i32, i32, i32, i32, P, P, P, P,
                                         i32, P, P, P, P, P, P, P, P, P]
         lib.oracle_ln_gate.argtypes = [i64, i32, P, P, P, P, f64, P, P, P]
+        lib.oracle_ln_gate_bwd.argtypes = [i64, i32, P, P, P, P, P, f64, P, P, P, P]
         lib.oracle_num_threads.restype = i32
         _lib = lib
     return _lib
@@ -162,3 +163,23 @@ def ln_gate(x, u, gamma=None, beta=None, eps=1e-5):
     _load().oracle_ln_gate(T, D, _p(x), _p(u), _p(g), _p(b), float(eps), _p(y),
                            _p(mean), _p(rstd))
     return y, mean, rstd
+
+
+def ln_gate_bwd(x, u, dy, gamma=None, beta=None, eps=1e-5):
+    """Gradient of <ln_gate(x, u, gamma, beta), dy> (Eq. 3 epilogue);
+    returns (dx, du, dgamma, dbeta), dgamma / dbeta None when gamma / beta
+    are None."""
+    x = _f64(x)
+    T = x.shape[0]
+    x = x.reshape(T, -1)
+    D = x.shape[1]
+    u = _f64(u).reshape(T, D)
+    dy = _f64(dy).reshape(T, D)
+    g, b = _f64(gamma), _f64(beta)
+    dx = np.empty((T, D), dtype=np.float64)
+    du = np.empty((T, D), dtype=np.float64)
+    dg = np.empty(D, dtype=np.float64) if g is not None else None
+    db = np.empty(D, dtype=np.float64) if b is not None else None
+    _load().oracle_ln_gate_bwd(T, D, _p(x), _p(u), _p(dy), _p(g), _p(b), float(eps), _p(dx),
+                               _p(du), _p(dg), _p(db))
+    return dx, du, dg, db

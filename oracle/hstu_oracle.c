@@ -21,7 +21,8 @@
  *     (diagonal included) in which the last n_t tokens (candidates) may
  *     not see one another; every candidate sits at position n_h = L - n_t;
  *   - Eq. 3 (pointwise transformation): Norm(A V) (.) U, Norm = layer norm
- *     over the h*d_v features of a token, biased variance, optional affine;
+ *     over the h*d_v features of a token, biased variance, optional affine,
+ *     and its gradient by the chain rule;
  *   - Appendix on the fused kernels: the backward recomputes attention
  *     and the relative bias; gradients flow into both bias tables.
  *
@@ -237,6 +238,50 @@ void oracle_ln_gate(int64_t T, int32_t D, const double* x, const double* u,
     if (mean) mean[t] = mu;
     if (rstd) rstd[t] = rs;
   }
+}
+
+/* Gradient of <Y, dY> for Y = (z * gamma + beta) (.) u, z = (x - mean) * rstd
+ * (the epilogue above), by the chain rule written out per token:
+ *   du = (z gamma + beta) dy,  dzn = dy u,  dgamma += dzn z,  dbeta += dzn,
+ *   dz = dzn gamma,  dx = rstd (dz - mean(dz) - z mean(dz z)).
+ * mean and rstd are recomputed from x.  dgamma, dbeta: [D] (overwritten)
+ * or NULL; summed over tokens in token order. */
+void oracle_ln_gate_bwd(int64_t T, int32_t D, const double* x, const double* u,
+                        const double* dy, const double* gamma, const double* beta,
+                        double eps, double* dx, double* du, double* dgamma,
+                        double* dbeta) {
+  if (dgamma)
+    for (int32_t c = 0; c < D; c++) dgamma[c] = 0.0;
+  if (dbeta)
+    for (int32_t c = 0; c < D; c++) dbeta[c] = 0.0;
+  double* z = (double*)malloc(sizeof(double) * (size_t)D);
+  double* dz = (double*)malloc(sizeof(double) * (size_t)D);
+  for (int64_t t = 0; t < T; t++) {
+    const double* xr = x + t * D;
+    double mu = 0.0, var = 0.0;
+    for (int32_t c = 0; c < D; c++) mu += xr[c];
+    mu /= (double)D;
+    for (int32_t c = 0; c < D; c++) var += (xr[c] - mu) * (xr[c] - mu);
+    var /= (double)D;
+    const double rs = 1.0 / sqrt(var + eps);
+    double m1 = 0.0, m2 = 0.0;
+    for (int32_t c = 0; c < D; c++) {
+      const double g = gamma ? gamma[c] : 1.0, bb = beta ? beta[c] : 0.0;
+      z[c] = (xr[c] - mu) * rs;
+      du[t * D + c] = (z[c] * g + bb) * dy[t * D + c];
+      const double dzn = dy[t * D + c] * u[t * D + c];
+      if (dgamma) dgamma[c] += dzn * z[c];
+      if (dbeta) dbeta[c] += dzn;
+      dz[c] = dzn * g;
+      m1 += dz[c];
+      m2 += dz[c] * z[c];
+    }
+    m1 /= (double)D;
+    m2 /= (double)D;
+    for (int32_t c = 0; c < D; c++) dx[t * D + c] = rs * (dz[c] - m1 - z[c] * m2);
+  }
+  free(z);
+  free(dz);
 }
 
 int32_t oracle_num_threads(void) {

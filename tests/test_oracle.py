@@ -392,6 +392,64 @@ def test_epilogue_layernorm(oracle_mod):
     np.testing.assert_allclose(ya, ref, rtol=1e-12, atol=1e-13)
 
 
+def test_epilogue_backward_finite_differences(oracle_mod):
+    """Gradient of <Y, dY> for the Eq. 3 epilogue (layer norm of the
+    token's features, affine, gate by U): central finite differences of
+    the oracle's forward in x, u, gamma and beta."""
+    rng = np.random.default_rng(21)
+    T, D, eps = 3, 10, 1e-5
+    x = rng.standard_normal((T, D)) * 2 + 0.5
+    u = rng.standard_normal((T, D))
+    g, b = rng.standard_normal(D), rng.standard_normal(D)
+    dy = rng.standard_normal((T, D))
+    dx, du, dg, db = oracle_mod.ln_gate_bwd(x, u, dy, g, b, eps)
+
+    def loss(x_, u_, g_, b_):
+        return float((oracle_mod.ln_gate(x_, u_, g_, b_, eps)[0] * dy).sum())
+
+    h = 1e-6
+    for name, arr, grad in (("x", x, dx), ("u", u, du), ("gamma", g, dg), ("beta", b, db)):
+        fd = np.zeros_like(arr)
+        for idx in np.ndindex(arr.shape):
+            args = {"x": x, "u": u, "gamma": g, "beta": b}
+            hi, lo = arr.copy(), arr.copy()
+            hi[idx] += h
+            lo[idx] -= h
+            args[name] = hi
+            fp = loss(args["x"], args["u"], args["gamma"], args["beta"])
+            args[name] = lo
+            fm = loss(args["x"], args["u"], args["gamma"], args["beta"])
+            fd[idx] = (fp - fm) / (2 * h)
+        np.testing.assert_allclose(grad, fd, rtol=1e-6, atol=1e-7, err_msg=name)
+
+
+def test_epilogue_backward_invariants(oracle_mod):
+    """Layer-norm backward: every dx row sums to zero (the mean is
+    removed); with eps = 0 it is also orthogonal to the normalised row;
+    without affine parameters and with U = dY = 1, dx vanishes; the
+    gradients are linear in dY."""
+    rng = np.random.default_rng(22)
+    x = rng.standard_normal((9, 48)) * 3 - 1
+    u = rng.standard_normal(x.shape)
+    dy = rng.standard_normal(x.shape)
+    g, b = rng.standard_normal(48), rng.standard_normal(48)
+    dx, du, dg, db = oracle_mod.ln_gate_bwd(x, u, dy, g, b, 0.0)
+    z = (x - x.mean(1, keepdims=True)) / x.std(1, keepdims=True)
+    np.testing.assert_allclose(dx.sum(1), 0, atol=1e-11)
+    np.testing.assert_allclose((dx * z).sum(1), 0, atol=1e-10)
+    ones = np.ones_like(x)
+    dx1, du1, dg1, db1 = oracle_mod.ln_gate_bwd(x, ones, ones, eps=1e-5)
+    np.testing.assert_allclose(dx1, 0, atol=1e-12)
+    assert dg1 is None and db1 is None
+    np.testing.assert_allclose(du1, oracle_mod.ln_gate(x, ones, eps=1e-5)[0], rtol=1e-13)
+    dy2 = rng.standard_normal(x.shape)
+    a = oracle_mod.ln_gate_bwd(x, u, dy, g, b, 1e-5)
+    c = oracle_mod.ln_gate_bwd(x, u, dy2, g, b, 1e-5)
+    m = oracle_mod.ln_gate_bwd(x, u, 2 * dy - 3 * dy2, g, b, 1e-5)
+    for k in range(4):
+        np.testing.assert_allclose(m[k], 2 * a[k] - 3 * c[k], rtol=1e-10, atol=1e-11)
+
+
 def test_empty_and_full_candidate_sequences(oracle_mod):
     """L_b = 0 contributes nothing; n_t = L_b means each token sees only
     itself at position 0 (diagonal of the Algorithm 1 mask)."""
