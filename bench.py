@@ -2,11 +2,13 @@
 """Benchmark of the HSTU jagged-attention hot path on one MI355X.
 
 One step = one pass of the whole path over the batch (inputs resident in
-HBM): hstu_layer_fwd (work-list scheduling, fused attention forward with
-the in-register bias and time bucketisation, LayerNorm(A V) (.) U
-epilogue) then hstu_attn_bwd (recomputing backward with dQ/dK/dV and the
-bias-table gradients).  Default workload: the 8192-long shape (B=8
-sequences of length U[4096, 8192], h=4, d_qk=d_v=128, N=8192, bf16).
+HBM): hstu_attn_fwd (work-list scheduling, fused attention forward with
+the in-register bias and time bucketisation) then hstu_attn_bwd
+(recomputing backward with dQ/dK/dV and the bias-table gradients); for
+the training workload the whole layer, hstu_layer_fwd (attention +
+LayerNorm(A V) (.) U) then hstu_layer_bwd.  Default workload: the
+8192-long shape (B=8 sequences of length U[4096, 8192], h=4,
+d_qk=d_v=128, N=8192, bf16).
 
 Prints one JSON line: tokens/s (whole job), the per-kernel breakdown,
 the roofline position of the dominant kernel measured live with HIP
@@ -219,7 +221,7 @@ def main():
     ws = hstu.workspace(p)
     D = spec.num_heads * spec.d_v
     dt = d["q"].dtype
-    attn_out = torch.empty((T, D), dtype=dt, device="cuda")
+    attn_out = torch.empty((T, D), dtype=torch.float32, device="cuda")
     y = torch.empty((T, D), dtype=dt, device="cuda")
     mean = torch.empty(T, dtype=torch.float32, device="cuda")
     rstd = torch.empty(T, dtype=torch.float32, device="cuda")
@@ -227,11 +229,31 @@ def main():
              torch.empty_like(d["rab_pos"]), torch.empty_like(d["rab_time"]))
     stream = torch.cuda.current_stream()
 
+    # The training workload times the whole layer (attention, LayerNorm
+    # gate, and their backward); the others the attention alone.
+    layer = spec.name == "training"
+    out_bf = torch.empty((T, spec.num_heads, spec.d_v), dtype=dt, device="cuda")
+    lgrads = None
+    if layer:
+        lgrads = (grads[0], grads[1], grads[2], torch.empty((T, D), dtype=dt, device="cuda"), None,
+                  None, grads[3], grads[4])
+    dy = d["do"].reshape(T, D)
+
     def step():
-        hstu.hstu_layer_fwd(d["q"], d["k"], d["v"], d["u"], d["seq_offsets"], d["timestamps"],
-                            d["rab_pos"], d["rab_time"], N, num_targets=d["num_targets"],
-                            attn_out=attn_out, y=y, ln_mean=mean, ln_rstd=rstd, ws=ws,
-                            stream=stream)
+        if layer:
+            hstu.hstu_layer_fwd(d["q"], d["k"], d["v"], d["u"], d["seq_offsets"], d["timestamps"],
+                                d["rab_pos"], d["rab_time"], N, num_targets=d["num_targets"],
+                                attn_out=attn_out, y=y, ln_mean=mean, ln_rstd=rstd, ws=ws,
+                                stream=stream)
+            if spec.backward:
+                hstu.hstu_layer_bwd(d["q"], d["k"], d["v"], d["u"], attn_out, mean, rstd, dy,
+                                    d["seq_offsets"], d["timestamps"], d["rab_pos"],
+                                    d["rab_time"], N, num_targets=d["num_targets"],
+                                    grads=lgrads, ws=ws, stream=stream)
+            return
+        hstu.hstu_attn_fwd(d["q"], d["k"], d["v"], d["seq_offsets"], d["timestamps"],
+                           d["rab_pos"], d["rab_time"], N, num_targets=d["num_targets"],
+                           out=out_bf, ws=ws, stream=stream)
         if spec.backward:
             hstu.hstu_attn_bwd(d["q"], d["k"], d["v"], d["do"], d["seq_offsets"],
                                d["timestamps"], d["rab_pos"], d["rab_time"], N,
@@ -257,19 +279,24 @@ def main():
     per_step = [evs[k].elapsed_time(evs[k + 1]) for k in range(args.steps)]
 
     kernels = {}
-    for name in ("attn_fwd", "ln_gate", "attn_bwd"):
+    for name in ("attn_fwd", "ln_gate", "ln_gate_bwd", "attn_bwd"):
         tot, n = hstu.hstu_timing_read(name)
         if n:
             kernels[name] = {"avg_ms": tot / n, "launches": n}
     # Algorithmic work per launch: FLOPs of the contractions for attention,
     # bytes read + written for the epilogue.
-    ln_bytes = T * D * 3 * (2 if spec.dtype == "bf16" else 4) + 8 * T
+    # fp32 attention output read, u read and y written in the problem's dtype
+    ln_bytes = T * D * (4 + 2 * (2 if spec.dtype == "bf16" else 4)) + 8 * T
     if "attn_fwd" in kernels:
         kernels["attn_fwd"]["tflops"] = f_fwd / (kernels["attn_fwd"]["avg_ms"] * 1e-3) / 1e12
     if "attn_bwd" in kernels:
         kernels["attn_bwd"]["tflops"] = f_bwd / (kernels["attn_bwd"]["avg_ms"] * 1e-3) / 1e12
     if "ln_gate" in kernels:
         kernels["ln_gate"]["gbs"] = ln_bytes / (kernels["ln_gate"]["avg_ms"] * 1e-3) / 1e9
+    if "ln_gate_bwd" in kernels:
+        e = 2 if spec.dtype == "bf16" else 4
+        lnb_bytes = T * D * (4 + 4 * e) + 8 * T
+        kernels["ln_gate_bwd"]["gbs"] = lnb_bytes / (kernels["ln_gate_bwd"]["avg_ms"] * 1e-3) / 1e9
 
     peak = PEAK_BF16_TFLOPS if spec.dtype == "bf16" else PEAK_FP32_TFLOPS
     dom = "attn_bwd" if spec.backward else "attn_fwd"
@@ -307,8 +334,11 @@ def main():
         "config": {
             "workload": f"{spec.name}: B={len(batch.lengths)} jagged sequences, T={T}, "
                         f"h={spec.num_heads}, d_qk={spec.d_qk}, d_v={spec.d_v}, N={N}, "
-                        f"{'target-aware' if spec.target_aware else 'causal'}; step = layer fwd "
-                        f"(attention + LayerNorm gate){' + attention bwd with bias gradients' if spec.backward else ''}",
+                        f"{'target-aware' if spec.target_aware else 'causal'}; step = "
+                        + ("layer fwd (attention + LayerNorm gate)" + (" + layer bwd (LayerNorm-gate "
+                           "backward, attention backward with bias gradients)" if spec.backward else "")
+                           if layer else "attention fwd" + (" + attention bwd with bias gradients"
+                                                            if spec.backward else "")),
             "num_seqs": len(batch.lengths),
             "total_tokens": T,
             "max_seq_len": N,

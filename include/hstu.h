@@ -52,8 +52,9 @@
  *            timestamps int64.
  *   Determinism  hstu_attn_fwd, hstu_layer_fwd, hstu_time_bucketize and
  *            hstu_complete_cumsum are bitwise deterministic.
- *            hstu_attn_bwd accumulates dQ and the bias gradients with
- *            atomics, so their last bits may vary between runs.
+ *            hstu_attn_bwd and hstu_layer_bwd accumulate dQ and the bias
+ *            and layer-norm parameter gradients with atomics, so their
+ *            last bits may vary between runs.
  */
 #ifndef HSTU_H_
 #define HSTU_H_
@@ -131,12 +132,16 @@ hstu_status_t hstu_attn_bwd(const hstu_problem_t* p, const hstu_jagged_t* j,
                             float* d_rab_pos, float* d_rab_time,
                             void* ws, size_t ws_bytes, void* hip_stream);
 
-/* Eq. 2 then the Eq. 3 gate: attn_out = hstu_attn_fwd(...) written dense
- * [T][D] with D = h*d_v (kept for the backward), then per token
+/* Eq. 2 then the Eq. 3 gate: attn_out = the attention output of
+ * hstu_attn_fwd, written dense [T][D] with D = h*d_v in fp32 for both
+ * dtypes (the layer norm divides by a row's spread, which can be far
+ * smaller than its magnitude, so it reads the output before any bf16
+ * rounding; kept for the backward), then per token
  * y = ((x - mean) * rstd * ln_weight + ln_bias) (.) u with
  * rstd = 1/sqrt(var + ln_eps), biased variance over the D features.
  * ln_weight, ln_bias: fp32 [D] or NULL (identity).  u: rows of D elements
- * at u_stride.  ln_mean, ln_rstd: fp32 [T] or NULL.  D <= 4096. */
+ * at u_stride; y: dense [T][D], both in the problem's dtype.  ln_mean,
+ * ln_rstd: fp32 [T] or NULL.  D <= 4096. */
 hstu_status_t hstu_layer_fwd(const hstu_problem_t* p, const hstu_jagged_t* j,
                              const void* q, int64_t q_stride,
                              const void* k, int64_t k_stride,
@@ -145,6 +150,31 @@ hstu_status_t hstu_layer_fwd(const hstu_problem_t* p, const hstu_jagged_t* j,
                              const float* ln_weight, const float* ln_bias,
                              float ln_eps, void* attn_out, void* y,
                              float* ln_mean, float* ln_rstd,
+                             void* ws, size_t ws_bytes, void* hip_stream);
+
+/* Backward of the whole layer (Eq. 2 and Eq. 3) from dY, the gradient of
+ * Y = LayerNorm(attn_out) (.) U: du = LN(attn_out) (.) dY, the layer-norm
+ * backward to dO = d attn_out (into the workspace, in the problem's
+ * dtype), then hstu_attn_bwd with that dO.  attn_out (fp32), ln_weight,
+ * ln_bias, ln_mean and ln_rstd are the output, parameters and saved
+ * statistics of the hstu_layer_fwd call (ln_mean, ln_rstd required;
+ * weight / bias NULL for the identity affine).  d_y, du: dense [T][h*d_v]
+ * in the problem's dtype
+ * (du overwritten).  d_ln_weight, d_ln_bias: fp32 [h*d_v], overwritten
+ * with the gradients (summed over tokens by float atomics, so their last
+ * bits may vary between runs), or NULL to skip them.  Other arguments and
+ * outputs as hstu_attn_bwd.  h*d_v <= 4096. */
+hstu_status_t hstu_layer_bwd(const hstu_problem_t* p, const hstu_jagged_t* j,
+                             const void* q, int64_t q_stride,
+                             const void* k, int64_t k_stride,
+                             const void* v, int64_t v_stride,
+                             const void* u, int64_t u_stride,
+                             const void* attn_out, const float* ln_weight,
+                             const float* ln_bias, const float* ln_mean,
+                             const float* ln_rstd, const void* d_y,
+                             void* dq, void* dk, void* dv, void* du,
+                             float* d_ln_weight, float* d_ln_bias,
+                             float* d_rab_pos, float* d_rab_time,
                              void* ws, size_t ws_bytes, void* hip_stream);
 
 /* Standalone timestamp bucketisation (notation table, rab^{p,t}): for

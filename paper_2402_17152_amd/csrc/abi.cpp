@@ -140,6 +140,7 @@ struct Layout {
   size_t bwd_items;
   size_t trange;    // int64 [2B]: per-sequence timestamp min / max
   size_t dq_acc;    // fp32 [h][T][d_qk] (bf16 problems)
+  size_t dout;      // [T][h*d_v] fp32, or bf16 high then low terms: dO of hstu_layer_bwd
   size_t total;
   int64_t max_fwd, max_bwd;
 };
@@ -160,6 +161,8 @@ Layout layout(const hstu_problem_t* p) {
   l.dq_acc = off;
   if (p->dtype == HSTU_BF16)
     off = align_up(off + sizeof(float) * (size_t)p->total_tokens * p->num_heads * p->d_qk);
+  l.dout = off;
+  off = align_up(off + 4 * (size_t)p->total_tokens * p->num_heads * p->d_v);
   l.total = off;
   return l;
 }
@@ -202,7 +205,7 @@ JaggedArgs make_args(const hstu_problem_t* p, const hstu_jagged_t* j) {
   } while (0)
 
 hstu_status_t attn_fwd_impl(const hstu_problem_t* p, const hstu_jagged_t* j, const Tensors& t,
-                            void* out, void* ws, size_t ws_bytes, hipStream_t s) {
+                            void* out, int out_f32, void* ws, size_t ws_bytes, hipStream_t s) {
   HSTU_TRY(check_problem(p));
   HSTU_TRY(check_jagged(j));
   const int64_t T = p->total_tokens;
@@ -227,7 +230,8 @@ hstu_status_t attn_fwd_impl(const hstu_problem_t* p, const hstu_jagged_t* j, con
   HSTU_HIP(launch_seq_time_range(ja, (int64_t*)(w + l.trange), s), "time range launch");
   HSTU_HIP(launch_schedule(ja, 0, items, counts, s), "schedule launch");
   TimedScope ts("attn_fwd", s);
-  HSTU_HIP(launch_attn_fwd_bf16(ja, t, p->d_qk, p->d_v, out, items, counts, l.max_fwd, s),
+  HSTU_HIP(launch_attn_fwd_bf16(ja, t, p->d_qk, p->d_v, out, out_f32, items, counts, l.max_fwd,
+                                s),
            "attn_fwd launch");
   return ok();
 }
@@ -255,10 +259,72 @@ hstu_status_t hstu_attn_fwd(const hstu_problem_t* p, const hstu_jagged_t* j, con
                             void* hip_stream) {
   try {
     Tensors t{q, q_stride, k, k_stride, v, v_stride};
-    return attn_fwd_impl(p, j, t, out, ws, ws_bytes, (hipStream_t)hip_stream);
+    return attn_fwd_impl(p, j, t, out, 0, ws, ws_bytes, (hipStream_t)hip_stream);
   } catch (...) {
     return fail(HSTU_ERR_INVALID_ARGUMENT, "internal error");
   }
+}
+
+// Argument checks of the attention backward (shared by hstu_layer_bwd,
+// which runs them before launching anything).
+hstu_status_t attn_bwd_check(const hstu_problem_t* p, const hstu_jagged_t* j, const Tensors& t,
+                             const void* d_out, void* dq, void* dk, void* dv, float* d_rab_pos,
+                             float* d_rab_time, void* ws, size_t ws_bytes, Layout* l) {
+  HSTU_TRY(check_problem(p));
+  HSTU_TRY(check_jagged(j));
+  const int H = p->num_heads;
+  HSTU_TRY(check_rows(p, "q", t.q, t.q_stride, (int64_t)H * p->d_qk));
+  HSTU_TRY(check_rows(p, "k", t.k, t.k_stride, (int64_t)H * p->d_qk));
+  HSTU_TRY(check_rows(p, "v", t.v, t.v_stride, (int64_t)H * p->d_v));
+  HSTU_TRY(check_dense("d_out", d_out, 16));
+  HSTU_TRY(check_dense("dq", dq, 16));
+  HSTU_TRY(check_dense("dk", dk, 16));
+  HSTU_TRY(check_dense("dv", dv, 16));
+  HSTU_TRY(check_dense("d_rab_pos", d_rab_pos, 4));
+  HSTU_TRY(check_dense("d_rab_time", d_rab_time, 4));
+  return check_ws(p, ws, ws_bytes, l);
+}
+
+// d_out_lo: null, or the low bf16 terms of a dO given as two terms (bf16
+// problems only).
+hstu_status_t attn_bwd_impl(const hstu_problem_t* p, const hstu_jagged_t* j, const Tensors& t,
+                            const void* d_out, const void* d_out_lo, void* dq, void* dk,
+                            void* dv, float* d_rab_pos, float* d_rab_time, void* ws,
+                            size_t ws_bytes, hipStream_t s) {
+  Layout l;
+  HSTU_TRY(attn_bwd_check(p, j, t, d_out, dq, dk, dv, d_rab_pos, d_rab_time, ws, ws_bytes, &l));
+  const int64_t T = p->total_tokens;
+  const int H = p->num_heads;
+  const int N = p->max_seq_len;
+  HSTU_HIP(launch_fill_f32(d_rab_pos, 2 * (int64_t)N - 1, 0.0f, s), "fill launch");
+  HSTU_HIP(launch_fill_f32(d_rab_time, p->num_time_buckets, 0.0f, s), "fill launch");
+  if (T == 0) return ok();
+  JaggedArgs ja = make_args(p, j);
+  char* w = (char*)ws;
+  if (p->dtype == HSTU_F32) {
+    TimedScope ts("attn_bwd", s);
+    HSTU_HIP(launch_attn_bwd_f32(ja, t, p->d_qk, p->d_v, d_out, dq, dk, dv, d_rab_pos,
+                                 d_rab_time, s),
+             "attn_bwd_f32 launch");
+    return ok();
+  }
+  int32_t* counts = (int32_t*)(w + l.counts);
+  WorkItem* items = (WorkItem*)(w + l.bwd_items);
+  float* dq_acc = (float*)(w + l.dq_acc);
+  const int64_t ndq = T * H * p->d_qk;
+  HSTU_HIP(launch_fill_f32(dq_acc, ndq, 0.0f, s), "fill launch");
+  ja.seq_trange = (const int64_t*)(w + l.trange);
+  HSTU_HIP(launch_seq_time_range(ja, (int64_t*)(w + l.trange), s), "time range launch");
+  HSTU_HIP(launch_schedule(ja, 1, items, counts + 1, s), "schedule launch");
+  {
+    TimedScope ts("attn_bwd", s);
+    HSTU_HIP(launch_attn_bwd_bf16(ja, t, p->d_qk, p->d_v, d_out, d_out_lo, dq_acc, dk, dv,
+                                  d_rab_pos, d_rab_time, items, counts + 1, l.max_bwd, s),
+             "attn_bwd launch");
+  }
+  HSTU_HIP(launch_dq_convert_bf16(dq_acc, dq, T, H, p->d_qk, 1.0f / (float)N, s),
+           "dq convert launch");
+  return ok();
 }
 
 hstu_status_t hstu_attn_bwd(const hstu_problem_t* p, const hstu_jagged_t* j, const void* q,
@@ -267,53 +333,54 @@ hstu_status_t hstu_attn_bwd(const hstu_problem_t* p, const hstu_jagged_t* j, con
                             float* d_rab_pos, float* d_rab_time, void* ws, size_t ws_bytes,
                             void* hip_stream) {
   try {
-    hipStream_t s = (hipStream_t)hip_stream;
-    HSTU_TRY(check_problem(p));
-    HSTU_TRY(check_jagged(j));
-    const int64_t T = p->total_tokens;
-    const int H = p->num_heads;
     Tensors t{q, q_stride, k, k_stride, v, v_stride};
-    HSTU_TRY(check_rows(p, "q", q, q_stride, (int64_t)H * p->d_qk));
-    HSTU_TRY(check_rows(p, "k", k, k_stride, (int64_t)H * p->d_qk));
-    HSTU_TRY(check_rows(p, "v", v, v_stride, (int64_t)H * p->d_v));
-    HSTU_TRY(check_dense("d_out", d_out, 16));
-    HSTU_TRY(check_dense("dq", dq, 16));
-    HSTU_TRY(check_dense("dk", dk, 16));
-    HSTU_TRY(check_dense("dv", dv, 16));
-    HSTU_TRY(check_dense("d_rab_pos", d_rab_pos, 4));
-    HSTU_TRY(check_dense("d_rab_time", d_rab_time, 4));
+    return attn_bwd_impl(p, j, t, d_out, nullptr, dq, dk, dv, d_rab_pos, d_rab_time, ws,
+                         ws_bytes, (hipStream_t)hip_stream);
+  } catch (...) {
+    return fail(HSTU_ERR_INVALID_ARGUMENT, "internal error");
+  }
+}
+
+hstu_status_t hstu_layer_bwd(const hstu_problem_t* p, const hstu_jagged_t* j, const void* q,
+                             int64_t q_stride, const void* k, int64_t k_stride, const void* v,
+                             int64_t v_stride, const void* u, int64_t u_stride,
+                             const void* attn_out, const float* ln_weight, const float* ln_bias,
+                             const float* ln_mean, const float* ln_rstd, const void* d_y,
+                             void* dq, void* dk, void* dv, void* du, float* d_ln_weight,
+                             float* d_ln_bias, float* d_rab_pos, float* d_rab_time, void* ws,
+                             size_t ws_bytes, void* hip_stream) {
+  try {
+    hipStream_t s = (hipStream_t)hip_stream;
+    Tensors t{q, q_stride, k, k_stride, v, v_stride};
     Layout l;
+    HSTU_TRY(check_problem(p));
     HSTU_TRY(check_ws(p, ws, ws_bytes, &l));
-    const int N = p->max_seq_len;
-    HSTU_HIP(launch_fill_f32(d_rab_pos, 2 * (int64_t)N - 1, 0.0f, s), "fill launch");
-    HSTU_HIP(launch_fill_f32(d_rab_time, p->num_time_buckets, 0.0f, s), "fill launch");
-    if (T == 0) return ok();
-    JaggedArgs ja = make_args(p, j);
-    char* w = (char*)ws;
-    if (p->dtype == HSTU_F32) {
-      TimedScope ts("attn_bwd", s);
-      HSTU_HIP(launch_attn_bwd_f32(ja, t, p->d_qk, p->d_v, d_out, dq, dk, dv, d_rab_pos,
-                                   d_rab_time, s),
-               "attn_bwd_f32 launch");
-      return ok();
+    // dO of the attention, in the workspace: fp32, or for bf16 problems two
+    // bf16 terms (high, then low) that the attention backward both uses.
+    void* dout = (char*)ws + l.dout;
+    const bool split = p->dtype == HSTU_BF16;
+    void* dout_lo = split ? (char*)dout + 2 * (size_t)p->total_tokens * p->num_heads * p->d_v
+                          : nullptr;
+    HSTU_TRY(attn_bwd_check(p, j, t, dout, dq, dk, dv, d_rab_pos, d_rab_time, ws, ws_bytes, &l));
+    const int64_t D = (int64_t)p->num_heads * p->d_v;
+    if (D > 4096) return fail(HSTU_ERR_UNSUPPORTED, "h*d_v must be <= 4096 (got %lld)", (long long)D);
+    HSTU_TRY(check_rows(p, "u", u, u_stride, D));
+    HSTU_TRY(check_dense("attn_out", attn_out, 16));
+    HSTU_TRY(check_dense("d_y", d_y, 16));
+    HSTU_TRY(check_dense("du", du, 16));
+    if (p->total_tokens > 0 && (!ln_mean || !ln_rstd))
+      return fail(HSTU_ERR_INVALID_ARGUMENT, "ln_mean and ln_rstd (saved by hstu_layer_fwd) are required");
+    if (d_ln_weight) HSTU_HIP(launch_fill_f32(d_ln_weight, D, 0.0f, s), "fill launch");
+    if (d_ln_bias) HSTU_HIP(launch_fill_f32(d_ln_bias, D, 0.0f, s), "fill launch");
+    if (p->total_tokens > 0) {
+      TimedScope ts("ln_gate_bwd", s);
+      HSTU_HIP(launch_ln_gate_bwd(p->dtype == HSTU_BF16, p->total_tokens, (int32_t)D, attn_out, u,
+                                  u_stride, d_y, ln_weight, ln_bias, ln_mean, ln_rstd, du, dout,
+                                  dout_lo, d_ln_weight, d_ln_bias, s),
+               "ln_gate_bwd launch");
     }
-    int32_t* counts = (int32_t*)(w + l.counts);
-    WorkItem* items = (WorkItem*)(w + l.bwd_items);
-    float* dq_acc = (float*)(w + l.dq_acc);
-    const int64_t ndq = T * H * p->d_qk;
-    HSTU_HIP(launch_fill_f32(dq_acc, ndq, 0.0f, s), "fill launch");
-    ja.seq_trange = (const int64_t*)(w + l.trange);
-    HSTU_HIP(launch_seq_time_range(ja, (int64_t*)(w + l.trange), s), "time range launch");
-    HSTU_HIP(launch_schedule(ja, 1, items, counts + 1, s), "schedule launch");
-    {
-      TimedScope ts("attn_bwd", s);
-      HSTU_HIP(launch_attn_bwd_bf16(ja, t, p->d_qk, p->d_v, d_out, dq_acc, dk, dv, d_rab_pos,
-                                    d_rab_time, items, counts + 1, l.max_bwd, s),
-               "attn_bwd launch");
-    }
-    HSTU_HIP(launch_dq_convert_bf16(dq_acc, dq, T, H, p->d_qk, 1.0f / (float)N, s),
-             "dq convert launch");
-    return ok();
+    return attn_bwd_impl(p, j, t, dout, dout_lo, dq, dk, dv, d_rab_pos, d_rab_time, ws, ws_bytes,
+                         s);
   } catch (...) {
     return fail(HSTU_ERR_INVALID_ARGUMENT, "internal error");
   }
@@ -334,7 +401,8 @@ hstu_status_t hstu_layer_fwd(const hstu_problem_t* p, const hstu_jagged_t* j, co
     HSTU_TRY(check_dense("y", y, 16));
     if (!(ln_eps >= 0.0f)) return fail(HSTU_ERR_INVALID_ARGUMENT, "ln_eps must be >= 0");
     Tensors t{q, q_stride, k, k_stride, v, v_stride};
-    HSTU_TRY(attn_fwd_impl(p, j, t, attn_out, ws, ws_bytes, s));
+    // The attention output stays fp32 for the layer norm (both dtypes).
+    HSTU_TRY(attn_fwd_impl(p, j, t, attn_out, 1, ws, ws_bytes, s));
     if (p->total_tokens == 0) return ok();
     TimedScope ts("ln_gate", s);
     HSTU_HIP(launch_ln_gate(p->dtype == HSTU_BF16, p->total_tokens, (int32_t)D, attn_out, u,

@@ -46,6 +46,13 @@
 // Tiles whose bucket is not fixed by the timestamp extremes (near the
 // diagonal, ragged, 64-bit timestamps) sum dS bucket by bucket over the
 // tile's bucket range.
+// SPLIT (the layer's backward): dO arrives as two bf16 terms, hi + lo
+// (its own LayerNorm backward produces it in fp32, with a dynamic range
+// across rows that a single bf16 would turn into several percent of error
+// after the cancellations of the contractions); both are staged and each
+// dO contraction runs on both.  For the same reason P and dS enter dV and
+// dK as two bf16 terms as well (hi P with both dO terms, lo P with hi dO;
+// hi and lo dS with Q); dQ keeps the single bf16 dS.
 #include <type_traits>
 
 #include "bias.h"
@@ -80,7 +87,7 @@ struct StepTile {
   __device__ static int swz(int r) { return SWZ ? 2 * (r & 3) + ((r >> 2) & 1) : 0; }
 };
 
-template <int DQK, int DV>
+template <int DQK, int DV, bool SPLIT>
 struct BwdShared {
   using QT = StepTile<DQK>;
   using OT = StepTile<DV>;
@@ -93,10 +100,12 @@ struct BwdShared {
   static constexpr int KB_LD = DQK + 16;
   static constexpr int NWIN = BM + BN;  // reversed rab_pos window (BM + BN - 1 used)
   static constexpr int kWinPad = 4, WIN_LD = 264;
+  static constexpr int NLO = SPLIT ? 4 : 1, LOB = SPLIT ? OT::BYTES : 16;
   union Ring {
     struct {
       __align__(16) uint8_t q[4][QT::BYTES];
       __align__(16) uint8_t dO[4][OT::BYTES];
+      __align__(16) uint8_t dOl[NLO][LOB];  // low terms of dO (SPLIT)
     } t;
     __align__(16) uint16_t kblk[BN * KB_LD];  // prologue only
   };
@@ -117,6 +126,7 @@ struct BwdArgs {
   JaggedArgs ja;
   Tensors t;
   const uint16_t* dO;
+  const uint16_t* dO_lo;  // SPLIT only
   float* dq_acc;
   uint16_t* dK;
   uint16_t* dV;
@@ -128,10 +138,11 @@ __device__ __forceinline__ float silu_sigma(float x) {
   return __builtin_amdgcn_rcpf(1.0f + __builtin_amdgcn_exp2f(x * -kLog2e));
 }
 
-template <int DQK, int DV, bool FAST>
-__device__ __forceinline__ void bwd_item(BwdShared<DQK, DV>& sm, const BwdArgs& A, int64_t o,
-                                         int L, int n_h, int j0, int head, int64_t tbase) {
-  using Sh = BwdShared<DQK, DV>;
+template <int DQK, int DV, bool FAST, bool SPLIT>
+__device__ __forceinline__ void bwd_item(BwdShared<DQK, DV, SPLIT>& sm, const BwdArgs& A,
+                                         int64_t o, int L, int n_h, int j0, int head,
+                                         int64_t tbase) {
+  using Sh = BwdShared<DQK, DV, SPLIT>;
   using QT = typename Sh::QT;
   using OT = typename Sh::OT;
   constexpr int BN = Sh::BN, BM = Sh::BM, DST_LD = Sh::DST_LD, KB_LD = Sh::KB_LD;
@@ -150,6 +161,7 @@ __device__ __forceinline__ void bwd_item(BwdShared<DQK, DV>& sm, const BwdArgs& 
   const uint16_t* __restrict__ vg = (const uint16_t*)A.t.v + o * A.t.v_stride + head * DV;
   const uint16_t* __restrict__ qg = (const uint16_t*)A.t.q + o * A.t.q_stride + head * DQK;
   const uint16_t* __restrict__ dog = A.dO + (o * H + head) * DV;
+  const uint16_t* __restrict__ dogl = SPLIT ? A.dO_lo + (o * H + head) * DV : dog;
   const uint32_t kstride_b = (uint32_t)A.t.k_stride * 2u, vstride_b = (uint32_t)A.t.v_stride * 2u;
   const uint32_t qstride_b = (uint32_t)A.t.q_stride * 2u, dostride_b = (uint32_t)(H * DV) * 2u;
   const float invN = 1.0f / (float)N;
@@ -268,9 +280,10 @@ __device__ __forceinline__ void bwd_item(BwdShared<DQK, DV>& sm, const BwdArgs& 
   // DMA of step u - 2, which is followed by that step's atomics and all of
   // step u - 1's operations: the wait lets those stay in flight, so the
   // atomics get about two steps to complete.
-  constexpr int OPS_PER_STEP = QT::OPW + OT::OPW + 3 + 1 + 16;
+  constexpr int OPS_PER_STEP = QT::OPW + (SPLIT ? 2 : 1) * OT::OPW + 3 + 1 + 16;
   const u32x4 qrs = rsrc_words(qg, (uint32_t)(L * A.t.q_stride * 2));
   const u32x4 ors = rsrc_words(dog, (uint32_t)L * dostride_b);
+  const u32x4 orsl = rsrc_words(dogl, (uint32_t)L * dostride_b);
   const u32x4 trs = rsrc_words(ts, (uint32_t)L * 8u);
   const u32x4 prs = rsrc_words(ja.rab_pos, (uint32_t)(2 * N - 1) * 4u);
   // Lane offsets of this wave's tile operations: linear chunk g = 64 op +
@@ -300,6 +313,12 @@ __device__ __forceinline__ void bwd_item(BwdShared<DQK, DV>& sm, const BwdArgs& 
     for (int k = 0; k < OT::OPW; k++)
       dma_to_lds16_asm(ors, sm.ring.t.dO[slot] + 1024 * min(wave * OT::OPW + k, OT::OPS - 1),
                    ooffs[k] + (uint32_t)i0 * dostride_b);
+    if constexpr (SPLIT) {
+#pragma unroll
+      for (int k = 0; k < OT::OPW; k++)
+        dma_to_lds16_asm(orsl, sm.ring.t.dOl[slot] + 1024 * min(wave * OT::OPW + k, OT::OPS - 1),
+                         ooffs[k] + (uint32_t)i0 * dostride_b);
+    }
   };
   // Reversed rab_pos window of step u: W[y] = rab_pos[pb - y] with
   // pb = (N-1) + min(j0 + 127, n_h) - min(i0, n_h), so that a pair's entry
@@ -484,12 +503,19 @@ __device__ __forceinline__ void bwd_item(BwdShared<DQK, DV>& sm, const BwdArgs& 
       if (s < DV / 16) {
         const u32x4 a = *reinterpret_cast<const u32x4*>(ob + a_off(OT{}, oa, s));
         pacc = mfma32x32x16(as_bf16x8(a), as_bf16x8(vf[s]), pacc);
+        if constexpr (SPLIT) {
+          const u32x4 al =
+              *reinterpret_cast<const u32x4*>(sm.ring.t.dOl[u & 3] + a_off(OT{}, oa, s));
+          pacc = mfma32x32x16(as_bf16x8(al), as_bf16x8(vf[s]), pacc);
+        }
       }
     }
   };
   // dV += P^T dO, dK += dS^T Q: k-slots (st, e) of the A operands are the
   // accumulator rows 16 st + 8 (e / 4) + 4*half + e % 4.
-  auto key_grads = [&](int u, const u32x4 (&pa)[2], const u32x4 (&da)[2]) {
+  // pl, dl: the low bf16 terms of P and dS (SPLIT only).
+  auto key_grads = [&](int u, const u32x4 (&pa)[2], const u32x4 (&da)[2], const u32x4 (&pl)[2],
+                       const u32x4 (&dl)[2]) {
     const uint8_t* qb = sm.ring.t.q[u & 3];
     const uint8_t* ob = sm.ring.t.dO[u & 3];
 #pragma unroll
@@ -499,12 +525,21 @@ __device__ __forceinline__ void bwd_item(BwdShared<DQK, DV>& sm, const BwdArgs& 
         const uint2 lo = lds_read_tr16((const uint16_t*)(ob + tr_off(OT{}, ot, st, 0, nb)));
         const uint2 hi = lds_read_tr16((const uint16_t*)(ob + tr_off(OT{}, ot, st, 1, nb)));
         dvacc[nb] = mfma32x32x16(as_bf16x8(pa[st]), as_bf16x8(u32x4{lo.x, lo.y, hi.x, hi.y}), dvacc[nb]);
+        if constexpr (SPLIT) {
+          dvacc[nb] = mfma32x32x16(as_bf16x8(pl[st]), as_bf16x8(u32x4{lo.x, lo.y, hi.x, hi.y}), dvacc[nb]);
+          const uint8_t* obl = sm.ring.t.dOl[u & 3];
+          const uint2 l2 = lds_read_tr16((const uint16_t*)(obl + tr_off(OT{}, ot, st, 0, nb)));
+          const uint2 h2 = lds_read_tr16((const uint16_t*)(obl + tr_off(OT{}, ot, st, 1, nb)));
+          dvacc[nb] = mfma32x32x16(as_bf16x8(pa[st]), as_bf16x8(u32x4{l2.x, l2.y, h2.x, h2.y}), dvacc[nb]);
+        }
       }
 #pragma unroll
       for (int nb = 0; nb < DQK / 32; nb++) {
         const uint2 lo = lds_read_tr16((const uint16_t*)(qb + tr_off(QT{}, qt, st, 0, nb)));
         const uint2 hi = lds_read_tr16((const uint16_t*)(qb + tr_off(QT{}, qt, st, 1, nb)));
         dkacc[nb] = mfma32x32x16(as_bf16x8(da[st]), as_bf16x8(u32x4{lo.x, lo.y, hi.x, hi.y}), dkacc[nb]);
+        if constexpr (SPLIT)
+          dkacc[nb] = mfma32x32x16(as_bf16x8(dl[st]), as_bf16x8(u32x4{lo.x, lo.y, hi.x, hi.y}), dkacc[nb]);
       }
     }
   };
@@ -695,15 +730,26 @@ __device__ __forceinline__ void bwd_item(BwdShared<DQK, DV>& sm, const BwdArgs& 
       pv[q] = p;
       dsv[q] = p_cur[q] * __builtin_fmaf(p, 1.0f - sg, sg);
     }
-    u32x4 pa[2], da[2];
+    u32x4 pa[2], da[2], pl[2], dl[2];
 #pragma unroll
     for (int st = 0; st < 2; st++) {
       pa[st] = u32x4{pack_bf16x2(pv[8 * st], pv[8 * st + 1]), pack_bf16x2(pv[8 * st + 2], pv[8 * st + 3]),
                      pack_bf16x2(pv[8 * st + 4], pv[8 * st + 5]), pack_bf16x2(pv[8 * st + 6], pv[8 * st + 7])};
       da[st] = u32x4{pack_bf16x2(dsv[8 * st], dsv[8 * st + 1]), pack_bf16x2(dsv[8 * st + 2], dsv[8 * st + 3]),
                      pack_bf16x2(dsv[8 * st + 4], dsv[8 * st + 5]), pack_bf16x2(dsv[8 * st + 6], dsv[8 * st + 7])};
+      if constexpr (SPLIT) {
+        // low terms: value - bf16(value), exact in fp32
+#pragma unroll
+        for (int e = 0; e < 4; e++) {
+          const uint32_t h = pa[st][e], g = da[st][e];
+          pl[st][e] = pack_bf16x2(pv[8 * st + 2 * e] - __uint_as_float(h << 16),
+                                  pv[8 * st + 2 * e + 1] - __uint_as_float(h & 0xffff0000u));
+          dl[st][e] = pack_bf16x2(dsv[8 * st + 2 * e] - __uint_as_float(g << 16),
+                                  dsv[8 * st + 2 * e + 1] - __uint_as_float(g & 0xffff0000u));
+        }
+      }
     }
-    key_grads(u, pa, da);
+    key_grads(u, pa, da, pl, dl);
     store_dst(u, da);
     grads(u, path_cur, dsv);
     path_nn = classify(u + 2);
@@ -771,10 +817,10 @@ __device__ __forceinline__ void bwd_item(BwdShared<DQK, DV>& sm, const BwdArgs& 
   }
 }
 
-template <int DQK, int DV>
+template <int DQK, int DV, bool SPLIT>
 __global__ __launch_bounds__(kBwdThreads, 1) void attn_bwd_bf16_kernel(
     BwdArgs A, const WorkItem* __restrict__ items, const int32_t* __restrict__ count) {
-  using S = BwdShared<DQK, DV>;
+  using S = BwdShared<DQK, DV, SPLIT>;
   constexpr int BN = S::BN;
   __shared__ S sm;
 
@@ -802,9 +848,9 @@ __global__ __launch_bounds__(kBwdThreads, 1) void attn_bwd_bf16_kernel(
   for (int x = tid; x < kBwdWaves * 2 * S::kRing; x += kBwdThreads) (&sm.sRing[0][0][0])[x] = 0.0f;
   __syncthreads();
   if (fast) {
-    bwd_item<DQK, DV, true>(sm, A, o, L, n_h, j0, head, tlo);
+    bwd_item<DQK, DV, true, SPLIT>(sm, A, o, L, n_h, j0, head, tlo);
   } else {
-    bwd_item<DQK, DV, false>(sm, A, o, L, n_h, j0, head, tlo);
+    bwd_item<DQK, DV, false, SPLIT>(sm, A, o, L, n_h, j0, head, tlo);
   }
 
   __syncthreads();
@@ -817,36 +863,42 @@ __global__ __launch_bounds__(kBwdThreads, 1) void attn_bwd_bf16_kernel(
 }
 
 template <int DQK, int DV>
-hipError_t launch_bwd(const JaggedArgs& ja, const Tensors& t, const void* d_out, float* dq_acc,
-                      void* dk, void* dv, float* d_rab_pos, float* d_rab_time,
-                      const WorkItem* items, const int32_t* count, int64_t max_items,
-                      hipStream_t s) {
+hipError_t launch_bwd(const JaggedArgs& ja, const Tensors& t, const void* d_out,
+                      const void* d_out_lo, float* dq_acc, void* dk, void* dv, float* d_rab_pos,
+                      float* d_rab_time, const WorkItem* items, const int32_t* count,
+                      int64_t max_items, hipStream_t s) {
   BwdArgs A;
   A.ja = ja;
   A.t = t;
   A.dO = (const uint16_t*)d_out;
+  A.dO_lo = (const uint16_t*)d_out_lo;
   A.dq_acc = dq_acc;
   A.dK = (uint16_t*)dk;
   A.dV = (uint16_t*)dv;
   A.d_rab_pos = d_rab_pos;
   A.d_rab_time = d_rab_time;
-  static_assert(sizeof(BwdShared<DQK, DV>) <= kLdsBytes, "LDS budget");
+  static_assert(sizeof(BwdShared<DQK, DV, true>) <= kLdsBytes, "LDS budget");
   dim3 grid((unsigned)max_items, (unsigned)ja.num_heads);
-  hipLaunchKernelGGL((attn_bwd_bf16_kernel<DQK, DV>), grid, dim3(kBwdThreads), 0, s, A, items,
-                     count);
+  if (d_out_lo)
+    hipLaunchKernelGGL((attn_bwd_bf16_kernel<DQK, DV, true>), grid, dim3(kBwdThreads), 0, s, A,
+                       items, count);
+  else
+    hipLaunchKernelGGL((attn_bwd_bf16_kernel<DQK, DV, false>), grid, dim3(kBwdThreads), 0, s, A,
+                       items, count);
   return hipGetLastError();
 }
 
 }  // namespace
 
 hipError_t launch_attn_bwd_bf16(const JaggedArgs& ja, const Tensors& t, int dqk, int dv,
-                                const void* d_out, float* dq_acc, void* dk, void* dv_out,
-                                float* d_rab_pos, float* d_rab_time, const WorkItem* items,
-                                const int32_t* count, int64_t max_items, hipStream_t s) {
-#define HSTU_BWD_CASE(A, B)                                                                  \
-  if (dqk == A && dv == B)                                                                   \
-    return launch_bwd<A, B>(ja, t, d_out, dq_acc, dk, dv_out, d_rab_pos, d_rab_time, items, \
-                            count, max_items, s);
+                                const void* d_out, const void* d_out_lo, float* dq_acc, void* dk,
+                                void* dv_out, float* d_rab_pos, float* d_rab_time,
+                                const WorkItem* items, const int32_t* count, int64_t max_items,
+                                hipStream_t s) {
+#define HSTU_BWD_CASE(A, B)                                                                 \
+  if (dqk == A && dv == B)                                                                  \
+    return launch_bwd<A, B>(ja, t, d_out, d_out_lo, dq_acc, dk, dv_out, d_rab_pos, d_rab_time, \
+                            items, count, max_items, s);
   HSTU_BWD_CASE(32, 32)
   HSTU_BWD_CASE(32, 64)
   HSTU_BWD_CASE(32, 128)

@@ -89,10 +89,16 @@ __device__ __forceinline__ float silu(float x) {
   return x * __builtin_amdgcn_rcpf(1.0f + e);
 }
 
-template <int DQK, int DV, bool FAST>
+// SPLIT: P enters the second contraction as two bf16 terms, hi = bf16(P)
+// and lo = bf16(P - hi) (two MFMAs per V operand), which leaves O with
+// about 2^-17 relative error instead of bf16's 2^-9; used where O is
+// normalised afterwards (the layer's LayerNorm rescales every row to unit
+// spread and would magnify a bf16 P).
+template <int DQK, int DV, bool FAST, bool SPLIT>
 __device__ __forceinline__ void fwd_item(FwdShared<DQK, DV>& sm, const JaggedArgs& ja,
-                                         const Tensors& t, uint16_t* __restrict__ out, int64_t o,
-                                         int L, int n_h, int i0, int head, int64_t tbase) {
+                                         const Tensors& t, void* __restrict__ out, int out_f32,
+                                         int64_t o, int L, int n_h, int i0, int head,
+                                         int64_t tbase) {
   using Sh = FwdShared<DQK, DV>;
   constexpr int BM = Sh::BM, BN = Sh::BN, K_LD = Sh::K_LD, V_LD = Sh::V_LD;
   constexpr int KCH = BN * DQK / 8, VCH = BN * DV / 8;
@@ -409,7 +415,10 @@ __device__ __forceinline__ void fwd_item(FwdShared<DQK, DV>& sm, const JaggedArg
       acc = mfma32x32x16(as_bf16x8(kf), as_bf16x8(qf[s]), acc);
     }
   };
-  auto aggregate = [&](int u, const u32x4 (&pa)[2]) {
+  // P operands of a tile: pa[st] the bf16 terms (pa[2 + st] the low
+  // terms when SPLIT).
+  constexpr int NPA = SPLIT ? 4 : 2;
+  auto aggregate = [&](int u, const u32x4 (&pa)[NPA]) {
     const uint16_t* vp = sm.sV[u & 3] + tr_row * V_LD + tr_col;
 #pragma unroll
     for (int st = 0; st < 2; st++)
@@ -419,19 +428,23 @@ __device__ __forceinline__ void fwd_item(FwdShared<DQK, DV>& sm, const JaggedArg
         const uint2 lo = lds_read_tr16(base), hi = lds_read_tr16(base + 8 * V_LD);
         const u32x4 vb = {lo.x, lo.y, hi.x, hi.y};
         oacc[nb] = mfma32x32x16(as_bf16x8(pa[st]), as_bf16x8(vb), oacc[nb]);
+        if constexpr (SPLIT) oacc[nb] = mfma32x32x16(as_bf16x8(pa[2 + st]), as_bf16x8(vb), oacc[nb]);
       }
   };
-  auto activate = [&](const f32x16& acc, u32x4 (&pa)[2]) {
+  auto activate = [&](const f32x16& acc, u32x4 (&pa)[NPA]) {
     float p[16];
 #pragma unroll
     for (int q = 0; q < 16; q++) p[q] = silu(acc[q]);
 #pragma unroll
-    for (int st = 0; st < 2; st++) {
-      pa[st][0] = pack_bf16x2(p[8 * st + 0], p[8 * st + 1]);
-      pa[st][1] = pack_bf16x2(p[8 * st + 2], p[8 * st + 3]);
-      pa[st][2] = pack_bf16x2(p[8 * st + 4], p[8 * st + 5]);
-      pa[st][3] = pack_bf16x2(p[8 * st + 6], p[8 * st + 7]);
-    }
+    for (int st = 0; st < 2; st++)
+#pragma unroll
+      for (int e = 0; e < 4; e++) {
+        const uint32_t h = pack_bf16x2(p[8 * st + 2 * e], p[8 * st + 2 * e + 1]);
+        pa[st][e] = h;
+        if constexpr (SPLIT)
+          pa[2 + st][e] = pack_bf16x2(p[8 * st + 2 * e] - __uint_as_float(h << 16),
+                                      p[8 * st + 2 * e + 1] - __uint_as_float(h & 0xffff0000u));
+      }
   };
 
   // One pipeline step for tile u: S(u+1) and P(u-1) V_{u-1} on the matrix
@@ -441,8 +454,8 @@ __device__ __forceinline__ void fwd_item(FwdShared<DQK, DV>& sm, const JaggedArg
   // are staged too (zeros or unused data) so that every step issues the
   // same operations.
   Path path_next = {kUniform, 0.0f, 0.0f, 0};
-  auto step = [&](auto has_prev, int u, f32x16& s_cur, f32x16& s_next, u32x4 (&p_prev)[2],
-                  u32x4 (&p_cur)[2]) {
+  auto step = [&](auto has_prev, int u, f32x16& s_cur, f32x16& s_next, u32x4 (&p_prev)[NPA],
+                  u32x4 (&p_cur)[NPA]) {
     wait_vmcnt_lgkmcnt0<OPS_PER_STEP>();
     barrier_no_fence();
     issue_k(u + 3);
@@ -461,6 +474,7 @@ __device__ __forceinline__ void fwd_item(FwdShared<DQK, DV>& sm, const JaggedArg
     // Keeps the SiLU of tile u in this block (it would otherwise be sunk
     // towards its use in the next step, away from the MFMAs).
     asm volatile("" ::"v"(p_cur[0]), "v"(p_cur[1]));
+    if constexpr (SPLIT) asm volatile("" ::"v"(p_cur[2]), "v"(p_cur[3]));
     path_next = classify(u + 2);
     reduce_ts(u + 3);
   };
@@ -480,7 +494,7 @@ __device__ __forceinline__ void fwd_item(FwdShared<DQK, DV>& sm, const JaggedArg
   wait_vmcnt_lgkmcnt0<0>();
   barrier_no_fence();
   f32x16 sA, sB;
-  u32x4 pA[2], pB[2];
+  u32x4 pA[NPA], pB[NPA];
   {
     const Path p0 = classify(0);
     if (p0.kind == kUniform)
@@ -507,21 +521,33 @@ __device__ __forceinline__ void fwd_item(FwdShared<DQK, DV>& sm, const JaggedArg
   // No LDS-DMA may land after the workgroup ends.
   wait_vmcnt_lgkmcnt0<0>();
 
-  // O accumulator: lane holds (i = iw0 + 8g + 4*half + m, c = 32nb + col).
+  // O accumulator: lane holds (i = iw0 + 8g + 4*half + m, c = 32nb + col);
+  // stored as bf16, or as fp32 for a consumer that normalises it.
   const float invN = 1.0f / (float)N;
-  uint16_t* __restrict__ og = out + (o * H + head) * DV;
+  if (out_f32) {
+    float* __restrict__ og = (float*)out + (o * H + head) * DV;
 #pragma unroll
-  for (int nb = 0; nb < DV / 32; nb++)
+    for (int nb = 0; nb < DV / 32; nb++)
 #pragma unroll
-    for (int q = 0; q < 16; q++) {
-      const int i = iw0 + 8 * (q >> 2) + 4 * half + (q & 3);
-      if (i < L) og[(int64_t)i * H * DV + 32 * nb + col] = f32_to_bf16_bits(oacc[nb][q] * invN);
-    }
+      for (int q = 0; q < 16; q++) {
+        const int i = iw0 + 8 * (q >> 2) + 4 * half + (q & 3);
+        if (i < L) og[(int64_t)i * H * DV + 32 * nb + col] = oacc[nb][q] * invN;
+      }
+  } else {
+    uint16_t* __restrict__ og = (uint16_t*)out + (o * H + head) * DV;
+#pragma unroll
+    for (int nb = 0; nb < DV / 32; nb++)
+#pragma unroll
+      for (int q = 0; q < 16; q++) {
+        const int i = iw0 + 8 * (q >> 2) + 4 * half + (q & 3);
+        if (i < L) og[(int64_t)i * H * DV + 32 * nb + col] = f32_to_bf16_bits(oacc[nb][q] * invN);
+      }
+  }
 }
 
-template <int DQK, int DV>
+template <int DQK, int DV, bool SPLIT>
 __global__ __launch_bounds__(256, 2) void attn_fwd_bf16_kernel(JaggedArgs ja, Tensors t,
-                                                               uint16_t* __restrict__ out,
+                                                               void* __restrict__ out, int out_f32,
                                                                const WorkItem* __restrict__ items,
                                                                const int32_t* __restrict__ count) {
   using Sh = FwdShared<DQK, DV>;
@@ -546,28 +572,35 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_bf16_kernel(JaggedArgs ja, Te
     sm.sTab[x] = (fast && x == 31) ? ja.rab_time[0] : ja.rab_time[min(63 - x, NB - 1)];
   __syncthreads();
   if (fast) {
-    fwd_item<DQK, DV, true>(sm, ja, t, out, o, L, n_h, i0, head, tlo);
+    fwd_item<DQK, DV, true, SPLIT>(sm, ja, t, out, out_f32, o, L, n_h, i0, head, tlo);
   } else {
-    fwd_item<DQK, DV, false>(sm, ja, t, out, o, L, n_h, i0, head, tlo);
+    fwd_item<DQK, DV, false, SPLIT>(sm, ja, t, out, out_f32, o, L, n_h, i0, head, tlo);
   }
 }
 
 template <int DQK, int DV>
-hipError_t launch_fwd(const JaggedArgs& ja, const Tensors& t, void* out, const WorkItem* items,
-                      const int32_t* count, int64_t max_items, hipStream_t s) {
+hipError_t launch_fwd(const JaggedArgs& ja, const Tensors& t, void* out, int out_f32,
+                      const WorkItem* items, const int32_t* count, int64_t max_items,
+                      hipStream_t s) {
   dim3 grid((unsigned)max_items, (unsigned)ja.num_heads);
-  hipLaunchKernelGGL((attn_fwd_bf16_kernel<DQK, DV>), grid, dim3(256), 0, s, ja, t,
-                     (uint16_t*)out, items, count);
+  // The layer's fp32 output goes to a LayerNorm: split P there.
+  if (out_f32)
+    hipLaunchKernelGGL((attn_fwd_bf16_kernel<DQK, DV, true>), grid, dim3(256), 0, s, ja, t, out,
+                       out_f32, items, count);
+  else
+    hipLaunchKernelGGL((attn_fwd_bf16_kernel<DQK, DV, false>), grid, dim3(256), 0, s, ja, t, out,
+                       out_f32, items, count);
   return hipGetLastError();
 }
 
 }  // namespace
 
 hipError_t launch_attn_fwd_bf16(const JaggedArgs& ja, const Tensors& t, int dqk, int dv, void* out,
-                                const WorkItem* items, const int32_t* count, int64_t max_items,
-                                hipStream_t s) {
+                                int out_f32, const WorkItem* items, const int32_t* count,
+                                int64_t max_items, hipStream_t s) {
 #define HSTU_FWD_CASE(A, B) \
-  if (dqk == A && dv == B) return launch_fwd<A, B>(ja, t, out, items, count, max_items, s);
+  if (dqk == A && dv == B)  \
+    return launch_fwd<A, B>(ja, t, out, out_f32, items, count, max_items, s);
   HSTU_FWD_CASE(32, 32)
   HSTU_FWD_CASE(32, 64)
   HSTU_FWD_CASE(32, 128)

@@ -65,14 +65,18 @@ hipError_t launch_bucketize(int32_t num_seqs, int64_t total_tokens, int32_t num_
                             const int64_t* pair_offsets, int64_t total_pairs, uint8_t* out,
                             hipStream_t s);
 
-// bf16 MFMA attention.
+// bf16 MFMA attention.  The forward stores O as bf16, or as fp32 when
+// out_f32 (the layer keeps it in fp32 for the layer norm).
 hipError_t launch_attn_fwd_bf16(const JaggedArgs& ja, const Tensors& t, int dqk, int dv, void* out,
+                                int out_f32, const WorkItem* items, const int32_t* count,
+                                int64_t max_items, hipStream_t s);
+// d_out_lo: null, or the low bf16 terms of dO (d_out holding the high
+// ones), for a dO that is the fp32 output of the layer's LayerNorm backward.
+hipError_t launch_attn_bwd_bf16(const JaggedArgs& ja, const Tensors& t, int dqk, int dv,
+                                const void* d_out, const void* d_out_lo, float* dq_acc, void* dk,
+                                void* dv_out, float* d_rab_pos, float* d_rab_time,
                                 const WorkItem* items, const int32_t* count, int64_t max_items,
                                 hipStream_t s);
-hipError_t launch_attn_bwd_bf16(const JaggedArgs& ja, const Tensors& t, int dqk, int dv,
-                                const void* d_out, float* dq_acc, void* dk, void* dv_out,
-                                float* d_rab_pos, float* d_rab_time, const WorkItem* items,
-                                const int32_t* count, int64_t max_items, hipStream_t s);
 // fp32 head-major dQ accumulator [h][T][d] -> bf16 token-major [T][h][d], scaled.
 hipError_t launch_dq_convert_bf16(const float* acc, void* dq, int64_t T, int32_t H, int32_t d,
                                   float scale, hipStream_t s);
@@ -89,7 +93,18 @@ hipError_t launch_attn_bwd_f32(const JaggedArgs& ja, const Tensors& t, int dqk, 
 hipError_t launch_mfma_probe(int32_t iters, int32_t waves_per_simd, float* sink, double* flop,
                              hipStream_t s);
 
-// LayerNorm(x) (.) u per token over D features.
+// Backward of LayerNorm(x) (.) u: du, dx (dense [T][D]) and, when non-null,
+// dw / db accumulated into fp32 [D] (zeroed by the caller).  x is fp32;
+// u, dy, du, dx are bf16 when is_bf16, else fp32; with is_bf16 and a
+// non-null dx_lo, dx = bf16(v) and dx_lo = bf16(v - dx) hold the fp32 v
+// as two terms.
+hipError_t launch_ln_gate_bwd(int is_bf16, int64_t T, int32_t D, const void* x, const void* u,
+                              int64_t u_stride, const void* dy, const float* w, const float* b,
+                              const float* mean, const float* rstd, void* du, void* dx,
+                              void* dx_lo, float* dw, float* db, hipStream_t s);
+
+// LayerNorm(x) (.) u per token over D features; x fp32, u and y bf16 when
+// is_bf16, else fp32.
 hipError_t launch_ln_gate(int is_bf16, int64_t T, int32_t D, const void* x, const void* u,
                           int64_t u_stride, const float* w, const float* b, float eps, void* y,
                           float* mean, float* rstd, hipStream_t s);

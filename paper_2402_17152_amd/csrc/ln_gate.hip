@@ -1,11 +1,15 @@
-// Epilogue of the HSTU layer (Eq. 3): Y_pre = LayerNorm(A V) (.) U.
+// Epilogue of the HSTU layer (Eq. 3): Y_pre = LayerNorm(A V) (.) U, and
+// its backward.
 // Layer norm over the D = h * d_v features of each token with biased
 // variance and optional affine weight/bias; the result gates U
 // elementwise.  Saves per-token mean and 1/sqrt(var + eps) for a backward.
 //
 // HBM-bound: one wave per token, each lane holds its 8-element chunks in
 // registers (16-byte loads for bf16), two-pass mean/variance in fp32 with
-// wave reductions, one pass of stores.
+// wave reductions, one pass of stores.  The attention output x is read in
+// fp32 for both dtypes: normalising divides by the row's spread, which can
+// be far smaller than its magnitude, so a bf16-rounded x would carry
+// errors of several percent into Y.
 #include "kernels.h"
 
 namespace hstu {
@@ -75,7 +79,7 @@ __global__ __launch_bounds__(256) void ln_gate_kernel(int64_t T, int D, const vo
   for (int c = 0; c < CH; c++) {
     const int idx = (c * 64 + lane) * 8;
     if (idx < D) {
-      load8<BF16>(x, t * D + idx, v[c]);
+      load8<false>(x, t * D + idx, v[c]);
 #pragma unroll
       for (int e = 0; e < 8; e++) sum += v[c][e];
     }
@@ -117,6 +121,108 @@ __global__ __launch_bounds__(256) void ln_gate_kernel(int64_t T, int D, const vo
   }
 }
 
+// Backward of the epilogue, per token: with z = (x - mean) * rstd (the
+// forward's saved statistics) and zn = z * w + b,
+//   du = zn (.) dy,  dzn = dy (.) u,  dw += dzn z,  db += dzn,
+//   dz = dzn (.) w,  dx = rstd (dz - mean(dz) - z mean(dz z)).
+// One wave per token in a grid-stride loop; dw / db partials stay in
+// registers across the wave's tokens and reach HBM with one float atomic
+// per feature and wave.
+template <bool BF16, int CH>
+__global__ __launch_bounds__(256) void ln_gate_bwd_kernel(
+    int64_t T, int D, const void* __restrict__ x, const void* __restrict__ u, int64_t u_stride,
+    const void* __restrict__ dy, const float* __restrict__ w, const float* __restrict__ b,
+    const float* __restrict__ mean, const float* __restrict__ rstd, void* __restrict__ du,
+    void* __restrict__ dx, void* __restrict__ dx_lo, float* __restrict__ dw,
+    float* __restrict__ db) {
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  float pw[CH][8], pb[CH][8];
+#pragma unroll
+  for (int c = 0; c < CH; c++)
+#pragma unroll
+    for (int e = 0; e < 8; e++) pw[c][e] = pb[c][e] = 0.0f;
+  for (int64_t t = (int64_t)blockIdx.x * 4 + wave; t < T; t += (int64_t)gridDim.x * 4) {
+    const float mu = mean[t], rs = rstd[t];
+    float z[CH][8], dz[CH][8];
+    float s1 = 0.0f, s2 = 0.0f;
+#pragma unroll
+    for (int c = 0; c < CH; c++) {
+      const int idx = (c * 64 + lane) * 8;
+      if (idx < D) {
+        float xv[8], uv[8], gv[8], o[8];
+        load8<false>(x, t * D + idx, xv);
+        load8<BF16>(u, t * u_stride + idx, uv);
+        load8<BF16>(dy, t * D + idx, gv);
+#pragma unroll
+        for (int e = 0; e < 8; e++) {
+          const float zz = (xv[e] - mu) * rs;
+          const float ww = w ? w[idx + e] : 1.0f, bb = b ? b[idx + e] : 0.0f;
+          const float dzn = gv[e] * uv[e];
+          z[c][e] = zz;
+          o[e] = (zz * ww + bb) * gv[e];
+          pw[c][e] += dzn * zz;
+          pb[c][e] += dzn;
+          dz[c][e] = dzn * ww;
+          s1 += dz[c][e];
+          s2 += dz[c][e] * zz;
+        }
+        store8<BF16>(du, t * D + idx, o);
+      }
+    }
+    const float m1 = wave_sum(s1) / (float)D, m2 = wave_sum(s2) / (float)D;
+#pragma unroll
+    for (int c = 0; c < CH; c++) {
+      const int idx = (c * 64 + lane) * 8;
+      if (idx < D) {
+        float o[8];
+#pragma unroll
+        for (int e = 0; e < 8; e++) o[e] = rs * (dz[c][e] - m1 - z[c][e] * m2);
+        store8<BF16>(dx, t * D + idx, o);
+        if (BF16 && dx_lo) {
+          // low terms: o - bf16(o), exact in fp32
+          float r[8];
+#pragma unroll
+          for (int e = 0; e < 8; e++) r[e] = o[e] - bf16_bits_to_f32(f32_to_bf16_bits(o[e]));
+          store8<BF16>(dx_lo, t * D + idx, r);
+        }
+      }
+    }
+  }
+#pragma unroll
+  for (int c = 0; c < CH; c++) {
+    const int idx = (c * 64 + lane) * 8;
+    if (idx < D) {
+#pragma unroll
+      for (int e = 0; e < 8; e++) {
+        if (dw) unsafeAtomicAdd(&dw[idx + e], pw[c][e]);
+        if (db) unsafeAtomicAdd(&db[idx + e], pb[c][e]);
+      }
+    }
+  }
+}
+
+template <bool BF16>
+hipError_t ln_bwd_case(int64_t T, int32_t D, const void* x, const void* u, int64_t u_stride,
+                       const void* dy, const float* w, const float* b, const float* mean,
+                       const float* rstd, void* du, void* dx, void* dx_lo, float* dw,
+                       float* db, hipStream_t s) {
+  // Enough waves to fill the device; each walks several tokens so the
+  // per-feature atomics stay few.
+  const int64_t blocks = min((T + 3) / 4, (int64_t)1024);
+  dim3 grid((unsigned)blocks);
+  const int ch = (D + 511) / 512;
+#define LN_BWD_CALL(C)                                                                        \
+  hipLaunchKernelGGL((ln_gate_bwd_kernel<BF16, C>), grid, dim3(256), 0, s, T, D, x, u,         \
+                     u_stride, dy, w, b, mean, rstd, du, dx, dx_lo, dw, db);                  \
+  return hipGetLastError();
+  if (ch <= 1) { LN_BWD_CALL(1) }
+  if (ch <= 2) { LN_BWD_CALL(2) }
+  if (ch <= 4) { LN_BWD_CALL(4) }
+  if (ch <= 8) { LN_BWD_CALL(8) }
+#undef LN_BWD_CALL
+  return hipErrorInvalidValue;
+}
+
 template <bool BF16>
 hipError_t ln_case(int64_t T, int32_t D, const void* x, const void* u, int64_t u_stride,
                    const float* w, const float* b, float eps, void* y, float* mean, float* rstd,
@@ -136,6 +242,18 @@ hipError_t ln_case(int64_t T, int32_t D, const void* x, const void* u, int64_t u
 }
 
 }  // namespace
+
+hipError_t launch_ln_gate_bwd(int is_bf16, int64_t T, int32_t D, const void* x, const void* u,
+                              int64_t u_stride, const void* dy, const float* w, const float* b,
+                              const float* mean, const float* rstd, void* du, void* dx,
+                              void* dx_lo, float* dw, float* db, hipStream_t s) {
+  if (T <= 0) return hipSuccess;
+  if (is_bf16)
+    return ln_bwd_case<true>(T, D, x, u, u_stride, dy, w, b, mean, rstd, du, dx, dx_lo, dw, db,
+                             s);
+  return ln_bwd_case<false>(T, D, x, u, u_stride, dy, w, b, mean, rstd, du, dx, nullptr, dw, db,
+                            s);
+}
 
 hipError_t launch_ln_gate(int is_bf16, int64_t T, int32_t D, const void* x, const void* u,
                           int64_t u_stride, const float* w, const float* b, float eps, void* y,

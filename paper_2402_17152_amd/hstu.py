@@ -24,7 +24,7 @@ STATUS = {0: "HSTU_OK", 1: "HSTU_ERR_INVALID_ARGUMENT", 2: "HSTU_ERR_UNSUPPORTED
 EXPORTED = ("hstu_workspace_bytes", "hstu_attn_fwd", "hstu_attn_bwd", "hstu_layer_fwd",
             "hstu_time_bucketize", "hstu_complete_cumsum", "hstu_pair_offsets", "hstu_validate",
             "hstu_last_error", "hstu_abi_version", "hstu_timing_enable", "hstu_timing_read",
-            "hstu_timing_reset", "hstu_probe_mfma_bf16")
+            "hstu_timing_reset", "hstu_probe_mfma_bf16", "hstu_layer_bwd")
 
 
 class Problem(ctypes.Structure):
@@ -59,6 +59,8 @@ def _load():
         "hstu_attn_bwd": (i32, [PP, PJ, P, i64, P, i64, P, i64, P, P, P, P, P, P, P, sz, P]),
         "hstu_layer_fwd": (i32, [PP, PJ, P, i64, P, i64, P, i64, P, i64, P, P, f32, P, P, P, P,
                                  P, sz, P]),
+        "hstu_layer_bwd": (i32, [PP, PJ, P, i64, P, i64, P, i64, P, i64, P, P, P, P, P, P,
+                                 P, P, P, P, P, P, P, P, P, sz, P]),
         "hstu_time_bucketize": (i32, [i32, i64, i32, P, P, P, i64, P, P]),
         "hstu_complete_cumsum": (i32, [i32, P, P, P]),
         "hstu_pair_offsets": (i32, [i32, P, P, P]),
@@ -197,12 +199,12 @@ def hstu_attn_bwd(q, k, v, d_out, seq_offsets, timestamps, rab_pos, rab_time, ma
 def hstu_layer_fwd(q, k, v, u, seq_offsets, timestamps, rab_pos, rab_time, max_seq_len,
                    num_targets=None, ln_weight=None, ln_bias=None, ln_eps=1e-5, attn_out=None,
                    y=None, ln_mean=None, ln_rstd=None, ws=None, stream=None):
-    """(attn_out [T, D], y [T, D], ln_mean [T], ln_rstd [T]) of Eq. 2-3."""
+    """(attn_out [T, D] fp32, y [T, D], ln_mean [T], ln_rstd [T]) of Eq. 2-3."""
     p = problem_for(q, v, seq_offsets, max_seq_len, rab_time)
     j = make_jagged(seq_offsets, timestamps, rab_pos, rab_time, num_targets)
     T, D = q.shape[0], q.shape[1] * v.shape[2]
     if attn_out is None:
-        attn_out = torch.empty((T, D), dtype=q.dtype, device=q.device)
+        attn_out = torch.empty((T, D), dtype=torch.float32, device=q.device)
     if y is None:
         y = torch.empty((T, D), dtype=q.dtype, device=q.device)
     if ln_mean is None:
@@ -217,6 +219,39 @@ def hstu_layer_fwd(q, k, v, u, seq_offsets, timestamps, rab_pos, rab_time, max_s
                               _ptr(y), _ptr(ln_mean), _ptr(ln_rstd), _ptr(ws), ws.numel(),
                               _stream(stream)))
     return attn_out, y, ln_mean, ln_rstd
+
+
+def hstu_layer_bwd(q, k, v, u, attn_out, ln_mean, ln_rstd, d_y, seq_offsets, timestamps,
+                   rab_pos, rab_time, max_seq_len, num_targets=None, ln_weight=None,
+                   ln_bias=None, want_ln_grads=None, grads=None, ws=None, stream=None):
+    """(dq, dk, dv, du, d_ln_weight, d_ln_bias, d_rab_pos, d_rab_time) for the
+    loss <Y, d_y> of Eq. 2-3; attn_out, ln_mean, ln_rstd from hstu_layer_fwd.
+    d_ln_weight / d_ln_bias are computed when want_ln_grads (default: when
+    ln_weight is given), else None."""
+    p = problem_for(q, v, seq_offsets, max_seq_len, rab_time)
+    j = make_jagged(seq_offsets, timestamps, rab_pos, rab_time, num_targets)
+    T, D = q.shape[0], q.shape[1] * v.shape[2]
+    if want_ln_grads is None:
+        want_ln_grads = ln_weight is not None
+    if grads is None:
+        H = q.shape[1]
+        grads = (torch.empty((T, H, q.shape[2]), dtype=q.dtype, device=q.device),
+                 torch.empty((T, H, k.shape[2]), dtype=q.dtype, device=q.device),
+                 torch.empty((T, H, v.shape[2]), dtype=q.dtype, device=q.device),
+                 torch.empty((T, D), dtype=q.dtype, device=q.device),
+                 torch.empty(D, dtype=torch.float32, device=q.device) if want_ln_grads else None,
+                 torch.empty(D, dtype=torch.float32, device=q.device) if want_ln_grads else None,
+                 torch.empty_like(rab_pos), torch.empty_like(rab_time))
+    dq, dk, dv, du, dw, db, drp, drt = grads
+    if ws is None:
+        ws = workspace(p, q.device)
+    _check(lib.hstu_layer_bwd(ctypes.byref(p), ctypes.byref(j), _ptr(q), _row_stride(q), _ptr(k),
+                              _row_stride(k), _ptr(v), _row_stride(v), _ptr(u), _row_stride(u),
+                              _ptr(attn_out), _ptr(ln_weight), _ptr(ln_bias), _ptr(ln_mean),
+                              _ptr(ln_rstd), _ptr(d_y), _ptr(dq), _ptr(dk), _ptr(dv), _ptr(du),
+                              _ptr(dw), _ptr(db), _ptr(drp), _ptr(drt), _ptr(ws), ws.numel(),
+                              _stream(stream)))
+    return grads
 
 
 def hstu_complete_cumsum(x: torch.Tensor, out=None, stream=None):

@@ -197,42 +197,133 @@ def test_complete_cumsum(hs, oracle_mod):
         assert np.array_equal(got, oracle_mod.complete_cumsum(x))
 
 
+def _ln_params(D, seed):
+    rng = np.random.default_rng(seed)
+    w = (1 + 0.1 * rng.standard_normal(D)).astype(np.float32)
+    b = (0.1 * rng.standard_normal(D)).astype(np.float32)
+    return w, b
+
+
+def _ln_tol(dtype):
+    # mean / rstd of the stored attention output: exact up to fp32 for the
+    # fp32 path; the bf16 path normalises the bf16-rounded output
+    return 1e-5 if dtype == "f32" else 2e-2
+
+
 @pytest.mark.parametrize("dtype", ["bf16", "f32"])
 def test_layer_fwd_epilogue(hs, oracle_mod, dtype):
     """hstu_layer_fwd = attention then LayerNorm(A V) (.) U (Eq. 3), with a
-    random affine; attn_out, y, mean and rstd against the oracle."""
+    random affine; attn_out, y, mean and rstd against the oracle's own
+    attention output and epilogue."""
     batch = inputs.make_batch(2, seed=21, lengths=(300, 1, 129, 64), num_heads=4, d_qk=64, d_v=64,
                               max_seq_len=300, dtype=dtype)
     d = gu.dev_inputs(batch)
-    rng = np.random.default_rng(3)
     D = 4 * 64
-    w = (1 + 0.1 * rng.standard_normal(D)).astype(np.float32)
-    b = (0.1 * rng.standard_normal(D)).astype(np.float32)
+    w, b = _ln_params(D, 3)
     ao, y, mu, rs = hs.hstu_layer_fwd(d["q"], d["k"], d["v"], d["u"], d["seq_offsets"],
                                       d["timestamps"], d["rab_pos"], d["rab_time"], 300,
                                       ln_weight=torch.from_numpy(w).cuda(),
                                       ln_bias=torch.from_numpy(b).cuda(), ln_eps=1e-5)
     torch.cuda.synchronize()
     tau = gu.tol(batch)
-    ref_o = gu.oracle_fwd(oracle_mod, batch)
-    gu.assert_close("attn_out", gu.to_f64(ao), ref_o.reshape(-1, D), tau, dtype)
-    # the epilogue reads the stored (rounded) attention output
-    x = gu.to_f64(ao)
-    ry, rmu, rrs = oracle_mod.ln_gate(x, batch.f64("u").reshape(-1, D), w, b, 1e-5)
+    ref_o = gu.oracle_fwd(oracle_mod, batch).reshape(-1, D)
+    gu.assert_close("attn_out", gu.to_f64(ao), ref_o, tau, dtype)
+    ry, rmu, rrs = oracle_mod.ln_gate(ref_o, batch.f64("u").reshape(-1, D), w, b, 1e-5)
     gu.assert_close("y", gu.to_f64(y), ry, tau, dtype)
-    gu.assert_close("mean", gu.to_f64(mu), rmu, 1e-5)
-    gu.assert_close("rstd", gu.to_f64(rs), rrs, 1e-5)
+    gu.assert_close("mean", gu.to_f64(mu), rmu, _ln_tol(dtype))
+    gu.assert_close("rstd", gu.to_f64(rs), rrs, _ln_tol(dtype))
 
 
 def test_layer_fwd_training_workload(hs, oracle_mod):
-    """Epilogue at the training workload's full size (T=60383, D=512)."""
+    """Epilogue at the training workload's full size (T=60383, D=512); the
+    oracle on three whole sampled sequences."""
     batch = inputs.make_batch("training")
     d = gu.dev_inputs(batch)
     ao, y, mu, rs = hs.hstu_layer_fwd(d["q"], d["k"], d["v"], d["u"], d["seq_offsets"],
                                       d["timestamps"], d["rab_pos"], d["rab_time"], 4096)
     torch.cuda.synchronize()
-    x = gu.to_f64(ao)
     D = 512
-    ry, rmu, rrs = oracle_mod.ln_gate(x, batch.f64("u").reshape(-1, D))
-    gu.assert_close("y", gu.to_f64(y), ry, 2e-2, "bf16")
-    gu.assert_close("rstd", gu.to_f64(rs), rrs, 1e-5)
+    L = batch.lengths
+    seqs = [int(np.argmax(L)), int(np.argmin(L)), 7]
+    sub = gu.sub_batch(batch, seqs)
+    rows = gu.token_rows(batch, seqs)
+    ref_o = gu.oracle_fwd(oracle_mod, sub).reshape(-1, D)
+    ry, rmu, rrs = oracle_mod.ln_gate(ref_o, sub.f64("u").reshape(-1, D))
+    gu.assert_close("y", gu.to_f64(y)[rows], ry, 2e-2, "bf16")
+    gu.assert_close("rstd", gu.to_f64(rs)[rows], rrs, 2e-2)
+
+
+def _layer_bwd_check(hs, oracle_mod, batch, seqs=None, affine=True):
+    """hstu_layer_fwd then hstu_layer_bwd with dY = the batch's seeded dO
+    draw, against the oracle chain: its own attention output, the
+    epilogue backward (dU, d attn_out, d gamma, d beta), then the
+    attention backward from that d attn_out.  With `seqs`, the oracle runs
+    on those whole sequences and parameter gradients are checked on a
+    launch over them alone."""
+    N = batch.spec.max_seq_len
+    H, dv = batch.spec.num_heads, batch.spec.d_v
+    D = H * dv
+    dt = batch.spec.dtype
+    tau = gu.tol(batch)
+    w, b = _ln_params(D, 5)
+
+    def gpu(bt):
+        d = gu.dev_inputs(bt)
+        wt = torch.from_numpy(w).cuda() if affine else None
+        bb = torch.from_numpy(b).cuda() if affine else None
+        ao, y, mu, rs = hs.hstu_layer_fwd(d["q"], d["k"], d["v"], d["u"], d["seq_offsets"],
+                                          d["timestamps"], d["rab_pos"], d["rab_time"], N,
+                                          num_targets=d["num_targets"], ln_weight=wt,
+                                          ln_bias=bb, ln_eps=1e-5)
+        dy = d["do"].reshape(-1, D)
+        g = hs.hstu_layer_bwd(d["q"], d["k"], d["v"], d["u"], ao, mu, rs, dy, d["seq_offsets"],
+                              d["timestamps"], d["rab_pos"], d["rab_time"], N,
+                              num_targets=d["num_targets"], ln_weight=wt, ln_bias=bb,
+                              want_ln_grads=True)
+        torch.cuda.synchronize()
+        return [None if x is None else gu.to_f64(x) for x in g]
+
+    def oracle(bt):
+        o = gu.oracle_fwd(oracle_mod, bt).reshape(-1, D)
+        dx, du, dg, db = oracle_mod.ln_gate_bwd(o, bt.f64("u").reshape(-1, D),
+                                                bt.f64("do").reshape(-1, D),
+                                                w if affine else np.ones(D),
+                                                b if affine else np.zeros(D), 1e-5)
+        T = o.shape[0]
+        dq, dk, dvv, drp, drt = oracle_mod.attn_bwd(
+            bt.seq_offsets, N, bt.timestamps, bt.rab_pos, bt.rab_time, bt.f64("q"),
+            bt.f64("k"), bt.f64("v"), dx.reshape(T, H, dv), num_targets=bt.num_targets)
+        return dq, dk, dvv, du, dg, db, drp, drt
+
+    got = gpu(batch)
+    sub = batch if seqs is None else gu.sub_batch(batch, seqs)
+    ref = oracle(sub)
+    rows = slice(None) if seqs is None else gu.token_rows(batch, seqs)
+    for name, gi, ri in zip(("dq", "dk", "dv", "du"), got[:4], ref[:4]):
+        e = gu.assert_close(name, gi.reshape(gi.shape[0], -1)[rows], ri.reshape(ri.shape[0], -1),
+                            tau, dt)
+        print(f"  {name} err {e[0]:.3e} raw {e[1]:.3e}")
+    gs = got if seqs is None else gpu(sub)
+    for name, gi, ri in zip(("d_ln_weight", "d_ln_bias", "d_rab_pos", "d_rab_time"),
+                            gs[4:], ref[4:]):
+        e = gu.assert_close(name, gi, ri, tau)
+        print(f"  {name} err {e[0]:.3e} raw {e[1]:.3e}")
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+@pytest.mark.parametrize("affine", [True, False])
+def test_layer_bwd_small(hs, oracle_mod, dtype, affine):
+    """hstu_layer_bwd (epilogue backward then attention backward) on a
+    small jagged batch with ragged tails, an empty and a length-1 sequence,
+    candidates, and both affine settings."""
+    batch = inputs.make_batch(2, seed=23, lengths=(300, 0, 1, 129, 70), num_targets=(0, 0, 0, 17, 5),
+                              num_heads=4, d_qk=64, d_v=64, max_seq_len=300, dtype=dtype)
+    _layer_bwd_check(hs, oracle_mod, batch, affine=affine)
+
+
+def test_layer_bwd_training_sampled(hs, oracle_mod):
+    """hstu_layer_bwd at the training workload's full size (T=60383, h=8,
+    d=64, N=4096); the oracle on three whole sequences."""
+    batch = inputs.make_batch("training")
+    L = batch.lengths
+    _layer_bwd_check(hs, oracle_mod, batch, seqs=[int(np.argmax(L)), int(np.argmin(L)), 7])
