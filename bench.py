@@ -121,8 +121,83 @@ def aux_measurements(hstu, torch, d, batch, stream):
     out["plain_fill_reference"] = {"ms": ms, "gbs": total_pairs / (ms * 1e-3) / 1e9,
                                    "bytes": total_pairs}
     del flush
+    out["mfalcon"] = mfalcon_measurement(hstu, torch, stream)
     out["gpu_clock"] = gpu_clock()
     return out
+
+
+def _time_ms(torch, stream, fn, reps=6):
+    ts = []
+    for _ in range(reps):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        fn()
+        e1.record(stream)
+        torch.cuda.synchronize()
+        ts.append(e0.elapsed_time(e1))
+    return percentile(ts[1:], 0.5)
+
+
+def mfalcon_measurement(hstu, torch, stream):
+    """M-FALCON on the target workload (16 users, 2048 prefix tokens, 1024
+    candidates, h=4, d=128, N=3072): the uncached target-aware forward over
+    prefix ++ all candidates against cached passes that compute only the
+    candidate rows from the prefix's cached K and V, as one microbatch of
+    1024 and as four of 256 (inputs of each microbatch gathered beforehand)."""
+    import numpy as np
+    from paper_2402_17152_amd import inputs
+    batch = inputs.make_batch("target")
+    s = batch.spec
+    d = inputs.to_device(batch)
+    N = s.max_seq_len
+    offs, nt = batch.seq_offsets, batch.num_targets
+    B = len(nt)
+    nh = np.diff(offs) - nt
+
+    def idx(parts):
+        return torch.from_numpy(np.concatenate(parts).astype(np.int64)).cuda()
+
+    pre = idx([np.arange(offs[b], offs[b] + nh[b]) for b in range(B)])
+    kc, vc = d["k"].index_select(0, pre), d["v"].index_select(0, pre)
+    cts = d["timestamps"].index_select(0, pre)
+    coffs = torch.from_numpy(np.concatenate([[0], np.cumsum(nh)]).astype(np.int64)).cuda()
+
+    def microbatches(b_m):
+        mbs = []
+        for i in range((int(nt.max()) + b_m - 1) // b_m):
+            c0, c1 = np.minimum(i * b_m, nt), np.minimum((i + 1) * b_m, nt)
+            r = idx([np.arange(offs[b] + nh[b] + c0[b], offs[b] + nh[b] + c1[b])
+                     for b in range(B)])
+            co = torch.from_numpy(np.concatenate([[0], np.cumsum(c1 - c0)]).astype(np.int64))
+            q, k, v = (d[x].index_select(0, r) for x in ("q", "k", "v"))
+            ts = d["timestamps"].index_select(0, r)
+            p = hstu.problem_for(q, v, co, N, d["rab_time"])
+            mbs.append((q, k, v, co.cuda(), ts, torch.empty_like(v), hstu.workspace(p)))
+        return mbs
+
+    full_out = torch.empty_like(d["v"])
+    ws_full = hstu.workspace(hstu.problem_for(d["q"], d["v"], d["seq_offsets"], N, d["rab_time"]))
+    ms_uncached = _time_ms(torch, stream, lambda: hstu.hstu_attn_fwd(
+        d["q"], d["k"], d["v"], d["seq_offsets"], d["timestamps"], d["rab_pos"], d["rab_time"],
+        N, num_targets=d["num_targets"], out=full_out, ws=ws_full, stream=stream))
+    cand = int(nt.sum())
+    flop_cached = 2 * (s.d_qk + s.d_v) * s.num_heads * int((nt * (nh + 1)).sum())
+    res = {"workload": "target: 16 users x (2048 prefix + 1024 candidates), h=4, d=128, N=3072",
+           "uncached_ms": ms_uncached,
+           "cached_flop": flop_cached}
+    for b_m in (1024, 256):
+        mbs = microbatches(b_m)
+
+        def run():
+            for (q, k, v, co, ts, o, ws) in mbs:
+                hstu.hstu_attn_fwd_cached(q, k, v, co, ts, kc, vc, coffs, cts, d["rab_pos"],
+                                          d["rab_time"], N, out=o, ws=ws, stream=stream)
+        ms = _time_ms(torch, stream, run)
+        res[f"cached_b{b_m}"] = {"ms": ms, "passes": len(mbs),
+                                 "tflops": flop_cached / (ms * 1e-3) / 1e12,
+                                 "candidates_per_s": cand / (ms * 1e-3),
+                                 "speedup_vs_uncached": ms_uncached / ms}
+    return res
 
 
 def source_hash(*names) -> str:

@@ -118,6 +118,37 @@ hstu_status_t hstu_attn_fwd(const hstu_problem_t* p, const hstu_jagged_t* j,
                             void* out, void* ws, size_t ws_bytes,
                             void* hip_stream);
 
+/* M-FALCON cached candidate pass (Algorithm 1, one microbatch; the
+ * encoder-level cache of the appendix on M-FALCON): the attention output
+ * of a microbatch of ranking candidates against the cached keys and
+ * values of their users' histories, without recomputing the histories.
+ * j describes the candidates: sequence b owns candidate rows
+ * [seq_offsets[b], seq_offsets[b+1]) of q, k, v (as in hstu_attn_fwd) and
+ * their timestamps; j->num_targets is ignored.  The histories form a
+ * jagged batch of their own: cache_offsets [B+1] (device), history b having
+ * n_b = cache_offsets[b+1] - cache_offsets[b] tokens, cache_timestamps
+ * [cache_tokens], and the history K and V rows k_cache, v_cache (h*d_qk
+ * and h*d_v elements at kc_stride / vc_stride), e.g. the k and v of an
+ * hstu_attn_fwd call over the histories.  Every candidate sits at
+ * position n_b and sees all n_b history keys and itself, no other
+ * candidate: out (dense [T][h][d_v], T = candidate rows) equals the
+ * candidate rows of hstu_attn_fwd over history ++ candidates with
+ * num_targets = the candidate count (the target-aware mask), for any
+ * split of a user's candidates into microbatches.  p: num_seqs = B,
+ * total_tokens = T, max_seq_len = N, the normaliser (n_b + candidates of
+ * b <= N, not checked); bf16 problems only (HSTU_ERR_UNSUPPORTED for fp32). */
+hstu_status_t hstu_attn_fwd_cached(const hstu_problem_t* p, const hstu_jagged_t* j,
+                                   const void* q, int64_t q_stride,
+                                   const void* k, int64_t k_stride,
+                                   const void* v, int64_t v_stride,
+                                   const int64_t* cache_offsets,
+                                   const int64_t* cache_timestamps,
+                                   int64_t cache_tokens,
+                                   const void* k_cache, int64_t kc_stride,
+                                   const void* v_cache, int64_t vc_stride,
+                                   void* out, void* ws, size_t ws_bytes,
+                                   void* hip_stream);
+
 /* Backward of hstu_attn_fwd for the loss <out, d_out>.
  * d_out: dense [T][h][d_v].  dq, dk: dense [T][h][d_qk]; dv: dense
  * [T][h][d_v]; d_rab_pos [2N-1] and d_rab_time [B_t] (fp32, summed over

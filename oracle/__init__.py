@@ -183,3 +183,42 @@ def ln_gate_bwd(x, u, dy, gamma=None, beta=None, eps=1e-5):
     _load().oracle_ln_gate_bwd(T, D, _p(x), _p(u), _p(dy), _p(g), _p(b), float(eps), _p(dx),
                                _p(du), _p(dg), _p(db))
     return dx, du, dg, db
+
+
+def mfalcon_fwd(seq_offsets, num_targets, b_m, max_seq_len, timestamps, rab_pos, rab_time,
+                q, k, v):
+    """Algorithm 1 (M-FALCON) for one attention layer.  Sequence b of the
+    merged batch holds its n_b prefix tokens followed by its m_b candidates
+    (m_b = num_targets[b]).  The candidates are taken b_m at a time: pass i
+    runs the target-aware attention (candidates see the prefix and
+    themselves, never each other) over prefix ++ candidates
+    [i b_m, min((i+1) b_m, m_b)) of every sequence, and keeps the outputs of
+    those candidates.  Returns O of the candidate rows, in the order of the
+    merged batch ([sum m_b, h, d_v]); the prefix rows are not outputs."""
+    offs, nt, ts = _i64(seq_offsets), _i64(num_targets), _i64(timestamps)
+    q, k, v = _f64(q), _f64(k), _f64(v)
+    B = len(offs) - 1
+    if b_m < 1:
+        raise ValueError("b_m must be >= 1")
+    lens = np.diff(offs)
+    nh = lens - nt
+    cand_start = np.concatenate([[0], np.cumsum(nt)])
+    out = np.full((int(cand_start[-1]), q.shape[1], v.shape[2]), np.nan)
+    passes = (int(nt.max()) + b_m - 1) // b_m if B and nt.max() > 0 else 0
+    for i in range(passes):
+        rows, keep, counts = [], [], []
+        for b in range(B):
+            c0, c1 = min(i * b_m, int(nt[b])), min((i + 1) * b_m, int(nt[b]))
+            rows.append(np.arange(offs[b], offs[b] + nh[b]))
+            rows.append(np.arange(offs[b] + nh[b] + c0, offs[b] + nh[b] + c1))
+            keep.append(cand_start[b] + np.arange(c0, c1))
+            counts.append(c1 - c0)
+        counts = np.asarray(counts, dtype=np.int64)
+        sub_offs = np.concatenate([[0], np.cumsum(nh + counts)])
+        r = np.concatenate(rows)
+        o = attn_fwd(sub_offs, max_seq_len, ts[r], rab_pos, rab_time, q[r], k[r], v[r],
+                     num_targets=counts)
+        # Candidate rows of the pass, in sequence order.
+        sel = np.concatenate([np.arange(sub_offs[b] + nh[b], sub_offs[b + 1]) for b in range(B)])
+        out[np.concatenate(keep)] = o[sel]
+    return out

@@ -184,6 +184,8 @@ JaggedArgs make_args(const hstu_problem_t* p, const hstu_jagged_t* j) {
   a.rab_pos = j->rab_pos;
   a.rab_time = j->rab_time;
   a.seq_trange = nullptr;
+  a.key_offsets = nullptr;
+  a.key_timestamps = nullptr;
   a.num_seqs = p->num_seqs;
   a.max_seq_len = p->max_seq_len;
   a.num_heads = p->num_heads;
@@ -230,8 +232,8 @@ hstu_status_t attn_fwd_impl(const hstu_problem_t* p, const hstu_jagged_t* j, con
   HSTU_HIP(launch_seq_time_range(ja, (int64_t*)(w + l.trange), s), "time range launch");
   HSTU_HIP(launch_schedule(ja, 0, items, counts, s), "schedule launch");
   TimedScope ts("attn_fwd", s);
-  HSTU_HIP(launch_attn_fwd_bf16(ja, t, p->d_qk, p->d_v, out, out_f32, items, counts, l.max_fwd,
-                                s),
+  HSTU_HIP(launch_attn_fwd_bf16(ja, t, p->d_qk, p->d_v, out, out_f32, out_f32, items, counts,
+                                l.max_fwd, s),
            "attn_fwd launch");
   return ok();
 }
@@ -260,6 +262,61 @@ hstu_status_t hstu_attn_fwd(const hstu_problem_t* p, const hstu_jagged_t* j, con
   try {
     Tensors t{q, q_stride, k, k_stride, v, v_stride};
     return attn_fwd_impl(p, j, t, out, 0, ws, ws_bytes, (hipStream_t)hip_stream);
+  } catch (...) {
+    return fail(HSTU_ERR_INVALID_ARGUMENT, "internal error");
+  }
+}
+
+hstu_status_t hstu_attn_fwd_cached(const hstu_problem_t* p, const hstu_jagged_t* j, const void* q,
+                                   int64_t q_stride, const void* k, int64_t k_stride,
+                                   const void* v, int64_t v_stride, const int64_t* cache_offsets,
+                                   const int64_t* cache_timestamps, int64_t cache_tokens,
+                                   const void* k_cache, int64_t kc_stride, const void* v_cache,
+                                   int64_t vc_stride, void* out, void* ws, size_t ws_bytes,
+                                   void* hip_stream) {
+  try {
+    hipStream_t s = (hipStream_t)hip_stream;
+    HSTU_TRY(check_problem(p));
+    HSTU_TRY(check_jagged(j));
+    if (p->dtype != HSTU_BF16)
+      return fail(HSTU_ERR_UNSUPPORTED, "hstu_attn_fwd_cached supports bf16 problems only");
+    const int H = p->num_heads;
+    HSTU_TRY(check_rows(p, "q", q, q_stride, (int64_t)H * p->d_qk));
+    HSTU_TRY(check_rows(p, "k", k, k_stride, (int64_t)H * p->d_qk));
+    HSTU_TRY(check_rows(p, "v", v, v_stride, (int64_t)H * p->d_v));
+    HSTU_TRY(check_dense("out", out, 16));
+    if (!cache_offsets) return fail(HSTU_ERR_INVALID_ARGUMENT, "cache_offsets is NULL");
+    if (cache_tokens < 0) return fail(HSTU_ERR_INVALID_ARGUMENT, "cache_tokens must be >= 0");
+    if (cache_tokens > 0) {
+      if (!cache_timestamps) return fail(HSTU_ERR_INVALID_ARGUMENT, "cache_timestamps is NULL");
+      HSTU_TRY(check_rows(p, "k_cache", k_cache, kc_stride, (int64_t)H * p->d_qk));
+      HSTU_TRY(check_rows(p, "v_cache", v_cache, vc_stride, (int64_t)H * p->d_v));
+    }
+    Layout l;
+    HSTU_TRY(check_ws(p, ws, ws_bytes, &l));
+    const int64_t T = p->total_tokens;
+    if (T == 0) return ok();
+    JaggedArgs ja = make_args(p, j);
+    ja.num_targets = nullptr;
+    ja.key_offsets = cache_offsets;
+    ja.key_timestamps = cache_timestamps;
+    char* w = (char*)ws;
+    int32_t* counts = (int32_t*)(w + l.counts);
+    WorkItem* items = (WorkItem*)(w + l.fwd_items);
+    float* o32 = (float*)(w + l.dout);  // fp32 partial output (history keys only)
+    ja.seq_trange = (const int64_t*)(w + l.trange);
+    HSTU_HIP(launch_seq_time_range(ja, (int64_t*)(w + l.trange), s), "time range launch");
+    HSTU_HIP(launch_schedule(ja, 0, items, counts, s), "schedule launch");
+    TimedScope ts("attn_fwd_cached", s);
+    const Tensors keys{q, q_stride, k_cache, kc_stride, v_cache, vc_stride};
+    HSTU_HIP(launch_attn_fwd_bf16(ja, keys, p->d_qk, p->d_v, o32, 1, 0, items, counts, l.max_fwd,
+                                  s),
+             "attn_fwd_cached launch");
+    const Tensors cand{q, q_stride, k, k_stride, v, v_stride};
+    HSTU_HIP(launch_cached_self(1, T, H, p->d_qk, p->d_v, cand, j->rab_pos, j->rab_time,
+                                p->max_seq_len, o32, out, s),
+             "cached self-term launch");
+    return ok();
   } catch (...) {
     return fail(HSTU_ERR_INVALID_ARGUMENT, "internal error");
   }

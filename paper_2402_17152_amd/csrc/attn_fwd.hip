@@ -94,11 +94,14 @@ __device__ __forceinline__ float silu(float x) {
 // about 2^-17 relative error instead of bf16's 2^-9; used where O is
 // normalised afterwards (the layer's LayerNorm rescales every row to unit
 // spread and would magnify a bf16 P).
+// Row i of the item is global row orow + i, key j global key okey + j;
+// keys at or past key_lim do not exist (cross mode: the cached prefix has
+// n_h keys).
 template <int DQK, int DV, bool FAST, bool SPLIT>
 __device__ __forceinline__ void fwd_item(FwdShared<DQK, DV>& sm, const JaggedArgs& ja,
                                          const Tensors& t, void* __restrict__ out, int out_f32,
-                                         int64_t o, int L, int n_h, int i0, int head,
-                                         int64_t tbase) {
+                                         int64_t orow, int64_t okey, int L, int n_h, int key_lim,
+                                         int i0, int head, int64_t tbase) {
   using Sh = FwdShared<DQK, DV>;
   constexpr int BM = Sh::BM, BN = Sh::BN, K_LD = Sh::K_LD, V_LD = Sh::V_LD;
   constexpr int KCH = BN * DQK / 8, VCH = BN * DV / 8;
@@ -114,7 +117,8 @@ __device__ __forceinline__ void fwd_item(FwdShared<DQK, DV>& sm, const JaggedArg
   const bool row_ok = my_i < L;
   const int wave_last = min(iw0 + 31, L - 1);
   const int R = min(i0 + BM - 1, n_h);  // largest row position of the block
-  const int64_t* __restrict__ ts = ja.timestamps + o;
+  const int64_t* __restrict__ ts = ja.timestamps + orow;  // row timestamps
+  const int64_t* __restrict__ tsk = (ja.key_timestamps ? ja.key_timestamps : ja.timestamps) + okey;
   const uint16_t* __restrict__ qg = (const uint16_t*)t.q;
   const uint16_t* __restrict__ kg = (const uint16_t*)t.k;
   const uint16_t* __restrict__ vg = (const uint16_t*)t.v;
@@ -124,7 +128,7 @@ __device__ __forceinline__ void fwd_item(FwdShared<DQK, DV>& sm, const JaggedArg
   u32x4 qf[DQK / 16];
 #pragma unroll
   for (int s = 0; s < DQK / 16; s++)
-    qf[s] = row_ok ? *reinterpret_cast<const u32x4*>(qg + (o + my_i) * t.q_stride + head * DQK +
+    qf[s] = row_ok ? *reinterpret_cast<const u32x4*>(qg + (orow + my_i) * t.q_stride + head * DQK +
                                                      16 * s + 8 * half)
                    : zero_u32x4();
   const int64_t ti64 = row_ok ? ts[my_i] : tbase;
@@ -144,7 +148,7 @@ __device__ __forceinline__ void fwd_item(FwdShared<DQK, DV>& sm, const JaggedArg
   // Key tiles visited: [0, nA) then [bstart, kend).  Tiles made only of
   // candidates that precede every row of the block are fully masked and
   // skipped.
-  const int kend = (rows_end + BN - 1) / BN;
+  const int kend = (min(rows_end, key_lim) + BN - 1) / BN;
   const int nh_blk = (n_h + BN - 1) / BN;
   const int nA = min(nh_blk, kend);
   const int bstart = max(nh_blk, i0 / BN);
@@ -165,10 +169,10 @@ __device__ __forceinline__ void fwd_item(FwdShared<DQK, DV>& sm, const JaggedArg
   constexpr int KOPW = (KOPS + 3) / 4, VOPW = (VOPS + 3) / 4;
   constexpr int OPS_PER_STEP = KOPW + VOPW + 3 + 1;
   const __amdgpu_buffer_rsrc_t krs =
-      make_rsrc(kg + o * t.k_stride + head * DQK, (uint32_t)(L * t.k_stride * 2));
+      make_rsrc(kg + okey * t.k_stride + head * DQK, (uint32_t)(key_lim * t.k_stride * 2));
   const __amdgpu_buffer_rsrc_t vrs =
-      make_rsrc(vg + o * t.v_stride + head * DV, (uint32_t)(L * t.v_stride * 2));
-  const __amdgpu_buffer_rsrc_t trs = make_rsrc(ts, (uint32_t)L * 8u);
+      make_rsrc(vg + okey * t.v_stride + head * DV, (uint32_t)(key_lim * t.v_stride * 2));
+  const __amdgpu_buffer_rsrc_t trs = make_rsrc(tsk, (uint32_t)key_lim * 8u);
   const __amdgpu_buffer_rsrc_t prs = make_rsrc(ja.rab_pos, (uint32_t)(2 * N - 1) * 4u);
   const uint32_t kstride_b = (uint32_t)t.k_stride * 2u, vstride_b = (uint32_t)t.v_stride * 2u;
   // Lane offsets of this wave's K / V operations: chunk g = 64 op + lane
@@ -244,6 +248,13 @@ __device__ __forceinline__ void fwd_item(FwdShared<DQK, DV>& sm, const JaggedArg
   // time term is a select on t_j <= t_i - 2^(b+1) ("two").  Everything
   // else evaluates each pair ("general").
   enum { kUniform = 0, kTwo = 1, kGeneral = 2 };
+  // Full tile: every pair valid, either history rows after every key
+  // (j0 + BN - 1 <= iw0), or candidate rows (all at position n_h) against
+  // history keys (j0 + BN - 1 < n_h); a wave mixing both has none.  Either
+  // way the tiles with j0 <= full_lim (wave-uniform).
+  const int full_lim = __builtin_amdgcn_readfirstlane(
+      iw0 + 31 >= L ? -1 : iw0 + 31 < n_h ? iw0 - (BN - 1) : iw0 >= n_h ? n_h - BN : -1);
+  auto full_tile = [&](int j0) { return j0 <= full_lim; };
   struct Path {
     int kind;
     float cb, cb_far;  // time term (nearer bucket) and, for "two", the farther one
@@ -256,7 +267,7 @@ __device__ __forceinline__ void fwd_item(FwdShared<DQK, DV>& sm, const JaggedArg
       return r;
     }
     const int j0 = kb_of(u) * BN;
-    const bool full = (j0 + BN - 1 <= iw0) && (iw0 + 31 < L) && (iw0 + 31 < n_h);
+    const bool full = full_tile(j0);
     if constexpr (FAST) {
       if (full) {
         const uint32_t klo = __builtin_amdgcn_readfirstlane(sm.sKr32[u & 3][0]);
@@ -290,7 +301,7 @@ __device__ __forceinline__ void fwd_item(FwdShared<DQK, DV>& sm, const JaggedArg
   };
 
   // ---- bias seed of tile u for this wave ----
-  const int a_win = R - my_i + 4 * half;  // window index of (i, j0 + 4*half) in a full tile
+  const int a_win = R - pi + 4 * half;  // window index of (i, j0 + 4*half) in a full tile
   auto seed_uniform = [&](int u, float cb, f32x16& acc) {
     // window index of (i, j) = (j - j0) + (R - i); the lane reads
     // a + 8g + m, a = R - i + 4*half, from the copy that makes it aligned.
@@ -368,7 +379,7 @@ __device__ __forceinline__ void fwd_item(FwdShared<DQK, DV>& sm, const JaggedArg
   auto seed_general = [&](int u, f32x16& acc) {
     const int ks = u % 3;
     const int j0 = kb_of(u) * BN;
-    const bool full = (j0 + BN - 1 <= iw0) && (iw0 + 31 < L) && (iw0 + 31 < n_h);
+    const bool full = full_tile(j0);
     if (!full && (iw0 >= L || j0 > wave_last || (j0 >= n_h && j0 + BN - 1 < iw0))) {
 #pragma unroll
       for (int q = 0; q < 16; q++) acc[q] = kMaskedBias;
@@ -396,7 +407,7 @@ __device__ __forceinline__ void fwd_item(FwdShared<DQK, DV>& sm, const JaggedArg
 #pragma unroll
       for (int q = 0; q < 16; q++) {
         const int j = j0 + 8 * (q >> 2) + 4 * half + (q & 3);
-        ok[q] = row_ok && j < L && pair_valid(my_i, j, n_h);
+        ok[q] = row_ok && j < key_lim && pair_valid(my_i, j, n_h);
         x[q] = ok[q] ? bias_pos(j, n_h) - pb + R - pi : 0;
       }
 #pragma unroll
@@ -525,7 +536,7 @@ __device__ __forceinline__ void fwd_item(FwdShared<DQK, DV>& sm, const JaggedArg
   // stored as bf16, or as fp32 for a consumer that normalises it.
   const float invN = 1.0f / (float)N;
   if (out_f32) {
-    float* __restrict__ og = (float*)out + (o * H + head) * DV;
+    float* __restrict__ og = (float*)out + (orow * H + head) * DV;
 #pragma unroll
     for (int nb = 0; nb < DV / 32; nb++)
 #pragma unroll
@@ -534,7 +545,7 @@ __device__ __forceinline__ void fwd_item(FwdShared<DQK, DV>& sm, const JaggedArg
         if (i < L) og[(int64_t)i * H * DV + 32 * nb + col] = oacc[nb][q] * invN;
       }
   } else {
-    uint16_t* __restrict__ og = (uint16_t*)out + (o * H + head) * DV;
+    uint16_t* __restrict__ og = (uint16_t*)out + (orow * H + head) * DV;
 #pragma unroll
     for (int nb = 0; nb < DV / 32; nb++)
 #pragma unroll
@@ -557,9 +568,22 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_bf16_kernel(JaggedArgs ja, Te
   const int head = blockIdx.y;
   const int NB = ja.num_buckets;
   const int64_t o = ja.seq_offsets[it.seq];
-  const int L = (int)(ja.seq_offsets[it.seq + 1] - o);
-  const int n_h = L - (ja.num_targets ? (int)ja.num_targets[it.seq] : 0);
-  const int i0 = it.blk * Sh::BM;
+  const int Lr = (int)(ja.seq_offsets[it.seq + 1] - o);
+  // Self-attention: rows and keys are the sequence's L tokens.  Cross mode:
+  // the rows are its candidates, virtual positions n_h .. n_h + Lr - 1
+  // after the n_h keys of its cached prefix.
+  int64_t orow = o, okey = o;
+  int L = Lr, n_h = Lr - (ja.num_targets ? (int)ja.num_targets[it.seq] : 0), key_lim = Lr, i0;
+  if (ja.key_offsets) {
+    okey = ja.key_offsets[it.seq];
+    n_h = (int)(ja.key_offsets[it.seq + 1] - okey);
+    L = n_h + Lr;
+    orow = o - n_h;
+    key_lim = n_h;
+    i0 = n_h + it.blk * Sh::BM;
+  } else {
+    i0 = it.blk * Sh::BM;
+  }
   const int tid = threadIdx.x;
 
   // The 32-bit fast path applies when the sequence's timestamps span less
@@ -572,19 +596,20 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_bf16_kernel(JaggedArgs ja, Te
     sm.sTab[x] = (fast && x == 31) ? ja.rab_time[0] : ja.rab_time[min(63 - x, NB - 1)];
   __syncthreads();
   if (fast) {
-    fwd_item<DQK, DV, true, SPLIT>(sm, ja, t, out, out_f32, o, L, n_h, i0, head, tlo);
+    fwd_item<DQK, DV, true, SPLIT>(sm, ja, t, out, out_f32, orow, okey, L, n_h, key_lim, i0, head,
+                                   tlo);
   } else {
-    fwd_item<DQK, DV, false, SPLIT>(sm, ja, t, out, out_f32, o, L, n_h, i0, head, tlo);
+    fwd_item<DQK, DV, false, SPLIT>(sm, ja, t, out, out_f32, orow, okey, L, n_h, key_lim, i0, head,
+                                    tlo);
   }
 }
 
 template <int DQK, int DV>
-hipError_t launch_fwd(const JaggedArgs& ja, const Tensors& t, void* out, int out_f32,
+hipError_t launch_fwd(const JaggedArgs& ja, const Tensors& t, void* out, int out_f32, int split,
                       const WorkItem* items, const int32_t* count, int64_t max_items,
                       hipStream_t s) {
   dim3 grid((unsigned)max_items, (unsigned)ja.num_heads);
-  // The layer's fp32 output goes to a LayerNorm: split P there.
-  if (out_f32)
+  if (split)
     hipLaunchKernelGGL((attn_fwd_bf16_kernel<DQK, DV, true>), grid, dim3(256), 0, s, ja, t, out,
                        out_f32, items, count);
   else
@@ -593,14 +618,62 @@ hipError_t launch_fwd(const JaggedArgs& ja, const Tensors& t, void* out, int out
   return hipGetLastError();
 }
 
+// Self term of the cached candidate pass: the cross-mode kernel leaves out
+// each candidate's own key (position n_h, dt = 0, so rab = rab_pos[N-1] +
+// rab_time[0]); one wave per (row, head) adds SiLU(q.k + rab) v / N to
+// the fp32 partial output and stores the result once.
+template <bool BF16>
+__global__ __launch_bounds__(256) void cached_self_kernel(int64_t T, int H, int dqk, int dv,
+                                                          Tensors t, const float* rab_pos,
+                                                          const float* rab_time, int N,
+                                                          const float* __restrict__ o32,
+                                                          void* __restrict__ out) {
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int64_t w = (int64_t)blockIdx.x * 4 + wave;
+  if (w >= T * H) return;
+  const int64_t row = w / H;
+  const int h = (int)(w - row * H);
+  auto ld = [&](const void* base, int64_t stride, int dim, int c) -> float {
+    const int64_t idx = row * stride + (int64_t)h * dim + c;
+    return BF16 ? bf16_bits_to_f32(((const uint16_t*)base)[idx]) : ((const float*)base)[idx];
+  };
+  float part = 0.0f;
+  for (int c = lane; c < dqk; c += 64) part += ld(t.q, t.q_stride, dqk, c) * ld(t.k, t.k_stride, dqk, c);
+  const float x = wave_sum_f32(part) + rab_pos[N - 1] + rab_time[0];
+  const float pN = silu(x) / (float)N;
+  for (int c = lane; c < dv; c += 64) {
+    const int64_t oi = (row * H + h) * dv + c;
+    const float y = o32[oi] + pN * ld(t.v, t.v_stride, dv, c);
+    if constexpr (BF16)
+      ((uint16_t*)out)[oi] = f32_to_bf16_bits(y);
+    else
+      ((float*)out)[oi] = y;
+  }
+}
+
 }  // namespace
 
+hipError_t launch_cached_self(int is_bf16, int64_t T, int32_t H, int32_t dqk, int32_t dv,
+                              const Tensors& t, const float* rab_pos, const float* rab_time,
+                              int32_t N, const float* o32, void* out, hipStream_t s) {
+  const int64_t waves = T * H;
+  if (waves <= 0) return hipSuccess;
+  const dim3 grid((unsigned)((waves + 3) / 4));
+  if (is_bf16)
+    hipLaunchKernelGGL(cached_self_kernel<true>, grid, dim3(256), 0, s, T, H, dqk, dv, t, rab_pos,
+                       rab_time, N, o32, out);
+  else
+    hipLaunchKernelGGL(cached_self_kernel<false>, grid, dim3(256), 0, s, T, H, dqk, dv, t, rab_pos,
+                       rab_time, N, o32, out);
+  return hipGetLastError();
+}
+
 hipError_t launch_attn_fwd_bf16(const JaggedArgs& ja, const Tensors& t, int dqk, int dv, void* out,
-                                int out_f32, const WorkItem* items, const int32_t* count,
-                                int64_t max_items, hipStream_t s) {
+                                int out_f32, int split, const WorkItem* items,
+                                const int32_t* count, int64_t max_items, hipStream_t s) {
 #define HSTU_FWD_CASE(A, B) \
   if (dqk == A && dv == B)  \
-    return launch_fwd<A, B>(ja, t, out, out_f32, items, count, max_items, s);
+    return launch_fwd<A, B>(ja, t, out, out_f32, split, items, count, max_items, s);
   HSTU_FWD_CASE(32, 32)
   HSTU_FWD_CASE(32, 64)
   HSTU_FWD_CASE(32, 128)

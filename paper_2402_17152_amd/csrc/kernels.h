@@ -19,6 +19,12 @@ struct JaggedArgs {
   // [2B] per-sequence timestamp min / max (workspace, filled by
   // launch_seq_time_range before the attention kernels run).
   const int64_t* seq_trange;
+  // Cross mode (the cached candidate pass of M-FALCON): the rows of
+  // sequence b are its candidates, all at position n_h, and the keys its
+  // cached prefix, a jagged batch of its own (key_offsets [B+1],
+  // key_timestamps); null for self-attention over seq_offsets.
+  const int64_t* key_offsets;
+  const int64_t* key_timestamps;
   int32_t num_seqs;
   int32_t max_seq_len;  // N
   int32_t num_heads;
@@ -49,8 +55,9 @@ inline int64_t max_work_items(int64_t T, int32_t B, int blk) {
 }
 
 // Scheduler: builds the work list (longest first) into `items` and
-// its length into `count`.  mode 0: forward (seq, q-block of kFwdBM rows);
-// mode 1: backward (seq, k-block of kBwdBN keys).
+// its length into `count`.  mode 0: forward (seq, q-block of kFwdBM rows;
+// in cross mode the candidate rows in blocks of kFwdBM); mode 1: backward
+// (seq, k-block of kBwdBN keys).
 hipError_t launch_schedule(const JaggedArgs& ja, int mode, WorkItem* items, int32_t* count,
                            hipStream_t s);
 
@@ -66,10 +73,17 @@ hipError_t launch_bucketize(int32_t num_seqs, int64_t total_tokens, int32_t num_
                             hipStream_t s);
 
 // bf16 MFMA attention.  The forward stores O as bf16, or as fp32 when
-// out_f32 (the layer keeps it in fp32 for the layer norm).
+// out_f32; with split, P enters P V as two bf16 terms (the layer path).
+// In cross mode (ja.key_offsets) the rows are candidates and the keys the
+// cached prefix, without the candidates' own keys.
 hipError_t launch_attn_fwd_bf16(const JaggedArgs& ja, const Tensors& t, int dqk, int dv, void* out,
-                                int out_f32, const WorkItem* items, const int32_t* count,
-                                int64_t max_items, hipStream_t s);
+                                int out_f32, int split, const WorkItem* items,
+                                const int32_t* count, int64_t max_items, hipStream_t s);
+// The self term of the cached candidate pass: out = o32 + SiLU(q.k +
+// rab_pos[N-1] + rab_time[0]) v / N per (row, head), in bf16 or fp32.
+hipError_t launch_cached_self(int is_bf16, int64_t T, int32_t H, int32_t dqk, int32_t dv,
+                              const Tensors& t, const float* rab_pos, const float* rab_time,
+                              int32_t N, const float* o32, void* out, hipStream_t s);
 // d_out_lo: null, or the low bf16 terms of dO (d_out holding the high
 // ones), for a dO that is the fp32 output of the layer's LayerNorm backward.
 hipError_t launch_attn_bwd_bf16(const JaggedArgs& ja, const Tensors& t, int dqk, int dv,

@@ -28,6 +28,10 @@ __device__ __forceinline__ int fwd_weight(int L, int n_h, int qb) {
   return kend - skipped;
 }
 
+// Cross-mode forward item: every candidate block visits the n_h keys of
+// its cached prefix.
+__device__ __forceinline__ int cross_weight(int n_h) { return ceil_div(n_h, kFwdBN); }
+
 // Backward item (k-block kb): number of query steps of kBwdBM rows.
 __device__ __forceinline__ int bwd_weight(int L, int n_h, int kb) {
   int j0 = kb * kBwdBN;
@@ -43,6 +47,7 @@ __global__ __launch_bounds__(kSchedThreads) void schedule_kernel(JaggedArgs ja, 
   const int tid = threadIdx.x;
   const int blk = mode == 0 ? kFwdBM : kBwdBN;
   const int maxw = mode == 0 ? ceil_div(ja.max_seq_len, kFwdBN) : ceil_div(ja.max_seq_len, kBwdBM);
+  // (cross mode: a candidate block's weight ceil(n_h / kFwdBN) <= maxw since n_h < N)
   const int nbins = maxw + 1;
   for (int i = tid; i < nbins; i += kSchedThreads) s_bins[i] = 0;
   __syncthreads();
@@ -52,9 +57,11 @@ __global__ __launch_bounds__(kSchedThreads) void schedule_kernel(JaggedArgs ja, 
   for (int b = tid; b < ja.num_seqs; b += kSchedThreads) {
     int L = (int)(ja.seq_offsets[b + 1] - ja.seq_offsets[b]);
     int n_h = L - (ja.num_targets ? (int)ja.num_targets[b] : 0);
+    const bool cross = mode == 0 && ja.key_offsets;
+    if (cross) n_h = (int)(ja.key_offsets[b + 1] - ja.key_offsets[b]);
     int nblk = ceil_div(L, blk);
     for (int x = 0; x < nblk; x++) {
-      int w = mode == 0 ? fwd_weight(L, n_h, x) : bwd_weight(L, n_h, x);
+      int w = cross ? cross_weight(n_h) : mode == 0 ? fwd_weight(L, n_h, x) : bwd_weight(L, n_h, x);
       w = min(max(w, 0), maxw);
       atomicAdd(&s_bins[maxw - w], 1);
     }
@@ -87,9 +94,11 @@ __global__ __launch_bounds__(kSchedThreads) void schedule_kernel(JaggedArgs ja, 
   for (int b = tid; b < ja.num_seqs; b += kSchedThreads) {
     int L = (int)(ja.seq_offsets[b + 1] - ja.seq_offsets[b]);
     int n_h = L - (ja.num_targets ? (int)ja.num_targets[b] : 0);
+    const bool cross = mode == 0 && ja.key_offsets;
+    if (cross) n_h = (int)(ja.key_offsets[b + 1] - ja.key_offsets[b]);
     int nblk = ceil_div(L, blk);
     for (int x = 0; x < nblk; x++) {
-      int w = mode == 0 ? fwd_weight(L, n_h, x) : bwd_weight(L, n_h, x);
+      int w = cross ? cross_weight(n_h) : mode == 0 ? fwd_weight(L, n_h, x) : bwd_weight(L, n_h, x);
       w = min(max(w, 0), maxw);
       int pos = atomicAdd(&s_bins[maxw - w], 1);
       WorkItem it;
@@ -183,6 +192,18 @@ __global__ __launch_bounds__(kRangeThreads) void seq_time_range_kernel(JaggedArg
       hi = v[k] > hi ? v[k] : hi;
     }
   }
+  // Cross mode: the cached prefix's timestamps count too.
+  int Lk = 0;
+  if (ja.key_offsets) {
+    const int64_t ok = ja.key_offsets[b];
+    Lk = (int)(ja.key_offsets[b + 1] - ok);
+    const int64_t* tk = ja.key_timestamps + ok;
+    for (int x = tid; x < Lk; x += kRangeThreads) {
+      const int64_t v = tk[x];
+      lo = v < lo ? v : lo;
+      hi = v > hi ? v : hi;
+    }
+  }
 #pragma unroll
   for (int off = 32; off > 0; off >>= 1) {
     const int64_t a = __shfl_xor(lo, off, 64), c = __shfl_xor(hi, off, 64);
@@ -199,8 +220,8 @@ __global__ __launch_bounds__(kRangeThreads) void seq_time_range_kernel(JaggedArg
       lo = red[0][w] < lo ? red[0][w] : lo;
       hi = red[1][w] > hi ? red[1][w] : hi;
     }
-    out[2 * b] = L > 0 ? lo : 0;
-    out[2 * b + 1] = L > 0 ? hi : 0;
+    out[2 * b] = L + Lk > 0 ? lo : 0;
+    out[2 * b + 1] = L + Lk > 0 ? hi : 0;
   }
 }
 

@@ -24,7 +24,8 @@ STATUS = {0: "HSTU_OK", 1: "HSTU_ERR_INVALID_ARGUMENT", 2: "HSTU_ERR_UNSUPPORTED
 EXPORTED = ("hstu_workspace_bytes", "hstu_attn_fwd", "hstu_attn_bwd", "hstu_layer_fwd",
             "hstu_time_bucketize", "hstu_complete_cumsum", "hstu_pair_offsets", "hstu_validate",
             "hstu_last_error", "hstu_abi_version", "hstu_timing_enable", "hstu_timing_read",
-            "hstu_timing_reset", "hstu_probe_mfma_bf16", "hstu_layer_bwd")
+            "hstu_timing_reset", "hstu_probe_mfma_bf16", "hstu_layer_bwd",
+            "hstu_attn_fwd_cached")
 
 
 class Problem(ctypes.Structure):
@@ -61,6 +62,8 @@ def _load():
                                  P, sz, P]),
         "hstu_layer_bwd": (i32, [PP, PJ, P, i64, P, i64, P, i64, P, i64, P, P, P, P, P, P,
                                  P, P, P, P, P, P, P, P, P, sz, P]),
+        "hstu_attn_fwd_cached": (i32, [PP, PJ, P, i64, P, i64, P, i64, P, P, i64, P, i64, P, i64,
+                                       P, P, sz, P]),
         "hstu_time_bucketize": (i32, [i32, i64, i32, P, P, P, i64, P, P]),
         "hstu_complete_cumsum": (i32, [i32, P, P, P]),
         "hstu_pair_offsets": (i32, [i32, P, P, P]),
@@ -172,6 +175,27 @@ def hstu_attn_fwd(q, k, v, seq_offsets, timestamps, rab_pos, rab_time, max_seq_l
     _check(lib.hstu_attn_fwd(ctypes.byref(p), ctypes.byref(j), _ptr(q), _row_stride(q), _ptr(k),
                              _row_stride(k), _ptr(v), _row_stride(v), _ptr(out), _ptr(ws),
                              ws.numel(), _stream(stream)))
+    return out
+
+
+def hstu_attn_fwd_cached(q, k, v, seq_offsets, timestamps, k_cache, v_cache, cache_offsets,
+                         cache_timestamps, rab_pos, rab_time, max_seq_len, out=None, ws=None,
+                         stream=None):
+    """O [T, h, d_v] of the candidate rows q, k, v (offsets seq_offsets) against
+    the cached history keys and values k_cache, v_cache (offsets
+    cache_offsets); see include/hstu.h."""
+    p = problem_for(q, v, seq_offsets, max_seq_len, rab_time)
+    j = make_jagged(seq_offsets, timestamps, rab_pos, rab_time, None)
+    if out is None:
+        out = torch.empty((q.shape[0], q.shape[1], v.shape[2]), dtype=q.dtype, device=q.device)
+    if ws is None:
+        ws = workspace(p, q.device)
+    _check(lib.hstu_attn_fwd_cached(ctypes.byref(p), ctypes.byref(j), _ptr(q), _row_stride(q),
+                                    _ptr(k), _row_stride(k), _ptr(v), _row_stride(v),
+                                    _ptr(cache_offsets), _ptr(cache_timestamps),
+                                    int(k_cache.shape[0]), _ptr(k_cache), _row_stride(k_cache),
+                                    _ptr(v_cache), _row_stride(v_cache), _ptr(out), _ptr(ws),
+                                    ws.numel(), _stream(stream)))
     return out
 
 

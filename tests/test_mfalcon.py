@@ -1,0 +1,172 @@
+"""GPU parity of the M-FALCON cached candidate pass (Algorithm 1 and the
+appendix on M-FALCON).
+
+Algorithm 1 for one attention layer: the first microbatch runs the
+target-aware attention over prefix ++ candidates (hstu_attn_fwd with
+num_targets), which also yields the prefix's keys and values for the
+cache; every later microbatch runs hstu_attn_fwd_cached against the
+cached prefix K and V.  Checks:
+
+* against the oracle's own Algorithm 1 (same b_m), tau = 2e-2 RMS (bf16);
+* a candidate's cached output does not depend on the other candidates of
+  its call: every partition of the candidates gives the same bits;
+* the cached pass agrees with the uncached target-aware forward over
+  prefix ++ all m candidates (the target workload: 16 users, 2048 prefix
+  tokens, 1024 candidates, h = 4, d = 128, N = 3072) for every b_m tried,
+  at the same tolerance, and with the oracle on sampled users."""
+import numpy as np
+import pytest
+import torch
+
+from paper_2402_17152_amd import inputs
+from tests import gpu_util as gu
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def hs():
+    assert torch.cuda.is_available(), "GPU tests need a GPU"
+    from paper_2402_17152_amd import hstu
+    return hstu
+
+
+def _idx(rows):
+    return torch.from_numpy(np.asarray(rows, dtype=np.int64)).cuda()
+
+
+def _cat(parts):
+    return np.concatenate(parts) if parts else np.zeros(0, np.int64)
+
+
+def mfalcon_gpu(hs, batch, d, b_m, first_uncached=True):
+    """Candidate outputs [sum m_b, h, d_v] (merged-batch order), microbatch
+    by microbatch.  The cache holds the prefix rows of k and v, gathered
+    once into a jagged batch of their own."""
+    offs = batch.seq_offsets
+    nt = batch.num_targets
+    B = len(nt)
+    nh = np.diff(offs) - nt
+    N = batch.spec.max_seq_len
+    cstart = np.concatenate([[0], np.cumsum(nt)])
+    prefix = _cat([np.arange(offs[b], offs[b] + nh[b]) for b in range(B)])
+    pi = _idx(prefix)
+    k_cache, v_cache = d["k"].index_select(0, pi), d["v"].index_select(0, pi)
+    cache_offsets = _idx(np.concatenate([[0], np.cumsum(nh)]))
+    cache_ts = d["timestamps"].index_select(0, pi)
+    out = torch.full((int(cstart[-1]), d["v"].shape[1], d["v"].shape[2]), float("nan"),
+                     dtype=d["v"].dtype, device="cuda")
+    passes = (int(nt.max()) + b_m - 1) // b_m if nt.max() > 0 else 0
+    for i in range(passes):
+        c0 = np.minimum(i * b_m, nt)
+        c1 = np.minimum((i + 1) * b_m, nt)
+        cnt = (c1 - c0).astype(np.int64)
+        cand = _cat([np.arange(offs[b] + nh[b] + c0[b], offs[b] + nh[b] + c1[b])
+                     for b in range(B)])
+        keep = _idx(_cat([cstart[b] + np.arange(c0[b], c1[b]) for b in range(B)]))
+        if i == 0 and first_uncached:
+            rows = _cat([np.r_[np.arange(offs[b], offs[b] + nh[b]),
+                               np.arange(offs[b] + nh[b] + c0[b], offs[b] + nh[b] + c1[b])]
+                         for b in range(B)])
+            sub_offs = np.concatenate([[0], np.cumsum(nh + cnt)])
+            r = _idx(rows)
+            o = hs.hstu_attn_fwd(d["q"].index_select(0, r), d["k"].index_select(0, r),
+                                 d["v"].index_select(0, r), _idx(sub_offs),
+                                 d["timestamps"].index_select(0, r), d["rab_pos"],
+                                 d["rab_time"], N, num_targets=_idx(cnt))
+            sel = _idx(_cat([np.arange(sub_offs[b] + nh[b], sub_offs[b + 1])
+                             for b in range(B)]))
+            out[keep] = o.index_select(0, sel)
+        else:
+            c = _idx(cand)
+            o = hs.hstu_attn_fwd_cached(d["q"].index_select(0, c), d["k"].index_select(0, c),
+                                        d["v"].index_select(0, c),
+                                        _idx(np.concatenate([[0], np.cumsum(cnt)])),
+                                        d["timestamps"].index_select(0, c), k_cache, v_cache,
+                                        cache_offsets, cache_ts, d["rab_pos"], d["rab_time"], N)
+            out[keep] = o
+    torch.cuda.synchronize()
+    return out
+
+
+def _cand_rows(batch):
+    offs, nt = batch.seq_offsets, batch.num_targets
+    return _cat([np.arange(offs[b + 1] - nt[b], offs[b + 1]) for b in range(len(nt))])
+
+
+SMALL = [
+    # (prefix lengths, candidate counts, h, d_qk, d_v, N)
+    ((0, 1, 45, 200, 97), (12, 0, 130, 37, 24), 2, 64, 64, 256),
+    ((300, 31, 64), (9, 140, 33), 2, 128, 128, 448),
+    ((129, 7), (5, 70), 1, 32, 128, 200),
+]
+
+
+@pytest.mark.parametrize("case", range(len(SMALL)))
+def test_mfalcon_small(hs, oracle_mod, case):
+    nh, nt, h, dqk, dv, N = SMALL[case]
+    nh, nt = np.array(nh), np.array(nt)
+    batch = inputs.make_batch("target", seed=100 + case, lengths=nh + nt, num_targets=nt,
+                              num_heads=h, d_qk=dqk, d_v=dv, max_seq_len=N)
+    d = gu.dev_inputs(batch)
+    f64 = [batch.f64(x) for x in ("q", "k", "v")]
+    full = gu.to_f64(gu.gpu_fwd(hs, d, batch))[_cand_rows(batch)]
+    ref_full = gu.oracle_fwd(oracle_mod, batch)[_cand_rows(batch)]
+    gu.assert_close("uncached", full, ref_full, 2e-2, "bf16")
+    cached = {}
+    for b_m in (1, 5, 12, 37, int(nt.max())):
+        ref = oracle_mod.mfalcon_fwd(batch.seq_offsets, nt, b_m, N, batch.timestamps,
+                                     batch.rab_pos, batch.rab_time, *f64)
+        got = gu.to_f64(mfalcon_gpu(hs, batch, d, b_m))
+        e = gu.assert_close(f"algorithm 1, b_m={b_m}", got, ref, 2e-2, "bf16")
+        print(f"\n  b_m={b_m}: err {e[0]:.3e} raw {e[1]:.3e}")
+        cached[b_m] = mfalcon_gpu(hs, batch, d, b_m, first_uncached=False)
+    base = cached[1]
+    for b_m, o in cached.items():
+        assert torch.equal(o.view(torch.int16), base.view(torch.int16)), \
+            f"cached outputs depend on the partition (b_m={b_m})"
+    gu.assert_close("cached vs oracle", gu.to_f64(base), ref_full, 2e-2, "bf16")
+    gu.assert_close("cached vs uncached", gu.to_f64(base), full, 2e-2, "bf16")
+
+
+def test_mfalcon_cached_rejects_fp32(hs):
+    batch = inputs.make_batch("target", seed=7, lengths=[10], num_targets=[4], num_heads=1,
+                              d_qk=32, d_v=32, max_seq_len=16, dtype="f32")
+    d = gu.dev_inputs(batch)
+    with pytest.raises(RuntimeError, match="bf16"):
+        hs.hstu_attn_fwd_cached(d["q"][6:], d["k"][6:], d["v"][6:], _idx([0, 4]),
+                                d["timestamps"][6:], d["k"][:6], d["v"][:6], _idx([0, 6]),
+                                d["timestamps"][:6], d["rab_pos"], d["rab_time"], 16)
+
+
+def test_mfalcon_target_workload(hs, oracle_mod):
+    """Full target workload: every b_m in (1024, 256, 16, 1) gives the same
+    cached outputs bit for bit; Algorithm 1 with b_m = 256 and the cached
+    pass both agree with the uncached target-aware forward on every
+    candidate, and with the oracle on users 0 and 11."""
+    batch = inputs.make_batch("target")
+    d = gu.dev_inputs(batch)
+    rows = _cand_rows(batch)
+    full = gu.to_f64(gu.gpu_fwd(hs, d, batch))[rows]
+    base = None
+    for b_m in (1024, 256, 16, 1):
+        o = mfalcon_gpu(hs, batch, d, b_m, first_uncached=False)
+        if base is None:
+            base = o
+        else:
+            assert torch.equal(o.view(torch.int16), base.view(torch.int16)), f"b_m={b_m}"
+    cached = gu.to_f64(base)
+    e = gu.assert_close("cached vs uncached", cached, full, 2e-2, "bf16")
+    print(f"\n  cached vs uncached: {e[0]:.3e} raw {e[1]:.3e}")
+    alg1 = gu.to_f64(mfalcon_gpu(hs, batch, d, 256))
+    gu.assert_close("algorithm 1 vs uncached", alg1, full, 2e-2, "bf16")
+    nt = batch.num_targets
+    cstart = np.concatenate([[0], np.cumsum(nt)])
+    for b in (0, 11):
+        sub = gu.sub_batch(batch, [b])
+        ref = gu.oracle_fwd(oracle_mod, sub)[-nt[b]:]
+        got = cached[cstart[b]:cstart[b + 1]]
+        e = gu.assert_close(f"user {b} vs oracle", got, ref, 2e-2, "bf16")
+        print(f"  user {b}: err {e[0]:.3e} raw {e[1]:.3e}")
+        gu.assert_close(f"user {b} algorithm 1", alg1[cstart[b]:cstart[b + 1]], ref, 2e-2,
+                        "bf16")

@@ -251,6 +251,35 @@ def test_mfalcon_equivalence(oracle_mod):
         np.testing.assert_array_equal(O[:nh], O1[:nh])
 
 
+def test_mfalcon_microbatch_partition(oracle_mod):
+    """Algorithm 1: splitting the m candidates into microbatches of any size
+    b_m (dividing m or not, down to 1 and up to m) changes no candidate's
+    output: every partition equals the single target-aware pass over
+    prefix ++ all candidates, including prefixes of length 0 and a
+    sequence without candidates."""
+    nh = np.array([9, 0, 14, 5])
+    nt = np.array([12, 7, 0, 12])
+    c = _small(lengths=tuple(nh + nt), nt=tuple(nt), h=2, d=5, N=30, seed=3)
+    full = _fwd(oracle_mod, c)
+    cand = np.concatenate([np.arange(c["offs"][b] + nh[b], c["offs"][b + 1])
+                           for b in range(len(nh))])
+    for b_m in (1, 2, 3, 4, 5, 6, 12, 40):
+        got = oracle_mod.mfalcon_fwd(c["offs"], c["nt"], b_m, c["N"], c["ts"], c["rp"], c["rt"],
+                                     c["q"], c["k"], c["v"])
+        np.testing.assert_allclose(got, full[cand], rtol=1e-13, atol=1e-15)
+    # A candidate alone (b_m = 1) is the last row of a plain causal pass
+    # over prefix ++ [candidate] (appendix on M-FALCON).
+    b, m = 3, 7
+    o = c["offs"][b]
+    idx = list(range(o, o + nh[b])) + [o + nh[b] + m]
+    c1 = dict(c, offs=np.array([0, nh[b] + 1]), nt=None, ts=c["ts"][idx], q=c["q"][idx],
+              k=c["k"][idx], v=c["v"][idx])
+    single = _fwd(oracle_mod, c1)[nh[b]]
+    got = oracle_mod.mfalcon_fwd(c["offs"], c["nt"], 1, c["N"], c["ts"], c["rp"], c["rt"],
+                                 c["q"], c["k"], c["v"])
+    np.testing.assert_allclose(got[nt[:b].sum() + m], single, rtol=1e-13, atol=1e-15)
+
+
 def test_time_shift_invariance(oracle_mod):
     """Only timestamp differences enter rab (notation table): shifting a
     sequence's timestamps by a constant changes nothing, bitwise."""
