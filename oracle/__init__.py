@@ -222,3 +222,64 @@ def mfalcon_fwd(seq_offsets, num_targets, b_m, max_seq_len, timestamps, rab_pos,
         sel = np.concatenate([np.arange(sub_offs[b] + nh[b], sub_offs[b + 1]) for b in range(B)])
         out[np.concatenate(keep)] = o[sel]
     return out
+
+
+# ------------------------------------------------ projections (Eq. 1, Eq. 3)
+# f_1 and f_2 are single linear layers (Sec. 3.1, after Eq. 3): a weight
+# matrix stored [out][in] and a bias.  Plain definitions in fp64 numpy.
+
+def _silu(x):
+    return x / (1.0 + np.exp(-x))
+
+
+def _silu_grad(x):
+    s = 1.0 / (1.0 + np.exp(-x))
+    return s * (1.0 + x * (1.0 - s))
+
+
+def proj_in_fwd(x, w1, b1=None):
+    """Eq. 1: pre = x W1^T + b1, Z = SiLU(pre) per token row, Z = [U | V | Q | K]
+    (the split of the fused projection output, notation table entry for
+    Split).  x [T, D], w1 [F, D], b1 [F].  Returns (Z, pre), both [T, F]."""
+    x, w1 = _f64(x), _f64(w1)
+    pre = x @ w1.T
+    if b1 is not None:
+        pre = pre + _f64(b1)[None, :]
+    return _silu(pre), pre
+
+
+def split_uvqk(z, num_heads, d_qk, d_v):
+    """U, V, Q, K views of Z [T, F] as [T, h, d]: U first, then V, Q, K."""
+    T = z.shape[0]
+    hv, hq = num_heads * d_v, num_heads * d_qk
+    u = z[:, :hv].reshape(T, num_heads, d_v)
+    v = z[:, hv:2 * hv].reshape(T, num_heads, d_v)
+    q = z[:, 2 * hv:2 * hv + hq].reshape(T, num_heads, d_qk)
+    k = z[:, 2 * hv + hq:2 * hv + 2 * hq].reshape(T, num_heads, d_qk)
+    return u, v, q, k
+
+
+def proj_in_bwd(x, w1, b1, dz):
+    """Gradient of <Z, dZ> for Z = SiLU(x W1^T + b1): returns (dx, dw1, db1)."""
+    x, w1, dz = _f64(x), _f64(w1), _f64(dz)
+    _, pre = proj_in_fwd(x, w1, b1)
+    dpre = dz * _silu_grad(pre)
+    return dpre @ w1, dpre.T @ x, dpre.sum(axis=0)
+
+
+def proj_out_fwd(g, w2, b2=None, residual=None):
+    """Eq. 3's f_2 plus the residual connection between layers (Sec. 3.1):
+    Y = g W2^T + b2 (+ residual).  g [T, h d_v], w2 [D, h d_v]."""
+    g, w2 = _f64(g), _f64(w2)
+    y = g @ w2.T
+    if b2 is not None:
+        y = y + _f64(b2)[None, :]
+    if residual is not None:
+        y = y + _f64(residual)
+    return y
+
+
+def proj_out_bwd(g, w2, dy):
+    """Gradient of <Y, dY> for Y = g W2^T + b2: returns (dg, dw2, db2)."""
+    g, w2, dy = _f64(g), _f64(w2), _f64(dy)
+    return dy @ w2, dy.T @ g, dy.sum(axis=0)

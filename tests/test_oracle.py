@@ -526,3 +526,78 @@ def test_bf16_rounding():
     assert got[1] == 1.0          # tie -> even (mantissa 0)
     assert got[2] == 1.0 + 2**-6  # tie -> even (rounds up)
     assert got[3] == -1.0
+
+
+# ----------------------------------------------------------- projections
+
+def _proj_case(seed=5, T=7, D=6, h=2, dqk=3, dv=2):
+    rng = np.random.default_rng(seed)
+    F = 2 * h * (dqk + dv)
+    return (rng.standard_normal((T, D)), rng.standard_normal((F, D)) * 0.5,
+            rng.standard_normal(F) * 0.3, rng.standard_normal((T, h * dv)),
+            rng.standard_normal((D, h * dv)) * 0.5, rng.standard_normal(D) * 0.3, (h, dqk, dv))
+
+
+def test_proj_forward_brute_force(oracle_mod):
+    """Eq. 1 and Eq. 3 (f_i a linear layer): element by element with plain
+    Python loops, weights stored [out][in]."""
+    x, w1, b1, g, w2, b2, _ = _proj_case()
+    z, pre = oracle_mod.proj_in_fwd(x, w1, b1)
+    y = oracle_mod.proj_out_fwd(g, w2, b2, residual=x)
+    for t in range(x.shape[0]):
+        for f in range(w1.shape[0]):
+            s = b1[f] + sum(x[t, c] * w1[f, c] for c in range(x.shape[1]))
+            assert abs(pre[t, f] - s) < 1e-12
+            assert abs(z[t, f] - s / (1.0 + math.exp(-s))) < 1e-12
+        for dd in range(w2.shape[0]):
+            s = b2[dd] + x[t, dd] + sum(g[t, c] * w2[dd, c] for c in range(g.shape[1]))
+            assert abs(y[t, dd] - s) < 1e-12
+
+
+def test_proj_split_order(oracle_mod):
+    """Notation table, Split: the fused output is U, V, Q, K in that order
+    (U, V of width h d_v, Q, K of width h d_qk).  A W1 whose rows pick
+    distinct inputs puts input column c(f) = f mod D at output f."""
+    h, dqk, dv = 2, 3, 2
+    F = 2 * h * (dqk + dv)
+    D = F
+    x = np.arange(1, D + 1, dtype=np.float64)[None, :] * 0.01
+    w1 = np.eye(F)
+    z, _ = oracle_mod.proj_in_fwd(x, w1)
+    u, v, q, k = oracle_mod.split_uvqk(z, h, dqk, dv)
+    sl = x[0] / (1.0 + np.exp(-x[0]))
+    np.testing.assert_allclose(u.reshape(-1), sl[:h * dv], rtol=1e-14)
+    np.testing.assert_allclose(v.reshape(-1), sl[h * dv:2 * h * dv], rtol=1e-14)
+    np.testing.assert_allclose(q.reshape(-1), sl[2 * h * dv:2 * h * dv + h * dqk], rtol=1e-14)
+    np.testing.assert_allclose(k.reshape(-1), sl[2 * h * dv + h * dqk:], rtol=1e-14)
+    assert u.shape == (1, h, dv) and q.shape == (1, h, dqk)
+
+
+def test_proj_backward_finite_differences(oracle_mod):
+    """Gradients of <Z, dZ> and <Y, dY> by central differences in fp64 on
+    every input, weight and bias entry."""
+    x, w1, b1, g, w2, b2, _ = _proj_case(T=4, D=3, h=1, dqk=2, dv=1)
+    rng = np.random.default_rng(9)
+    dz = rng.standard_normal((x.shape[0], w1.shape[0]))
+    dy = rng.standard_normal((g.shape[0], w2.shape[0]))
+    dx, dw1, db1 = oracle_mod.proj_in_bwd(x, w1, b1, dz)
+    dg, dw2, db2 = oracle_mod.proj_out_bwd(g, w2, dy)
+    eps = 1e-6
+
+    def fd(fn, arr):
+        out = np.empty_like(arr)
+        for i in np.ndindex(arr.shape):
+            a0 = arr[i]
+            arr[i] = a0 + eps
+            fp = fn()
+            arr[i] = a0 - eps
+            fm = fn()
+            arr[i] = a0
+            out[i] = (fp - fm) / (2 * eps)
+        return out
+
+    lz = lambda: float((oracle_mod.proj_in_fwd(x, w1, b1)[0] * dz).sum())
+    ly = lambda: float((oracle_mod.proj_out_fwd(g, w2, b2) * dy).sum())
+    for got, arr, fn in ((dx, x, lz), (dw1, w1, lz), (db1, b1, lz),
+                         (dg, g, ly), (dw2, w2, ly), (db2, b2, ly)):
+        np.testing.assert_allclose(got, fd(fn, arr), rtol=1e-7, atol=1e-8)
