@@ -122,6 +122,7 @@ def aux_measurements(hstu, torch, d, batch, stream):
                                    "bytes": total_pairs}
     del flush
     out["mfalcon"] = mfalcon_measurement(hstu, torch, stream)
+    out["projections"] = projection_measurement(hstu, torch, stream)
     out["gpu_clock"] = gpu_clock()
     return out
 
@@ -136,6 +137,50 @@ def _time_ms(torch, stream, fn, reps=6):
         torch.cuda.synchronize()
         ts.append(e0.elapsed_time(e1))
     return percentile(ts[1:], 0.5)
+
+
+def projection_measurement(hstu, torch, stream):
+    """The layer's linear maps at the training shape (T = 60383 tokens of the
+    training workload, d_model = 512, h = 8, d = 64, so F = 2048): f_1 with
+    SiLU (Eq. 1), f_2 with bias and residual (Eq. 3), and their backward
+    calls (input and weight gradients, bias sums); rate = matrix FLOPs of
+    each call / its time."""
+    from paper_2402_17152_amd import inputs
+    T = int(inputs.make_batch("training").seq_offsets[-1])
+    D, h, dqk, dv = 512, 8, 64, 64
+    hv, F = h * dv, 2 * h * (dqk + dv)
+    P = inputs.make_proj(T, D, h, dqk, dv, dtype="bf16", seed=7)
+    d = {k: inputs.array_to_device(v) for k, v in P.items()}
+    z, z_pre = hstu.hstu_proj_in_fwd(d["x"], d["w1"], d["b1"], h, dqk, dv, stream=stream)
+    y = torch.empty((T, D), dtype=torch.bfloat16, device="cuda")
+    dz = [d["dz"][:, a:b].contiguous().view(T, h, -1)
+          for a, b in ((0, hv), (hv, 2 * hv), (2 * hv, 2 * hv + h * dqk), (2 * hv + h * dqk, F))]
+    p = hstu.proj_problem(d["x"], h, dqk, dv)
+    ws = hstu.proj_workspace(p, D)
+    outs_in = (torch.empty_like(d["x"]), torch.empty((F, D), dtype=torch.float32, device="cuda"),
+               torch.empty(F, dtype=torch.float32, device="cuda"))
+    outs_out = (torch.empty_like(d["g"]), torch.empty((D, hv), dtype=torch.float32, device="cuda"),
+                torch.empty(D, dtype=torch.float32, device="cuda"))
+    calls = {
+        "proj_in_fwd": (2 * T * D * F, lambda: hstu.hstu_proj_in_fwd(
+            d["x"], d["w1"], d["b1"], h, dqk, dv, z=z, z_pre=z_pre, stream=stream)),
+        "proj_out_fwd": (2 * T * hv * D, lambda: hstu.hstu_proj_out_fwd(
+            d["g"], d["w2"], d["b2"], d["x"], h, dqk, dv, y=y, stream=stream)),
+        "proj_out_bwd": (4 * T * hv * D, lambda: hstu.hstu_proj_out_bwd(
+            d["g"], d["w2"], d["dy"], h, dqk, dv, out=outs_out, ws=ws, stream=stream)),
+        "proj_in_bwd": (4 * T * D * F, lambda: hstu.hstu_proj_in_bwd(
+            d["x"], d["w1"], z_pre, *dz, h, dqk, dv, dx_add=d["dy"], out=outs_in, ws=ws,
+            stream=stream)),
+    }
+    res = {"shape": f"T={T}, d_model={D}, h={h}, d_qk=d_v=64, F={F}, bf16"}
+    tot_ms, tot_flop = 0.0, 0
+    for name, (flop, fn) in calls.items():
+        ms = _time_ms(torch, stream, fn, reps=8)
+        res[name] = {"ms": ms, "tflops": flop / (ms * 1e-3) / 1e12, "flop": flop}
+        tot_ms += ms
+        tot_flop += flop
+    res["all_four"] = {"ms": tot_ms, "tflops": tot_flop / (tot_ms * 1e-3) / 1e12}
+    return res
 
 
 def mfalcon_measurement(hstu, torch, stream):

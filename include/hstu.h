@@ -254,6 +254,68 @@ hstu_status_t hstu_timing_read(const char* name, double* total_ms,
                                int64_t* launches);
 hstu_status_t hstu_timing_reset(void);
 
+/* ---- The layer's linear maps: f_1 with phi_1 (Eq. 1) and f_2 (Eq. 3) ----
+ * f_1 and f_2 are single linear layers with bias (Sec. 3.1, after Eq. 3).
+ * Weights are stored [out][in] row-major in the problem's dtype, biases
+ * are fp32 (NULL: none).  With D = d_model, hv = h*d_v, hq = h*d_qk and
+ * F = 2 hv + 2 hq (the width of the fused projection, notation table entry
+ * for Split), a token row of Z holds U (hv), V (hv), Q (hq), K (hq) in that
+ * order, each [h][d]: pass z, z + hv, z + 2hv, z + 2hv + hq with row stride
+ * F as u, v, q, k to the attention entry points.  Activations are dense
+ * rows (x, g: given row strides) of p->total_tokens tokens; p's sequence
+ * fields are not used.  All pointers are device memory, 16-byte aligned.
+ * D must be a multiple of 8.  bf16 problems run on the matrix cores with
+ * fp32 accumulation and need D and hv to be multiples of 64 and
+ * T * max(F, D) * 2 below 2^31;
+ * fp32 problems run a plain vector-ALU product (meant for small shapes).
+ * Weight and bias gradients are written (not accumulated) in fp32; their
+ * sums over tokens run in a fixed order, so results are reproducible.
+ * Errors: HSTU_ERR_INVALID_ARGUMENT (NULL, misaligned, stride below the
+ * row), HSTU_ERR_UNSUPPORTED (shapes above), HSTU_ERR_WORKSPACE. */
+
+/* Workspace bytes needed by hstu_proj_in_bwd and hstu_proj_out_bwd for
+ * problem p and model width d_model (0 if the arguments are invalid). */
+size_t hstu_proj_workspace_bytes(const hstu_problem_t* p, int32_t d_model);
+
+/* Eq. 1: z = SiLU(x W1^T + b1), x [T][D] (row stride x_stride), w1 [F][D],
+ * b1 [F]; z [T][F] dense.  z_pre (NULL or [T][F] dense) receives the
+ * pre-activation x W1^T + b1, which hstu_proj_in_bwd needs. */
+hstu_status_t hstu_proj_in_fwd(const hstu_problem_t* p, int32_t d_model,
+                               const void* x, int64_t x_stride,
+                               const void* w1, const float* b1,
+                               void* z, void* z_pre, void* hip_stream);
+
+/* Eq. 3's f_2 and the residual connection between layers (Sec. 3.1):
+ * y = g W2^T + b2 + residual, g [T][hv] (row stride g_stride; the y output
+ * of hstu_layer_fwd), w2 [D][hv], b2 [D], residual NULL or [T][D] dense
+ * (the layer's input x), y [T][D] dense. */
+hstu_status_t hstu_proj_out_fwd(const hstu_problem_t* p, int32_t d_model,
+                                const void* g, int64_t g_stride,
+                                const void* w2, const float* b2,
+                                const void* residual, void* y, void* hip_stream);
+
+/* Backward of hstu_proj_out_fwd for the loss <y, dy>: dg = dy W2 ([T][hv]
+ * dense, the d_y of hstu_layer_bwd), dw2 = dy^T g (fp32 [D][hv]), db2 =
+ * column sums of dy (fp32 [D], skipped if NULL).  The residual's gradient
+ * is dy itself. */
+hstu_status_t hstu_proj_out_bwd(const hstu_problem_t* p, int32_t d_model,
+                                const void* g, int64_t g_stride, const void* w2,
+                                const void* dy, void* dg, float* dw2, float* db2,
+                                void* ws, size_t ws_bytes, void* hip_stream);
+
+/* Backward of hstu_proj_in_fwd for the loss <z, dZ>, dZ = [du|dv|dq|dk]
+ * given as four dense [T][h][d] tensors (the gradients of hstu_layer_bwd):
+ * with dpre = dZ * SiLU'(z_pre), dx = dpre W1 (+ dx_add, NULL or [T][D]
+ * dense, e.g. the residual's gradient), dw1 = dpre^T x (fp32 [F][D]),
+ * db1 = column sums of dpre (fp32 [F], skipped if NULL).  bf16 problems
+ * round dpre to bf16 before the two products. */
+hstu_status_t hstu_proj_in_bwd(const hstu_problem_t* p, int32_t d_model,
+                               const void* x, int64_t x_stride, const void* w1,
+                               const void* z_pre, const void* du, const void* dv,
+                               const void* dq, const void* dk, const void* dx_add,
+                               void* dx, float* dw1, float* db1,
+                               void* ws, size_t ws_bytes, void* hip_stream);
+
 /* Matrix-core rate probe for measurement: launches on `stream` a kernel
  * that issues only bf16 v_mfma_f32_32x32x16 instructions, `iters` x 8
  * independent ones per wave, with `waves_per_simd` (1 or 2) waves on every

@@ -259,11 +259,14 @@ def split_uvqk(z, num_heads, d_qk, d_v):
     return u, v, q, k
 
 
-def proj_in_bwd(x, w1, b1, dz):
-    """Gradient of <Z, dZ> for Z = SiLU(x W1^T + b1): returns (dx, dw1, db1)."""
+def proj_in_bwd(x, w1, b1, dz, pre=None):
+    """Gradient of <Z, dZ> for Z = SiLU(x W1^T + b1): returns (dx, dw1, db1).
+    ``pre`` (optional): the pre-activation to differentiate SiLU at, e.g.
+    as the layer stored it; recomputed from x, w1, b1 when None."""
     x, w1, dz = _f64(x), _f64(w1), _f64(dz)
-    _, pre = proj_in_fwd(x, w1, b1)
-    dpre = dz * _silu_grad(pre)
+    if pre is None:
+        _, pre = proj_in_fwd(x, w1, b1)
+    dpre = dz * _silu_grad(_f64(pre))
     return dpre @ w1, dpre.T @ x, dpre.sum(axis=0)
 
 
@@ -283,3 +286,69 @@ def proj_out_bwd(g, w2, dy):
     """Gradient of <Y, dY> for Y = g W2^T + b2: returns (dg, dw2, db2)."""
     g, w2, dy = _f64(g), _f64(w2), _f64(dy)
     return dy @ w2, dy.T @ g, dy.sum(axis=0)
+
+
+def round_store(a, store):
+    """Storage rounding of an interface tensor: None keeps fp64, "f32" rounds
+    to float32, "bf16" to bfloat16 (round to nearest even, via float32)."""
+    if store is None:
+        return a
+    a32 = np.ascontiguousarray(a, dtype=np.float32)
+    if store == "f32":
+        return a32.astype(np.float64)
+    if store != "bf16":
+        raise ValueError(f"unknown storage type {store}")
+    u = a32.view(np.uint32).astype(np.uint64)
+    u = (u + 0x7FFF + ((u >> 16) & 1)) & 0xFFFF0000
+    return u.astype(np.uint32).view(np.float32).astype(np.float64)
+
+
+def layer_full_fwd(seq_offsets, max_seq_len, timestamps, rab_pos, rab_time, x, w1, b1, w2, b2,
+                   num_heads, d_qk, d_v, num_targets=None, ln_weight=None, ln_bias=None,
+                   eps=1e-5, store=None):
+    """One whole HSTU layer with its residual (Sec. 3.1): Eq. 1, Eq. 2, Eq. 3,
+    x_next = x + f_2(Norm(A V) * U).  Returns the intermediates and x_next.
+    ``store``: storage type of the tensors a layer built from separate calls
+    hands from one call to the next (Z and its pre-activation, the gated
+    output g); they are rounded to it, everything else stays fp64."""
+    x = _f64(x)
+    T = x.shape[0]
+    z, pre = proj_in_fwd(x, w1, b1)
+    z, pre = round_store(z, store), round_store(pre, store)
+    u, v, q, k = split_uvqk(z, num_heads, d_qk, d_v)
+    o = attn_fwd(seq_offsets, max_seq_len, timestamps, rab_pos, rab_time, q, k, v,
+                 num_targets=num_targets)
+    g, mean, rstd = ln_gate(o.reshape(T, -1), u.reshape(T, -1), ln_weight, ln_bias, eps)
+    g = round_store(g, store)
+    xn = proj_out_fwd(g, w2, b2, residual=x)
+    return {"z": z, "pre": pre, "o": o, "g": g, "mean": mean, "rstd": rstd, "x_next": xn}
+
+
+def layer_full_bwd(seq_offsets, max_seq_len, timestamps, rab_pos, rab_time, x, w1, b1, w2, b2,
+                   num_heads, d_qk, d_v, d_x_next, num_targets=None, ln_weight=None,
+                   ln_bias=None, eps=1e-5, store=None):
+    """Gradients of <x_next, d_x_next> for layer_full_fwd: dx (residual
+    included), dw1, db1, dw2, db2, d_ln_weight, d_ln_bias, d_rab_pos,
+    d_rab_time, and the intermediate gradients dg, do, dz.  With ``store``
+    the gradients handed between calls (dg, dz) are rounded to it as well
+    and SiLU is differentiated at the stored pre-activation."""
+    x = _f64(x)
+    T = x.shape[0]
+    f = layer_full_fwd(seq_offsets, max_seq_len, timestamps, rab_pos, rab_time, x, w1, b1, w2, b2,
+                       num_heads, d_qk, d_v, num_targets, ln_weight, ln_bias, eps, store)
+    dxn = _f64(d_x_next)
+    dg, dw2, db2 = proj_out_bwd(f["g"], w2, dxn)
+    dg = round_store(dg, store)
+    u, v, q, k = split_uvqk(f["z"], num_heads, d_qk, d_v)
+    do, du, dlw, dlb = ln_gate_bwd(f["o"].reshape(T, -1), u.reshape(T, -1), dg, ln_weight,
+                                   ln_bias, eps)
+    dq, dk, dv, drp, drt = attn_bwd(seq_offsets, max_seq_len, timestamps, rab_pos, rab_time,
+                                    q, k, v, do.reshape(T, num_heads, d_v),
+                                    num_targets=num_targets)
+    dz = np.concatenate([du.reshape(T, -1), dv.reshape(T, -1), dq.reshape(T, -1),
+                         dk.reshape(T, -1)], axis=1)
+    dz = round_store(dz, store)
+    dx, dw1, db1 = proj_in_bwd(x, w1, b1, dz, pre=f["pre"])
+    return {"dx": dx + dxn, "dw1": dw1, "db1": db1, "dw2": dw2, "db2": db2,
+            "d_ln_weight": dlw, "d_ln_bias": dlb, "d_rab_pos": drp, "d_rab_time": drt,
+            "dg": dg, "do": do, "dz": dz}

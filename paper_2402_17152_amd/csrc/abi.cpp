@@ -238,9 +238,303 @@ hstu_status_t attn_fwd_impl(const hstu_problem_t* p, const hstu_jagged_t* j, con
   return ok();
 }
 
+// ---- linear maps f_1 (Eq. 1) and f_2 (Eq. 3) -----------------------------
+
+struct ProjDims {
+  int64_t T;
+  int D, hv, hq, F;
+  bool bf16;
+  size_t e;
+};
+
+hstu_status_t proj_dims(const hstu_problem_t* p, int32_t d_model, ProjDims* d) {
+  HSTU_TRY(check_problem(p));
+  d->T = p->total_tokens;
+  d->D = d_model;
+  d->hv = p->num_heads * p->d_v;
+  d->hq = p->num_heads * p->d_qk;
+  d->F = 2 * d->hv + 2 * d->hq;
+  d->bf16 = p->dtype == HSTU_BF16;
+  d->e = elem_size(p);
+  if (d_model < 8 || d_model > 65536 || d_model % 8)
+    return fail(HSTU_ERR_UNSUPPORTED, "d_model must be a multiple of 8 in [8, 65536] (got %d)",
+                d_model);
+  if (d->bf16) {
+    // The matrix-core kernels take contraction lengths in steps of 64.
+    if (d_model % 64 || d->hv % 64)
+      return fail(HSTU_ERR_UNSUPPORTED,
+                  "bf16 projections need d_model and h*d_v to be multiples of 64 (got %d, %d)",
+                  d_model, d->hv);
+    const int64_t widest = d->F > d_model ? d->F : d_model;
+    if (d->T * widest * 2 >= ((int64_t)1 << 31))
+      return fail(HSTU_ERR_UNSUPPORTED, "T * max(F, d_model) * 2 bytes must stay below 2 GiB");
+  }
+  return HSTU_OK;
+}
+
+// A [rows][width] matrix with row stride `stride` (NULL allowed when it has no rows).
+hstu_status_t check_mat(const char* name, const void* ptr, int64_t stride, int64_t width,
+                        size_t e, int64_t rows) {
+  if (!ptr && rows == 0) return HSTU_OK;
+  if (!ptr) return fail(HSTU_ERR_INVALID_ARGUMENT, "%s is NULL", name);
+  if ((uintptr_t)ptr % 16) return fail(HSTU_ERR_INVALID_ARGUMENT, "%s is not 16-byte aligned", name);
+  if (stride < width)
+    return fail(HSTU_ERR_INVALID_ARGUMENT, "%s_stride %lld is smaller than a row (%lld)", name,
+                (long long)stride, (long long)width);
+  if ((stride * (int64_t)e) % 16)
+    return fail(HSTU_ERR_INVALID_ARGUMENT, "%s_stride must be a multiple of 16 bytes", name);
+  return HSTU_OK;
+}
+
+hstu_status_t check_opt(const char* name, const void* ptr) {
+  if (ptr && (uintptr_t)ptr % 16)
+    return fail(HSTU_ERR_INVALID_ARGUMENT, "%s is not 16-byte aligned", name);
+  return HSTU_OK;
+}
+
+struct ProjLayout {
+  size_t dpre, partial, slab, total;
+  int splits_in, ksplit_in, splits_out, ksplit_out;
+};
+
+ProjLayout proj_layout(const ProjDims& d) {
+  ProjLayout l{};
+  const size_t cb = (size_t)colsum_blocks(d.T);
+  l.splits_in = gemm_num_splits(d.F, d.D, d.T, &l.ksplit_in);
+  l.splits_out = gemm_num_splits(d.D, d.hv, d.T, &l.ksplit_out);
+  size_t off = 0;
+  l.dpre = off;
+  off = align_up(off + d.e * (size_t)d.T * d.F);
+  l.partial = off;
+  const size_t wide = (size_t)(d.F > d.D ? d.F : d.D);
+  off = align_up(off + sizeof(float) * cb * wide);
+  l.slab = off;
+  if (d.bf16) {
+    const size_t a = (size_t)l.splits_in * d.F * d.D, b = (size_t)l.splits_out * d.D * d.hv;
+    off = align_up(off + sizeof(float) * (a > b ? a : b));
+  }
+  l.total = off > kAlign ? off : kAlign;  // never 0, which means "invalid"
+  return l;
+}
+
+hstu_status_t check_proj_ws(const ProjDims& d, void* ws, size_t ws_bytes, ProjLayout* l) {
+  *l = proj_layout(d);
+  if (!ws) return fail(HSTU_ERR_WORKSPACE, "workspace is NULL (need %zu bytes)", l->total);
+  if ((uintptr_t)ws % kAlign) return fail(HSTU_ERR_WORKSPACE, "workspace must be 256-byte aligned");
+  if (ws_bytes < l->total)
+    return fail(HSTU_ERR_WORKSPACE, "workspace too small: %zu < %zu bytes", ws_bytes, l->total);
+  return HSTU_OK;
+}
+
+// C = A(m, k) B(n, k) in either dtype; a_km / b_km: operand stored k-major.
+// For fp32 operands the same layouts become element strides.
+hipError_t proj_gemm(const ProjDims& d, int epi, const void* a, int64_t lda, int a_km,
+                     const void* b, int64_t ldb, int b_km, int M, int N, int64_t K,
+                     const float* bias, const void* res, int64_t ldr, void* c, int64_t ldc,
+                     void* c2, float* slab, int splits, int ksplit, hipStream_t s) {
+  if (d.bf16) {
+    GemmArgs g{};
+    g.a = (const uint16_t*)a;
+    g.lda = lda;
+    g.b = (const uint16_t*)b;
+    g.ldb = ldb;
+    g.M = M;
+    g.N = N;
+    g.K = (int32_t)K;
+    g.k_split = ksplit;
+    g.bias = bias;
+    g.res = (const uint16_t*)res;
+    g.ldr = ldr;
+    g.c = (uint16_t*)c;
+    g.ldc = ldc;
+    g.c2 = (uint16_t*)c2;
+    g.ldc2 = ldc;
+    g.slab = slab;
+    return launch_gemm_bf16(g, a_km, b_km, epi, splits, s);
+  }
+  GemmArgsF32 g{};
+  g.a = (const float*)a;
+  g.sam = a_km ? 1 : lda;
+  g.sak = a_km ? lda : 1;
+  g.b = (const float*)b;
+  g.sbn = b_km ? 1 : ldb;
+  g.sbk = b_km ? ldb : 1;
+  g.M = M;
+  g.N = N;
+  g.K = (int32_t)K;
+  g.bias = bias;
+  g.res = (const float*)res;
+  g.ldr = ldr;
+  g.c = (float*)c;
+  g.ldc = ldc;
+  g.c2 = (float*)c2;
+  g.ldc2 = ldc;
+  return launch_gemm_f32(g, epi, s);
+}
+
+// Weight gradient dW [M][N] = sum_t A(m, t) B(n, t) over all tokens, both
+// operands k-major: fp32 slabs per token split, then their ordered sum
+// (bf16), or one direct product (fp32).
+hipError_t weight_grad(const ProjDims& d, const void* a, int64_t lda, const void* b,
+                       int64_t ldb, int M, int N, float* dw, float* slab, int splits,
+                       int ksplit, hipStream_t s) {
+  if (d.T == 0) return launch_reduce_slabs((int64_t)M * N, 0, nullptr, dw, s);
+  if (!d.bf16)
+    return proj_gemm(d, kEpiSlab, a, lda, 1, b, ldb, 1, M, N, d.T, nullptr, nullptr, 0, dw, N,
+                     nullptr, nullptr, 1, 0, s);
+  hipError_t e = proj_gemm(d, kEpiSlab, a, lda, 1, b, ldb, 1, M, N, d.T, nullptr, nullptr, 0,
+                           nullptr, 0, nullptr, slab, splits, ksplit, s);
+  if (e != hipSuccess) return e;
+  return launch_reduce_slabs((int64_t)M * N, splits, slab, dw, s);
+}
+
 }  // namespace
 
 extern "C" {
+
+size_t hstu_proj_workspace_bytes(const hstu_problem_t* p, int32_t d_model) {
+  try {
+    ProjDims d;
+    if (proj_dims(p, d_model, &d) != HSTU_OK) return 0;
+    return proj_layout(d).total;
+  } catch (...) {
+    return 0;
+  }
+}
+
+hstu_status_t hstu_proj_in_fwd(const hstu_problem_t* p, int32_t d_model, const void* x,
+                               int64_t x_stride, const void* w1, const float* b1, void* z,
+                               void* z_pre, void* hip_stream) {
+  try {
+    hipStream_t s = (hipStream_t)hip_stream;
+    ProjDims d;
+    HSTU_TRY(proj_dims(p, d_model, &d));
+    HSTU_TRY(check_mat("x", x, x_stride, d.D, d.e, d.T));
+    HSTU_TRY(check_mat("w1", w1, d.D, d.D, d.e, d.F));
+    HSTU_TRY(check_opt("b1", b1));
+    HSTU_TRY(check_mat("z", z, d.F, d.F, d.e, d.T));
+    HSTU_TRY(check_opt("z_pre", z_pre));
+    if (d.T == 0) return ok();
+    TimedScope ts("proj_in_fwd", s);
+    HSTU_HIP(proj_gemm(d, kEpiSilu, x, x_stride, 0, w1, d.D, 0, (int)d.T, d.F, d.D, b1, nullptr,
+                       0, z, d.F, z_pre, nullptr, 1, d.D, s),
+             "proj_in_fwd launch");
+    return ok();
+  } catch (...) {
+    return fail(HSTU_ERR_INVALID_ARGUMENT, "internal error");
+  }
+}
+
+hstu_status_t hstu_proj_out_fwd(const hstu_problem_t* p, int32_t d_model, const void* g,
+                                int64_t g_stride, const void* w2, const float* b2,
+                                const void* residual, void* y, void* hip_stream) {
+  try {
+    hipStream_t s = (hipStream_t)hip_stream;
+    ProjDims d;
+    HSTU_TRY(proj_dims(p, d_model, &d));
+    HSTU_TRY(check_mat("g", g, g_stride, d.hv, d.e, d.T));
+    HSTU_TRY(check_mat("w2", w2, d.hv, d.hv, d.e, d.D));
+    HSTU_TRY(check_opt("b2", b2));
+    HSTU_TRY(check_opt("residual", residual));
+    HSTU_TRY(check_mat("y", y, d.D, d.D, d.e, d.T));
+    if (d.T == 0) return ok();
+    TimedScope ts("proj_out_fwd", s);
+    HSTU_HIP(proj_gemm(d, kEpiAdd, g, g_stride, 0, w2, d.hv, 0, (int)d.T, d.D, d.hv, b2, residual,
+                       d.D, y, d.D, nullptr, nullptr, 1, d.hv, s),
+             "proj_out_fwd launch");
+    return ok();
+  } catch (...) {
+    return fail(HSTU_ERR_INVALID_ARGUMENT, "internal error");
+  }
+}
+
+hstu_status_t hstu_proj_out_bwd(const hstu_problem_t* p, int32_t d_model, const void* g,
+                                int64_t g_stride, const void* w2, const void* dy, void* dg,
+                                float* dw2, float* db2, void* ws, size_t ws_bytes,
+                                void* hip_stream) {
+  try {
+    hipStream_t s = (hipStream_t)hip_stream;
+    ProjDims d;
+    HSTU_TRY(proj_dims(p, d_model, &d));
+    HSTU_TRY(check_mat("g", g, g_stride, d.hv, d.e, d.T));
+    HSTU_TRY(check_mat("w2", w2, d.hv, d.hv, d.e, d.D));
+    HSTU_TRY(check_mat("dy", dy, d.D, d.D, d.e, d.T));
+    HSTU_TRY(check_mat("dg", dg, d.hv, d.hv, d.e, d.T));
+    HSTU_TRY(check_dense("dw2", dw2, 16));
+    HSTU_TRY(check_opt("db2", db2));
+    ProjLayout l;
+    HSTU_TRY(check_proj_ws(d, ws, ws_bytes, &l));
+    char* w = (char*)ws;
+    float* partial = (float*)(w + l.partial);
+    float* slab = (float*)(w + l.slab);
+    TimedScope ts("proj_out_bwd", s);
+    // dG = dY W2 (W2 [D][h d_v] read k-major).
+    if (d.T > 0)
+      HSTU_HIP(proj_gemm(d, kEpiAdd, dy, d.D, 0, w2, d.hv, 1, (int)d.T, d.hv, d.D, nullptr,
+                         nullptr, 0, dg, d.hv, nullptr, nullptr, 1, d.D, s),
+               "proj_out_bwd dgrad launch");
+    // dW2 = dY^T G over the tokens.
+    HSTU_HIP(weight_grad(d, dy, d.D, g, g_stride, d.D, d.hv, dw2, slab, l.splits_out,
+                         l.ksplit_out, s),
+             "proj_out_bwd wgrad launch");
+    if (db2) {
+      HSTU_HIP(launch_colsum(d.bf16, d.T, d.D, d.D, dy, partial, s), "colsum launch");
+      HSTU_HIP(launch_reduce_cols(d.D, (int)colsum_blocks(d.T), partial, db2, s),
+               "bias reduce launch");
+    }
+    return ok();
+  } catch (...) {
+    return fail(HSTU_ERR_INVALID_ARGUMENT, "internal error");
+  }
+}
+
+hstu_status_t hstu_proj_in_bwd(const hstu_problem_t* p, int32_t d_model, const void* x,
+                               int64_t x_stride, const void* w1, const void* z_pre,
+                               const void* du, const void* dv, const void* dq, const void* dk,
+                               const void* dx_add, void* dx, float* dw1, float* db1, void* ws,
+                               size_t ws_bytes, void* hip_stream) {
+  try {
+    hipStream_t s = (hipStream_t)hip_stream;
+    ProjDims d;
+    HSTU_TRY(proj_dims(p, d_model, &d));
+    HSTU_TRY(check_mat("x", x, x_stride, d.D, d.e, d.T));
+    HSTU_TRY(check_mat("w1", w1, d.D, d.D, d.e, d.F));
+    HSTU_TRY(check_mat("z_pre", z_pre, d.F, d.F, d.e, d.T));
+    HSTU_TRY(check_mat("du", du, d.hv, d.hv, d.e, d.T));
+    HSTU_TRY(check_mat("dv", dv, d.hv, d.hv, d.e, d.T));
+    HSTU_TRY(check_mat("dq", dq, d.hq, d.hq, d.e, d.T));
+    HSTU_TRY(check_mat("dk", dk, d.hq, d.hq, d.e, d.T));
+    HSTU_TRY(check_opt("dx_add", dx_add));
+    HSTU_TRY(check_mat("dx", dx, d.D, d.D, d.e, d.T));
+    HSTU_TRY(check_dense("dw1", dw1, 16));
+    HSTU_TRY(check_opt("db1", db1));
+    ProjLayout l;
+    HSTU_TRY(check_proj_ws(d, ws, ws_bytes, &l));
+    char* w = (char*)ws;
+    void* dpre = w + l.dpre;
+    float* partial = (float*)(w + l.partial);
+    float* slab = (float*)(w + l.slab);
+    TimedScope ts("proj_in_bwd", s);
+    HSTU_HIP(launch_silu_bwd(d.bf16, d.T, d.F, d.hv, d.hq, z_pre, du, dv, dq, dk, dpre, partial,
+                             s),
+             "silu backward launch");
+    // dX = dpre W1 (+ dx_add), W1 [F][D] read k-major.
+    if (d.T > 0)
+      HSTU_HIP(proj_gemm(d, kEpiAdd, dpre, d.F, 0, w1, d.D, 1, (int)d.T, d.D, d.F, nullptr,
+                         dx_add, d.D, dx, d.D, nullptr, nullptr, 1, d.F, s),
+               "proj_in_bwd dgrad launch");
+    // dW1 = dpre^T X over the tokens.
+    HSTU_HIP(weight_grad(d, dpre, d.F, x, x_stride, d.F, d.D, dw1, slab, l.splits_in,
+                         l.ksplit_in, s),
+             "proj_in_bwd wgrad launch");
+    if (db1)
+      HSTU_HIP(launch_reduce_cols(d.F, (int)colsum_blocks(d.T), partial, db1, s),
+               "bias reduce launch");
+    return ok();
+  } catch (...) {
+    return fail(HSTU_ERR_INVALID_ARGUMENT, "internal error");
+  }
+}
 
 int32_t hstu_abi_version(void) { return HSTU_ABI_VERSION; }
 

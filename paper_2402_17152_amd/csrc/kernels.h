@@ -123,4 +123,74 @@ hipError_t launch_ln_gate(int is_bf16, int64_t T, int32_t D, const void* x, cons
                           int64_t u_stride, const float* w, const float* b, float eps, void* y,
                           float* mean, float* rstd, hipStream_t s);
 
+// ---- dense products of the linear maps f_1 (Eq. 1) and f_2 (Eq. 3) ----
+// C[m][n] = sum_k A(m, k) B(n, k).  Epilogues: kEpiSilu stores
+// SiLU(acc + bias) to c and, if c2, the pre-activation acc + bias to c2;
+// kEpiAdd stores acc (+ bias) (+ res); kEpiSlab stores the fp32 partial of
+// contraction split blockIdx.y to slab[split][M][N].
+enum { kEpiSilu = 1, kEpiAdd = 2, kEpiSlab = 3 };
+
+// bf16 operands.  A k-contiguous: element (m, k) at a[m * lda + k]; k-major:
+// a[k * lda + m] (likewise B with n).  Requirements (checked by the
+// callers): K a multiple of 64 for a k-contiguous operand and a single
+// split; the contiguous dimension of a k-major operand a multiple of 8;
+// N a multiple of 8; every byte offset of an operand below 2^31; the
+// output row strides multiples of 8 elements.
+struct GemmArgs {
+  const uint16_t* a;
+  int64_t lda;
+  const uint16_t* b;
+  int64_t ldb;
+  int32_t M, N, K;
+  int32_t k_split;  // contraction rows per split (multiple of 64)
+  const float* bias;
+  const uint16_t* res;
+  int64_t ldr;
+  uint16_t* c;
+  int64_t ldc;
+  uint16_t* c2;
+  int64_t ldc2;
+  float* slab;
+};
+hipError_t launch_gemm_bf16(const GemmArgs& g, int a_kmajor, int b_kmajor, int epi, int splits,
+                            hipStream_t s);
+// Contraction splits for a k-major x k-major product of M x N outputs over
+// K rows: about 512 workgroups, at least 256 rows per split.
+int gemm_num_splits(int M, int N, int64_t K, int* k_split);
+
+// fp32 operands with arbitrary element strides (A(m, k) = a[m sam + k sak],
+// B(n, k) = b[n sbn + k sbk]); kEpiSlab stores the plain product to c.
+struct GemmArgsF32 {
+  const float* a;
+  int64_t sam, sak;
+  const float* b;
+  int64_t sbn, sbk;
+  int32_t M, N, K;
+  const float* bias;
+  const float* res;
+  int64_t ldr;
+  float* c;
+  int64_t ldc;
+  float* c2;
+  int64_t ldc2;
+};
+hipError_t launch_gemm_f32(const GemmArgsF32& g, int epi, hipStream_t s);
+
+// dpre = [dU|dV|dQ|dK] * SiLU'(pre) ([T][F], dtype of the problem; the
+// gradients dense [T][h][d], hv = h d_v, hq = h d_qk) and partial column
+// sums of dpre, [colsum_blocks(T)][F] fp32.
+int64_t colsum_blocks(int64_t T);
+hipError_t launch_silu_bwd(int is_bf16, int64_t T, int F, int hv, int hq, const void* pre,
+                           const void* du, const void* dv, const void* dq, const void* dk,
+                           void* dpre, float* partial, hipStream_t s);
+// Partial column sums of x [T][N] (row stride ld; N and ld multiples of
+// 8): [colsum_blocks(T)][N].  Activations 16-byte aligned.
+hipError_t launch_colsum(int is_bf16, int64_t T, int N, int64_t ld, const void* x, float* partial,
+                         hipStream_t s);
+// out[i] = sum_s part[s][i] (s = 0 .. S-1 in order), i < n.
+hipError_t launch_reduce_slabs(int64_t n, int S, const float* part, float* out, hipStream_t s);
+// The same fixed-order-per-group sum for many rows S and few columns n
+// (bias partials): 16 row groups per column, then the groups in order.
+hipError_t launch_reduce_cols(int n, int S, const float* part, float* out, hipStream_t s);
+
 }  // namespace hstu

@@ -25,7 +25,8 @@ EXPORTED = ("hstu_workspace_bytes", "hstu_attn_fwd", "hstu_attn_bwd", "hstu_laye
             "hstu_time_bucketize", "hstu_complete_cumsum", "hstu_pair_offsets", "hstu_validate",
             "hstu_last_error", "hstu_abi_version", "hstu_timing_enable", "hstu_timing_read",
             "hstu_timing_reset", "hstu_probe_mfma_bf16", "hstu_layer_bwd",
-            "hstu_attn_fwd_cached")
+            "hstu_attn_fwd_cached", "hstu_proj_workspace_bytes", "hstu_proj_in_fwd",
+            "hstu_proj_out_fwd", "hstu_proj_out_bwd", "hstu_proj_in_bwd")
 
 
 class Problem(ctypes.Structure):
@@ -75,6 +76,11 @@ def _load():
                                    ctypes.POINTER(ctypes.c_int64)]),
         "hstu_timing_reset": (i32, []),
         "hstu_probe_mfma_bf16": (i32, [i32, i32, P, ctypes.POINTER(ctypes.c_double), P]),
+        "hstu_proj_workspace_bytes": (sz, [PP, i32]),
+        "hstu_proj_in_fwd": (i32, [PP, i32, P, i64, P, P, P, P, P]),
+        "hstu_proj_out_fwd": (i32, [PP, i32, P, i64, P, P, P, P, P]),
+        "hstu_proj_out_bwd": (i32, [PP, i32, P, i64, P, P, P, P, P, P, sz, P]),
+        "hstu_proj_in_bwd": (i32, [PP, i32, P, i64, P, P, P, P, P, P, P, P, P, P, P, sz, P]),
     }
     for name, (res, args) in sig.items():
         fn = getattr(lib, name)
@@ -323,6 +329,102 @@ def hstu_timing_enable(on: bool = True):
 
 def hstu_timing_reset():
     _check(lib.hstu_timing_reset())
+
+
+# ------------------------------------------------ linear maps (Eq. 1, Eq. 3)
+
+def proj_problem(x, num_heads, d_qk, d_v) -> Problem:
+    """Problem of a projection call: only T, h, d_qk, d_v and the dtype
+    matter (one placeholder sequence, N = 1, one time bucket)."""
+    return make_problem(1, x.shape[0], 1, num_heads, d_qk, d_v, 1, _dtype_code(x))
+
+
+def _row_stride2(t: torch.Tensor) -> int:
+    if t.dim() == 2 and t.shape[0] == 0:
+        return t.shape[1]
+    if t.dim() != 2 or t.stride(1) != 1:
+        raise ValueError("expected a [T, width] tensor with contiguous rows")
+    return t.stride(0)
+
+
+def proj_workspace(p: Problem, d_model: int, device=None) -> torch.Tensor:
+    n = int(lib.hstu_proj_workspace_bytes(ctypes.byref(p), int(d_model)))
+    if n == 0:
+        raise HstuError(1, "invalid projection problem")
+    return torch.empty(n, dtype=torch.uint8, device=device or "cuda")
+
+
+def hstu_proj_in_fwd(x, w1, b1, num_heads, d_qk, d_v, z=None, z_pre=None, want_pre=True,
+                     stream=None):
+    """Eq. 1: returns (z, z_pre), z [T, F] = SiLU(x w1^T + b1) laid out U|V|Q|K."""
+    p = proj_problem(x, num_heads, d_qk, d_v)
+    F = 2 * num_heads * (d_qk + d_v)
+    if z is None:
+        z = torch.empty((x.shape[0], F), dtype=x.dtype, device=x.device)
+    if z_pre is None and want_pre:
+        z_pre = torch.empty_like(z)
+    _check(lib.hstu_proj_in_fwd(ctypes.byref(p), int(x.shape[1]), _ptr(x), _row_stride2(x),
+                                _ptr(w1), _ptr(b1), _ptr(z), _ptr(z_pre), _stream(stream)))
+    return z, z_pre
+
+
+def split_uvqk(z, num_heads, d_qk, d_v):
+    """[T, h, d] views U, V, Q, K of z [T, F] (row stride F)."""
+    T = z.shape[0]
+    hv, hq = num_heads * d_v, num_heads * d_qk
+    F = z.shape[1]
+
+    def view(c0, d):
+        return z.as_strided((T, num_heads, d), (F, d, 1), z.storage_offset() + c0)
+    return view(0, d_v), view(hv, d_v), view(2 * hv, d_qk), view(2 * hv + hq, d_qk)
+
+
+def hstu_proj_out_fwd(g, w2, b2, residual, num_heads, d_qk, d_v, y=None, stream=None):
+    """Eq. 3's f_2 plus the residual: y [T, D] = g w2^T + b2 + residual."""
+    p = proj_problem(g, num_heads, d_qk, d_v)
+    D = w2.shape[0]
+    if y is None:
+        y = torch.empty((g.shape[0], D), dtype=g.dtype, device=g.device)
+    _check(lib.hstu_proj_out_fwd(ctypes.byref(p), int(D), _ptr(g), _row_stride2(g), _ptr(w2),
+                                 _ptr(b2), _ptr(residual), _ptr(y), _stream(stream)))
+    return y
+
+
+def hstu_proj_out_bwd(g, w2, dy, num_heads, d_qk, d_v, want_db=True, out=None, ws=None,
+                      stream=None):
+    """Returns (dg, dw2, db2) for the loss <y, dy>."""
+    p = proj_problem(g, num_heads, d_qk, d_v)
+    D, hv = w2.shape
+    if out is None:
+        out = (torch.empty((g.shape[0], hv), dtype=g.dtype, device=g.device),
+               torch.empty((D, hv), dtype=torch.float32, device=g.device),
+               torch.empty(D, dtype=torch.float32, device=g.device) if want_db else None)
+    dg, dw2, db2 = out
+    if ws is None:
+        ws = proj_workspace(p, D, g.device)
+    _check(lib.hstu_proj_out_bwd(ctypes.byref(p), int(D), _ptr(g), _row_stride2(g), _ptr(w2),
+                                 _ptr(dy), _ptr(dg), _ptr(dw2), _ptr(db2), _ptr(ws), ws.numel(),
+                                 _stream(stream)))
+    return dg, dw2, db2
+
+
+def hstu_proj_in_bwd(x, w1, z_pre, du, dv, dq, dk, num_heads, d_qk, d_v, dx_add=None,
+                     want_db=True, out=None, ws=None, stream=None):
+    """Returns (dx, dw1, db1) for the loss <z, [du|dv|dq|dk]>."""
+    p = proj_problem(x, num_heads, d_qk, d_v)
+    F, D = w1.shape
+    if out is None:
+        out = (torch.empty_like(x, memory_format=torch.contiguous_format),
+               torch.empty((F, D), dtype=torch.float32, device=x.device),
+               torch.empty(F, dtype=torch.float32, device=x.device) if want_db else None)
+    dx, dw1, db1 = out
+    if ws is None:
+        ws = proj_workspace(p, D, x.device)
+    _check(lib.hstu_proj_in_bwd(ctypes.byref(p), int(D), _ptr(x), _row_stride2(x), _ptr(w1),
+                                _ptr(z_pre), _ptr(du), _ptr(dv), _ptr(dq), _ptr(dk),
+                                _ptr(dx_add), _ptr(dx), _ptr(dw1), _ptr(db1), _ptr(ws),
+                                ws.numel(), _stream(stream)))
+    return dx, dw1, db1
 
 
 def hstu_probe_mfma_bf16(iters: int, waves_per_simd: int, sink: torch.Tensor, stream=None):

@@ -240,6 +240,42 @@ def sub_batch(batch: Batch, seqs) -> Batch:
                  batch.rab_time, store)
 
 
+def make_proj(num_tokens, d_model, num_heads, d_qk, d_v, dtype="bf16", seed=0) -> dict:
+    """Seeded inputs of the layer's linear maps (Eq. 1 and Eq. 3's f_2):
+    x [T, D], w1 [F, D], w2 [D, h d_v] with N(0, 1/fan_in) entries; b1 [F],
+    b2 [D] ~ N(0, 0.1^2) (kept fp32); g [T, h d_v] (the gated layer-norm
+    output), dz [T, F] and dy [T, D] ~ N(0, 1).  Matrices are stored in
+    ``dtype`` (bf16 bit patterns or fp32)."""
+    rng = np.random.default_rng(seed)
+    T, D = int(num_tokens), int(d_model)
+    hv = num_heads * d_v
+    F = 2 * num_heads * (d_qk + d_v)
+    out = {
+        "x": _store(rng.standard_normal((T, D)), dtype),
+        "w1": _store(rng.standard_normal((F, D)) / np.sqrt(D), dtype),
+        "b1": (0.1 * rng.standard_normal(F)).astype(np.float32),
+        "w2": _store(rng.standard_normal((D, hv)) / np.sqrt(hv), dtype),
+        "b2": (0.1 * rng.standard_normal(D)).astype(np.float32),
+        "g": _store(rng.standard_normal((T, hv)), dtype),
+        "dz": _store(rng.standard_normal((T, F)), dtype),
+        "dy": _store(rng.standard_normal((T, D)), dtype),
+    }
+    return out
+
+
+def stored_f64(a: np.ndarray) -> np.ndarray:
+    """The exact values of a stored array (bf16 bit patterns or fp32) in fp64."""
+    return bf16_bits_to_f64(a) if a.dtype == np.uint16 else a.astype(np.float64)
+
+
+def array_to_device(a: np.ndarray, device="cuda"):
+    """One stored array as a torch tensor (bf16 bit patterns reinterpreted)."""
+    import torch
+    if a.dtype == np.uint16:
+        return torch.from_numpy(a.view(np.int16).copy()).view(torch.bfloat16).to(device)
+    return torch.from_numpy(np.ascontiguousarray(a)).to(device)
+
+
 def to_device(batch: Batch, device="cuda") -> dict:
     """Copies a batch to device memory as torch tensors (bf16 bit patterns
     are reinterpreted, not converted)."""

@@ -601,3 +601,58 @@ def test_proj_backward_finite_differences(oracle_mod):
     for got, arr, fn in ((dx, x, lz), (dw1, w1, lz), (db1, b1, lz),
                          (dg, g, ly), (dw2, w2, ly), (db2, b2, ly)):
         np.testing.assert_allclose(got, fd(fn, arr), rtol=1e-7, atol=1e-8)
+
+
+def test_round_store(oracle_mod):
+    """Storage rounding: float32 and bfloat16 round to nearest, ties to even
+    (bf16 = the top 16 bits of the float32 pattern)."""
+    one = 1.0
+    ulp = 2.0 ** -7  # bf16 spacing just above 1
+    x = np.array([one, one + ulp / 2, one + 3 * ulp / 2, one + ulp * 0.49, -2.5, 0.0, 1e-40])
+    got = oracle_mod.round_store(x, "bf16")
+    np.testing.assert_array_equal(got[:6], [one, one, one + 2 * ulp, one, -2.5, 0.0])
+    assert oracle_mod.round_store(np.array([1 + 2.0 ** -30]), "f32")[0] == 1.0
+    assert oracle_mod.round_store(x, None) is x
+
+
+def test_full_layer_finite_differences(oracle_mod):
+    """The whole layer (Eq. 1-3 with the residual of Sec. 3.1): gradients of
+    <x_next, d> by central differences on sampled entries of every input,
+    weight and table, target-aware mask included."""
+    rng = np.random.default_rng(21)
+    h, dqk, dv, D, N = 1, 2, 2, 3, 8
+    lengths, nt = np.array([5, 3]), np.array([2, 0])
+    offs = np.concatenate([[0], np.cumsum(lengths)])
+    T = int(offs[-1])
+    ts = np.concatenate([1000 + np.cumsum(rng.integers(1, 900, L)) for L in lengths])
+    F = 2 * h * (dqk + dv)
+    P = dict(x=rng.standard_normal((T, D)), w1=rng.standard_normal((F, D)) * 0.6,
+             b1=rng.standard_normal(F) * 0.2, w2=rng.standard_normal((D, h * dv)) * 0.6,
+             b2=rng.standard_normal(D) * 0.2, rp=rng.standard_normal(2 * N - 1) * 0.3,
+             rt=rng.standard_normal(16) * 0.3, lw=1.0 + 0.2 * rng.standard_normal(h * dv),
+             lb=0.1 * rng.standard_normal(h * dv))
+    d = rng.standard_normal((T, D))
+
+    def fwd():
+        return oracle_mod.layer_full_fwd(offs, N, ts, P["rp"], P["rt"], P["x"], P["w1"], P["b1"],
+                                         P["w2"], P["b2"], h, dqk, dv, num_targets=nt,
+                                         ln_weight=P["lw"], ln_bias=P["lb"])["x_next"]
+
+    g = oracle_mod.layer_full_bwd(offs, N, ts, P["rp"], P["rt"], P["x"], P["w1"], P["b1"],
+                                  P["w2"], P["b2"], h, dqk, dv, d, num_targets=nt,
+                                  ln_weight=P["lw"], ln_bias=P["lb"])
+    names = {"x": "dx", "w1": "dw1", "b1": "db1", "w2": "dw2", "b2": "db2", "rp": "d_rab_pos",
+             "rt": "d_rab_time", "lw": "d_ln_weight", "lb": "d_ln_bias"}
+    eps = 1e-6
+    for key, gname in names.items():
+        arr = P[key]
+        idx = list(np.ndindex(arr.shape))
+        for i in [idx[j] for j in rng.choice(len(idx), size=min(6, len(idx)), replace=False)]:
+            a0 = arr[i]
+            arr[i] = a0 + eps
+            fp = float((fwd() * d).sum())
+            arr[i] = a0 - eps
+            fm = float((fwd() * d).sum())
+            arr[i] = a0
+            num = (fp - fm) / (2 * eps)
+            assert abs(g[gname][i] - num) <= 1e-6 * max(1.0, abs(num)), (key, i, g[gname][i], num)
