@@ -352,3 +352,87 @@ def layer_full_bwd(seq_offsets, max_seq_len, timestamps, rab_pos, rab_time, x, w
     return {"dx": dx + dxn, "dw1": dw1, "db1": db1, "dw2": dw2, "db2": db2,
             "d_ln_weight": dlw, "d_ln_bias": dlb, "d_rab_pos": drp, "d_rab_time": drt,
             "dg": dg, "do": do, "dz": dz}
+
+
+# -------------------------------------------- Stochastic Length (Eq. 4)
+# Random draws are inputs: u_keep [B] ~ U[0, 1) decides whether a long
+# history is kept whole; e_rand [T] ~ Exp(1) per token drives the random
+# and feature-weighted selections.
+
+SL_GREEDY, SL_RANDOM, SL_WEIGHTED = 0, 1, 2
+
+
+def sl_subseq_len(max_seq_len, alpha):
+    """L = N_c^(alpha/2) of Eq. 4 (floor, with N_c the maximum length)."""
+    return int(np.floor(float(max_seq_len) ** (alpha / 2.0) + 1e-9))
+
+
+def _sl_keys(ts, e, mode):
+    """Selection keys of one history (smaller = chosen first), following the
+    subsequence selection appendix: greedy takes the most recent items
+    (f_i = t_n - t_i, t_n the latest timestamp); random takes items
+    uniformly (exponential-race keys E_i); feature-weighted takes items with
+    probability proportional to w_i = 1 - f_i / sum_k f_k, by
+    exponential-race keys E_i / w_i, ordered identically as E_i / (F - f_i)
+    with F = sum_k f_k (Efraimidis and Spirakis' weighted sampling without
+    replacement).  Greedy keys are integers; the others fp64."""
+    f = [int(ts.max()) - int(t) for t in ts] if len(ts) else []
+    if mode == SL_GREEDY:
+        return f
+    if mode == SL_RANDOM:
+        return [float(x) for x in e]
+    F = sum(f)
+    if F >= (1 << 53):
+        raise ValueError("feature-weighted selection needs the elapsed-time sum below 2^53")
+    keys = []
+    for ei, fi in zip(e, f):
+        den = F - fi
+        if F == 0:
+            keys.append(float(ei))      # all weights equal
+        elif den == 0:
+            keys.append(float("inf"))   # weight 0: never chosen before the others
+        else:
+            keys.append(float(ei) / float(den))
+    return keys
+
+
+def stochastic_length(seq_offsets, timestamps, num_targets, subseq_len, mode, u_keep, e_rand):
+    """Eq. 4 per sequence: with n_h history tokens (the candidates, if any,
+    are always kept after them), keep the sequence whole if n_h <= L or
+    u_keep[b] < L^2 / n_h^2; otherwise keep L history tokens chosen by the
+    selection keys (the L smallest; equal keys: the later token first),
+    in their original order.  Returns (new_offsets [B+1], gather [T'] of
+    original token indices)."""
+    offs = _i64(seq_offsets)
+    ts = _i64(timestamps)
+    B = len(offs) - 1
+    L = int(subseq_len)
+    if L < 1:
+        raise ValueError("subseq_len must be >= 1")
+    u = np.asarray(u_keep, dtype=np.float64)
+    e = None if e_rand is None else np.asarray(e_rand, dtype=np.float64)
+    gather, lens = [], []
+    for b in range(B):
+        o, n = int(offs[b]), int(offs[b + 1] - offs[b])
+        nt = 0 if num_targets is None else int(num_targets[b])
+        nh = n - nt
+        if nh <= L or u[b] < (L * L) / float(nh * nh):
+            sel = list(range(o, o + n))
+        else:
+            keys = _sl_keys(ts[o:o + nh], None if e is None else e[o:o + nh], mode)
+            order = sorted(range(nh), key=lambda i: (keys[i], -i))
+            sel = [o + i for i in sorted(order[:L])] + list(range(o + nh, o + n))
+        gather += sel
+        lens.append(len(sel))
+    new_offs = np.concatenate([[0], np.cumsum(lens)]).astype(np.int64)
+    return new_offs, np.asarray(gather, dtype=np.int64)
+
+
+def sl_sparsity(lengths, max_seq_len):
+    """Sequence sparsity of the Stochastic Length appendix: 1 - mean length
+    / maximum length; and s2 = 1 - sparsity of the attention matrix, i.e.
+    the share of the B padded N x N score matrices that lies inside the
+    sequences, sum_b n_b^2 / (B N^2)."""
+    n = np.asarray(lengths, dtype=np.float64)
+    N = float(max_seq_len)
+    return 1.0 - n.mean() / N, float((n * n).sum() / (len(n) * N * N))

@@ -656,3 +656,149 @@ def test_full_layer_finite_differences(oracle_mod):
             arr[i] = a0
             num = (fp - fm) / (2 * eps)
             assert abs(g[gname][i] - num) <= 1e-6 * max(1.0, abs(num)), (key, i, g[gname][i], num)
+
+
+# ------------------------------------------------------ Stochastic Length
+
+def _sl_batch(lengths, seed=0, nt=None):
+    rng = np.random.default_rng(seed)
+    lengths = np.asarray(lengths, dtype=np.int64)
+    offs = np.concatenate([[0], np.cumsum(lengths)]).astype(np.int64)
+    T = int(offs[-1])
+    ts = np.concatenate([1_700_000_000 + np.cumsum(rng.integers(0, 5000, L)) for L in lengths]
+                        ) if T else np.zeros(0, np.int64)
+    return offs, ts.astype(np.int64), T
+
+
+def test_sl_keep_decision_closed_form(oracle_mod):
+    """Eq. 4: a history of n > L tokens stays whole exactly when the draw u
+    falls below L^2 / n^2 (probability N_c^alpha / n^2 with L = N_c^(alpha/2));
+    n <= L always stays whole."""
+    L = 10
+    lengths = [5, 10, 11, 20, 40]
+    offs, ts, T = _sl_batch(lengths)
+    e = np.ones(T)
+    for b, n in enumerate(lengths):
+        p = L * L / (n * n)
+        for u, whole in ((np.nextafter(p, 0), True), (p, False), (0.999999, n <= L)):
+            if n <= L:
+                whole = True
+            uk = np.full(len(lengths), 0.999999)
+            uk[b] = u
+            no, g = oracle_mod.stochastic_length(offs, ts, None, L, oracle_mod.SL_RANDOM, uk, e)
+            assert (no[b + 1] - no[b] == n) == whole, (n, u)
+            if not whole:
+                assert no[b + 1] - no[b] == L
+
+
+def test_sl_greedy_is_most_recent(oracle_mod):
+    """Greedy selection keeps the L items with the smallest elapsed time
+    t_n - t_i: for increasing timestamps, the last L tokens; equal
+    timestamps prefer the later token."""
+    offs = np.array([0, 8])
+    ts = np.array([1, 2, 3, 5, 5, 5, 9, 9], dtype=np.int64)
+    no, g = oracle_mod.stochastic_length(offs, ts, None, 4, oracle_mod.SL_GREEDY, [0.99], None)
+    assert list(g) == [4, 5, 6, 7]
+    no, g = oracle_mod.stochastic_length(offs, ts, None, 3, oracle_mod.SL_GREEDY, [0.99], None)
+    assert list(g) == [5, 6, 7]
+
+
+def test_sl_candidates_kept(oracle_mod):
+    """With targets, Stochastic Length shortens the history only: every
+    candidate is kept, after the chosen history tokens."""
+    offs = np.array([0, 30])
+    ts = np.arange(30, dtype=np.int64) * 7
+    no, g = oracle_mod.stochastic_length(offs, ts, np.array([5]), 6, oracle_mod.SL_GREEDY,
+                                         [0.99], None)
+    assert list(g) == list(range(19, 25)) + list(range(25, 30))
+
+
+def test_sl_random_inclusion_probability(oracle_mod):
+    """Random selection: every history token is kept with probability L / n
+    (Monte Carlo over exponential draws, 5-sigma binomial band)."""
+    rng = np.random.default_rng(3)
+    n, L, R = 12, 5, 4000
+    offs = np.array([0, n])
+    ts = np.arange(n, dtype=np.int64)
+    counts = np.zeros(n)
+    for _ in range(R):
+        _, g = oracle_mod.stochastic_length(offs, ts, None, L, oracle_mod.SL_RANDOM, [0.999],
+                                            rng.exponential(size=n))
+        counts[g] += 1
+    p = L / n
+    assert np.all(np.abs(counts / R - p) < 5 * np.sqrt(p * (1 - p) / R))
+
+
+def test_sl_weighted_inclusion_probability(oracle_mod):
+    """Feature-weighted selection is weighted sampling without replacement
+    with w_i = 1 - f_i / sum f: with L = 1 a token is chosen with probability
+    w_i / sum w; with L = 2 the inclusion probability of token i is
+    sum over j of P(first = j) P(i second | j first) (successive sampling,
+    enumerated exactly), both within a 5-sigma band."""
+    rng = np.random.default_rng(4)
+    ts = np.array([0, 10, 25, 60, 100, 100], dtype=np.int64)
+    n = len(ts)
+    f = ts.max() - ts
+    w = 1.0 - f / f.sum()
+    offs = np.array([0, n])
+    R = 6000
+    for L in (1, 2):
+        counts = np.zeros(n)
+        for _ in range(R):
+            _, g = oracle_mod.stochastic_length(offs, ts, None, L, oracle_mod.SL_WEIGHTED, [0.999],
+                                                rng.exponential(size=n))
+            counts[g] += 1
+        P = w / w.sum()
+        if L == 2:
+            incl = P.copy()
+            for j in range(n):
+                rest = w.sum() - w[j]
+                for i in range(n):
+                    if i != j:
+                        incl[i] += P[j] * w[i] / rest
+            P = incl
+        assert np.all(np.abs(counts / R - P) < 5 * np.sqrt(P * (1 - P) / R) + 1e-12), (L, counts / R, P)
+
+
+def test_sl_expected_cost(oracle_mod):
+    """Eq. 4's point: the expected attention cost of a history of n > L
+    tokens is (1 - p) L^2 + p n^2 = 2 L^2 - L^4 / n^2 <= 2 N_c^alpha with
+    p = L^2 / n^2; averaged over a uniform grid of keep draws."""
+    L, n, G = 16, 64, 4096
+    offs = np.array([0, n])
+    ts = np.arange(n, dtype=np.int64)
+    cost = 0.0
+    for k in range(G):
+        no, _ = oracle_mod.stochastic_length(offs, ts, None, L, oracle_mod.SL_GREEDY,
+                                             [(k + 0.5) / G], None)
+        cost += float(no[1]) ** 2
+    assert abs(cost / G - (2 * L * L - L ** 4 / n ** 2)) < 1e-9 * n * n
+
+
+def test_sl_paper_example(oracle_mod):
+    """The paper's worked example (tests/golden/sl_alpha_1.6_len_4096.txt,
+    Sec. 4 on Stochastic Length): N = 4096, alpha = 1.6 turns a 4096-token
+    sequence into 776 tokens the majority of the time, removing more than
+    80 % of them."""
+    import os
+    path = os.path.join(os.path.dirname(__file__), "golden", "sl_alpha_1.6_len_4096.txt")
+    N, alpha, n, want = [float(x) for x in
+                         [ln for ln in open(path) if not ln.startswith("#")][0].split()]
+    L = oracle_mod.sl_subseq_len(int(N), alpha)
+    assert L == int(want)
+    p_whole = L * L / (n * n)
+    assert 1.0 - p_whole > 0.5 and 1.0 - L / n > 0.8
+    offs, ts = np.array([0, int(n)]), np.arange(int(n), dtype=np.int64)
+    no, _ = oracle_mod.stochastic_length(offs, ts, None, L, oracle_mod.SL_GREEDY, [0.5], None)
+    assert no[1] == L
+
+
+def test_sl_subseq_len_and_sparsity(oracle_mod):
+    """L = N^(alpha/2); sparsity = 1 - mean/max and s2 = sum n^2 / (B N^2) on
+    lengths with closed forms."""
+    assert oracle_mod.sl_subseq_len(4096, 2.0) == 4096
+    assert oracle_mod.sl_subseq_len(4096, 1.5) == 512
+    sp, s2 = oracle_mod.sl_sparsity([512, 512, 512, 512], 1024)
+    assert sp == 0.5 and s2 == 0.25
+    sp, s2 = oracle_mod.sl_sparsity([1024, 0], 1024)
+    assert sp == 0.5 and s2 == 0.5
