@@ -123,6 +123,7 @@ def aux_measurements(hstu, torch, d, batch, stream):
     del flush
     out["mfalcon"] = mfalcon_measurement(hstu, torch, stream)
     out["projections"] = projection_measurement(hstu, torch, stream)
+    out["stochastic_length"] = sl_measurement(hstu, torch, stream)
     out["gpu_clock"] = gpu_clock()
     return out
 
@@ -181,6 +182,57 @@ def projection_measurement(hstu, torch, stream):
         tot_flop += flop
     res["all_four"] = {"ms": tot_ms, "tflops": tot_flop / (tot_ms * 1e-3) / 1e12}
     return res
+
+
+def sl_measurement(hstu, torch, stream):
+    """Stochastic Length (Eq. 4) on the training workload (B = 64, power-law
+    lengths up to N = 4096, h = 8, d = 64) at alpha = 1.6 (L = 776), random
+    selection: the sampler plus the gather of q, k, v, u and timestamps, the
+    sparsity before and after, and the attention forward + backward on the
+    shrunk batch against the full one."""
+    import numpy as np
+    from paper_2402_17152_amd import inputs
+    batch = inputs.make_batch("training")
+    d = inputs.to_device(batch)
+    N = batch.spec.max_seq_len
+    L = hstu.hstu_sl_subseq_len(N, 1.6)
+    u, e = inputs.make_sl_draws(len(batch.lengths), batch.seq_offsets[-1], seed=5)
+    ud, ed = torch.from_numpy(u).cuda(), torch.from_numpy(e).cuda()
+    T = batch.total_tokens
+    new_offs = torch.empty(len(batch.lengths) + 1, dtype=torch.int64, device="cuda")
+    gather = torch.empty(T, dtype=torch.int64, device="cuda")
+    ws = torch.empty(hstu.hstu_sl_workspace_bytes(len(batch.lengths)), dtype=torch.uint8,
+                     device="cuda")
+    bufs = {k: torch.empty_like(d[k]) for k in ("q", "k", "v", "u", "timestamps")}
+
+    def sample():
+        hstu.hstu_stochastic_length(d["seq_offsets"], d["timestamps"], L, hstu.HSTU_SL_RANDOM, ud,
+                                    ed, out=(new_offs, gather), ws=ws, stream=stream)
+        for k, dst in bufs.items():
+            hstu.hstu_gather_rows(d[k], gather, new_offs[-1:], max_rows=T, dst=dst, stream=stream)
+    ms_sample = _time_ms(torch, stream, sample)
+    offs_new = new_offs.cpu().numpy()
+    T2 = int(offs_new[-1])
+    sp0, s20 = hstu.hstu_sl_sparsity(batch.seq_offsets, N)
+    sp1, s21 = hstu.hstu_sl_sparsity(offs_new, N)
+
+    def attn(dd, offs, ntok):
+        q, k, v = dd["q"][:ntok], dd["k"][:ntok], dd["v"][:ntok]
+        do = d["do"][:ntok]
+        def run():
+            hstu.hstu_attn_fwd(q, k, v, offs, dd["timestamps"][:ntok], d["rab_pos"], d["rab_time"],
+                               N, stream=stream)
+            hstu.hstu_attn_bwd(q, k, v, do, offs, dd["timestamps"][:ntok], d["rab_pos"],
+                               d["rab_time"], N, stream=stream)
+        return _time_ms(torch, stream, run)
+    ms_full = attn(d, d["seq_offsets"], T)
+    ms_sl = attn(bufs, new_offs, T2)
+    return {"workload": f"training: B={len(batch.lengths)}, T={T}, N={N}, alpha=1.6, L={L}, "
+                        "random selection",
+            "sampler_and_gather_ms": ms_sample, "tokens_before": T, "tokens_after": T2,
+            "sparsity_before": sp0, "sparsity_after": sp1, "s2_before": s20, "s2_after": s21,
+            "attn_fwd_bwd_ms_full": ms_full, "attn_fwd_bwd_ms_sl": ms_sl,
+            "attention_speedup": ms_full / ms_sl}
 
 
 def mfalcon_measurement(hstu, torch, stream):

@@ -316,6 +316,59 @@ hstu_status_t hstu_proj_in_bwd(const hstu_problem_t* p, int32_t d_model,
                                void* dx, float* dw1, float* db1,
                                void* ws, size_t ws_bytes, void* hip_stream);
 
+/* ---- Stochastic Length (Eq. 4; subsequence selection and sparsity in
+ * the appendix on Stochastic Length) ----
+ * Shrinks a jagged batch before attention.  With L = subseq_len
+ * (N_c^(alpha/2) of Eq. 4, see hstu_sl_subseq_len) and n_h the number of
+ * history tokens of sequence b (its tokens before the num_targets[b]
+ * candidates; num_targets NULL: no candidates), the sequence is kept whole
+ * if n_h <= L or u_keep[b] < L^2 / n_h^2 (fp64), else it keeps exactly L
+ * history tokens, chosen by `selection`, in their original order, and then
+ * all its candidates.  Selection keys (the L smallest win; equal keys: the
+ * later token first), with f_i = t_max - t_i over the history:
+ *   HSTU_SL_GREEDY    f_i: the most recent tokens;
+ *   HSTU_SL_RANDOM    e_rand[i]: a uniformly random subset;
+ *   HSTU_SL_WEIGHTED  e_rand[i] / (F - f_i), F = sum f_i: weighted sampling
+ *                     without replacement with weights 1 - f_i / F (the
+ *                     exponential-race form; +inf when F - f_i = 0, e_rand
+ *                     alone when F = 0).  Needs F < 2^53 to be exact.
+ * The random draws are inputs (device memory): u_keep [B] uniform in
+ * [0, 1); e_rand [T] Exp(1) draws (values <= 0 count as 0; unused and may
+ * be NULL for greedy).  Outputs (device): new_offsets [B+1] of the new
+ * batch, gather [T] of which the first new_offsets[B] entries are the
+ * original indices of the kept tokens in order (new num_targets equal the
+ * old).  Results are exact and deterministic.  ws: hstu_sl_workspace_bytes
+ * (num_seqs) bytes, 256-byte aligned.  Apply the selection to any per-token
+ * tensor with hstu_gather_rows. */
+enum { HSTU_SL_GREEDY = 0, HSTU_SL_RANDOM = 1, HSTU_SL_WEIGHTED = 2 };
+
+/* L = floor(max_seq_len^(alpha/2)) for alpha in (0, 2]; 0 if invalid. */
+int32_t hstu_sl_subseq_len(int32_t max_seq_len, double alpha);
+
+size_t hstu_sl_workspace_bytes(int32_t num_seqs);
+
+hstu_status_t hstu_stochastic_length(int32_t num_seqs, const int64_t* seq_offsets,
+                                     const int64_t* timestamps, const int64_t* num_targets,
+                                     int32_t subseq_len, int32_t selection,
+                                     const double* u_keep, const double* e_rand,
+                                     int64_t* new_offsets, int64_t* gather,
+                                     void* ws, size_t ws_bytes, void* hip_stream);
+
+/* dst row r = src row index[r] for r < min(*count, max_rows) (count and
+ * index in device memory, e.g. new_offsets + B and gather of
+ * hstu_stochastic_length); rows of row_bytes bytes at byte strides
+ * src_stride / dst_stride; all multiples of 4 (16-byte rows move as
+ * 16-byte words when everything is 16-byte aligned). */
+hstu_status_t hstu_gather_rows(const void* src, int64_t src_stride, int64_t row_bytes,
+                               const int64_t* index, const int64_t* count, int64_t max_rows,
+                               void* dst, int64_t dst_stride, void* hip_stream);
+
+/* Sparsity metrics of a batch (host memory offsets): sparsity = 1 - mean
+ * length / max_seq_len; s2 = one minus the sparsity of the attention
+ * matrix = sum_b L_b^2 / (B max_seq_len^2). */
+hstu_status_t hstu_sl_sparsity(int32_t num_seqs, const int64_t* seq_offsets, int32_t max_seq_len,
+                               double* sparsity, double* s2);
+
 /* Matrix-core rate probe for measurement: launches on `stream` a kernel
  * that issues only bf16 v_mfma_f32_32x32x16 instructions, `iters` x 8
  * independent ones per wave, with `waves_per_simd` (1 or 2) waves on every

@@ -379,8 +379,9 @@ def _sl_keys(ts, e, mode):
     f = [int(ts.max()) - int(t) for t in ts] if len(ts) else []
     if mode == SL_GREEDY:
         return f
+    e = [float(x) if x > 0 else 0.0 for x in e]  # an Exp(1) draw is >= 0
     if mode == SL_RANDOM:
-        return [float(x) for x in e]
+        return e
     F = sum(f)
     if F >= (1 << 53):
         raise ValueError("feature-weighted selection needs the elapsed-time sum below 2^53")

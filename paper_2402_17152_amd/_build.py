@@ -14,7 +14,7 @@ BUILD = os.path.join(ROOT, "_build")
 LIB = os.path.join(PKG, "libhstu.so")
 
 SOURCES = ["abi.cpp", "sched.hip", "bucketize.hip", "attn_fwd.hip", "attn_bwd.hip",
-           "attn_f32.hip", "ln_gate.hip", "probe.hip", "gemm.hip"]
+           "attn_f32.hip", "ln_gate.hip", "probe.hip", "gemm.hip", "sl.hip"]
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 ARCH = "gfx950"

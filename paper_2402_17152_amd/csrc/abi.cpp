@@ -4,6 +4,7 @@
 
 #include <hip/hip_runtime.h>
 
+#include <cmath>
 #include <cstdarg>
 #include <cstdio>
 #include <cstring>
@@ -391,6 +392,91 @@ hipError_t weight_grad(const ProjDims& d, const void* a, int64_t lda, const void
 }  // namespace
 
 extern "C" {
+
+// ---- Stochastic Length (Eq. 4) ----------------------------------------
+
+int32_t hstu_sl_subseq_len(int32_t max_seq_len, double alpha) {
+  if (max_seq_len < 1 || !(alpha > 0.0) || alpha > 2.0) return 0;
+  return (int32_t)std::floor(std::pow((double)max_seq_len, alpha / 2.0) + 1e-9);
+}
+
+size_t hstu_sl_workspace_bytes(int32_t num_seqs) {
+  if (num_seqs < 1) return 0;
+  return align_up(sizeof(int64_t) * (size_t)num_seqs) + align_up(sizeof(int32_t) * (size_t)num_seqs);
+}
+
+hstu_status_t hstu_stochastic_length(int32_t num_seqs, const int64_t* seq_offsets,
+                                     const int64_t* timestamps, const int64_t* num_targets,
+                                     int32_t subseq_len, int32_t selection, const double* u_keep,
+                                     const double* e_rand, int64_t* new_offsets, int64_t* gather,
+                                     void* ws, size_t ws_bytes, void* hip_stream) {
+  try {
+    hipStream_t s = (hipStream_t)hip_stream;
+    if (num_seqs < 1) return fail(HSTU_ERR_INVALID_ARGUMENT, "num_seqs must be >= 1");
+    if (subseq_len < 1) return fail(HSTU_ERR_INVALID_ARGUMENT, "subseq_len must be >= 1");
+    if (selection < HSTU_SL_GREEDY || selection > HSTU_SL_WEIGHTED)
+      return fail(HSTU_ERR_INVALID_ARGUMENT, "unknown selection %d", selection);
+    if (!seq_offsets || !timestamps || !u_keep || !new_offsets || !gather)
+      return fail(HSTU_ERR_INVALID_ARGUMENT, "NULL pointer");
+    if (selection != HSTU_SL_GREEDY && !e_rand)
+      return fail(HSTU_ERR_INVALID_ARGUMENT, "e_rand is NULL (needed by this selection)");
+    const size_t need = hstu_sl_workspace_bytes(num_seqs);
+    if (!ws || ws_bytes < need)
+      return fail(HSTU_ERR_WORKSPACE, "workspace too small: %zu < %zu bytes", ws_bytes, need);
+    if ((uintptr_t)ws % kAlign) return fail(HSTU_ERR_WORKSPACE, "workspace must be 256-byte aligned");
+    char* w = (char*)ws;
+    int64_t* new_len = (int64_t*)w;
+    int32_t* whole = (int32_t*)(w + align_up(sizeof(int64_t) * (size_t)num_seqs));
+    TimedScope ts("stochastic_length", s);
+    HSTU_HIP(launch_sl_lengths(num_seqs, seq_offsets, num_targets, subseq_len, u_keep, new_len,
+                               whole, s),
+             "sl lengths launch");
+    HSTU_HIP(launch_complete_cumsum(num_seqs, new_len, new_offsets, 0, s), "sl offsets launch");
+    HSTU_HIP(launch_sl_select(num_seqs, seq_offsets, timestamps, num_targets, subseq_len,
+                              selection, e_rand, whole, new_offsets, gather, s),
+             "sl select launch");
+    return ok();
+  } catch (...) {
+    return fail(HSTU_ERR_INVALID_ARGUMENT, "internal error");
+  }
+}
+
+hstu_status_t hstu_gather_rows(const void* src, int64_t src_stride, int64_t row_bytes,
+                               const int64_t* index, const int64_t* count, int64_t max_rows,
+                               void* dst, int64_t dst_stride, void* hip_stream) {
+  try {
+    if (max_rows < 0 || row_bytes < 0) return fail(HSTU_ERR_INVALID_ARGUMENT, "negative size");
+    if (max_rows == 0 || row_bytes == 0) return ok();
+    if (!src || !index || !count || !dst) return fail(HSTU_ERR_INVALID_ARGUMENT, "NULL pointer");
+    if (row_bytes % 4 || src_stride % 4 || dst_stride % 4 || (uintptr_t)src % 4 ||
+        (uintptr_t)dst % 4)
+      return fail(HSTU_ERR_INVALID_ARGUMENT, "rows, strides and pointers must be 4-byte aligned");
+    if (src_stride < row_bytes || dst_stride < row_bytes)
+      return fail(HSTU_ERR_INVALID_ARGUMENT, "stride smaller than a row");
+    HSTU_HIP(launch_gather_rows(src, src_stride, row_bytes, index, count, max_rows, dst,
+                                dst_stride, (hipStream_t)hip_stream),
+             "gather launch");
+    return ok();
+  } catch (...) {
+    return fail(HSTU_ERR_INVALID_ARGUMENT, "internal error");
+  }
+}
+
+hstu_status_t hstu_sl_sparsity(int32_t num_seqs, const int64_t* seq_offsets, int32_t max_seq_len,
+                               double* sparsity, double* s2) {
+  if (num_seqs < 1 || max_seq_len < 1) return fail(HSTU_ERR_INVALID_ARGUMENT, "bad sizes");
+  if (!seq_offsets || !sparsity || !s2) return fail(HSTU_ERR_INVALID_ARGUMENT, "NULL pointer");
+  double sum = 0.0, sq = 0.0;
+  for (int32_t b = 0; b < num_seqs; b++) {
+    const double n = (double)(seq_offsets[b + 1] - seq_offsets[b]);
+    sum += n;
+    sq += n * n;
+  }
+  const double N = (double)max_seq_len;
+  *sparsity = 1.0 - sum / num_seqs / N;
+  *s2 = sq / ((double)num_seqs * N * N);
+  return ok();
+}
 
 size_t hstu_proj_workspace_bytes(const hstu_problem_t* p, int32_t d_model) {
   try {

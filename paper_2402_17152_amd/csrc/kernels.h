@@ -193,4 +193,19 @@ hipError_t launch_reduce_slabs(int64_t n, int S, const float* part, float* out, 
 // (bias partials): 16 row groups per column, then the groups in order.
 hipError_t launch_reduce_cols(int n, int S, const float* part, float* out, hipStream_t s);
 
+// ---- Stochastic Length (Eq. 4) ----
+enum { kSlGreedy = 0, kSlRandom = 1, kSlWeighted = 2 };
+// new_len[b] and whole[b] (1: the sequence stays whole) per sequence.
+hipError_t launch_sl_lengths(int32_t B, const int64_t* offs, const int64_t* nt, int32_t L,
+                             const double* u_keep, int64_t* new_len, int32_t* whole,
+                             hipStream_t s);
+// gather[new_offs[b] ..] = the original indices a sequence keeps.
+hipError_t launch_sl_select(int32_t B, const int64_t* offs, const int64_t* ts, const int64_t* nt,
+                            int32_t L, int32_t mode, const double* e_rand, const int32_t* whole,
+                            const int64_t* new_offs, int64_t* gather, hipStream_t s);
+// dst row r = src row index[r], r < min(*count, max_rows); strides in bytes.
+hipError_t launch_gather_rows(const void* src, int64_t src_stride, int64_t row_bytes,
+                              const int64_t* index, const int64_t* count, int64_t max_rows,
+                              void* dst, int64_t dst_stride, hipStream_t s);
+
 }  // namespace hstu

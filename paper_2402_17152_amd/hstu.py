@@ -12,6 +12,7 @@ import ctypes
 import os
 from typing import Optional
 
+import numpy as np
 import torch
 
 _PKG = os.path.dirname(os.path.abspath(__file__))
@@ -26,7 +27,9 @@ EXPORTED = ("hstu_workspace_bytes", "hstu_attn_fwd", "hstu_attn_bwd", "hstu_laye
             "hstu_last_error", "hstu_abi_version", "hstu_timing_enable", "hstu_timing_read",
             "hstu_timing_reset", "hstu_probe_mfma_bf16", "hstu_layer_bwd",
             "hstu_attn_fwd_cached", "hstu_proj_workspace_bytes", "hstu_proj_in_fwd",
-            "hstu_proj_out_fwd", "hstu_proj_out_bwd", "hstu_proj_in_bwd")
+            "hstu_proj_out_fwd", "hstu_proj_out_bwd", "hstu_proj_in_bwd",
+            "hstu_sl_subseq_len", "hstu_sl_workspace_bytes", "hstu_stochastic_length",
+            "hstu_gather_rows", "hstu_sl_sparsity")
 
 
 class Problem(ctypes.Structure):
@@ -77,6 +80,12 @@ def _load():
         "hstu_timing_reset": (i32, []),
         "hstu_probe_mfma_bf16": (i32, [i32, i32, P, ctypes.POINTER(ctypes.c_double), P]),
         "hstu_proj_workspace_bytes": (sz, [PP, i32]),
+        "hstu_sl_subseq_len": (i32, [i32, ctypes.c_double]),
+        "hstu_sl_workspace_bytes": (sz, [i32]),
+        "hstu_stochastic_length": (i32, [i32, P, P, P, i32, i32, P, P, P, P, P, sz, P]),
+        "hstu_gather_rows": (i32, [P, i64, i64, P, P, i64, P, i64, P]),
+        "hstu_sl_sparsity": (i32, [i32, P, i32, ctypes.POINTER(ctypes.c_double),
+                                   ctypes.POINTER(ctypes.c_double)]),
         "hstu_proj_in_fwd": (i32, [PP, i32, P, i64, P, P, P, P, P]),
         "hstu_proj_out_fwd": (i32, [PP, i32, P, i64, P, P, P, P, P]),
         "hstu_proj_out_bwd": (i32, [PP, i32, P, i64, P, P, P, P, P, P, sz, P]),
@@ -347,6 +356,10 @@ def _row_stride2(t: torch.Tensor) -> int:
     return t.stride(0)
 
 
+def hstu_proj_workspace_bytes(p: Problem, d_model: int) -> int:
+    return int(lib.hstu_proj_workspace_bytes(ctypes.byref(p), int(d_model)))
+
+
 def proj_workspace(p: Problem, d_model: int, device=None) -> torch.Tensor:
     n = int(lib.hstu_proj_workspace_bytes(ctypes.byref(p), int(d_model)))
     if n == 0:
@@ -425,6 +438,64 @@ def hstu_proj_in_bwd(x, w1, z_pre, du, dv, dq, dk, num_heads, d_qk, d_v, dx_add=
                                 _ptr(dx_add), _ptr(dx), _ptr(dw1), _ptr(db1), _ptr(ws),
                                 ws.numel(), _stream(stream)))
     return dx, dw1, db1
+
+
+# ------------------------------------------------ Stochastic Length (Eq. 4)
+
+HSTU_SL_GREEDY, HSTU_SL_RANDOM, HSTU_SL_WEIGHTED = 0, 1, 2
+
+
+def hstu_sl_subseq_len(max_seq_len: int, alpha: float) -> int:
+    return int(lib.hstu_sl_subseq_len(int(max_seq_len), float(alpha)))
+
+
+def hstu_sl_workspace_bytes(num_seqs: int) -> int:
+    return int(lib.hstu_sl_workspace_bytes(int(num_seqs)))
+
+
+def hstu_stochastic_length(seq_offsets, timestamps, subseq_len, selection, u_keep, e_rand=None,
+                           num_targets=None, out=None, ws=None, stream=None):
+    """(new_offsets [B+1], gather [T]) on the device; the first
+    new_offsets[B] entries of gather are valid (see include/hstu.h)."""
+    B = seq_offsets.numel() - 1
+    T = timestamps.numel()
+    if out is None:
+        out = (torch.empty(B + 1, dtype=torch.int64, device=seq_offsets.device),
+               torch.empty(max(T, 1), dtype=torch.int64, device=seq_offsets.device))
+    new_offsets, gather = out
+    if ws is None:
+        ws = torch.empty(int(lib.hstu_sl_workspace_bytes(B)), dtype=torch.uint8,
+                         device=seq_offsets.device)
+    _check(lib.hstu_stochastic_length(B, _ptr(seq_offsets), _ptr(timestamps), _ptr(num_targets),
+                                      int(subseq_len), int(selection), _ptr(u_keep), _ptr(e_rand),
+                                      _ptr(new_offsets), _ptr(gather), _ptr(ws), ws.numel(),
+                                      _stream(stream)))
+    return new_offsets, gather
+
+
+def hstu_gather_rows(src, gather, count, max_rows=None, dst=None, stream=None):
+    """dst[r] = src[gather[r]] for r < count[0] (a one-element device tensor,
+    e.g. new_offsets[-1:]); src rows are its first dimension."""
+    rows = src.shape[0]
+    row_elems = src[0].numel() if rows else int(np.prod(src.shape[1:]))
+    if max_rows is None:
+        max_rows = gather.numel()
+    if dst is None:
+        dst = torch.empty((max_rows,) + tuple(src.shape[1:]), dtype=src.dtype, device=src.device)
+    es = src.element_size()
+    _check(lib.hstu_gather_rows(_ptr(src), src.stride(0) * es, row_elems * es, _ptr(gather),
+                                _ptr(count), int(max_rows), _ptr(dst), dst.stride(0) * es,
+                                _stream(stream)))
+    return dst
+
+
+def hstu_sl_sparsity(seq_offsets_host, max_seq_len):
+    """(sparsity, s2) of a batch from host int64 offsets."""
+    offs = np.ascontiguousarray(seq_offsets_host, dtype=np.int64)
+    sp, s2 = ctypes.c_double(0.0), ctypes.c_double(0.0)
+    _check(lib.hstu_sl_sparsity(len(offs) - 1, offs.ctypes.data_as(ctypes.c_void_p),
+                                int(max_seq_len), ctypes.byref(sp), ctypes.byref(s2)))
+    return sp.value, s2.value
 
 
 def hstu_probe_mfma_bf16(iters: int, waves_per_simd: int, sink: torch.Tensor, stream=None):

@@ -263,6 +263,13 @@ def make_proj(num_tokens, d_model, num_heads, d_qk, d_v, dtype="bf16", seed=0) -
     return out
 
 
+def make_sl_draws(num_seqs, num_tokens, seed=0):
+    """The random draws Stochastic Length consumes: u_keep [B] ~ U[0, 1)
+    (keep-whole decision of Eq. 4) and e_rand [T] ~ Exp(1) (selection keys)."""
+    rng = np.random.default_rng(seed)
+    return rng.random(int(num_seqs)), rng.exponential(size=int(num_tokens))
+
+
 def stored_f64(a: np.ndarray) -> np.ndarray:
     """The exact values of a stored array (bf16 bit patterns or fp32) in fp64."""
     return bf16_bits_to_f64(a) if a.dtype == np.uint16 else a.astype(np.float64)

@@ -1,0 +1,136 @@
+"""Stochastic Length (Eq. 4, the subsequence selection appendix): the
+device sampler against the oracle, bit for bit (offsets and gather lists
+are index work), plus the host-side helpers.
+
+GPU cases: all three selections; sequences shorter than, equal to and one
+longer than L, empty ones and 8192-token ones; keep draws exactly at the
+threshold; tied keys (repeated timestamps, repeated exponential draws);
+candidates; the training workload's lengths (B = 64 up to 4096) at
+alpha = 1.6.  The row gather is checked against numpy indexing."""
+import numpy as np
+import pytest
+import torch
+
+from paper_2402_17152_amd import inputs
+
+
+def _hs():
+    from paper_2402_17152_amd import hstu
+    return hstu
+
+
+# ------------------------------------------------------------- host side
+
+def test_sl_host_helpers_match_oracle(oracle_mod):
+    hs = _hs()
+    for N, a in ((4096, 1.6), (4096, 2.0), (8192, 1.7), (1024, 1.5), (3072, 1.9)):
+        assert hs.hstu_sl_subseq_len(N, a) == oracle_mod.sl_subseq_len(N, a)
+    assert hs.hstu_sl_subseq_len(4096, 0.0) == 0
+    rng = np.random.default_rng(1)
+    lens = rng.integers(0, 4097, 37)
+    offs = np.concatenate([[0], np.cumsum(lens)]).astype(np.int64)
+    sp, s2 = hs.hstu_sl_sparsity(offs, 4096)
+    rsp, rs2 = oracle_mod.sl_sparsity(lens, 4096)
+    assert abs(sp - rsp) < 1e-12 and abs(s2 - rs2) < 1e-12
+
+
+# ------------------------------------------------------------- device side
+
+def _batch(lengths, seed, dup_ts=False):
+    rng = np.random.default_rng(seed)
+    lengths = np.asarray(lengths, dtype=np.int64)
+    offs = np.concatenate([[0], np.cumsum(lengths)]).astype(np.int64)
+    parts = []
+    for L in lengths:
+        gaps = rng.integers(0, 3 if dup_ts else 5000, L)   # gaps of 0: equal timestamps
+        parts.append(1_700_000_000 + np.cumsum(gaps))
+    ts = np.concatenate(parts).astype(np.int64) if len(parts) else np.zeros(0, np.int64)
+    return offs, ts
+
+
+def _run(hs, offs, ts, nt, L, mode, u, e):
+    dev = lambda a: torch.from_numpy(np.ascontiguousarray(a)).cuda()
+    no, g = hs.hstu_stochastic_length(dev(offs), dev(ts), L, mode, dev(u),
+                                      None if e is None else dev(e),
+                                      num_targets=None if nt is None else dev(nt))
+    torch.cuda.synchronize()
+    no = no.cpu().numpy()
+    return no, g.cpu().numpy()[:no[-1]]
+
+
+def _check(hs, oracle_mod, offs, ts, nt, L, mode, u, e):
+    got_o, got_g = _run(hs, offs, ts, nt, L, mode, u, e)
+    ref_o, ref_g = oracle_mod.stochastic_length(offs, ts, nt, L, mode, u, e)
+    np.testing.assert_array_equal(got_o, ref_o)
+    np.testing.assert_array_equal(got_g, ref_g)
+    return ref_o
+
+
+MODES = [0, 1, 2]
+
+
+@pytest.mark.gpu
+@pytest.mark.parametrize("mode", MODES)
+def test_sl_small_bit_exact(oracle_mod, mode):
+    hs = _hs()
+    L = 10
+    lengths = [0, 1, 5, 10, 11, 40, 300, 1000, 8192, 257]
+    for seed, dup in ((0, False), (1, True)):
+        offs, ts = _batch(lengths, seed, dup_ts=dup)
+        u, e = inputs.make_sl_draws(len(lengths), offs[-1], seed=seed)
+        if dup:  # tied exponential keys and zero draws
+            e[::7] = e[3]
+            e[::11] = 0.0
+        # keep draws exactly at, just below and far from the threshold
+        n = np.diff(offs)
+        with np.errstate(divide="ignore"):
+            thr = (L * L) / (n.astype(np.float64) ** 2)
+        u[5] = thr[5]
+        u[6] = np.nextafter(thr[6], 0)
+        u[7] = 0.9999
+        ref_o = _check(hs, oracle_mod, offs, ts, None, L, mode, u, e)
+        assert (np.diff(ref_o) < n).any()  # something was shortened
+
+
+@pytest.mark.gpu
+@pytest.mark.parametrize("mode", MODES)
+def test_sl_candidates_bit_exact(oracle_mod, mode):
+    hs = _hs()
+    lengths = np.array([30, 600, 5, 2048 + 1024, 77])
+    nt = np.array([5, 100, 5, 1024, 0])
+    offs, ts = _batch(lengths, 7)
+    u, e = inputs.make_sl_draws(len(lengths), offs[-1], seed=7)
+    u[:] = 0.99
+    ref_o = _check(hs, oracle_mod, offs, ts, nt, 16, mode, u, e)
+    assert list(np.diff(ref_o)) == [21, 116, 5, 1040, 16]
+
+
+@pytest.mark.gpu
+@pytest.mark.parametrize("mode", MODES)
+def test_sl_training_workload(oracle_mod, mode):
+    """The training workload's lengths (B = 64, power law up to N = 4096)
+    and timestamps at alpha = 1.6 (L = 776)."""
+    hs = _hs()
+    b = inputs.make_batch("training")
+    L = oracle_mod.sl_subseq_len(b.spec.max_seq_len, 1.6)
+    u, e = inputs.make_sl_draws(len(b.lengths), b.seq_offsets[-1], seed=5)
+    _check(hs, oracle_mod, b.seq_offsets, b.timestamps, None, L, mode, u, e)
+
+
+@pytest.mark.gpu
+def test_sl_gather_rows():
+    """Gathering per-token rows (bf16 rows of 1024 bytes, int64 timestamps,
+    fp32 rows of 12 bytes) equals numpy indexing."""
+    hs = _hs()
+    rng = np.random.default_rng(9)
+    T = 5000
+    idx = np.sort(rng.choice(T, 1234, replace=False)).astype(np.int64)
+    gi = torch.from_numpy(idx).cuda()
+    cnt = torch.tensor([len(idx)], dtype=torch.int64, device="cuda")
+    x = torch.randn(T, 512, device="cuda").to(torch.bfloat16)
+    t = torch.from_numpy(rng.integers(0, 1 << 40, T)).cuda()
+    f = torch.randn(T, 3, device="cuda")
+    for src in (x, t, f):
+        got = hs.hstu_gather_rows(src, gi, cnt, max_rows=T)[:len(idx)]
+        torch.cuda.synchronize()
+        assert torch.equal(got.cpu(), src.cpu()[torch.from_numpy(idx)])
