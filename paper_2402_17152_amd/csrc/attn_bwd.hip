@@ -824,10 +824,14 @@ __global__ __launch_bounds__(kBwdThreads, 1) void attn_bwd_bf16_kernel(
   constexpr int BN = S::BN;
   __shared__ S sm;
 
-  if ((int)blockIdx.x >= *count) return;
-  const WorkItem it = items[blockIdx.x];
-  const int head = blockIdx.y;
+  // Workgroup id = item * H + head: the dispatcher walks the (longest
+  // first) work list with all heads of an item together, so the long items
+  // of every head start early.
   const JaggedArgs& ja = A.ja;
+  const int item = (int)(blockIdx.x / (unsigned)ja.num_heads);
+  const int head = (int)blockIdx.x - item * ja.num_heads;
+  if (item >= *count) return;
+  const WorkItem it = items[item];
   const int N = ja.max_seq_len, NB = ja.num_buckets;
   const int64_t o = ja.seq_offsets[it.seq];
   const int L = (int)(ja.seq_offsets[it.seq + 1] - o);
@@ -878,7 +882,7 @@ hipError_t launch_bwd(const JaggedArgs& ja, const Tensors& t, const void* d_out,
   A.d_rab_pos = d_rab_pos;
   A.d_rab_time = d_rab_time;
   static_assert(sizeof(BwdShared<DQK, DV, true>) <= kLdsBytes, "LDS budget");
-  dim3 grid((unsigned)max_items, (unsigned)ja.num_heads);
+  dim3 grid((unsigned)(max_items * ja.num_heads));
   if (d_out_lo)
     hipLaunchKernelGGL((attn_bwd_bf16_kernel<DQK, DV, true>), grid, dim3(kBwdThreads), 0, s, A,
                        items, count);

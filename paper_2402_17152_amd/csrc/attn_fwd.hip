@@ -563,9 +563,13 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_bf16_kernel(JaggedArgs ja, Te
                                                                const int32_t* __restrict__ count) {
   using Sh = FwdShared<DQK, DV>;
   __shared__ Sh sm;
-  if ((int)blockIdx.x >= *count) return;
-  const WorkItem it = items[blockIdx.x];
-  const int head = blockIdx.y;
+  // Workgroup id = item * H + head: the dispatcher walks the (longest
+  // first) work list with all heads of an item together, so the long items
+  // of every head start early.
+  const int item = (int)(blockIdx.x / (unsigned)ja.num_heads);
+  const int head = (int)blockIdx.x - item * ja.num_heads;
+  if (item >= *count) return;
+  const WorkItem it = items[item];
   const int NB = ja.num_buckets;
   const int64_t o = ja.seq_offsets[it.seq];
   const int Lr = (int)(ja.seq_offsets[it.seq + 1] - o);
@@ -608,7 +612,7 @@ template <int DQK, int DV>
 hipError_t launch_fwd(const JaggedArgs& ja, const Tensors& t, void* out, int out_f32, int split,
                       const WorkItem* items, const int32_t* count, int64_t max_items,
                       hipStream_t s) {
-  dim3 grid((unsigned)max_items, (unsigned)ja.num_heads);
+  dim3 grid((unsigned)(max_items * ja.num_heads));
   if (split)
     hipLaunchKernelGGL((attn_fwd_bf16_kernel<DQK, DV, true>), grid, dim3(256), 0, s, ja, t, out,
                        out_f32, items, count);
