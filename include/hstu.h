@@ -136,7 +136,15 @@ hstu_status_t hstu_attn_fwd(const hstu_problem_t* p, const hstu_jagged_t* j,
  * num_targets = the candidate count (the target-aware mask), for any
  * split of a user's candidates into microbatches.  p: num_seqs = B,
  * total_tokens = T, max_seq_len = N, the normaliser (n_b + candidates of
- * b <= N, not checked); bf16 problems only (HSTU_ERR_UNSUPPORTED for fp32). */
+ * b <= N, not checked); bf16 problems only (HSTU_ERR_UNSUPPORTED for fp32).
+ * The prefix keys are processed in chunks of 512 (one work item per
+ * candidate block and chunk, so small microbatches still fill the device)
+ * whose fp32 partial outputs are added in chunk order: a candidate's
+ * output does not depend on the other candidates of the call, bit for bit.
+ * ws: hstu_attn_fwd_cached_workspace_bytes(p) bytes (not the
+ * hstu_workspace_bytes of the uncached calls), 256-byte aligned. */
+size_t hstu_attn_fwd_cached_workspace_bytes(const hstu_problem_t* p);
+
 hstu_status_t hstu_attn_fwd_cached(const hstu_problem_t* p, const hstu_jagged_t* j,
                                    const void* q, int64_t q_stride,
                                    const void* k, int64_t k_stride,

@@ -177,6 +177,32 @@ hstu_status_t check_ws(const hstu_problem_t* p, void* ws, size_t ws_bytes, Layou
   return HSTU_OK;
 }
 
+// Workspace of the cached candidate pass: its own work list (one item per
+// candidate block and prefix-key chunk) and the fp32 partial outputs, one
+// slot of [T][h][d_v] per chunk.
+struct CachedLayout {
+  size_t counts, items, trange, partial, total;
+  int64_t max_items;
+  int32_t chunks;
+};
+
+CachedLayout cached_layout(const hstu_problem_t* p) {
+  CachedLayout l;
+  l.chunks = (p->max_seq_len + kCrossChunk - 1) / kCrossChunk;
+  l.max_items = max_work_items(p->total_tokens, p->num_seqs, kFwdBM) * l.chunks;
+  size_t off = 0;
+  l.counts = off;
+  off = align_up(off + 2 * sizeof(int32_t));
+  l.items = off;
+  off = align_up(off + sizeof(WorkItem) * (size_t)l.max_items);
+  l.trange = off;
+  off = align_up(off + 2 * sizeof(int64_t) * (size_t)p->num_seqs);
+  l.partial = off;
+  off = align_up(off + sizeof(float) * (size_t)l.chunks * p->total_tokens * p->num_heads * p->d_v);
+  l.total = off;
+  return l;
+}
+
 JaggedArgs make_args(const hstu_problem_t* p, const hstu_jagged_t* j) {
   JaggedArgs a;
   a.seq_offsets = j->seq_offsets;
@@ -187,6 +213,8 @@ JaggedArgs make_args(const hstu_problem_t* p, const hstu_jagged_t* j) {
   a.seq_trange = nullptr;
   a.key_offsets = nullptr;
   a.key_timestamps = nullptr;
+  a.key_chunks = 0;
+  a.chunk_stride = 0;
   a.num_seqs = p->num_seqs;
   a.max_seq_len = p->max_seq_len;
   a.num_heads = p->num_heads;
@@ -647,6 +675,15 @@ hstu_status_t hstu_attn_fwd(const hstu_problem_t* p, const hstu_jagged_t* j, con
   }
 }
 
+size_t hstu_attn_fwd_cached_workspace_bytes(const hstu_problem_t* p) {
+  try {
+    if (check_problem(p) != HSTU_OK) return 0;
+    return cached_layout(p).total;
+  } catch (...) {
+    return 0;
+  }
+}
+
 hstu_status_t hstu_attn_fwd_cached(const hstu_problem_t* p, const hstu_jagged_t* j, const void* q,
                                    int64_t q_stride, const void* k, int64_t k_stride,
                                    const void* v, int64_t v_stride, const int64_t* cache_offsets,
@@ -672,29 +709,33 @@ hstu_status_t hstu_attn_fwd_cached(const hstu_problem_t* p, const hstu_jagged_t*
       HSTU_TRY(check_rows(p, "k_cache", k_cache, kc_stride, (int64_t)H * p->d_qk));
       HSTU_TRY(check_rows(p, "v_cache", v_cache, vc_stride, (int64_t)H * p->d_v));
     }
-    Layout l;
-    HSTU_TRY(check_ws(p, ws, ws_bytes, &l));
+    const CachedLayout l = cached_layout(p);
+    if (!ws) return fail(HSTU_ERR_WORKSPACE, "workspace is NULL (need %zu bytes)", l.total);
+    if ((uintptr_t)ws % kAlign) return fail(HSTU_ERR_WORKSPACE, "workspace must be 256-byte aligned");
+    if (ws_bytes < l.total)
+      return fail(HSTU_ERR_WORKSPACE, "workspace too small: %zu < %zu bytes", ws_bytes, l.total);
     const int64_t T = p->total_tokens;
     if (T == 0) return ok();
     JaggedArgs ja = make_args(p, j);
     ja.num_targets = nullptr;
     ja.key_offsets = cache_offsets;
     ja.key_timestamps = cache_timestamps;
+    ja.key_chunks = l.chunks;
+    ja.chunk_stride = T * H * p->d_v;
     char* w = (char*)ws;
     int32_t* counts = (int32_t*)(w + l.counts);
-    WorkItem* items = (WorkItem*)(w + l.fwd_items);
-    float* o32 = (float*)(w + l.dout);  // fp32 partial output (history keys only)
+    WorkItem* items = (WorkItem*)(w + l.items);
+    float* o32 = (float*)(w + l.partial);  // fp32 partial outputs, one slot per key chunk
     ja.seq_trange = (const int64_t*)(w + l.trange);
     HSTU_HIP(launch_seq_time_range(ja, (int64_t*)(w + l.trange), s), "time range launch");
     HSTU_HIP(launch_schedule(ja, 0, items, counts, s), "schedule launch");
     TimedScope ts("attn_fwd_cached", s);
     const Tensors keys{q, q_stride, k_cache, kc_stride, v_cache, vc_stride};
-    HSTU_HIP(launch_attn_fwd_bf16(ja, keys, p->d_qk, p->d_v, o32, 1, 0, items, counts, l.max_fwd,
+    HSTU_HIP(launch_attn_fwd_bf16(ja, keys, p->d_qk, p->d_v, o32, 1, 0, items, counts, l.max_items,
                                   s),
              "attn_fwd_cached launch");
     const Tensors cand{q, q_stride, k, k_stride, v, v_stride};
-    HSTU_HIP(launch_cached_self(1, T, H, p->d_qk, p->d_v, cand, j->rab_pos, j->rab_time,
-                                p->max_seq_len, o32, out, s),
+    HSTU_HIP(launch_cached_self(1, ja, p->d_qk, p->d_v, cand, o32, out, s),
              "cached self-term launch");
     return ok();
   } catch (...) {

@@ -101,7 +101,7 @@ template <int DQK, int DV, bool FAST, bool SPLIT>
 __device__ __forceinline__ void fwd_item(FwdShared<DQK, DV>& sm, const JaggedArgs& ja,
                                          const Tensors& t, void* __restrict__ out, int out_f32,
                                          int64_t orow, int64_t okey, int L, int n_h, int key_lim,
-                                         int i0, int head, int64_t tbase) {
+                                         int kt0, int kt1, int i0, int head, int64_t tbase) {
   using Sh = FwdShared<DQK, DV>;
   constexpr int BM = Sh::BM, BN = Sh::BN, K_LD = Sh::K_LD, V_LD = Sh::V_LD;
   constexpr int KCH = BN * DQK / 8, VCH = BN * DV / 8;
@@ -145,15 +145,16 @@ __device__ __forceinline__ void fwd_item(FwdShared<DQK, DV>& sm, const JaggedArg
 #pragma unroll
     for (int q = 0; q < 16; q++) oacc[nb][q] = 0.0f;
 
-  // Key tiles visited: [0, nA) then [bstart, kend).  Tiles made only of
-  // candidates that precede every row of the block are fully masked and
-  // skipped.
+  // Key tiles visited: history tiles [kt0, min(kt1, kend)), then
+  // candidate tiles [bstart, kend).  Tiles made only of candidates that
+  // precede every row of the block are fully masked and skipped.  Self
+  // mode passes [0, all history tiles); cross mode one chunk of the prefix.
   const int kend = (min(rows_end, key_lim) + BN - 1) / BN;
   const int nh_blk = (n_h + BN - 1) / BN;
-  const int nA = min(nh_blk, kend);
+  const int nA = max(0, min(kt1, kend) - kt0);
   const int bstart = max(nh_blk, i0 / BN);
   const int n = nA + max(0, kend - bstart);
-  auto kb_of = [&](int u) { return u < nA ? u : bstart + (u - nA); };
+  auto kb_of = [&](int u) { return u < nA ? kt0 + u : bstart + (u - nA); };
   auto pos_base_of = [&](int j0) { return (N - 1) + min(j0, n_h) - R; };
 
   const int tr_row = 4 * (lane >> 5) + ((lane & 15) >> 2);
@@ -576,15 +577,23 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_bf16_kernel(JaggedArgs ja, Te
   // Self-attention: rows and keys are the sequence's L tokens.  Cross mode:
   // the rows are its candidates, virtual positions n_h .. n_h + Lr - 1
   // after the n_h keys of its cached prefix.
+  // Cross mode splits the prefix keys into chunks of kCrossChunk, one item
+  // each, whose fp32 partial outputs go to separate slots.
   int64_t orow = o, okey = o;
   int L = Lr, n_h = Lr - (ja.num_targets ? (int)ja.num_targets[it.seq] : 0), key_lim = Lr, i0;
+  int kt0 = 0, kt1 = (n_h + Sh::BN - 1) / Sh::BN;
+  void* outp = out;
   if (ja.key_offsets) {
     okey = ja.key_offsets[it.seq];
     n_h = (int)(ja.key_offsets[it.seq + 1] - okey);
     L = n_h + Lr;
     orow = o - n_h;
     key_lim = n_h;
-    i0 = n_h + it.blk * Sh::BM;
+    const int qb = it.blk / ja.key_chunks, ch = it.blk - qb * ja.key_chunks;
+    i0 = n_h + qb * Sh::BM;
+    kt0 = ch * (kCrossChunk / Sh::BN);
+    kt1 = min((n_h + Sh::BN - 1) / Sh::BN, kt0 + kCrossChunk / Sh::BN);
+    outp = (float*)out + (int64_t)ch * ja.chunk_stride;
   } else {
     i0 = it.blk * Sh::BM;
   }
@@ -600,11 +609,11 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_bf16_kernel(JaggedArgs ja, Te
     sm.sTab[x] = (fast && x == 31) ? ja.rab_time[0] : ja.rab_time[min(63 - x, NB - 1)];
   __syncthreads();
   if (fast) {
-    fwd_item<DQK, DV, true, SPLIT>(sm, ja, t, out, out_f32, orow, okey, L, n_h, key_lim, i0, head,
-                                   tlo);
+    fwd_item<DQK, DV, true, SPLIT>(sm, ja, t, outp, out_f32, orow, okey, L, n_h, key_lim, kt0, kt1,
+                                   i0, head, tlo);
   } else {
-    fwd_item<DQK, DV, false, SPLIT>(sm, ja, t, out, out_f32, orow, okey, L, n_h, key_lim, i0, head,
-                                    tlo);
+    fwd_item<DQK, DV, false, SPLIT>(sm, ja, t, outp, out_f32, orow, okey, L, n_h, key_lim, kt0, kt1,
+                                    i0, head, tlo);
   }
 }
 
@@ -622,32 +631,46 @@ hipError_t launch_fwd(const JaggedArgs& ja, const Tensors& t, void* out, int out
   return hipGetLastError();
 }
 
-// Self term of the cached candidate pass: the cross-mode kernel leaves out
+// Self term of the cached candidate pass: the cross-mode items leave out
 // each candidate's own key (position n_h, dt = 0, so rab = rab_pos[N-1] +
-// rab_time[0]); one wave per (row, head) adds SiLU(q.k + rab) v / N to
-// the fp32 partial output and stores the result once.
+// rab_time[0]).  One wave per (row, head) finds the row's sequence, adds
+// the fp32 partials of its key chunks in chunk order, then
+// SiLU(q.k + rab) v / N, and stores the result once.
 template <bool BF16>
-__global__ __launch_bounds__(256) void cached_self_kernel(int64_t T, int H, int dqk, int dv,
-                                                          Tensors t, const float* rab_pos,
-                                                          const float* rab_time, int N,
+__global__ __launch_bounds__(256) void cached_self_kernel(JaggedArgs ja, int dqk, int dv,
+                                                          Tensors t,
                                                           const float* __restrict__ o32,
                                                           void* __restrict__ out) {
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int H = ja.num_heads, N = ja.max_seq_len;
   const int64_t w = (int64_t)blockIdx.x * 4 + wave;
-  if (w >= T * H) return;
+  if (w >= ja.total_tokens * H) return;
   const int64_t row = w / H;
   const int h = (int)(w - row * H);
+  // Sequence of the row: the largest b with seq_offsets[b] <= row.
+  int lo = 0, hi = ja.num_seqs - 1;
+  while (lo < hi) {
+    const int mid = (lo + hi + 1) >> 1;
+    if (ja.seq_offsets[mid] <= row)
+      lo = mid;
+    else
+      hi = mid - 1;
+  }
+  const int n_h = (int)(ja.key_offsets[lo + 1] - ja.key_offsets[lo]);
+  const int nch = min((n_h + kCrossChunk - 1) / kCrossChunk, ja.key_chunks);
   auto ld = [&](const void* base, int64_t stride, int dim, int c) -> float {
     const int64_t idx = row * stride + (int64_t)h * dim + c;
     return BF16 ? bf16_bits_to_f32(((const uint16_t*)base)[idx]) : ((const float*)base)[idx];
   };
   float part = 0.0f;
   for (int c = lane; c < dqk; c += 64) part += ld(t.q, t.q_stride, dqk, c) * ld(t.k, t.k_stride, dqk, c);
-  const float x = wave_sum_f32(part) + rab_pos[N - 1] + rab_time[0];
+  const float x = wave_sum_f32(part) + ja.rab_pos[N - 1] + ja.rab_time[0];
   const float pN = silu(x) / (float)N;
   for (int c = lane; c < dv; c += 64) {
     const int64_t oi = (row * H + h) * dv + c;
-    const float y = o32[oi] + pN * ld(t.v, t.v_stride, dv, c);
+    float y = 0.0f;
+    for (int ch = 0; ch < nch; ch++) y += o32[(int64_t)ch * ja.chunk_stride + oi];
+    y += pN * ld(t.v, t.v_stride, dv, c);
     if constexpr (BF16)
       ((uint16_t*)out)[oi] = f32_to_bf16_bits(y);
     else
@@ -657,18 +680,15 @@ __global__ __launch_bounds__(256) void cached_self_kernel(int64_t T, int H, int 
 
 }  // namespace
 
-hipError_t launch_cached_self(int is_bf16, int64_t T, int32_t H, int32_t dqk, int32_t dv,
-                              const Tensors& t, const float* rab_pos, const float* rab_time,
-                              int32_t N, const float* o32, void* out, hipStream_t s) {
-  const int64_t waves = T * H;
+hipError_t launch_cached_self(int is_bf16, const JaggedArgs& ja, int32_t dqk, int32_t dv,
+                              const Tensors& t, const float* o32, void* out, hipStream_t s) {
+  const int64_t waves = ja.total_tokens * ja.num_heads;
   if (waves <= 0) return hipSuccess;
   const dim3 grid((unsigned)((waves + 3) / 4));
   if (is_bf16)
-    hipLaunchKernelGGL(cached_self_kernel<true>, grid, dim3(256), 0, s, T, H, dqk, dv, t, rab_pos,
-                       rab_time, N, o32, out);
+    hipLaunchKernelGGL(cached_self_kernel<true>, grid, dim3(256), 0, s, ja, dqk, dv, t, o32, out);
   else
-    hipLaunchKernelGGL(cached_self_kernel<false>, grid, dim3(256), 0, s, T, H, dqk, dv, t, rab_pos,
-                       rab_time, N, o32, out);
+    hipLaunchKernelGGL(cached_self_kernel<false>, grid, dim3(256), 0, s, ja, dqk, dv, t, o32, out);
   return hipGetLastError();
 }
 

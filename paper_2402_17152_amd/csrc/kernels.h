@@ -25,6 +25,11 @@ struct JaggedArgs {
   // key_timestamps); null for self-attention over seq_offsets.
   const int64_t* key_offsets;
   const int64_t* key_timestamps;
+  // Cross mode: the prefix keys of a candidate block are split into chunks
+  // of kCrossChunk keys, one work item each (blk = q-block * key_chunks +
+  // chunk); chunk c writes its fp32 partial output at out + c * chunk_stride.
+  int32_t key_chunks;
+  int64_t chunk_stride;
   int32_t num_seqs;
   int32_t max_seq_len;  // N
   int32_t num_heads;
@@ -44,6 +49,7 @@ struct Tensors {
 // Tile sizes of the bf16 MFMA kernels.
 constexpr int kFwdBM = 128;  // query rows per forward workgroup
 constexpr int kFwdBN = 32;   // keys per forward step
+constexpr int kCrossChunk = 512;  // prefix keys per cross-mode work item (16 steps)
 constexpr int kBwdBN = 128;  // keys owned by a backward workgroup (4 waves x 32)
 constexpr int kBwdBM = 32;   // query rows per backward step
 constexpr size_t kLdsBytes = 160 * 1024;  // LDS a gfx950 workgroup may allocate
@@ -79,11 +85,13 @@ hipError_t launch_bucketize(int32_t num_seqs, int64_t total_tokens, int32_t num_
 hipError_t launch_attn_fwd_bf16(const JaggedArgs& ja, const Tensors& t, int dqk, int dv, void* out,
                                 int out_f32, int split, const WorkItem* items,
                                 const int32_t* count, int64_t max_items, hipStream_t s);
-// The self term of the cached candidate pass: out = o32 + SiLU(q.k +
-// rab_pos[N-1] + rab_time[0]) v / N per (row, head), in bf16 or fp32.
-hipError_t launch_cached_self(int is_bf16, int64_t T, int32_t H, int32_t dqk, int32_t dv,
-                              const Tensors& t, const float* rab_pos, const float* rab_time,
-                              int32_t N, const float* o32, void* out, hipStream_t s);
+// The self term of the cached candidate pass: out = (sum over the row's
+// key chunks, in order, of the fp32 partials at o32 + c * ja.chunk_stride)
+// + SiLU(q.k + rab_pos[N-1] + rab_time[0]) v / N per (row, head), in bf16
+// or fp32.  ja: the cross-mode arguments (seq_offsets of the candidates,
+// key_offsets, key_chunks, chunk_stride, num_seqs, max_seq_len, rab tables).
+hipError_t launch_cached_self(int is_bf16, const JaggedArgs& ja, int32_t dqk, int32_t dv,
+                              const Tensors& t, const float* o32, void* out, hipStream_t s);
 // d_out_lo: null, or the low bf16 terms of dO (d_out holding the high
 // ones), for a dO that is the fp32 output of the layer's LayerNorm backward.
 hipError_t launch_attn_bwd_bf16(const JaggedArgs& ja, const Tensors& t, int dqk, int dv,

@@ -28,9 +28,11 @@ __device__ __forceinline__ int fwd_weight(int L, int n_h, int qb) {
   return kend - skipped;
 }
 
-// Cross-mode forward item: every candidate block visits the n_h keys of
-// its cached prefix.
-__device__ __forceinline__ int cross_weight(int n_h) { return ceil_div(n_h, kFwdBN); }
+// Cross-mode forward item: key chunk c of a candidate block visits keys
+// [c kCrossChunk, min(n_h, (c + 1) kCrossChunk)) of the cached prefix.
+__device__ __forceinline__ int cross_weight(int n_h, int c) {
+  return ceil_div(min(kCrossChunk, n_h - c * kCrossChunk), kFwdBN);
+}
 
 // Backward item (k-block kb): number of query steps of kBwdBM rows.
 __device__ __forceinline__ int bwd_weight(int L, int n_h, int kb) {
@@ -47,7 +49,7 @@ __global__ __launch_bounds__(kSchedThreads) void schedule_kernel(JaggedArgs ja, 
   const int tid = threadIdx.x;
   const int blk = mode == 0 ? kFwdBM : kBwdBN;
   const int maxw = mode == 0 ? ceil_div(ja.max_seq_len, kFwdBN) : ceil_div(ja.max_seq_len, kBwdBM);
-  // (cross mode: a candidate block's weight ceil(n_h / kFwdBN) <= maxw since n_h < N)
+  // (cross mode: a chunk's weight is at most kCrossChunk / kFwdBN <= maxw)
   const int nbins = maxw + 1;
   for (int i = tid; i < nbins; i += kSchedThreads) s_bins[i] = 0;
   __syncthreads();
@@ -60,11 +62,14 @@ __global__ __launch_bounds__(kSchedThreads) void schedule_kernel(JaggedArgs ja, 
     const bool cross = mode == 0 && ja.key_offsets;
     if (cross) n_h = (int)(ja.key_offsets[b + 1] - ja.key_offsets[b]);
     int nblk = ceil_div(L, blk);
-    for (int x = 0; x < nblk; x++) {
-      int w = cross ? cross_weight(n_h) : mode == 0 ? fwd_weight(L, n_h, x) : bwd_weight(L, n_h, x);
-      w = min(max(w, 0), maxw);
-      atomicAdd(&s_bins[maxw - w], 1);
-    }
+    // (chunks past key_chunks exist only if n_h >= N: they are not scheduled)
+    const int nch = cross ? min(ceil_div(n_h, kCrossChunk), ja.key_chunks) : 1;
+    for (int x = 0; x < nblk; x++)
+      for (int c = 0; c < nch; c++) {
+        int w = cross ? cross_weight(n_h, c) : mode == 0 ? fwd_weight(L, n_h, x) : bwd_weight(L, n_h, x);
+        w = min(max(w, 0), maxw);
+        atomicAdd(&s_bins[maxw - w], 1);
+      }
   }
   __syncthreads();
 
@@ -97,15 +102,18 @@ __global__ __launch_bounds__(kSchedThreads) void schedule_kernel(JaggedArgs ja, 
     const bool cross = mode == 0 && ja.key_offsets;
     if (cross) n_h = (int)(ja.key_offsets[b + 1] - ja.key_offsets[b]);
     int nblk = ceil_div(L, blk);
-    for (int x = 0; x < nblk; x++) {
-      int w = cross ? cross_weight(n_h) : mode == 0 ? fwd_weight(L, n_h, x) : bwd_weight(L, n_h, x);
-      w = min(max(w, 0), maxw);
-      int pos = atomicAdd(&s_bins[maxw - w], 1);
-      WorkItem it;
-      it.seq = b;
-      it.blk = x;
-      items[pos] = it;
-    }
+    // (chunks past key_chunks exist only if n_h >= N: they are not scheduled)
+    const int nch = cross ? min(ceil_div(n_h, kCrossChunk), ja.key_chunks) : 1;
+    for (int x = 0; x < nblk; x++)
+      for (int c = 0; c < nch; c++) {
+        int w = cross ? cross_weight(n_h, c) : mode == 0 ? fwd_weight(L, n_h, x) : bwd_weight(L, n_h, x);
+        w = min(max(w, 0), maxw);
+        int pos = atomicAdd(&s_bins[maxw - w], 1);
+        WorkItem it;
+        it.seq = b;
+        it.blk = cross ? x * ja.key_chunks + c : x;
+        items[pos] = it;
+      }
   }
 }
 

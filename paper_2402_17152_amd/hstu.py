@@ -26,7 +26,8 @@ EXPORTED = ("hstu_workspace_bytes", "hstu_attn_fwd", "hstu_attn_bwd", "hstu_laye
             "hstu_time_bucketize", "hstu_complete_cumsum", "hstu_pair_offsets", "hstu_validate",
             "hstu_last_error", "hstu_abi_version", "hstu_timing_enable", "hstu_timing_read",
             "hstu_timing_reset", "hstu_probe_mfma_bf16", "hstu_layer_bwd",
-            "hstu_attn_fwd_cached", "hstu_proj_workspace_bytes", "hstu_proj_in_fwd",
+            "hstu_attn_fwd_cached", "hstu_attn_fwd_cached_workspace_bytes",
+            "hstu_proj_workspace_bytes", "hstu_proj_in_fwd",
             "hstu_proj_out_fwd", "hstu_proj_out_bwd", "hstu_proj_in_bwd",
             "hstu_sl_subseq_len", "hstu_sl_workspace_bytes", "hstu_stochastic_length",
             "hstu_gather_rows", "hstu_sl_sparsity")
@@ -80,6 +81,7 @@ def _load():
         "hstu_timing_reset": (i32, []),
         "hstu_probe_mfma_bf16": (i32, [i32, i32, P, ctypes.POINTER(ctypes.c_double), P]),
         "hstu_proj_workspace_bytes": (sz, [PP, i32]),
+        "hstu_attn_fwd_cached_workspace_bytes": (sz, [PP]),
         "hstu_sl_subseq_len": (i32, [i32, ctypes.c_double]),
         "hstu_sl_workspace_bytes": (sz, [i32]),
         "hstu_stochastic_length": (i32, [i32, P, P, P, i32, i32, P, P, P, P, P, sz, P]),
@@ -193,6 +195,17 @@ def hstu_attn_fwd(q, k, v, seq_offsets, timestamps, rab_pos, rab_time, max_seq_l
     return out
 
 
+def hstu_attn_fwd_cached_workspace_bytes(problem: Problem) -> int:
+    return int(lib.hstu_attn_fwd_cached_workspace_bytes(ctypes.byref(problem)))
+
+
+def cached_workspace(problem: Problem, device=None) -> torch.Tensor:
+    n = hstu_attn_fwd_cached_workspace_bytes(problem)
+    if n == 0:
+        raise HstuError(1, "invalid problem")
+    return torch.empty(n, dtype=torch.uint8, device=device or "cuda")
+
+
 def hstu_attn_fwd_cached(q, k, v, seq_offsets, timestamps, k_cache, v_cache, cache_offsets,
                          cache_timestamps, rab_pos, rab_time, max_seq_len, out=None, ws=None,
                          stream=None):
@@ -204,7 +217,7 @@ def hstu_attn_fwd_cached(q, k, v, seq_offsets, timestamps, k_cache, v_cache, cac
     if out is None:
         out = torch.empty((q.shape[0], q.shape[1], v.shape[2]), dtype=q.dtype, device=q.device)
     if ws is None:
-        ws = workspace(p, q.device)
+        ws = cached_workspace(p, q.device)
     _check(lib.hstu_attn_fwd_cached(ctypes.byref(p), ctypes.byref(j), _ptr(q), _row_stride(q),
                                     _ptr(k), _row_stride(k), _ptr(v), _row_stride(v),
                                     _ptr(cache_offsets), _ptr(cache_timestamps),
