@@ -9,9 +9,9 @@
 // forward) or k-major (A[k][m], B[k][n]: the transposed operands of the
 // gradients).  A workgroup of 4 waves computes a 256 x 128 tile, each wave
 // 128 x 64 (8 accumulator tiles), over k-steps of 32 staged in LDS (double
-// buffered, one barrier per step, the next step's global loads in flight
-// during the current step's MFMAs); two workgroups share a CU, so one's
-// epilogue and staging overlap the other's matrix-core work.  A k-contiguous tile gives a
+// buffered, one barrier per step; global loads run two steps ahead through
+// two register sets); two workgroups share a CU, so one's epilogue and
+// staging overlap the other's matrix-core work.  A k-contiguous tile gives a
 // lane its 8 contraction elements in one 16-byte LDS read; a k-major tile
 // is read with two transposing reads (ds_read_b64_tr_b16) that return the
 // same 8 elements in the same order.  The products are computed
@@ -135,21 +135,12 @@ __global__ __launch_bounds__(256, 2) void gemm_bf16_kernel(GemmArgs g) {
 #pragma unroll
       for (int q = 0; q < 16; q++) acc[i][j][q] = 0.0f;
 
-  u32x4 ra[SA::kPer], rb[SB::kPer];
-  if (nk > 0) {
-    sa.load(ra, kb, tid);
-    sb.load(rb, kb, tid);
-    SA::store(sm.a[0], ra, tid);
-    SB::store(sm.b[0], rb, tid);
-  }
-  __syncthreads();
-  for (int kt = 0; kt < nk; kt++) {
-    const int cur = kt & 1;
-    const bool more = kt + 1 < nk;
-    if (more) {
-      sa.load(ra, kb + (kt + 1) * kGBK, tid);
-      sb.load(rb, kb + (kt + 1) * kGBK, tid);
-    }
+  // Two register sets stage k-steps two ahead: while step kt is computed
+  // from LDS, the loads of step kt + 2 go into the set that step kt came
+  // through, and the set holding step kt + 1 (loaded during step kt - 1)
+  // is written to the other LDS buffer.
+  u32x4 ra0[SA::kPer], rb0[SB::kPer], ra1[SA::kPer], rb1[SB::kPer];
+  auto compute = [&](int cur) {
     const uint16_t* ta = sm.a[cur];
     const uint16_t* tb = sm.b[cur];
     // Both contraction blocks' operands are read before the first MFMA.
@@ -168,12 +159,39 @@ __global__ __launch_bounds__(256, 2) void gemm_bf16_kernel(GemmArgs g) {
 #pragma unroll
         for (int j = 0; j < 2; j++)
           acc[i][j] = mfma32x32x16(as_bf16x8(bf[s][j]), as_bf16x8(af[s][i]), acc[i][j]);
-    if (more) {
-      SA::store(sm.a[cur ^ 1], ra, tid);
-      SB::store(sm.b[cur ^ 1], rb, tid);
+  };
+  // One k-step: ra/rb_free receive step kt + 2, ra/rb_next (step kt + 1)
+  // go to LDS buffer (kt + 1) & 1.
+  auto kstep = [&](int kt, u32x4 (&ra_free)[SA::kPer], u32x4 (&rb_free)[SB::kPer],
+                   u32x4 (&ra_next)[SA::kPer], u32x4 (&rb_next)[SB::kPer]) {
+    if (kt + 2 < nk) {
+      sa.load(ra_free, kb + (kt + 2) * kGBK, tid);
+      sb.load(rb_free, kb + (kt + 2) * kGBK, tid);
+    }
+    compute(kt & 1);
+    if (kt + 1 < nk) {
+      SA::store(sm.a[(kt + 1) & 1], ra_next, tid);
+      SB::store(sm.b[(kt + 1) & 1], rb_next, tid);
     }
     __syncthreads();
+  };
+  if (nk > 0) {
+    sa.load(ra0, kb, tid);
+    sb.load(rb0, kb, tid);
+    if (nk > 1) {
+      sa.load(ra1, kb + kGBK, tid);
+      sb.load(rb1, kb + kGBK, tid);
+    }
+    SA::store(sm.a[0], ra0, tid);
+    SB::store(sm.b[0], rb0, tid);
   }
+  __syncthreads();
+  int kt = 0;
+  for (; kt + 1 < nk; kt += 2) {
+    kstep(kt, ra0, rb0, ra1, rb1);      // step kt came through set 0
+    kstep(kt + 1, ra1, rb1, ra0, rb0);  // step kt + 1 through set 1
+  }
+  if (kt < nk) kstep(kt, ra0, rb0, ra1, rb1);
 
   // Epilogue, per group of 32 rows: the wave writes its 32 x 64 fp32 block
   // to a private LDS region (acc[i][j] register 4 g4 + e is row lane % 32,
