@@ -360,7 +360,7 @@ def cpu_baseline(batch, flops_full):
 def main():
     args = parse()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
-        print("bench.py: this build runs on exactly one GPU (the path shards by sequence and "
+        print("bench.py: the library runs on exactly one GPU (the path shards by sequence and "
               "needs no collective until the bias-gradient all-reduce, which is not built); "
               f"--gpus {args.gpus} is not supported", file=sys.stderr)
         sys.exit(2)

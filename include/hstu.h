@@ -71,7 +71,7 @@ extern "C" {
 typedef enum {
   HSTU_OK = 0,
   HSTU_ERR_INVALID_ARGUMENT = 1, /* null pointer, bad size or stride      */
-  HSTU_ERR_UNSUPPORTED = 2,      /* a shape this build has no kernel for  */
+  HSTU_ERR_UNSUPPORTED = 2,      /* a shape the library has no kernel for */
   HSTU_ERR_WORKSPACE = 3,        /* workspace missing or too small        */
   HSTU_ERR_HIP = 4,              /* a HIP runtime call failed             */
   HSTU_ERR_DATA = 5              /* hstu_validate found bad device data   */
