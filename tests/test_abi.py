@@ -134,3 +134,88 @@ def test_other_entry_points_validate(hs):
                               P(FAKE), 512, P(FAKE), P(FAKE), P(FAKE), None, P(FAKE), P(FAKE),
                               P(FAKE), 1 << 40, None)
     assert st == 1 and "dv" in hs.hstu_last_error()
+
+
+def test_projection_entry_points_validate(hs):
+    """f_1 / f_2 calls reject bad shapes, pointers and workspaces on the host."""
+    P = ctypes.c_void_p
+    p = _problem(hs, num_heads=8, d_qk=64, d_v=64, total_tokens=1000)
+    pf = _problem(hs, num_heads=8, d_qk=64, d_v=64, total_tokens=1000, dtype=hs.HSTU_F32)
+    L = hs.lib
+    assert L.hstu_proj_workspace_bytes(ctypes.byref(p), 512) > 0
+    assert L.hstu_proj_workspace_bytes(ctypes.byref(p), 96) == 0     # bf16: multiple of 64
+    assert L.hstu_proj_workspace_bytes(ctypes.byref(pf), 12) == 0    # multiple of 8
+    assert L.hstu_proj_workspace_bytes(ctypes.byref(pf), 24) > 0
+    cases = [
+        (lambda: L.hstu_proj_in_fwd(ctypes.byref(p), 96, P(FAKE), 96, P(FAKE), None, P(FAKE), None,
+                                    None), 2, "multiples of 64"),
+        (lambda: L.hstu_proj_in_fwd(ctypes.byref(pf), 12, P(FAKE), 12, P(FAKE), None, P(FAKE), None,
+                                    None), 2, "multiple of 8"),
+        (lambda: L.hstu_proj_in_fwd(ctypes.byref(p), 512, None, 512, P(FAKE), None, P(FAKE), None,
+                                    None), 1, "x is NULL"),
+        (lambda: L.hstu_proj_in_fwd(ctypes.byref(p), 512, P(FAKE), 256, P(FAKE), None, P(FAKE), None,
+                                    None), 1, "x_stride"),
+        (lambda: L.hstu_proj_in_fwd(ctypes.byref(p), 512, P(FAKE), 512, P(FAKE), P(FAKE + 4),
+                                    P(FAKE), None, None), 1, "b1"),
+        (lambda: L.hstu_proj_out_fwd(ctypes.byref(p), 512, P(FAKE), 512, P(FAKE), None, None, None,
+                                     None), 1, "y is NULL"),
+        (lambda: L.hstu_proj_out_bwd(ctypes.byref(p), 512, P(FAKE), 512, P(FAKE), P(FAKE), P(FAKE),
+                                     P(FAKE), None, None, 0, None), 3, "workspace"),
+        (lambda: L.hstu_proj_in_bwd(ctypes.byref(p), 512, P(FAKE), 512, P(FAKE), P(FAKE), P(FAKE),
+                                    P(FAKE), P(FAKE), None, None, P(FAKE), P(FAKE), None, P(FAKE),
+                                    100, None), 1, "dk is NULL"),
+        (lambda: L.hstu_proj_in_bwd(ctypes.byref(p), 512, P(FAKE), 512, P(FAKE), P(FAKE), P(FAKE),
+                                    P(FAKE), P(FAKE), P(FAKE), None, P(FAKE), P(FAKE), None, P(FAKE),
+                                    100, None), 3, "too small"),
+    ]
+    big = _problem(hs, num_heads=8, d_qk=64, d_v=64, total_tokens=600000)  # T*F*2 >= 2^31
+    cases.append((lambda: L.hstu_proj_in_fwd(ctypes.byref(big), 512, P(FAKE), 512, P(FAKE), None,
+                                             P(FAKE), None, None), 2, "2 GiB"))
+    for call, status, needle in cases:
+        assert call() == status, needle
+        assert needle in hs.hstu_last_error(), (needle, hs.hstu_last_error())
+
+
+def test_stochastic_length_entry_points_validate(hs):
+    P = ctypes.c_void_p
+    L = hs.lib
+    assert hs.hstu_sl_workspace_bytes(0) == 0 and hs.hstu_sl_workspace_bytes(64) > 0
+    assert hs.hstu_sl_subseq_len(4096, 2.5) == 0 and hs.hstu_sl_subseq_len(0, 1.6) == 0
+
+    def sl(B=8, Ls=16, mode=1, e=FAKE, ws=FAKE, wsb=1 << 20, offs=FAKE):
+        return L.hstu_stochastic_length(B, P(offs), P(FAKE), None, Ls, mode, P(FAKE),
+                                        P(e) if e else None, P(FAKE), P(FAKE), P(ws) if ws else None,
+                                        wsb, None)
+    for kw, status, needle in ((dict(B=0), 1, "num_seqs"), (dict(Ls=0), 1, "subseq_len"),
+                               (dict(mode=5), 1, "selection"), (dict(e=None), 1, "e_rand"),
+                               (dict(offs=0), 1, "NULL"), (dict(ws=None), 3, "workspace"),
+                               (dict(wsb=16), 3, "too small"), (dict(ws=FAKE + 64), 3, "aligned")):
+        assert sl(**kw) == status, kw
+        assert needle in hs.hstu_last_error(), (needle, hs.hstu_last_error())
+    assert L.hstu_gather_rows(P(FAKE), 8, 6, P(FAKE), P(FAKE), 10, P(FAKE), 8, None) == 1
+    assert "4-byte" in hs.hstu_last_error()
+    assert L.hstu_gather_rows(P(FAKE), 4, 8, P(FAKE), P(FAKE), 10, P(FAKE), 8, None) == 1
+    assert "stride" in hs.hstu_last_error()
+    assert L.hstu_gather_rows(P(FAKE), 8, 8, P(FAKE), P(FAKE), 0, P(FAKE), 8, None) == 0
+    sp, s2 = ctypes.c_double(), ctypes.c_double()
+    assert L.hstu_sl_sparsity(0, P(FAKE), 16, ctypes.byref(sp), ctypes.byref(s2)) == 1
+
+
+def test_cached_pass_validates(hs):
+    P = ctypes.c_void_p
+    L = hs.lib
+    p = _problem(hs, num_seqs=16, total_tokens=4096, max_seq_len=3072)
+    pf = _problem(hs, num_seqs=16, total_tokens=4096, max_seq_len=3072, dtype=hs.HSTU_F32)
+    j = _jagged(hs)
+    assert L.hstu_attn_fwd_cached_workspace_bytes(ctypes.byref(p)) > 0
+    assert L.hstu_attn_fwd_cached_workspace_bytes(ctypes.byref(_problem(hs, d_qk=48))) == 0
+
+    def cached(pp=p, co=FAKE, ct=100, ws=FAKE, wsb=1 << 40):
+        return L.hstu_attn_fwd_cached(ctypes.byref(pp), ctypes.byref(j), P(FAKE), 512, P(FAKE), 512,
+                                      P(FAKE), 512, P(co) if co else None, P(FAKE), ct, P(FAKE), 512,
+                                      P(FAKE), 512, P(FAKE), P(ws) if ws else None, wsb, None)
+    for kw, status, needle in ((dict(pp=pf), 2, "bf16"), (dict(co=0), 1, "cache_offsets"),
+                               (dict(ct=-1), 1, "cache_tokens"), (dict(ws=None), 3, "workspace"),
+                               (dict(wsb=1000), 3, "too small")):
+        assert cached(**kw) == status, kw
+        assert needle in hs.hstu_last_error(), (needle, hs.hstu_last_error())
