@@ -54,23 +54,33 @@ __global__ __launch_bounds__(kSchedThreads) void schedule_kernel(JaggedArgs ja, 
   for (int i = tid; i < nbins; i += kSchedThreads) s_bins[i] = 0;
   __syncthreads();
 
-  // Pass 1: histogram of item weights (bin index = maxw - weight, so that
-  // an ascending scan orders items by descending weight).
-  for (int b = tid; b < ja.num_seqs; b += kSchedThreads) {
-    int L = (int)(ja.seq_offsets[b + 1] - ja.seq_offsets[b]);
-    int n_h = L - (ja.num_targets ? (int)ja.num_targets[b] : 0);
-    const bool cross = mode == 0 && ja.key_offsets;
-    if (cross) n_h = (int)(ja.key_offsets[b + 1] - ja.key_offsets[b]);
-    int nblk = ceil_div(L, blk);
-    // (chunks past key_chunks exist only if n_h >= N: they are not scheduled)
-    const int nch = cross ? min(ceil_div(n_h, kCrossChunk), ja.key_chunks) : 1;
-    for (int x = 0; x < nblk; x++)
-      for (int c = 0; c < nch; c++) {
+  // Sequences are handed to groups of G lanes (G a power of two up to a
+  // wave, larger for fewer sequences); a group's lanes share its items.
+  int G = 1;
+  while (G < 64 && G * ja.num_seqs < kSchedThreads) G <<= 1;
+  const int group = tid / G, sub = tid % G, ngroups = kSchedThreads / G;
+  // Calls f(seq, block, weight) for every item.
+  auto for_items = [&](auto&& f) {
+    for (int b = group; b < ja.num_seqs; b += ngroups) {
+      const int L = (int)(ja.seq_offsets[b + 1] - ja.seq_offsets[b]);
+      int n_h = L - (ja.num_targets ? (int)ja.num_targets[b] : 0);
+      const bool cross = mode == 0 && ja.key_offsets;
+      if (cross) n_h = (int)(ja.key_offsets[b + 1] - ja.key_offsets[b]);
+      const int nblk = ceil_div(L, blk);
+      // (chunks past key_chunks exist only if n_h >= N: they are not scheduled)
+      const int nch = cross ? min(ceil_div(n_h, kCrossChunk), ja.key_chunks) : 1;
+      for (int e = sub; e < nblk * nch; e += G) {
+        const int x = e / nch, c = e - x * nch;
         int w = cross ? cross_weight(n_h, c) : mode == 0 ? fwd_weight(L, n_h, x) : bwd_weight(L, n_h, x);
         w = min(max(w, 0), maxw);
-        atomicAdd(&s_bins[maxw - w], 1);
+        f(b, cross ? x * ja.key_chunks + c : x, w);
       }
-  }
+    }
+  };
+
+  // Pass 1: histogram of item weights (bin index = maxw - weight, so that
+  // an ascending scan orders items by descending weight).
+  for_items([&](int, int, int w) { atomicAdd(&s_bins[maxw - w], 1); });
   __syncthreads();
 
   // Exclusive scan of the bins: each thread owns a contiguous run.
@@ -96,25 +106,13 @@ __global__ __launch_bounds__(kSchedThreads) void schedule_kernel(JaggedArgs ja, 
   __syncthreads();
 
   // Pass 2: scatter the items to their sorted positions.
-  for (int b = tid; b < ja.num_seqs; b += kSchedThreads) {
-    int L = (int)(ja.seq_offsets[b + 1] - ja.seq_offsets[b]);
-    int n_h = L - (ja.num_targets ? (int)ja.num_targets[b] : 0);
-    const bool cross = mode == 0 && ja.key_offsets;
-    if (cross) n_h = (int)(ja.key_offsets[b + 1] - ja.key_offsets[b]);
-    int nblk = ceil_div(L, blk);
-    // (chunks past key_chunks exist only if n_h >= N: they are not scheduled)
-    const int nch = cross ? min(ceil_div(n_h, kCrossChunk), ja.key_chunks) : 1;
-    for (int x = 0; x < nblk; x++)
-      for (int c = 0; c < nch; c++) {
-        int w = cross ? cross_weight(n_h, c) : mode == 0 ? fwd_weight(L, n_h, x) : bwd_weight(L, n_h, x);
-        w = min(max(w, 0), maxw);
-        int pos = atomicAdd(&s_bins[maxw - w], 1);
-        WorkItem it;
-        it.seq = b;
-        it.blk = cross ? x * ja.key_chunks + c : x;
-        items[pos] = it;
-      }
-  }
+  for_items([&](int b, int x, int w) {
+    const int pos = atomicAdd(&s_bins[maxw - w], 1);
+    WorkItem it;
+    it.seq = b;
+    it.blk = x;
+    items[pos] = it;
+  });
 }
 
 __global__ void fill_f32_kernel(float* p, int64_t n, float value) {
