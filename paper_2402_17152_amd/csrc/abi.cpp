@@ -258,8 +258,8 @@ hstu_status_t attn_fwd_impl(const hstu_problem_t* p, const hstu_jagged_t* j, con
   int32_t* counts = (int32_t*)(w + l.counts);
   WorkItem* items = (WorkItem*)(w + l.fwd_items);
   ja.seq_trange = (const int64_t*)(w + l.trange);
-  HSTU_HIP(launch_seq_time_range(ja, (int64_t*)(w + l.trange), s), "time range launch");
-  HSTU_HIP(launch_schedule(ja, 0, items, counts, s), "schedule launch");
+  HSTU_HIP(launch_prep(ja, 0, items, counts, (int64_t*)(w + l.trange), PrepFills{}, s),
+           "prep launch");
   TimedScope ts("attn_fwd", s);
   HSTU_HIP(launch_attn_fwd_bf16(ja, t, p->d_qk, p->d_v, out, out_f32, out_f32, items, counts,
                                 l.max_fwd, s),
@@ -727,8 +727,8 @@ hstu_status_t hstu_attn_fwd_cached(const hstu_problem_t* p, const hstu_jagged_t*
     WorkItem* items = (WorkItem*)(w + l.items);
     float* o32 = (float*)(w + l.partial);  // fp32 partial outputs, one slot per key chunk
     ja.seq_trange = (const int64_t*)(w + l.trange);
-    HSTU_HIP(launch_seq_time_range(ja, (int64_t*)(w + l.trange), s), "time range launch");
-    HSTU_HIP(launch_schedule(ja, 0, items, counts, s), "schedule launch");
+    HSTU_HIP(launch_prep(ja, 0, items, counts, (int64_t*)(w + l.trange), PrepFills{}, s),
+             "prep launch");
     TimedScope ts("attn_fwd_cached", s);
     const Tensors keys{q, q_stride, k_cache, kc_stride, v_cache, vc_stride};
     HSTU_HIP(launch_attn_fwd_bf16(ja, keys, p->d_qk, p->d_v, o32, 1, 0, items, counts, l.max_items,
@@ -774,8 +774,10 @@ hstu_status_t attn_bwd_impl(const hstu_problem_t* p, const hstu_jagged_t* j, con
   const int64_t T = p->total_tokens;
   const int H = p->num_heads;
   const int N = p->max_seq_len;
-  HSTU_HIP(launch_fill_f32(d_rab_pos, 2 * (int64_t)N - 1, 0.0f, s), "fill launch");
-  HSTU_HIP(launch_fill_f32(d_rab_time, p->num_time_buckets, 0.0f, s), "fill launch");
+  if (T == 0 || p->dtype == HSTU_F32) {
+    HSTU_HIP(launch_fill_f32(d_rab_pos, 2 * (int64_t)N - 1, 0.0f, s), "fill launch");
+    HSTU_HIP(launch_fill_f32(d_rab_time, p->num_time_buckets, 0.0f, s), "fill launch");
+  }
   if (T == 0) return ok();
   JaggedArgs ja = make_args(p, j);
   char* w = (char*)ws;
@@ -790,10 +792,12 @@ hstu_status_t attn_bwd_impl(const hstu_problem_t* p, const hstu_jagged_t* j, con
   WorkItem* items = (WorkItem*)(w + l.bwd_items);
   float* dq_acc = (float*)(w + l.dq_acc);
   const int64_t ndq = T * H * p->d_qk;
-  HSTU_HIP(launch_fill_f32(dq_acc, ndq, 0.0f, s), "fill launch");
   ja.seq_trange = (const int64_t*)(w + l.trange);
-  HSTU_HIP(launch_seq_time_range(ja, (int64_t*)(w + l.trange), s), "time range launch");
-  HSTU_HIP(launch_schedule(ja, 1, items, counts + 1, s), "schedule launch");
+  // The dQ accumulator and both bias-gradient tables start at zero.
+  const PrepFills fills{{dq_acc, d_rab_pos, d_rab_time},
+                        {ndq, 2 * (int64_t)N - 1, (int64_t)p->num_time_buckets}, 3};
+  HSTU_HIP(launch_prep(ja, 1, items, counts + 1, (int64_t*)(w + l.trange), fills, s),
+           "prep launch");
   {
     TimedScope ts("attn_bwd", s);
     HSTU_HIP(launch_attn_bwd_bf16(ja, t, p->d_qk, p->d_v, d_out, d_out_lo, dq_acc, dk, dv,

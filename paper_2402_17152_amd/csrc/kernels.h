@@ -17,7 +17,7 @@ struct JaggedArgs {
   const float* rab_pos;
   const float* rab_time;
   // [2B] per-sequence timestamp min / max (workspace, filled by
-  // launch_seq_time_range before the attention kernels run).
+  // launch_prep before the attention kernels run).
   const int64_t* seq_trange;
   // Cross mode (the cached candidate pass of M-FALCON): the rows of
   // sequence b are its candidates, all at position n_h, and the keys its
@@ -60,17 +60,25 @@ inline int64_t max_work_items(int64_t T, int32_t B, int blk) {
   return (T + blk - 1) / blk + B;
 }
 
-// Scheduler: builds the work list (longest first) into `items` and
-// its length into `count`.  mode 0: forward (seq, q-block of kFwdBM rows;
-// in cross mode the candidate rows in blocks of kFwdBM); mode 1: backward
-// (seq, k-block of kBwdBN keys).
-hipError_t launch_schedule(const JaggedArgs& ja, int mode, WorkItem* items, int32_t* count,
-                           hipStream_t s);
+// Up to three float arrays an attention call zeroes before its main kernel.
+struct PrepFills {
+  float* ptr[3];
+  int64_t count[3];
+  int n;
+};
+
+// The work an attention call does before its main kernel, in one launch:
+//  - the scheduler: the work list (longest first) into `items` and its
+//    length into `count`; mode 0: forward (seq, q-block of kFwdBM rows;
+//    in cross mode the candidate rows in blocks of kFwdBM), mode 1:
+//    backward (seq, k-block of kBwdBN keys);
+//  - per-sequence timestamp min / max into trange[2b], trange[2b+1] (0, 0
+//    for an empty sequence);
+//  - zeroing the arrays in `fills`.
+hipError_t launch_prep(const JaggedArgs& ja, int mode, WorkItem* items, int32_t* count,
+                       int64_t* trange, const PrepFills& fills, hipStream_t s);
 
 hipError_t launch_fill_f32(float* p, int64_t n, float value, hipStream_t s);
-// Per-sequence timestamp min / max into out[2b], out[2b+1] (0, 0 for an
-// empty sequence).
-hipError_t launch_seq_time_range(const JaggedArgs& ja, int64_t* out, hipStream_t s);
 hipError_t launch_complete_cumsum(int32_t n, const int64_t* in, int64_t* out, int square_of_diff,
                                   hipStream_t s);
 hipError_t launch_bucketize(int32_t num_seqs, int64_t total_tokens, int32_t num_buckets,

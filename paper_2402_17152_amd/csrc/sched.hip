@@ -41,11 +41,10 @@ __device__ __forceinline__ int bwd_weight(int L, int n_h, int kb) {
   return ceil_div(i_end - j0, kBwdBM);
 }
 
-__global__ __launch_bounds__(kSchedThreads) void schedule_kernel(JaggedArgs ja, int mode,
-                                                                 WorkItem* items,
-                                                                 int32_t* count) {
-  extern __shared__ int s_bins[];  // [nbins]
-  __shared__ int s_scan[kSchedThreads];
+// One workgroup of kSchedThreads builds the whole list; s_bins holds
+// maxw + 1 ints (dynamic LDS), s_scan kSchedThreads.
+__device__ void schedule_block(const JaggedArgs& ja, int mode, WorkItem* items, int32_t* count,
+                               int* s_bins, int* s_scan) {
   const int tid = threadIdx.x;
   const int blk = mode == 0 ? kFwdBM : kBwdBN;
   const int maxw = mode == 0 ? ceil_div(ja.max_seq_len, kFwdBN) : ceil_div(ja.max_seq_len, kBwdBM);
@@ -180,18 +179,16 @@ int grid_for(int64_t n, int threads) {
 // Per-sequence timestamp extremes (one workgroup per sequence; eight
 // independent loads in flight per thread).  The attention kernels use them
 // to pick 32-bit rebased time arithmetic when a sequence spans < 2^31.
-constexpr int kRangeThreads = 256;
-__global__ __launch_bounds__(kRangeThreads) void seq_time_range_kernel(JaggedArgs ja, int64_t* out) {
-  __shared__ int64_t red[2][kRangeThreads / 64];
-  const int b = blockIdx.x, tid = threadIdx.x;
+__device__ void time_range_block(const JaggedArgs& ja, int b, int64_t* out, int64_t (*red)[kSchedThreads / 64]) {
+  const int tid = threadIdx.x;
   const int64_t o = ja.seq_offsets[b];
   const int L = (int)(ja.seq_offsets[b + 1] - o);
   const int64_t* ts = ja.timestamps + o;
   int64_t lo = 0x7fffffffffffffffll, hi = -0x7fffffffffffffffll - 1;
-  for (int x0 = 0; x0 < L; x0 += 8 * kRangeThreads) {
+  for (int x0 = 0; x0 < L; x0 += 8 * kSchedThreads) {
     int64_t v[8];
 #pragma unroll
-    for (int k = 0; k < 8; k++) v[k] = ts[min(x0 + k * kRangeThreads + tid, L - 1)];
+    for (int k = 0; k < 8; k++) v[k] = ts[min(x0 + k * kSchedThreads + tid, L - 1)];
 #pragma unroll
     for (int k = 0; k < 8; k++) {
       lo = v[k] < lo ? v[k] : lo;
@@ -204,7 +201,7 @@ __global__ __launch_bounds__(kRangeThreads) void seq_time_range_kernel(JaggedArg
     const int64_t ok = ja.key_offsets[b];
     Lk = (int)(ja.key_offsets[b + 1] - ok);
     const int64_t* tk = ja.key_timestamps + ok;
-    for (int x = tid; x < Lk; x += kRangeThreads) {
+    for (int x = tid; x < Lk; x += kSchedThreads) {
       const int64_t v = tk[x];
       lo = v < lo ? v : lo;
       hi = v > hi ? v : hi;
@@ -222,7 +219,7 @@ __global__ __launch_bounds__(kRangeThreads) void seq_time_range_kernel(JaggedArg
   }
   __syncthreads();
   if (tid == 0) {
-    for (int w = 1; w < kRangeThreads / 64; w++) {
+    for (int w = 1; w < kSchedThreads / 64; w++) {
       lo = red[0][w] < lo ? red[0][w] : lo;
       hi = red[1][w] > hi ? red[1][w] : hi;
     }
@@ -231,20 +228,60 @@ __global__ __launch_bounds__(kRangeThreads) void seq_time_range_kernel(JaggedArg
   }
 }
 
-}  // namespace
-
-hipError_t launch_schedule(const JaggedArgs& ja, int mode, WorkItem* items, int32_t* count,
-                           hipStream_t s) {
-  int maxw = mode == 0 ? (ja.max_seq_len + kFwdBN - 1) / kFwdBN
-                       : (ja.max_seq_len + kBwdBM - 1) / kBwdBM;
-  size_t lds = sizeof(int) * (size_t)(maxw + 1);
-  hipLaunchKernelGGL(schedule_kernel, dim3(1), dim3(kSchedThreads), lds, s, ja, mode, items, count);
-  return hipGetLastError();
+// Zero fills: fill block f of nf covers a grid-stride share of every job.
+__device__ void fill_blocks(const PrepFills& fills, int f, int nf) {
+  const int64_t stride = (int64_t)nf * kSchedThreads;
+  for (int k = 0; k < fills.n; k++) {
+    float* p = fills.ptr[k];
+    const int64_t n = fills.count[k];
+    int64_t done = 0;
+    if (((uintptr_t)p & 15) == 0) {
+      const int64_t n4 = n / 4;
+      const f32x4 z = {0.0f, 0.0f, 0.0f, 0.0f};
+      for (int64_t i = (int64_t)f * kSchedThreads + threadIdx.x; i < n4; i += stride)
+        reinterpret_cast<f32x4*>(p)[i] = z;
+      done = 4 * n4;
+    }
+    for (int64_t i = done + (int64_t)f * kSchedThreads + threadIdx.x; i < n; i += stride) p[i] = 0.0f;
+  }
 }
 
-hipError_t launch_seq_time_range(const JaggedArgs& ja, int64_t* out, hipStream_t s) {
-  if (ja.num_seqs <= 0) return hipSuccess;
-  hipLaunchKernelGGL(seq_time_range_kernel, dim3(ja.num_seqs), dim3(kRangeThreads), 0, s, ja, out);
+// Everything an attention call needs before its main kernel, in one
+// launch: workgroup 0 builds the work list, workgroups 1..B take one
+// sequence's timestamp range each, the rest zero the fills.
+__global__ __launch_bounds__(kSchedThreads) void prep_kernel(JaggedArgs ja, int mode,
+                                                             WorkItem* items, int32_t* count,
+                                                             int64_t* trange, PrepFills fills,
+                                                             int nfill_blocks) {
+  extern __shared__ int s_bins[];  // [maxw + 1]
+  __shared__ int s_scan[kSchedThreads];
+  __shared__ int64_t red[2][kSchedThreads / 64];
+  const int g = (int)blockIdx.x;
+  if (g == 0) {
+    schedule_block(ja, mode, items, count, s_bins, s_scan);
+  } else if (g <= ja.num_seqs) {
+    time_range_block(ja, g - 1, trange, red);
+  } else {
+    fill_blocks(fills, g - 1 - ja.num_seqs, nfill_blocks);
+  }
+}
+
+}  // namespace
+
+hipError_t launch_prep(const JaggedArgs& ja, int mode, WorkItem* items, int32_t* count,
+                       int64_t* trange, const PrepFills& fills, hipStream_t s) {
+  const int maxw = mode == 0 ? (ja.max_seq_len + kFwdBN - 1) / kFwdBN
+                             : (ja.max_seq_len + kBwdBM - 1) / kBwdBM;
+  const size_t lds = sizeof(int) * (size_t)(maxw + 1);
+  int64_t work4 = 0;
+  for (int k = 0; k < fills.n; k++) work4 += (fills.count[k] + 3) / 4;
+  // About four float4 stores per thread for large fills, at most 1024 blocks.
+  int64_t nf = (work4 + 4 * kSchedThreads - 1) / (4 * kSchedThreads);
+  nf = nf > 1024 ? 1024 : nf;
+  if (work4 > 0 && nf < 1) nf = 1;
+  const int64_t grid = 1 + (int64_t)ja.num_seqs + nf;
+  hipLaunchKernelGGL(prep_kernel, dim3((unsigned)grid), dim3(kSchedThreads), lds, s, ja, mode,
+                     items, count, trange, fills, (int)nf);
   return hipGetLastError();
 }
 
