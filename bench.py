@@ -318,6 +318,24 @@ def counters_traffic(kernel: str, workload: str, src: str):
     return rec.get("hbm_bytes_per_launch")
 
 
+def dq_atomic_bytes(batch, block_keys=128):
+    """Bytes the bf16 backward adds to its fp32 dQ accumulator with
+    atomics: every (sequence, 128-key block, head) work item adds a
+    d_qk-wide fp32 row for each row it visits (from its first key to the
+    sequence end; candidate key blocks visit their own rows only)."""
+    s = batch.spec
+    offs = batch.seq_offsets
+    nt = batch.num_targets
+    rows = 0
+    for b in range(len(offs) - 1):
+        L = int(offs[b + 1] - offs[b])
+        n_h = L - (int(nt[b]) if nt is not None else 0)
+        for j0 in range(0, L, block_keys):
+            i_end = min(j0 + block_keys, L) if j0 >= n_h else L
+            rows += i_end - j0
+    return rows * s.num_heads * s.d_qk * 4
+
+
 def cpu_baseline(batch, flops_full):
     """The oracle, untuned, on the shortest sequences of the batch (one
     OpenMP task per sequence x head, as many sequences as there are
@@ -481,6 +499,12 @@ def main():
                     "traffic": counters_traffic(dom, args.workload, src),
                     "flop_per_launch": f_bwd if dom == "attn_bwd" else f_fwd,
                     "source_hash": src}
+        if dom == "attn_bwd" and spec.dtype == "bf16":
+            # The dQ partial sums of the 128-key work items reach memory as
+            # fp32 atomics; their rate, not the matrix cores, bounds this kernel.
+            qb = dq_atomic_bytes(batch)
+            roofline["dq_atomic_bytes"] = qb
+            roofline["dq_atomic_tbs"] = qb / (kernels[dom]["avg_ms"] * 1e-3) / 1e12
 
     aux = None if args.no_aux else aux_measurements(hstu, torch, d, batch, stream)
     if roofline is not None and aux is not None:
