@@ -24,6 +24,8 @@ import os
 import sys
 import time
 
+import numpy as np
+
 ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
@@ -318,6 +320,19 @@ def counters_traffic(kernel: str, workload: str, src: str):
     return rec.get("hbm_bytes_per_launch")
 
 
+def dq_partial_bytes(batch, block_rows=32, block_keys=128):
+    """Bytes of bf16 partial dQ blocks the two-role backward stores (and
+    its reduce pass reads back): one 32-row x d_qk block per 32-row step of
+    every 128-key block and head."""
+    s = batch.spec
+    slots = 0
+    for L in np.diff(batch.seq_offsets):
+        S = (int(L) + block_rows - 1) // block_rows
+        K = (int(L) + block_keys - 1) // block_keys
+        slots += K * S - 2 * K * (K - 1)
+    return slots * s.num_heads * s.d_qk * block_rows * 2
+
+
 def dq_atomic_bytes(batch, block_keys=128):
     """Bytes the bf16 backward adds to its fp32 dQ accumulator with
     atomics: every (sequence, 128-key block, head) work item adds a
@@ -469,7 +484,7 @@ def main():
     per_step = [evs[k].elapsed_time(evs[k + 1]) for k in range(args.steps)]
 
     kernels = {}
-    for name in ("attn_fwd", "ln_gate", "ln_gate_bwd", "attn_bwd"):
+    for name in ("attn_fwd", "ln_gate", "ln_gate_bwd", "attn_bwd", "dq_reduce"):
         tot, n = hstu.hstu_timing_read(name)
         if n:
             kernels[name] = {"avg_ms": tot / n, "launches": n}
@@ -481,6 +496,10 @@ def main():
         kernels["attn_fwd"]["tflops"] = f_fwd / (kernels["attn_fwd"]["avg_ms"] * 1e-3) / 1e12
     if "attn_bwd" in kernels:
         kernels["attn_bwd"]["tflops"] = f_bwd / (kernels["attn_bwd"]["avg_ms"] * 1e-3) / 1e12
+    if "dq_reduce" in kernels:
+        # bf16 partial blocks read, bf16 dQ written
+        rb = dq_partial_bytes(batch) + T * spec.num_heads * spec.d_qk * 2
+        kernels["dq_reduce"]["gbs"] = rb / (kernels["dq_reduce"]["avg_ms"] * 1e-3) / 1e9
     if "ln_gate" in kernels:
         kernels["ln_gate"]["gbs"] = ln_bytes / (kernels["ln_gate"]["avg_ms"] * 1e-3) / 1e9
     if "ln_gate_bwd" in kernels:
@@ -500,11 +519,16 @@ def main():
                     "flop_per_launch": f_bwd if dom == "attn_bwd" else f_fwd,
                     "source_hash": src}
         if dom == "attn_bwd" and spec.dtype == "bf16":
-            # The dQ partial sums of the 128-key work items reach memory as
-            # fp32 atomics; their rate, not the matrix cores, bounds this kernel.
-            qb = dq_atomic_bytes(batch)
-            roofline["dq_atomic_bytes"] = qb
-            roofline["dq_atomic_tbs"] = qb / (kernels[dom]["avg_ms"] * 1e-3) / 1e12
+            if layer:
+                # Two-term dO: the single-role kernel adds the dQ partial sums
+                # of its 128-key work items to memory as fp32 atomics.
+                qb = dq_atomic_bytes(batch)
+                roofline["dq_atomic_bytes"] = qb
+                roofline["dq_atomic_tbs"] = qb / (kernels[dom]["avg_ms"] * 1e-3) / 1e12
+            else:
+                # The two-role kernel stores them as bf16 blocks; a reduce
+                # pass (kernels.dq_reduce) reads them back.
+                roofline["dq_partial_bytes"] = dq_partial_bytes(batch)
 
     aux = None if args.no_aux else aux_measurements(hstu, torch, d, batch, stream)
     if roofline is not None and aux is not None:

@@ -51,9 +51,11 @@
  *            Bias tables and their gradients are fp32; offsets and
  *            timestamps int64.
  *   Determinism  hstu_attn_fwd, hstu_layer_fwd, hstu_time_bucketize and
- *            hstu_complete_cumsum are bitwise deterministic.
- *            hstu_attn_bwd and hstu_layer_bwd accumulate dQ and the bias
- *            and layer-norm parameter gradients with atomics, so their
+ *            hstu_complete_cumsum are bitwise deterministic, and so are
+ *            dQ, dK and dV of hstu_attn_bwd for HSTU_BF16 (dQ is summed
+ *            from per-key-block partials in a fixed order).  The bias
+ *            gradients, and in hstu_layer_bwd also dQ and the layer-norm
+ *            parameter gradients, are accumulated with atomics, so their
  *            last bits may vary between runs.
  */
 #ifndef HSTU_H_
@@ -104,7 +106,10 @@ typedef struct {
 /* Bytes of device workspace the attention calls need for problem p (host
  * pointer).  0 only if p is invalid.  One workspace of this size serves
  * every call below for the same shape; it may be reused between calls
- * on one stream but not by calls that overlap. */
+ * on one stream but not by calls that overlap.  For HSTU_BF16 it holds
+ * the backward's partial dQ blocks: about (N T / 8192 + T / 20) h d_qk
+ * 64 bytes at most (bounded from T, B and N alone; 1.6 GB for T = 48118,
+ * N = 8192, h = 4, d_qk = 128). */
 size_t hstu_workspace_bytes(const hstu_problem_t* p);
 
 /* Eq. 2 forward: out[t][a][:] = (1/N) sum_{j kept} SiLU(q.k + rab) v_j.

@@ -4,6 +4,7 @@
 
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
 #include <cmath>
 #include <cstdarg>
 #include <cstdio>
@@ -140,8 +141,12 @@ struct Layout {
   size_t fwd_items;
   size_t bwd_items;
   size_t trange;    // int64 [2B]: per-sequence timestamp min / max
-  size_t dq_acc;    // fp32 [h][T][d_qk] (bf16 problems)
+  size_t bases;     // int64 [2 (B + 1)]: slot tables of the partial dQ blocks
+  size_t dq_acc;    // fp32 [h][T][d_qk] (bf16 problems; hstu_layer_bwd)
   size_t dout;      // [T][h*d_v] fp32, or bf16 high then low terms: dO of hstu_layer_bwd
+  size_t dq_part;   // f16 partial dQ blocks of hstu_attn_bwd (bf16 problems), then their
+  size_t dq_scale;  // fp32 block scales; both share the space of dq_acc and dout, which
+                    // that call does not use
   size_t total;
   int64_t max_fwd, max_bwd;
 };
@@ -159,11 +164,24 @@ Layout layout(const hstu_problem_t* p) {
   off = align_up(off + sizeof(WorkItem) * (size_t)l.max_bwd);
   l.trange = off;
   off = align_up(off + 2 * sizeof(int64_t) * (size_t)p->num_seqs);
+  l.bases = off;
+  off = align_up(off + 2 * sizeof(int64_t) * ((size_t)p->num_seqs + 1));
+  const size_t shared = off;
   l.dq_acc = off;
   if (p->dtype == HSTU_BF16)
     off = align_up(off + sizeof(float) * (size_t)p->total_tokens * p->num_heads * p->d_qk);
   l.dout = off;
   off = align_up(off + 4 * (size_t)p->total_tokens * p->num_heads * p->d_v);
+  l.dq_part = shared;
+  l.dq_scale = shared;
+  if (p->dtype == HSTU_BF16) {
+    // Per slot and head, d_qk / 32 blocks of 32 x 32 f16 and one fp32 scale each.
+    const size_t slots =
+        (size_t)dq_part_slots_bound(p->total_tokens, p->num_seqs, p->max_seq_len) *
+        (size_t)p->num_heads;
+    l.dq_scale = align_up(shared + slots * (size_t)p->d_qk * 64);
+    off = std::max(off, align_up(l.dq_scale + slots * (size_t)(p->d_qk / 32) * 4));
+  }
   l.total = off;
   return l;
 }
@@ -258,7 +276,7 @@ hstu_status_t attn_fwd_impl(const hstu_problem_t* p, const hstu_jagged_t* j, con
   int32_t* counts = (int32_t*)(w + l.counts);
   WorkItem* items = (WorkItem*)(w + l.fwd_items);
   ja.seq_trange = (const int64_t*)(w + l.trange);
-  HSTU_HIP(launch_prep(ja, 0, items, counts, (int64_t*)(w + l.trange), PrepFills{}, s),
+  HSTU_HIP(launch_prep(ja, 0, items, counts, (int64_t*)(w + l.trange), PrepFills{}, nullptr, s),
            "prep launch");
   TimedScope ts("attn_fwd", s);
   HSTU_HIP(launch_attn_fwd_bf16(ja, t, p->d_qk, p->d_v, out, out_f32, out_f32, items, counts,
@@ -727,7 +745,8 @@ hstu_status_t hstu_attn_fwd_cached(const hstu_problem_t* p, const hstu_jagged_t*
     WorkItem* items = (WorkItem*)(w + l.items);
     float* o32 = (float*)(w + l.partial);  // fp32 partial outputs, one slot per key chunk
     ja.seq_trange = (const int64_t*)(w + l.trange);
-    HSTU_HIP(launch_prep(ja, 0, items, counts, (int64_t*)(w + l.trange), PrepFills{}, s),
+    HSTU_HIP(launch_prep(ja, 0, items, counts, (int64_t*)(w + l.trange), PrepFills{}, nullptr,
+                         s),
              "prep launch");
     TimedScope ts("attn_fwd_cached", s);
     const Tensors keys{q, q_stride, k_cache, kc_stride, v_cache, vc_stride};
@@ -791,21 +810,38 @@ hstu_status_t attn_bwd_impl(const hstu_problem_t* p, const hstu_jagged_t* j, con
   int32_t* counts = (int32_t*)(w + l.counts);
   WorkItem* items = (WorkItem*)(w + l.bwd_items);
   float* dq_acc = (float*)(w + l.dq_acc);
+  uint16_t* dq_part = (uint16_t*)(w + l.dq_part);
+  float* dq_scale = (float*)(w + l.dq_scale);
+  int64_t* bases = (int64_t*)(w + l.bases);
   const int64_t ndq = T * H * p->d_qk;
   ja.seq_trange = (const int64_t*)(w + l.trange);
-  // The dQ accumulator and both bias-gradient tables start at zero.
-  const PrepFills fills{{dq_acc, d_rab_pos, d_rab_time},
-                        {ndq, 2 * (int64_t)N - 1, (int64_t)p->num_time_buckets}, 3};
-  HSTU_HIP(launch_prep(ja, 1, items, counts + 1, (int64_t*)(w + l.trange), fills, s),
+  // Both bias-gradient tables start at zero, and so does the fp32 dQ
+  // accumulator of the single-role (two-term dO) kernel; the two-role
+  // kernel needs the slot tables of its partial dQ blocks instead.
+  const bool split = d_out_lo != nullptr;
+  const PrepFills fills =
+      split ? PrepFills{{dq_acc, d_rab_pos, d_rab_time},
+                        {ndq, 2 * (int64_t)N - 1, (int64_t)p->num_time_buckets}, 3}
+            : PrepFills{{d_rab_pos, d_rab_time, nullptr},
+                        {2 * (int64_t)N - 1, (int64_t)p->num_time_buckets, 0}, 2};
+  HSTU_HIP(launch_prep(ja, 1, items, counts + 1, (int64_t*)(w + l.trange), fills,
+                       split ? nullptr : bases, s),
            "prep launch");
   {
     TimedScope ts("attn_bwd", s);
-    HSTU_HIP(launch_attn_bwd_bf16(ja, t, p->d_qk, p->d_v, d_out, d_out_lo, dq_acc, dk, dv,
-                                  d_rab_pos, d_rab_time, items, counts + 1, l.max_bwd, s),
+    HSTU_HIP(launch_attn_bwd_bf16(ja, t, p->d_qk, p->d_v, d_out, d_out_lo, dq_acc, dq_part,
+                                  dq_scale, bases, dk, dv, d_rab_pos, d_rab_time, items,
+                                  counts + 1, l.max_bwd, s),
              "attn_bwd launch");
   }
-  HSTU_HIP(launch_dq_convert_bf16(dq_acc, dq, T, H, p->d_qk, 1.0f / (float)N, s),
-           "dq convert launch");
+  if (split)
+    HSTU_HIP(launch_dq_convert_bf16(dq_acc, dq, T, H, p->d_qk, 1.0f / (float)N, s),
+             "dq convert launch");
+  else {
+    TimedScope ts("dq_reduce", s);
+    HSTU_HIP(launch_dq_reduce_bf16(ja, p->d_qk, dq_part, dq_scale, bases, dq, s),
+             "dq reduce launch");
+  }
   return ok();
 }
 

@@ -127,7 +127,10 @@ struct BwdArgs {
   Tensors t;
   const uint16_t* dO;
   const uint16_t* dO_lo;  // SPLIT only
-  float* dq_acc;
+  float* dq_acc;         // single-role kernel: fp32 [h][T][d_qk], atomics
+  uint16_t* dq_part;     // two-role kernel: f16 partial dQ blocks (see dq_step)
+  float* dq_scale;       // two-role kernel: one power-of-two scale per partial block
+  const int64_t* pbase;  // two-role kernel: [B+1] first partial slot of each sequence
   uint16_t* dK;
   uint16_t* dV;
   float* d_rab_pos;
@@ -817,6 +820,842 @@ __device__ __forceinline__ void bwd_item(BwdShared<DQK, DV, SPLIT>& sm, const Bw
   }
 }
 
+// ---------------------------------------------------------------------------
+// Role-split backward: 8 waves, two per SIMD, no duplicated work.
+//
+// With one wave per SIMD the step above is bound by the latency of one
+// instruction stream: its 40 MFMAs keep the matrix core busy for under a
+// fifth of the step.  Here each SIMD runs two waves that own the same 32
+// keys and divide a step between them:
+//   role A (waves 0-3): S = Q K^T and dP = dO V^T (bias-seeded), SiLU and
+//        SiLU', the bias gradients, and P, dS rounded to bf16 into LDS;
+//   role B (waves 4-7), one step behind: dV += P^T dO, dK += dS^T Q (the
+//        dK, dV accumulators live only here) and the dQ product.
+// The dQ product of a step (32 rows x d_qk over the block's 128 keys) is
+// not added to a shared accumulator with atomics: their memory-side rate
+// would bind the kernel (one fp32 row per key block and visited row,
+// 16x the algorithmic traffic).  It is stored in the step's own slot of a
+// partial buffer as f16 scaled by a power of two that puts the block's
+// largest magnitude in [2^13, 2^14) (half the bytes of fp32, 2^-11
+// relative rounding, no overflow whatever the data), and dq_reduce_kernel
+// sums the slots of every row in key-block order (deterministic).
+// A holds K and V as MFMA operands, B the dK / dV accumulators and the dQ
+// operand, so each role fits in half the register file.  One barrier per
+// step orders the hand-over: A writes P and dS of step u into slot u & 1;
+// B reads them, and the Q / dO tile of step u, after the next barrier.  B
+// lags one step, so the Q / dO ring has five slots (DMA three ahead).
+template <int DQK, int DV>
+struct BwdSharedRS {
+  using QT = StepTile<DQK>;
+  using OT = StepTile<DV>;
+  static constexpr int BN = kBwdBN, BM = kBwdBM;
+  static constexpr int kSlots = 5;
+  static constexpr int DST_LD = 48;   // dS^T [128 keys][32 rows] bf16 (as above)
+  static constexpr int KB_LD = DQK + 16;
+  static constexpr int kWinPad = 4, WIN_LD = 264;
+  union Ring {
+    struct {
+      __align__(16) uint8_t q[kSlots][QT::BYTES];
+      __align__(16) uint8_t dO[kSlots][OT::BYTES];
+    } t;
+    __align__(16) uint16_t kblk[BN * KB_LD];  // prologue only
+  };
+  Ring ring;
+  __align__(16) uint16_t sdST[2][BN * DST_LD];
+  // P as role A's MFMA operand registers: [slot][wave][k-step][lane].
+  __align__(16) u32x4 sPA[2][4][2][64];
+  __align__(16) float sWin[4][4][WIN_LD];
+  __align__(16) uint32_t sT[8][64];
+  __align__(16) uint32_t sTr[8][32];
+  uint32_t sRr[4][2];
+  float sTab[64];
+  float sTacc[64];
+  static constexpr int kRing = 256;
+  float sRing[4][2][kRing];
+};
+
+// Everything both roles compute from the item (no per-role state).
+struct RsItem {
+  int64_t o;
+  int seq, L, n_h, j0, head, nsteps;
+};
+
+template <int DQK, int DV, bool FAST>
+__device__ __forceinline__ void bwd_role_a(BwdSharedRS<DQK, DV>& sm, const BwdArgs& A,
+                                           const RsItem& it, int64_t tbase) {
+  using Sh = BwdSharedRS<DQK, DV>;
+  using QT = typename Sh::QT;
+  using OT = typename Sh::OT;
+  constexpr int BN = Sh::BN, BM = Sh::BM, DST_LD = Sh::DST_LD, kSlots = Sh::kSlots;
+  const JaggedArgs& ja = A.ja;
+  const int H = ja.num_heads, N = ja.max_seq_len;
+  const int64_t o = it.o;
+  const int L = it.L, n_h = it.n_h, j0 = it.j0, head = it.head, nsteps = it.nsteps;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // 0..3
+  const int col = lane & 31, half = lane >> 5;
+  const int jw0 = j0 + 32 * wave;
+  const int my_j = jw0 + col;
+  const bool key_ok = my_j < L;
+  const int pj = bias_pos(my_j, n_h);
+  const int64_t* __restrict__ ts = ja.timestamps + o;
+  const uint16_t* __restrict__ kg = (const uint16_t*)A.t.k + o * A.t.k_stride + head * DQK;
+  const uint16_t* __restrict__ vg = (const uint16_t*)A.t.v + o * A.t.v_stride + head * DV;
+  const uint16_t* __restrict__ qg = (const uint16_t*)A.t.q + o * A.t.q_stride + head * DQK;
+  const uint16_t* __restrict__ dog = A.dO + (o * H + head) * DV;
+  const uint32_t kstride_b = (uint32_t)A.t.k_stride * 2u, vstride_b = (uint32_t)A.t.v_stride * 2u;
+  const uint32_t qstride_b = (uint32_t)A.t.q_stride * 2u, dostride_b = (uint32_t)(H * DV) * 2u;
+  const float invN = 1.0f / (float)N;
+  auto row0 = [&](int u) { return j0 + BM * u; };
+
+  // K, V of the wave's keys: B operands of S and dP (keys past the end read as zeros).
+  const __amdgpu_buffer_rsrc_t krs = make_rsrc(kg, (uint32_t)(L * A.t.k_stride * 2));
+  const __amdgpu_buffer_rsrc_t vrs = make_rsrc(vg, (uint32_t)(L * A.t.v_stride * 2));
+  u32x4 kf[DQK / 16], vf[DV / 16];
+#pragma unroll
+  for (int s = 0; s < DQK / 16; s++)
+    kf[s] = buffer_load16(krs, (uint32_t)my_j * kstride_b + (uint32_t)(16 * s + 8 * half) * 2u);
+#pragma unroll
+  for (int s = 0; s < DV / 16; s++)
+    vf[s] = buffer_load16(vrs, (uint32_t)my_j * vstride_b + (uint32_t)(16 * s + 8 * half) * 2u);
+
+  const int64_t tj64 = key_ok ? ts[my_j] : tbase;
+  const uint32_t tjr = (uint32_t)(tj64 - tbase);
+  const uint32_t klo32 =
+      __builtin_amdgcn_readfirstlane((uint32_t)(wave_min_i64(key_ok ? tj64 : kI64Max) - tbase));
+  const uint32_t khi32 =
+      __builtin_amdgcn_readfirstlane((uint32_t)(wave_max_i64(key_ok ? tj64 : kI64Min) - tbase));
+
+  // A-operand reads of row `col`, 16-byte chunk (2s + half) (as in bwd_item).
+  auto a_base = [&](auto tile_tag, uint32_t (&ab)[4]) {
+    using T = decltype(tile_tag);
+    const int sw = T::swz(col);
+#pragma unroll
+    for (int k = 0; k < 4; k++)
+      ab[k] = (uint32_t)(col * T::RB + 16 * (half ^ (sw & 1)) + 32 * (k ^ (sw >> 1)));
+  };
+  auto a_off = [&](auto tile_tag, const uint32_t (&ab)[4], int s) -> uint32_t {
+    using T = decltype(tile_tag);
+    if constexpr (T::SWZ)
+      return ab[s & 3] + 128u * (uint32_t)(s >> 2);
+    else
+      return (uint32_t)(col * T::RB + 16 * (2 * s + half));
+  };
+  uint32_t qa[4], oa[4];
+  a_base(QT{}, qa);
+  a_base(OT{}, oa);
+
+  // ---- staging by LDS DMA: Q, dO and the rab_pos window three steps
+  // ahead, row timestamps five.  Only role A issues DMA; the wait at step
+  // u needs the tiles and window of step u + 1, issued at step u - 2 and
+  // followed by that step's timestamp operation and all of step u - 1's
+  // (later atomics only make the wait stricter).
+  constexpr int OPS_PER_STEP = QT::OPW + OT::OPW + 3 + 1;
+  const u32x4 qrs = rsrc_words(qg, (uint32_t)(L * A.t.q_stride * 2));
+  const u32x4 ors = rsrc_words(dog, (uint32_t)L * dostride_b);
+  const u32x4 trs = rsrc_words(ts, (uint32_t)L * 8u);
+  const u32x4 prs = rsrc_words(ja.rab_pos, (uint32_t)(2 * N - 1) * 4u);
+  uint32_t qoffs[QT::OPW], ooffs[OT::OPW];
+  auto tile_offs = [&](auto tile_tag, uint32_t* offs, uint32_t stride_b) {
+    using T = decltype(tile_tag);
+#pragma unroll
+    for (int k = 0; k < T::OPW; k++) {
+      const int op = min(wave * T::OPW + k, T::OPS - 1), g = 64 * op + lane;
+      const int r = g / T::PC, p = g % T::PC;
+      const int c = p < T::CPR ? (p ^ T::swz(r)) : 0;
+      offs[k] = (uint32_t)r * stride_b + (uint32_t)c * 16u;
+    }
+  };
+  tile_offs(QT{}, qoffs, qstride_b);
+  tile_offs(OT{}, ooffs, dostride_b);
+  auto issue_tiles = [&](int u) {
+    const int i0 = row0(u), slot = u % kSlots;
+#pragma unroll
+    for (int k = 0; k < QT::OPW; k++)
+      dma_to_lds16_asm(qrs, sm.ring.t.q[slot] + 1024 * min(wave * QT::OPW + k, QT::OPS - 1),
+                       qoffs[k] + (uint32_t)i0 * qstride_b);
+#pragma unroll
+    for (int k = 0; k < OT::OPW; k++)
+      dma_to_lds16_asm(ors, sm.ring.t.dO[slot] + 1024 * min(wave * OT::OPW + k, OT::OPS - 1),
+                       ooffs[k] + (uint32_t)i0 * dostride_b);
+  };
+  const int Pk = min(j0 + BN - 1, n_h);
+  auto issue_win = [&](int u) {
+    const int pb = (N - 1) + Pk - min(row0(u), n_h);
+#pragma unroll
+    for (int k = 0; k < 3; k++) {
+      const int op = 3 * wave + k, c = op / 3, ch = op % 3;
+      dma_to_lds4_asm(prs, &sm.sWin[u & 3][c][Sh::kWinPad + 64 * ch],
+                      (uint32_t)(pb - 64 * ch - lane - c) * 4u);
+    }
+  };
+  auto issue_ts = [&](int u) {
+    dma_to_lds4_asm(trs, sm.sT[u & 7], (uint32_t)row0(u) * 8u + 4u * (uint32_t)lane);
+  };
+  auto reduce_ts = [&](int u) {
+    if constexpr (FAST) {
+      if (wave == 0) {
+        const uint32_t v = sm.sT[u & 7][2 * (lane & 31)] - (uint32_t)tbase;
+        const uint32_t lo = wave_min_dpp(v), hi = wave_max_dpp(v);
+        sm.sTr[u & 7][lane & 31] = v;
+        if (lane < 2) sm.sRr[u & 3][lane] = lane ? hi : lo;
+      }
+    }
+  };
+
+  // ---- bias path of a (wave, step) tile (as in bwd_item) ----
+  enum { kUniform = 0, kTwo = 1, kGeneral = 2 };
+  struct Path {
+    int code;
+    float cb, cb_far;
+    __device__ int kind() const { return code & 3; }
+    __device__ int slot() const { return (code >> 2) & 63; }
+    __device__ int slot_far() const { return (code >> 8) & 63; }
+    __device__ uint32_t thr() const { return 1u << ((code >> 14) & 31); }
+  };
+  auto full_tile = [&](int i0) {
+    return (jw0 + 31 <= i0) && (i0 + BM - 1 < L) && (i0 + BM - 1 < n_h);
+  };
+  auto classify = [&](int u) -> Path {
+    Path r{kGeneral, 0.0f, 0.0f};
+    if (u >= nsteps) {
+      r.code = kUniform;
+      return r;
+    }
+    if constexpr (FAST) {
+      if (full_tile(row0(u))) {
+        const uint32_t rlo = __builtin_amdgcn_readfirstlane(sm.sRr[u & 3][0]);
+        const uint32_t rhi = __builtin_amdgcn_readfirstlane(sm.sRr[u & 3][1]);
+        const bool ordered = rlo >= khi32;
+        uint32_t dmin, dmax;
+        if (ordered) {
+          dmin = rlo - khi32;
+          dmax = rhi - klo32;
+        } else if (klo32 >= rhi) {
+          dmin = klo32 - rhi;
+          dmax = khi32 - rlo;
+        } else {
+          dmin = 0;
+          dmax = max(rhi - klo32, khi32 - rlo);
+        }
+        const int bnear = 31 - __clz((int)(dmin | 1u)), bfar = 31 - __clz((int)(dmax | 1u));
+        if (bnear == bfar) {
+          r.code = kUniform | (63 - bnear) << 2;
+          r.cb = sm.sTab[63 - bnear];
+        } else if (ordered && bfar == bnear + 1) {
+          r.code = kTwo | (63 - bnear) << 2 | (63 - bfar) << 8 | bfar << 14;
+          r.cb = sm.sTab[63 - bnear];
+          r.cb_far = sm.sTab[63 - bfar];
+        }
+      }
+    }
+    return r;
+  };
+  const int a_y = Pk - my_j + 4 * half;
+  auto win_reads = [&](int u, float (&w)[16]) {
+    const int c = a_y & 3;
+    const float* wp = &sm.sWin[u & 3][c][Sh::kWinPad + a_y - c];
+#pragma unroll
+    for (int g = 0; g < 4; g++) {
+      const f32x4 v = *reinterpret_cast<const f32x4*>(wp + 8 * g);
+#pragma unroll
+      for (int m = 0; m < 4; m++) w[4 * g + m] = v[m];
+    }
+  };
+  auto row_ts = [&](int u, uint32_t (&ti)[16]) {
+    const uint32_t* tp = sm.sTr[u & 7] + 4 * half;
+#pragma unroll
+    for (int g = 0; g < 4; g++) {
+      const u32x4 v = *reinterpret_cast<const u32x4*>(tp + 8 * g);
+#pragma unroll
+      for (int m = 0; m < 4; m++) ti[4 * g + m] = v[m];
+    }
+  };
+  auto pair_slots = [&](int u, int (&sl)[16]) {
+    if constexpr (FAST) {
+      uint32_t ti[16];
+      row_ts(u, ti);
+#pragma unroll
+      for (int q = 0; q < 16; q++) {
+        uint32_t d, z;
+        asm("v_sad_u32 %0, %1, %2, 0" : "=v"(d) : "v"(ti[q]), "v"(tjr));
+        asm("v_ffbh_u32 %0, %1" : "=v"(z) : "v"(d));
+        sl[q] = 32 + (int)z;
+      }
+    } else {
+      const uint32_t* tp = sm.sT[u & 7] + 2 * (4 * half);
+#pragma unroll
+      for (int q = 0; q < 16; q++) {
+        const int r = 8 * (q >> 2) + (q & 3);
+        const int64_t ti = (int64_t)(((uint64_t)tp[2 * r + 1] << 32) | tp[2 * r]);
+        sl[q] = slot64(ti - tj64);
+      }
+    }
+  };
+  auto seed = [&](int u, const Path& pth, f32x16& acc) {
+    if (pth.kind() == kUniform) {
+      float w[16];
+      win_reads(u, w);
+#pragma unroll
+      for (int q = 0; q < 16; q++) acc[q] = w[q] + pth.cb;
+    } else if (pth.kind() == kTwo) {
+      float w[16];
+      uint32_t ti[16];
+      win_reads(u, w);
+      row_ts(u, ti);
+      const uint32_t lim = tjr + pth.thr();
+#pragma unroll
+      for (int q = 0; q < 16; q++) acc[q] = w[q] + (ti[q] >= lim ? pth.cb_far : pth.cb);
+    } else {
+      const int i0 = row0(u), pi0 = min(i0, n_h);
+      int sl[16];
+      pair_slots(u, sl);
+      bool ok[16];
+      int y[16];
+#pragma unroll
+      for (int q = 0; q < 16; q++) {
+        const int i = i0 + 8 * (q >> 2) + 4 * half + (q & 3);
+        ok[q] = key_ok && i < L && pair_valid(i, my_j, n_h);
+        y[q] = ok[q] ? (Pk - pj) + (bias_pos(i, n_h) - pi0) : 0;
+      }
+      float w[16], tv[16];
+#pragma unroll
+      for (int q = 0; q < 16; q++) {
+        w[q] = sm.sWin[u & 3][0][Sh::kWinPad + y[q]];
+        tv[q] = sm.sTab[sl[q]];
+      }
+#pragma unroll
+      for (int q = 0; q < 16; q++) acc[q] = ok[q] ? w[q] + tv[q] : kMaskedBias;
+    }
+  };
+  auto scores = [&](int u, f32x16& sacc, f32x16& pacc) {
+    const uint8_t* qb = sm.ring.t.q[u % kSlots];
+    const uint8_t* ob = sm.ring.t.dO[u % kSlots];
+    pacc = f32x16{};
+    constexpr int SMAX = DQK > DV ? DQK / 16 : DV / 16;
+#pragma unroll
+    for (int s = 0; s < SMAX; s++) {
+      if (s < DQK / 16) {
+        const u32x4 a = *reinterpret_cast<const u32x4*>(qb + a_off(QT{}, qa, s));
+        sacc = mfma32x32x16(as_bf16x8(a), as_bf16x8(kf[s]), sacc);
+      }
+      if (s < DV / 16) {
+        const u32x4 a = *reinterpret_cast<const u32x4*>(ob + a_off(OT{}, oa, s));
+        pacc = mfma32x32x16(as_bf16x8(a), as_bf16x8(vf[s]), pacc);
+      }
+    }
+  };
+  // Hand-over to role B: dS^T in the dQ layout (role B reads its dK
+  // operand from it too) and P as this lane's operand registers.
+  auto store_step = [&](int u, const u32x4 (&pa)[2], const u32x4 (&da)[2]) {
+    uint16_t* dp = sm.sdST[u & 1] + (32 * wave + col) * DST_LD + 4 * half;
+#pragma unroll
+    for (int st = 0; st < 2; st++) {
+      *reinterpret_cast<uint2*>(dp + 16 * st) = uint2{da[st][0], da[st][1]};
+      *reinterpret_cast<uint2*>(dp + 16 * st + 8) = uint2{da[st][2], da[st][3]};
+      sm.sPA[u & 1][wave][st][lane] = pa[st];
+    }
+  };
+
+  // ---- bias gradients (as in bwd_item) ----
+  int run_slot[2] = {-1, -1};
+  float run_acc[2] = {0.0f, 0.0f};
+  auto time_flush = [&](int r) {
+    if (run_slot[r] >= 0) {
+      const float v = wave_sum_dpp(run_acc[r]);
+      if (lane == 0) atomicAdd(&sm.sTacc[run_slot[r]], v);
+    }
+    run_acc[r] = 0.0f;
+  };
+  auto time_add = [&](int r, int slot, float v) {
+    if (slot != run_slot[r]) {
+      time_flush(r);
+      run_slot[r] = slot;
+    }
+    run_acc[r] += v;
+  };
+  constexpr int kRing = Sh::kRing;
+  const int perm_base = lane * 4;
+  float wrap_w[16];
+#pragma unroll
+  for (int q = 0; q < 16; q++) wrap_w[q] = col + 8 * (q >> 2) + (q & 3) >= 32 ? 1.0f : 0.0f;
+  float* const ring_mine = sm.sRing[wave][half];
+  const int d1_lane = 4 * half - col - 32 * wave;
+  float carry = 0.0f;
+  auto pos_step = [&](int u, const float (&ds)[16]) {
+    float sum = 0.0f, wsum = 0.0f;
+#pragma unroll
+    for (int q = 0; q < 16; q++) {
+      const float rv = __int_as_float(__builtin_amdgcn_ds_bpermute(
+          perm_base + 4 * (8 * (q >> 2) + (q & 3)), __float_as_int(ds[q])));
+      sum += rv;
+      wsum = __builtin_fmaf(rv, wrap_w[q], wsum);
+    }
+    ring_mine[(32 * u + d1_lane) & (kRing - 1)] = (sum - wsum) + carry;
+    carry = __int_as_float(__builtin_amdgcn_ds_bpermute(perm_base ^ 128, __float_as_int(wsum)));
+  };
+  const int R = L - j0;
+  auto ring_flush = [&](int c) {
+    if (lane < 32) {
+      const int k = 32 * c + lane, sl = k & (kRing - 1);
+      float v = 0.0f;
+#pragma unroll
+      for (int w = 0; w < 4; w++)
+#pragma unroll
+        for (int h = 0; h < 2; h++) {
+          v += sm.sRing[w][h][sl];
+          sm.sRing[w][h][sl] = 0.0f;
+        }
+      if (v != 0.0f && k < R) unsafeAtomicAdd(&A.d_rab_pos[(N - 1) - k], v * invN);
+    }
+  };
+  auto grads = [&](int u, const Path& pth, const float (&ds)[16]) {
+    const int i0 = row0(u);
+    if (i0 + BM - 1 >= n_h && i0 < L) {
+      float dh[16];
+#pragma unroll
+      for (int q = 0; q < 16; q++) {
+        const int i = i0 + 8 * (q >> 2) + 4 * half + (q & 3);
+        dh[q] = i < n_h ? ds[q] : 0.0f;
+        if (i >= n_h && i < L && key_ok && pair_valid(i, my_j, n_h))
+          unsafeAtomicAdd(&A.d_rab_pos[(N - 1) - (n_h - pj)], ds[q] * invN);
+      }
+      pos_step(u, dh);
+    } else {
+      pos_step(u, ds);
+    }
+    if (pth.kind() != kGeneral) {
+      float tot = 0.0f;
+#pragma unroll
+      for (int q = 0; q < 16; q++) tot += ds[q];
+      if (pth.kind() == kTwo) {
+        uint32_t ti[16];
+        row_ts(u, ti);
+        const uint32_t lim = tjr + pth.thr();
+        float far = 0.0f;
+#pragma unroll
+        for (int q = 0; q < 16; q++) far += ti[q] >= lim ? ds[q] : 0.0f;
+        time_add(0, pth.slot(), tot - far);
+        time_add(1, pth.slot_far(), far);
+      } else {
+        time_add(0, pth.slot(), tot);
+      }
+    } else {
+      int sl[16];
+      pair_slots(u, sl);
+      uint32_t lo = 64, hi = 0;
+#pragma unroll
+      for (int q = 0; q < 16; q++) {
+        const int i = i0 + 8 * (q >> 2) + 4 * half + (q & 3);
+        if (!(key_ok && i < L && pair_valid(i, my_j, n_h))) sl[q] = 64;
+        lo = min(lo, (uint32_t)sl[q]);
+        hi = sl[q] < 64 ? max(hi, (uint32_t)sl[q]) : hi;
+      }
+      lo = wave_min_dpp(lo);
+      hi = wave_max_dpp(hi);
+      for (int b = (int)lo; b <= (int)hi; b++) {
+        float acc = 0.0f;
+#pragma unroll
+        for (int q = 0; q < 16; q++) acc += sl[q] == b ? ds[q] : 0.0f;
+        acc = wave_sum_dpp(acc);
+        if (lane == 0 && acc != 0.0f) atomicAdd(&sm.sTacc[b], acc);
+      }
+    }
+  };
+
+  // ---- pipelined steps: S, dP of step u+1 issued while step u goes
+  // through SiLU'; one barrier per step (role B runs the same count).
+  Path path_cur, path_next, path_nn;
+  auto step = [&](int u, f32x16& s_cur, f32x16& p_cur, f32x16& s_next, f32x16& p_next) {
+    wait_vmcnt_lgkmcnt0<OPS_PER_STEP + 1>();
+    barrier_no_fence();
+    if (u >= 5 && wave == (u & 3)) ring_flush(u - 5);
+    issue_tiles(u + 3);
+    issue_win(u + 3);
+    issue_ts(u + 5);
+    if (u + 1 < nsteps) seed(u + 1, path_next, s_next);
+    scores(u + 1, s_next, p_next);
+    float pv[16], dsv[16];
+#pragma unroll
+    for (int q = 0; q < 16; q++) {
+      const float x = s_cur[q];
+      const float sg = silu_sigma(x);
+      const float p = x * sg;
+      pv[q] = p;
+      dsv[q] = p_cur[q] * __builtin_fmaf(p, 1.0f - sg, sg);
+    }
+    u32x4 pa[2], da[2];
+#pragma unroll
+    for (int st = 0; st < 2; st++) {
+      pa[st] = u32x4{pack_bf16x2(pv[8 * st], pv[8 * st + 1]), pack_bf16x2(pv[8 * st + 2], pv[8 * st + 3]),
+                     pack_bf16x2(pv[8 * st + 4], pv[8 * st + 5]), pack_bf16x2(pv[8 * st + 6], pv[8 * st + 7])};
+      da[st] = u32x4{pack_bf16x2(dsv[8 * st], dsv[8 * st + 1]), pack_bf16x2(dsv[8 * st + 2], dsv[8 * st + 3]),
+                     pack_bf16x2(dsv[8 * st + 4], dsv[8 * st + 5]), pack_bf16x2(dsv[8 * st + 6], dsv[8 * st + 7])};
+    }
+    store_step(u, pa, da);
+    grads(u, path_cur, dsv);
+    path_nn = classify(u + 2);
+    reduce_ts(u + 3);
+    path_cur = path_next;
+    path_next = path_nn;
+  };
+
+  // Prologue: timestamps of steps 0..4, tiles and windows 0..2.
+  for (int v = 0; v < 5; v++) issue_ts(v);
+  for (int v = 0; v < 3; v++) {
+    issue_tiles(v);
+    issue_win(v);
+  }
+  wait_vmcnt_lgkmcnt0<0>();
+  barrier_no_fence();  // (P1)
+  for (int v = 0; v < 3; v++) reduce_ts(v);
+  wait_vmcnt_lgkmcnt0<0>();
+  barrier_no_fence();  // (P2)
+  f32x16 sA, pA, sB, pB;
+  path_cur = classify(0);
+  path_next = classify(1);
+  seed(0, path_cur, sA);
+  scores(0, sA, pA);
+  int u = 0;
+  for (; u + 1 < nsteps; u += 2) {
+    step(u, sA, pA, sB, pB);
+    step(u + 1, sB, pB, sA, pA);
+  }
+  if (u < nsteps) step(u, sA, pA, sB, pB);
+  // Role B's last step.
+  wait_vmcnt_lgkmcnt0<0>();
+  barrier_no_fence();  // (L)
+  time_flush(0);
+  time_flush(1);
+  ring_mine[(32 * nsteps + d1_lane) & (kRing - 1)] = carry;
+  wait_vmcnt_lgkmcnt0<0>();
+  barrier_no_fence();  // (E)
+  {
+    const int c0 = max(0, nsteps - 5);
+    for (int c = c0 + wave; c <= nsteps; c += 4) ring_flush(c);
+  }
+}
+
+template <int DQK, int DV>
+__device__ __forceinline__ void bwd_role_b(BwdSharedRS<DQK, DV>& sm, const BwdArgs& A,
+                                           const RsItem& it, const u32x4* kq) {
+  using Sh = BwdSharedRS<DQK, DV>;
+  using QT = typename Sh::QT;
+  using OT = typename Sh::OT;
+  constexpr int BN = Sh::BN, BM = Sh::BM, DST_LD = Sh::DST_LD, kSlots = Sh::kSlots;
+  const JaggedArgs& ja = A.ja;
+  const int H = ja.num_heads, N = ja.max_seq_len;
+  const int64_t o = it.o;
+  const int L = it.L, j0 = it.j0, head = it.head, nsteps = it.nsteps;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane((tid >> 6) - 4);  // 0..3
+  const int col = lane & 31, half = lane >> 5;
+  const int jw0 = j0 + 32 * wave;
+  const float invN = 1.0f / (float)N;
+  auto row0 = [&](int u) { return j0 + BM * u; };
+  // dQ: column block `wave` (waves past DQK / 32 have none) over all 128 keys.
+  constexpr int NCB = DQK / 32, KSTEPS = BN / 16;
+  const int tr_row = 4 * half + ((lane & 15) >> 2);
+  const int tr_col = 16 * ((lane >> 4) & 1) + 4 * (lane & 3);
+
+  f32x16 dkacc[DQK / 32], dvacc[DV / 32];
+#pragma unroll
+  for (int nb = 0; nb < DQK / 32; nb++)
+#pragma unroll
+    for (int q = 0; q < 16; q++) dkacc[nb][q] = 0.0f;
+#pragma unroll
+  for (int nb = 0; nb < DV / 32; nb++)
+#pragma unroll
+    for (int q = 0; q < 16; q++) dvacc[nb][q] = 0.0f;
+
+  // Transposing reads of the Q / dO tiles (as in bwd_item).
+  auto tr_base = [&](auto tile_tag, uint32_t (&tb)[2]) {
+    using T = decltype(tile_tag);
+    const int sw = T::swz(tr_row);
+    const int c1 = tr_col >> 3, off = (tr_col & 7) * 2;
+    const int b = tr_row * T::RB + 16 * (c1 ^ (sw & 3)) + off;
+    tb[0] = (uint32_t)(b + 64 * (sw >> 2));
+    tb[1] = (uint32_t)(b - 64 * (sw >> 2));
+  };
+  auto tr_off = [&](auto tile_tag, const uint32_t (&tb)[2], int st, int hi, int nb) -> uint32_t {
+    using T = decltype(tile_tag);
+    const int rows = (16 * st + 8 * hi) * T::RB;
+    if constexpr (T::SWZ)
+      return tb[nb & 1] + (uint32_t)(rows + 64 * nb);
+    else
+      return (uint32_t)(tr_row * T::RB + rows + 64 * nb + tr_col * 2);
+  };
+  uint32_t qt[2], ot[2];
+  tr_base(QT{}, qt);
+  tr_base(OT{}, ot);
+
+  // dV += P^T dO, dK += dS^T Q of step u: P as role A's operand registers,
+  // dS read back from the dS^T tile in the same (accumulator-row) order.
+  auto key_grads = [&](int u) {
+    const uint8_t* qb = sm.ring.t.q[u % kSlots];
+    const uint8_t* ob = sm.ring.t.dO[u % kSlots];
+    const uint16_t* dp = sm.sdST[u & 1] + (32 * wave + col) * DST_LD + 4 * half;
+    u32x4 pa[2], da[2];
+#pragma unroll
+    for (int st = 0; st < 2; st++) {
+      pa[st] = sm.sPA[u & 1][wave][st][lane];
+      const uint2 lo = *reinterpret_cast<const uint2*>(dp + 16 * st);
+      const uint2 hi = *reinterpret_cast<const uint2*>(dp + 16 * st + 8);
+      da[st] = u32x4{lo.x, lo.y, hi.x, hi.y};
+    }
+#pragma unroll
+    for (int st = 0; st < 2; st++) {
+#pragma unroll
+      for (int nb = 0; nb < DV / 32; nb++) {
+        const uint2 lo = lds_read_tr16((const uint16_t*)(ob + tr_off(OT{}, ot, st, 0, nb)));
+        const uint2 hi = lds_read_tr16((const uint16_t*)(ob + tr_off(OT{}, ot, st, 1, nb)));
+        dvacc[nb] = mfma32x32x16(as_bf16x8(pa[st]), as_bf16x8(u32x4{lo.x, lo.y, hi.x, hi.y}), dvacc[nb]);
+      }
+#pragma unroll
+      for (int nb = 0; nb < DQK / 32; nb++) {
+        const uint2 lo = lds_read_tr16((const uint16_t*)(qb + tr_off(QT{}, qt, st, 0, nb)));
+        const uint2 hi = lds_read_tr16((const uint16_t*)(qb + tr_off(QT{}, qt, st, 1, nb)));
+        dkacc[nb] = mfma32x32x16(as_bf16x8(da[st]), as_bf16x8(u32x4{lo.x, lo.y, hi.x, hi.y}), dkacc[nb]);
+      }
+    }
+  };
+  // Partial slot of step u: slot0 + u, slot0 = pbase[seq] + kb S - 2 kb (kb - 1)
+  // (the steps of the sequence's earlier key blocks); a slot holds h x NCB
+  // blocks of 1024 f16, [head][column block], each block two halves of
+  // [lane][8 accumulator registers] (registers 0-7, then 8-15), so that
+  // every 16-byte store of a wave covers 1 KB; dq_scale one float per block.
+  const int S_b = (L + BM - 1) / BM, kb = j0 / BN;
+  const int64_t slot0 = A.pbase[it.seq] + (int64_t)kb * S_b - 2 * (int64_t)kb * (kb - 1);
+  const int64_t blk0 = (slot0 * H + head) * NCB + wave;
+  uint16_t* const part_lane = A.dq_part + blk0 * 1024 + (int64_t)lane * 8;
+  const int64_t blk_stride = (int64_t)H * NCB;
+  auto dq_step = [&](int u) {
+    const uint16_t* dp = sm.sdST[u & 1] + tr_row * DST_LD + tr_col;
+    f32x16 qacc = f32x16{};
+#pragma unroll
+    for (int ks = 0; ks < KSTEPS; ks++) {
+      const uint2 lo = lds_read_tr16(dp + 16 * ks * DST_LD);
+      const uint2 hi = lds_read_tr16(dp + (16 * ks + 8) * DST_LD);
+      qacc = mfma32x32x16(as_bf16x8(u32x4{lo.x, lo.y, hi.x, hi.y}), as_bf16x8(kq[ks]), qacc);
+    }
+    // Block scale 2^(140 - e), e the biased exponent of the largest
+    // magnitude (clamped so that it and its inverse are normal floats).
+    float mx = 0.0f;
+#pragma unroll
+    for (int q = 0; q < 16; q++) mx = fmaxf(mx, fabsf(qacc[q]));
+    const int e = (int)((wave_max_dpp(__float_as_uint(mx)) >> 23) & 0xffu);
+    const uint32_t se = (uint32_t)min(max(267 - e, 1), 253);
+    const float sc = __uint_as_float(se << 23);
+    uint32_t h[8];
+#pragma unroll
+    for (int k = 0; k < 8; k++) h[k] = pack_f16x2(qacc[2 * k] * sc, qacc[2 * k + 1] * sc);
+    uint16_t* dst = part_lane + (int64_t)u * blk_stride * 1024;
+    *reinterpret_cast<u32x4*>(dst) = u32x4{h[0], h[1], h[2], h[3]};
+    *reinterpret_cast<u32x4*>(dst + 512) = u32x4{h[4], h[5], h[6], h[7]};
+    if (lane == 0) A.dq_scale[blk0 + (int64_t)u * blk_stride] = __uint_as_float((254u - se) << 23);
+  };
+
+  // The same barriers as role A: two in its prologue, one per step, then
+  // one for the last hand-over and one before its final flushes.
+  barrier_no_fence();  // (P1)
+  barrier_no_fence();  // (P2)
+  for (int u = 0; u < nsteps; u++) {
+    wait_vmcnt_lgkmcnt0<63>();
+    barrier_no_fence();
+    if (u >= 1) {
+      key_grads(u - 1);
+      if (wave < NCB) dq_step(u - 1);
+    }
+  }
+  wait_vmcnt_lgkmcnt0<63>();
+  barrier_no_fence();  // (L)
+  key_grads(nsteps - 1);
+  if (wave < NCB) dq_step(nsteps - 1);
+  wait_vmcnt_lgkmcnt0<63>();
+  barrier_no_fence();  // (E)
+
+#pragma unroll
+  for (int q = 0; q < 16; q++) {
+    const int j = jw0 + 8 * (q >> 2) + 4 * half + (q & 3);
+    if (j < L) {
+#pragma unroll
+      for (int nb = 0; nb < DQK / 32; nb++)
+        A.dK[((o + j) * H + head) * DQK + 32 * nb + col] = f32_to_bf16_bits(dkacc[nb][q] * invN);
+#pragma unroll
+      for (int nb = 0; nb < DV / 32; nb++)
+        A.dV[((o + j) * H + head) * DV + 32 * nb + col] = f32_to_bf16_bits(dvacc[nb][q] * invN);
+    }
+  }
+}
+
+constexpr int kRsThreads = 512;
+
+template <int DQK, int DV>
+__global__ __launch_bounds__(kRsThreads, 1) void attn_bwd_rs_kernel(
+    BwdArgs A, const WorkItem* __restrict__ items, const int32_t* __restrict__ count) {
+  using S = BwdSharedRS<DQK, DV>;
+  constexpr int BN = S::BN, KB_LD = S::KB_LD;
+  __shared__ S sm;
+  const JaggedArgs& ja = A.ja;
+  const int item = (int)(blockIdx.x / (unsigned)ja.num_heads);
+  const int head = (int)blockIdx.x - item * ja.num_heads;
+  if (item >= *count) return;
+  const WorkItem wi = items[item];
+  const int N = ja.max_seq_len, NB = ja.num_buckets;
+  RsItem it;
+  it.o = ja.seq_offsets[wi.seq];
+  it.seq = wi.seq;
+  it.L = (int)(ja.seq_offsets[wi.seq + 1] - it.o);
+  it.n_h = it.L - (ja.num_targets ? (int)ja.num_targets[wi.seq] : 0);
+  it.j0 = wi.blk * BN;
+  it.head = head;
+  // Candidate keys see only themselves; otherwise every later row sees them.
+  const int i_end = it.j0 >= it.n_h ? min(it.j0 + BN, it.L) : it.L;
+  it.nsteps = (i_end - it.j0 + S::BM - 1) / S::BM;
+  const int tid = threadIdx.x;
+  const int64_t tlo = ja.seq_trange[2 * wi.seq], thi = ja.seq_trange[2 * wi.seq + 1];
+  const bool fast = thi - tlo < ((int64_t)1 << 31);
+  for (int x = tid; x < 64; x += kRsThreads) {
+    sm.sTab[x] = (fast && x == 31) ? ja.rab_time[0] : ja.rab_time[min(63 - x, NB - 1)];
+    sm.sTacc[x] = 0.0f;
+  }
+  for (int x = tid; x < 4 * 2 * S::kRing; x += kRsThreads) (&sm.sRing[0][0][0])[x] = 0.0f;
+
+  // The block's K, row-major in LDS, then role B's dQ operand down its rows.
+  const int lane = tid & 63, wave = tid >> 6;
+  constexpr int NCB = DQK / 32, KSTEPS = BN / 16;
+  u32x4 kq[KSTEPS];
+  {
+    const uint16_t* kg = (const uint16_t*)A.t.k + it.o * A.t.k_stride + head * DQK;
+    const __amdgpu_buffer_rsrc_t krs = make_rsrc(kg, (uint32_t)(it.L * A.t.k_stride * 2));
+    const uint32_t kstride_b = (uint32_t)A.t.k_stride * 2u;
+    constexpr int KCH = BN * DQK / 8;
+    for (int c = tid; c < KCH; c += kRsThreads) {
+      const int r = c / (DQK / 8), cc = c % (DQK / 8);
+      *reinterpret_cast<u32x4*>(sm.ring.kblk + r * KB_LD + 8 * cc) =
+          buffer_load16(krs, (uint32_t)(it.j0 + r) * kstride_b + (uint32_t)cc * 16u);
+    }
+    __syncthreads();
+    if (wave >= 4 && wave < 4 + NCB) {
+      const int cbw = wave - 4, half = lane >> 5;
+      const int tr_row = 4 * half + ((lane & 15) >> 2);
+      const int tr_col = 16 * ((lane >> 4) & 1) + 4 * (lane & 3);
+      const uint16_t* kp = sm.ring.kblk + tr_row * KB_LD + 32 * cbw + tr_col;
+#pragma unroll
+      for (int ks = 0; ks < KSTEPS; ks++) {
+        const uint2 lo = lds_read_tr16(kp + 16 * ks * KB_LD);
+        const uint2 hi = lds_read_tr16(kp + (16 * ks + 8) * KB_LD);
+        kq[ks] = u32x4{lo.x, lo.y, hi.x, hi.y};
+      }
+    }
+    __syncthreads();  // the ring may be overwritten from here on
+  }
+
+  if (wave < 4) {
+    if (fast)
+      bwd_role_a<DQK, DV, true>(sm, A, it, tlo);
+    else
+      bwd_role_a<DQK, DV, false>(sm, A, it, tlo);
+  } else {
+    bwd_role_b<DQK, DV>(sm, A, it, kq);
+  }
+
+  __syncthreads();
+  const float invN = 1.0f / (float)N;
+  if (tid < 64) {
+    const float v = sm.sTacc[tid];
+    const int b = (fast && tid == 31) ? 0 : min(63 - tid, NB - 1);
+    if (v != 0.0f) unsafeAtomicAdd(&A.d_rab_time[b], v * invN);
+  }
+}
+
+// dQ of the two-role kernel.  Workgroup = (row block of 32 rows of one
+// sequence, head); wave = column block of 32.  It sums, in key-block
+// order, the partial blocks (f16 times their block scale) of every key
+// block that visits the row block
+// (all history blocks up to it; a candidate block only its own rows),
+// scales by 1/N and stores bf16 [T][h][d_qk].  Lane l holds column
+// 32 cb + l % 32 and rows 8g + 4 (l / 32) + m, the MFMA accumulator layout
+// the partials were stored in.
+template <int NCB>
+__global__ __launch_bounds__(64 * NCB) void dq_reduce_kernel(JaggedArgs ja,
+                                                             const uint16_t* __restrict__ part,
+                                                             const float* __restrict__ scale,
+                                                             const int64_t* __restrict__ rbase,
+                                                             const int64_t* __restrict__ pbase,
+                                                             uint16_t* __restrict__ dq) {
+  constexpr int DQK = 32 * NCB;
+  const int H = ja.num_heads, B = ja.num_seqs;
+  const int64_t nrb = rbase[B];
+  const int64_t gi = (int64_t)(blockIdx.x / (unsigned)H);
+  const int head = (int)(blockIdx.x % (unsigned)H);
+  if (gi >= nrb) return;
+  // Last row blocks first: within a sequence the later rows have the most
+  // key blocks to sum.
+  const int64_t g = nrb - 1 - gi;
+  // The sequence whose row blocks hold g: the last b with rbase[b] <= g
+  // (empty sequences have no row blocks).
+  int lo = 0, hi = B;
+  while (hi - lo > 1) {
+    const int mid = (lo + hi) >> 1;
+    if (rbase[mid] <= g) lo = mid; else hi = mid;
+  }
+  const int b = lo;
+  const int64_t o = ja.seq_offsets[b];
+  const int L = (int)(ja.seq_offsets[b + 1] - o);
+  const int n_h = L - (ja.num_targets ? (int)ja.num_targets[b] : 0);
+  const int i0 = (int)(g - rbase[b]) * kBwdBM;
+  const int S_b = (L + kBwdBM - 1) / kBwdBM;
+  const int lane = threadIdx.x & 63, cb = threadIdx.x >> 6;
+  const int col = lane & 31, half = lane >> 5;
+  float acc[16];
+#pragma unroll
+  for (int q = 0; q < 16; q++) acc[q] = 0.0f;
+  const int kb_max = i0 / kBwdBN;  // every key block starts at or before i0
+  const int64_t pb = pbase[b];
+  // Four key blocks per round: their loads are all issued before the
+  // round's sums (kept in key-block order).
+  for (int kb0 = 0; kb0 <= kb_max; kb0 += 4) {
+    u32x4 w0[4], w1[4];
+    float inv[4];
+    bool ok[4];
+#pragma unroll
+    for (int t = 0; t < 4; t++) {
+      const int kb = kb0 + t, j0 = kb * kBwdBN;
+      const int i_end = j0 >= n_h ? min(j0 + kBwdBN, L) : L;
+      ok[t] = kb <= kb_max && i0 < i_end;
+      if (ok[t]) {
+        const int64_t slot =
+            pb + (int64_t)kb * S_b - 2 * (int64_t)kb * (kb - 1) + (i0 - j0) / kBwdBM;
+        const int64_t blk = (slot * H + head) * NCB + cb;
+        const uint16_t* src = part + blk * 1024 + (int64_t)lane * 8;
+        w0[t] = *reinterpret_cast<const u32x4*>(src);
+        w1[t] = *reinterpret_cast<const u32x4*>(src + 512);
+        inv[t] = scale[blk];
+      }
+    }
+#pragma unroll
+    for (int t = 0; t < 4; t++) {
+      if (!ok[t]) continue;
+      const uint32_t w[8] = {w0[t][0], w0[t][1], w0[t][2], w0[t][3],
+                             w1[t][0], w1[t][1], w1[t][2], w1[t][3]};
+#pragma unroll
+      for (int k = 0; k < 8; k++) {
+        const float flo = (float)__builtin_bit_cast(_Float16, (uint16_t)(w[k] & 0xffffu));
+        const float fhi = (float)__builtin_bit_cast(_Float16, (uint16_t)(w[k] >> 16));
+        acc[2 * k] = __builtin_fmaf(flo, inv[t], acc[2 * k]);
+        acc[2 * k + 1] = __builtin_fmaf(fhi, inv[t], acc[2 * k + 1]);
+      }
+    }
+  }
+  const float invN = 1.0f / (float)ja.max_seq_len;
+#pragma unroll
+  for (int q = 0; q < 16; q++) {
+    const int i = i0 + 8 * (q >> 2) + 4 * half + (q & 3);
+    if (i < L) dq[((o + i) * H + head) * DQK + 32 * cb + col] = f32_to_bf16_bits(acc[q] * invN);
+  }
+}
+
 template <int DQK, int DV, bool SPLIT>
 __global__ __launch_bounds__(kBwdThreads, 1) void attn_bwd_bf16_kernel(
     BwdArgs A, const WorkItem* __restrict__ items, const int32_t* __restrict__ count) {
@@ -868,7 +1707,8 @@ __global__ __launch_bounds__(kBwdThreads, 1) void attn_bwd_bf16_kernel(
 
 template <int DQK, int DV>
 hipError_t launch_bwd(const JaggedArgs& ja, const Tensors& t, const void* d_out,
-                      const void* d_out_lo, float* dq_acc, void* dk, void* dv, float* d_rab_pos,
+                      const void* d_out_lo, float* dq_acc, uint16_t* dq_part, float* dq_scale,
+                      const int64_t* bases, void* dk, void* dv, float* d_rab_pos,
                       float* d_rab_time, const WorkItem* items, const int32_t* count,
                       int64_t max_items, hipStream_t s) {
   BwdArgs A;
@@ -877,32 +1717,37 @@ hipError_t launch_bwd(const JaggedArgs& ja, const Tensors& t, const void* d_out,
   A.dO = (const uint16_t*)d_out;
   A.dO_lo = (const uint16_t*)d_out_lo;
   A.dq_acc = dq_acc;
+  A.dq_part = dq_part;
+  A.dq_scale = dq_scale;
+  A.pbase = bases ? bases + (ja.num_seqs + 1) : nullptr;
   A.dK = (uint16_t*)dk;
   A.dV = (uint16_t*)dv;
   A.d_rab_pos = d_rab_pos;
   A.d_rab_time = d_rab_time;
   static_assert(sizeof(BwdShared<DQK, DV, true>) <= kLdsBytes, "LDS budget");
+  static_assert(sizeof(BwdSharedRS<DQK, DV>) <= kLdsBytes, "LDS budget");
   dim3 grid((unsigned)(max_items * ja.num_heads));
   if (d_out_lo)
     hipLaunchKernelGGL((attn_bwd_bf16_kernel<DQK, DV, true>), grid, dim3(kBwdThreads), 0, s, A,
                        items, count);
   else
-    hipLaunchKernelGGL((attn_bwd_bf16_kernel<DQK, DV, false>), grid, dim3(kBwdThreads), 0, s, A,
-                       items, count);
+    hipLaunchKernelGGL((attn_bwd_rs_kernel<DQK, DV>), grid, dim3(kRsThreads), 0, s, A, items,
+                       count);
   return hipGetLastError();
 }
 
 }  // namespace
 
 hipError_t launch_attn_bwd_bf16(const JaggedArgs& ja, const Tensors& t, int dqk, int dv,
-                                const void* d_out, const void* d_out_lo, float* dq_acc, void* dk,
-                                void* dv_out, float* d_rab_pos, float* d_rab_time,
+                                const void* d_out, const void* d_out_lo, float* dq_acc,
+                                uint16_t* dq_part, float* dq_scale, const int64_t* bases,
+                                void* dk, void* dv_out, float* d_rab_pos, float* d_rab_time,
                                 const WorkItem* items, const int32_t* count, int64_t max_items,
                                 hipStream_t s) {
-#define HSTU_BWD_CASE(A, B)                                                                 \
-  if (dqk == A && dv == B)                                                                  \
-    return launch_bwd<A, B>(ja, t, d_out, d_out_lo, dq_acc, dk, dv_out, d_rab_pos, d_rab_time, \
-                            items, count, max_items, s);
+#define HSTU_BWD_CASE(A, B)                                                                  \
+  if (dqk == A && dv == B)                                                                   \
+    return launch_bwd<A, B>(ja, t, d_out, d_out_lo, dq_acc, dq_part, dq_scale, bases, dk,     \
+                            dv_out, d_rab_pos, d_rab_time, items, count, max_items, s);
   HSTU_BWD_CASE(32, 32)
   HSTU_BWD_CASE(32, 64)
   HSTU_BWD_CASE(32, 128)
@@ -914,6 +1759,28 @@ hipError_t launch_attn_bwd_bf16(const JaggedArgs& ja, const Tensors& t, int dqk,
   HSTU_BWD_CASE(128, 128)
 #undef HSTU_BWD_CASE
   return hipErrorInvalidValue;
+}
+
+hipError_t launch_dq_reduce_bf16(const JaggedArgs& ja, int dqk, const uint16_t* dq_part,
+                                 const float* dq_scale, const int64_t* bases, void* dq,
+                                 hipStream_t s) {
+  // Row blocks: at most ceil(T / 32) + B; workgroups past the true count return.
+  const int64_t nrb = (ja.total_tokens + kBwdBM - 1) / kBwdBM + ja.num_seqs;
+  const dim3 grid((unsigned)(nrb * ja.num_heads));
+  const int64_t* rbase = bases;
+  const int64_t* pbase = bases + ja.num_seqs + 1;
+  if (dqk == 32)
+    hipLaunchKernelGGL((dq_reduce_kernel<1>), grid, dim3(64), 0, s, ja, dq_part, dq_scale, rbase,
+                       pbase, (uint16_t*)dq);
+  else if (dqk == 64)
+    hipLaunchKernelGGL((dq_reduce_kernel<2>), grid, dim3(128), 0, s, ja, dq_part, dq_scale, rbase,
+                       pbase, (uint16_t*)dq);
+  else if (dqk == 128)
+    hipLaunchKernelGGL((dq_reduce_kernel<4>), grid, dim3(256), 0, s, ja, dq_part, dq_scale, rbase,
+                       pbase, (uint16_t*)dq);
+  else
+    return hipErrorInvalidValue;
+  return hipGetLastError();
 }
 
 }  // namespace hstu

@@ -72,6 +72,16 @@ __device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
   return __builtin_bit_cast(uint32_t, r);
 }
 
+typedef _Float16 f16x2 __attribute__((ext_vector_type(2)));
+
+// Packs two floats into two f16 (round to nearest even) in one dword.
+__device__ __forceinline__ uint32_t pack_f16x2(float lo, float hi) {
+  f16x2 r;
+  r[0] = (_Float16)lo;
+  r[1] = (_Float16)hi;
+  return __builtin_bit_cast(uint32_t, r);
+}
+
 __device__ __forceinline__ float bf16_bits_to_f32(uint16_t b) {
   return __uint_as_float(((uint32_t)b) << 16);
 }

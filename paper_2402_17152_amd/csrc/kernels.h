@@ -74,9 +74,11 @@ struct PrepFills {
 //    backward (seq, k-block of kBwdBN keys);
 //  - per-sequence timestamp min / max into trange[2b], trange[2b+1] (0, 0
 //    for an empty sequence);
-//  - zeroing the arrays in `fills`.
+//  - zeroing the arrays in `fills`;
+//  - if `bases` is set, the slot tables of the two-role backward's partial
+//    dQ blocks (int64 [2 (B + 1)]: row-block and partial-slot prefixes).
 hipError_t launch_prep(const JaggedArgs& ja, int mode, WorkItem* items, int32_t* count,
-                       int64_t* trange, const PrepFills& fills, hipStream_t s);
+                       int64_t* trange, const PrepFills& fills, int64_t* bases, hipStream_t s);
 
 hipError_t launch_fill_f32(float* p, int64_t n, float value, hipStream_t s);
 hipError_t launch_complete_cumsum(int32_t n, const int64_t* in, int64_t* out, int square_of_diff,
@@ -102,11 +104,29 @@ hipError_t launch_cached_self(int is_bf16, const JaggedArgs& ja, int32_t dqk, in
                               const Tensors& t, const float* o32, void* out, hipStream_t s);
 // d_out_lo: null, or the low bf16 terms of dO (d_out holding the high
 // ones), for a dO that is the fp32 output of the layer's LayerNorm backward.
+// With d_out_lo null the two-role kernel runs and stores dQ as scaled f16
+// partial blocks in dq_part / dq_scale (slots from `bases`;
+// launch_dq_reduce_bf16 sums them); otherwise the single-role kernel adds dQ to the zeroed fp32
+// dq_acc [h][T][d_qk] with atomics (launch_dq_convert_bf16 then).
 hipError_t launch_attn_bwd_bf16(const JaggedArgs& ja, const Tensors& t, int dqk, int dv,
-                                const void* d_out, const void* d_out_lo, float* dq_acc, void* dk,
-                                void* dv_out, float* d_rab_pos, float* d_rab_time,
+                                const void* d_out, const void* d_out_lo, float* dq_acc,
+                                uint16_t* dq_part, float* dq_scale, const int64_t* bases,
+                                void* dk, void* dv_out, float* d_rab_pos, float* d_rab_time,
                                 const WorkItem* items, const int32_t* count, int64_t max_items,
                                 hipStream_t s);
+// dQ of the two-role backward (d_out_lo null): sums the f16 partial
+// blocks in dq_part times their scales in dq_scale (slots laid out by the
+// bases launch_prep writes) into bf16 dq [T][h][d_qk], scaled by 1/N.
+hipError_t launch_dq_reduce_bf16(const JaggedArgs& ja, int dqk, const uint16_t* dq_part,
+                                 const float* dq_scale, const int64_t* bases, void* dq,
+                                 hipStream_t s);
+// Partial-slot count bound of the two-role backward (32-row steps of every
+// 128-key block): sum over sequences of K S - 2 K (K - 1), K = ceil(L/128),
+// S = ceil(L/32), bounded from T, B and N alone.
+inline int64_t dq_part_slots_bound(int64_t T, int32_t B, int32_t N) {
+  return (N * T + 254 * T + 16129 * (int64_t)B + 8191) / 8192 + (T + 127 * (int64_t)B + 63) / 64 +
+         B;
+}
 // fp32 head-major dQ accumulator [h][T][d] -> bf16 token-major [T][h][d], scaled.
 hipError_t launch_dq_convert_bf16(const float* acc, void* dq, int64_t T, int32_t H, int32_t d,
                                   float scale, hipStream_t s);

@@ -246,30 +246,77 @@ __device__ void fill_blocks(const PrepFills& fills, int f, int nf) {
   }
 }
 
+// Slot tables of the two-role backward's partial dQ blocks: bases[b] =
+// sum over b' < b of ceil(L/32) (row blocks), bases[B + 1 + b] = sum over
+// b' < b of K S - 2 K (K - 1) with K = ceil(L/128), S = ceil(L/32) (the
+// 32-row steps of all 128-key blocks of a sequence).
+__device__ void bases_block(const JaggedArgs& ja, int64_t* bases, int64_t (*s)[kSchedThreads]) {
+  const int tid = threadIdx.x, B = ja.num_seqs;
+  int64_t* rbase = bases;
+  int64_t* pbase = bases + B + 1;
+  if (tid == 0) {
+    rbase[0] = 0;
+    pbase[0] = 0;
+  }
+  int64_t carry_r = 0, carry_p = 0;
+  for (int base = 0; base < B; base += kSchedThreads) {
+    const int b = base + tid;
+    int64_t r = 0, q = 0;
+    if (b < B) {
+      const int64_t L = ja.seq_offsets[b + 1] - ja.seq_offsets[b];
+      const int64_t S = (L + kBwdBM - 1) / kBwdBM, K = (L + kBwdBN - 1) / kBwdBN;
+      r = S;
+      q = K * S - 2 * K * (K - 1);
+    }
+    s[0][tid] = r;
+    s[1][tid] = q;
+    __syncthreads();
+    for (int off = 1; off < kSchedThreads; off <<= 1) {
+      const int64_t a = tid >= off ? s[0][tid - off] : 0;
+      const int64_t c = tid >= off ? s[1][tid - off] : 0;
+      __syncthreads();
+      s[0][tid] += a;
+      s[1][tid] += c;
+      __syncthreads();
+    }
+    if (b < B) {
+      rbase[b + 1] = carry_r + s[0][tid];
+      pbase[b + 1] = carry_p + s[1][tid];
+    }
+    carry_r += s[0][kSchedThreads - 1];
+    carry_p += s[1][kSchedThreads - 1];
+    __syncthreads();
+  }
+}
+
 // Everything an attention call needs before its main kernel, in one
 // launch: workgroup 0 builds the work list, workgroups 1..B take one
-// sequence's timestamp range each, the rest zero the fills.
+// sequence's timestamp range each, the next ones zero the fills, and (if
+// `bases` is set) the last one writes the backward's slot tables.
 __global__ __launch_bounds__(kSchedThreads) void prep_kernel(JaggedArgs ja, int mode,
                                                              WorkItem* items, int32_t* count,
                                                              int64_t* trange, PrepFills fills,
-                                                             int nfill_blocks) {
+                                                             int nfill_blocks, int64_t* bases) {
   extern __shared__ int s_bins[];  // [maxw + 1]
   __shared__ int s_scan[kSchedThreads];
   __shared__ int64_t red[2][kSchedThreads / 64];
+  __shared__ int64_t s_bases[2][kSchedThreads];
   const int g = (int)blockIdx.x;
   if (g == 0) {
     schedule_block(ja, mode, items, count, s_bins, s_scan);
   } else if (g <= ja.num_seqs) {
     time_range_block(ja, g - 1, trange, red);
-  } else {
+  } else if (g <= ja.num_seqs + nfill_blocks) {
     fill_blocks(fills, g - 1 - ja.num_seqs, nfill_blocks);
+  } else {
+    bases_block(ja, bases, s_bases);
   }
 }
 
 }  // namespace
 
 hipError_t launch_prep(const JaggedArgs& ja, int mode, WorkItem* items, int32_t* count,
-                       int64_t* trange, const PrepFills& fills, hipStream_t s) {
+                       int64_t* trange, const PrepFills& fills, int64_t* bases, hipStream_t s) {
   const int maxw = mode == 0 ? (ja.max_seq_len + kFwdBN - 1) / kFwdBN
                              : (ja.max_seq_len + kBwdBM - 1) / kBwdBM;
   const size_t lds = sizeof(int) * (size_t)(maxw + 1);
@@ -279,9 +326,9 @@ hipError_t launch_prep(const JaggedArgs& ja, int mode, WorkItem* items, int32_t*
   int64_t nf = (work4 + 4 * kSchedThreads - 1) / (4 * kSchedThreads);
   nf = nf > 1024 ? 1024 : nf;
   if (work4 > 0 && nf < 1) nf = 1;
-  const int64_t grid = 1 + (int64_t)ja.num_seqs + nf;
+  const int64_t grid = 1 + (int64_t)ja.num_seqs + nf + (bases ? 1 : 0);
   hipLaunchKernelGGL(prep_kernel, dim3((unsigned)grid), dim3(kSchedThreads), lds, s, ja, mode,
-                     items, count, trange, fills, (int)nf);
+                     items, count, trange, fills, (int)nf, bases);
   return hipGetLastError();
 }
 

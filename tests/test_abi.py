@@ -58,6 +58,32 @@ def test_workspace_bytes(hs):
     assert 0 < f < n
 
 
+def _partial_slots(lengths):
+    """Slots of the bf16 backward's partial dQ blocks: one per 32-row step
+    of every 128-key block (rows from the block's first key to the end)."""
+    n = 0
+    for L in lengths:
+        for j0 in range(0, L, 128):
+            n += (L - j0 + 31) // 32
+    return n
+
+
+@pytest.mark.parametrize("N,B,extra", [(8192, 8, 0), (4096, 64, 0), (129, 5, 0), (127, 3, 50),
+                                       (1, 40, 0), (300, 7, 299), (3072, 16, 0)])
+def test_workspace_covers_partial_dq(hs, N, B, extra):
+    """The workspace bound (computed from T, B and N only) holds the partial
+    dQ blocks of the worst jagged batch with that T: as many sequences of
+    length N as fit, the remainder in one more (the slot count is convex in
+    L, so that is its maximum)."""
+    lengths = [N] * B + ([extra] if extra else [])
+    T = sum(lengths)
+    for h, d in ((4, 128), (8, 64), (2, 32)):
+        p = _problem(hs, num_seqs=len(lengths), total_tokens=T, max_seq_len=N, num_heads=h, d_qk=d,
+                     d_v=d)
+        need = _partial_slots(lengths) * h * d * 32 * 2
+        assert hs.hstu_workspace_bytes(p) >= need
+
+
 FAKE = 0x10000  # 64 KiB-aligned, never dereferenced: every call fails validation first
 
 
