@@ -1,6 +1,18 @@
-"""Turns a rocprofv3 --stats kernel CSV into a short markdown table."""
+"""Turns rocprofv3 output into the short summaries kept under profiles/.
+
+  kernels <stats.csv> <title> <command> [note]
+      --kernel-trace --stats CSV -> markdown table of per-kernel times.
+  traffic <F.csv> <W.csv> <CF.csv> <CW.csv> <kernel-substring> <name> <workload> <source_hash>
+      two --pmc runs (FETCH_SIZE, WRITE_SIZE) of a workload and the same two
+      of the 256 MiB device copy (bench.py --calibrate-copy) -> the JSON
+      record bench.py reads (HBM bytes per launch of one kernel, each
+      counter scaled by what it reads for the copy).
+"""
 import csv
+import json
 import sys
+
+COPY_KIB = 256 * 1024  # the calibration copy moves 256 MiB each way
 
 
 def short_name(name: str) -> str:
@@ -8,7 +20,7 @@ def short_name(name: str) -> str:
     return name.split("(")[0]
 
 
-def main(csv_path: str, title: str, command: str, note: str = "") -> str:
+def kernels(csv_path: str, title: str, command: str, note: str = "") -> str:
     rows = list(csv.DictReader(open(csv_path)))
     out = [f"# {title}", "", "Command (on the GPU host, from /tmp with TMPDIR=/tmp):", "", "```",
            command, "```", ""]
@@ -22,5 +34,26 @@ def main(csv_path: str, title: str, command: str, note: str = "") -> str:
     return "\n".join(out) + "\n"
 
 
+def _mean_kib(path: str, counter: str, kernel_sub: str) -> float:
+    vals = [float(r["Counter_Value"]) for r in csv.DictReader(open(path))
+            if r["Counter_Name"] == counter and kernel_sub in r["Kernel_Name"]]
+    if not vals:
+        raise SystemExit(f"no {counter} rows for {kernel_sub!r} in {path}")
+    return sum(vals) / len(vals)
+
+
+def traffic(f_csv, w_csv, cf_csv, cw_csv, kernel_sub, name, workload, source_hash) -> str:
+    fetch = _mean_kib(f_csv, "FETCH_SIZE", kernel_sub)
+    write = _mean_kib(w_csv, "WRITE_SIZE", kernel_sub)
+    ff = COPY_KIB / _mean_kib(cf_csv, "FETCH_SIZE", "copyBuffer")
+    wf = COPY_KIB / _mean_kib(cw_csv, "WRITE_SIZE", "copyBuffer")
+    rec = {"kernel": name, "workload": workload, "source_hash": source_hash,
+           "fetch_kib": fetch, "write_kib": write, "fetch_factor": ff, "write_factor": wf,
+           "hbm_bytes_per_launch": (fetch * ff + write * wf) * 1024.0,
+           "summary": f"profiles/traffic_{workload}.md"}
+    return json.dumps(rec, indent=1) + "\n"
+
+
 if __name__ == "__main__":
-    print(main(*sys.argv[1:]), end="")
+    cmd, args = sys.argv[1], sys.argv[2:]
+    print({"kernels": kernels, "traffic": traffic}[cmd](*args), end="")
