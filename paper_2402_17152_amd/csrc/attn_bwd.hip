@@ -1176,23 +1176,25 @@ __device__ __forceinline__ void bwd_role_a(BwdSharedRS<DQK, DV>& sm, const BwdAr
   };
   constexpr int kRing = Sh::kRing;
   const int perm_base = lane * 4;
-  float wrap_w[16];
-#pragma unroll
-  for (int q = 0; q < 16; q++) wrap_w[q] = col + 8 * (q >> 2) + (q & 3) >= 32 ? 1.0f : 0.0f;
+  // Lane (col, half) reads register q = 4g + m from lane + r0(q), r0 =
+  // 8g + m (mod 64); the value crossed into the other half-wave when
+  // r0(q) >= 32 - col (a suffix of q, since r0 grows with q), so the
+  // lane's own diagonal gets the prefix sum before that point.
+  const int wrap_from = 32 - col;
   float* const ring_mine = sm.sRing[wave][half];
-  const int d1_lane = 4 * half - col - 32 * wave;
-  float carry = 0.0f;
+  const int d1_lane = 4 * half - col - 32 * wave;  // D1 = 32 u + d1_lane
+  float carry = 0.0f;  // partner's crossing sum of the previous step
   auto pos_step = [&](int u, const float (&ds)[16]) {
-    float sum = 0.0f, wsum = 0.0f;
+    float sum = 0.0f, nowrap = 0.0f;
 #pragma unroll
     for (int q = 0; q < 16; q++) {
       const float rv = __int_as_float(__builtin_amdgcn_ds_bpermute(
           perm_base + 4 * (8 * (q >> 2) + (q & 3)), __float_as_int(ds[q])));
       sum += rv;
-      wsum = __builtin_fmaf(rv, wrap_w[q], wsum);
+      if (8 * (q >> 2) + (q & 3) < wrap_from) nowrap = sum;
     }
-    ring_mine[(32 * u + d1_lane) & (kRing - 1)] = (sum - wsum) + carry;
-    carry = __int_as_float(__builtin_amdgcn_ds_bpermute(perm_base ^ 128, __float_as_int(wsum)));
+    ring_mine[(32 * u + d1_lane) & (kRing - 1)] = nowrap + carry;
+    carry = __int_as_float(__builtin_amdgcn_ds_bpermute(perm_base ^ 128, __float_as_int(sum - nowrap)));
   };
   const int R = L - j0;
   auto ring_flush = [&](int c) {
