@@ -946,10 +946,11 @@ __device__ __forceinline__ void bwd_role_a(BwdSharedRS<DQK, DV>& sm, const BwdAr
   a_base(OT{}, oa);
 
   // ---- staging by LDS DMA: Q, dO and the rab_pos window three steps
-  // ahead, row timestamps five.  Only role A issues DMA; the wait at step
-  // u needs the tiles and window of step u + 1, issued at step u - 2 and
-  // followed by that step's timestamp operation and all of step u - 1's
-  // (later atomics only make the wait stricter).
+  // ahead, row timestamps five.  Only role A issues DMA.  Step u needs the
+  // tiles and window of step u + 1 and (for reduce_ts(u + 3)) the row
+  // timestamps of step u + 3, all issued at step u - 2, the timestamps
+  // last; only step u - 1's operations follow them, so the wait at step
+  // u allows OPS_PER_STEP outstanding (later atomics only make it stricter).
   constexpr int OPS_PER_STEP = QT::OPW + OT::OPW + 3 + 1;
   const u32x4 qrs = rsrc_words(qg, (uint32_t)(L * A.t.q_stride * 2));
   const u32x4 ors = rsrc_words(dog, (uint32_t)L * dostride_b);
@@ -1269,7 +1270,7 @@ __device__ __forceinline__ void bwd_role_a(BwdSharedRS<DQK, DV>& sm, const BwdAr
   // through SiLU'; one barrier per step (role B runs the same count).
   Path path_cur, path_next, path_nn;
   auto step = [&](int u, f32x16& s_cur, f32x16& p_cur, f32x16& s_next, f32x16& p_next) {
-    wait_vmcnt_lgkmcnt0<OPS_PER_STEP + 1>();
+    wait_vmcnt_lgkmcnt0<OPS_PER_STEP>();
     barrier_no_fence();
     if (u >= 5 && wave == (u & 3)) ring_flush(u - 5);
     issue_tiles(u + 3);
