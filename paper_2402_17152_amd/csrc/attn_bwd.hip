@@ -1453,8 +1453,8 @@ __device__ __forceinline__ void bwd_role_b(BwdSharedRS<DQK, DV>& sm, const BwdAr
 #pragma unroll
     for (int k = 0; k < 8; k++) h[k] = pack_f16x2(qacc[2 * k] * sc, qacc[2 * k + 1] * sc);
     uint16_t* dst = part_lane + (int64_t)u * blk_stride * 1024;
-    *reinterpret_cast<u32x4*>(dst) = u32x4{h[0], h[1], h[2], h[3]};
-    *reinterpret_cast<u32x4*>(dst + 512) = u32x4{h[4], h[5], h[6], h[7]};
+    __builtin_nontemporal_store(u32x4{h[0], h[1], h[2], h[3]}, reinterpret_cast<u32x4*>(dst));
+    __builtin_nontemporal_store(u32x4{h[4], h[5], h[6], h[7]}, reinterpret_cast<u32x4*>(dst + 512));
     if (lane == 0) A.dq_scale[blk0 + (int64_t)u * blk_stride] = __uint_as_float((254u - se) << 23);
   };
 
@@ -1617,7 +1617,8 @@ __global__ __launch_bounds__(64 * NCB) void dq_reduce_kernel(JaggedArgs ja,
   const int kb_max = i0 / kBwdBN;  // every key block starts at or before i0
   const int64_t pb = pbase[b];
   // Four key blocks per round: their loads are all issued before the
-  // round's sums (kept in key-block order).
+  // round's sums (kept in key-block order).  The partial blocks are read
+  // once, so the loads are non-temporal (as are the backward's stores).
   for (int kb0 = 0; kb0 <= kb_max; kb0 += 4) {
     u32x4 w0[4], w1[4];
     float inv[4];
@@ -1632,8 +1633,8 @@ __global__ __launch_bounds__(64 * NCB) void dq_reduce_kernel(JaggedArgs ja,
             pb + (int64_t)kb * S_b - 2 * (int64_t)kb * (kb - 1) + (i0 - j0) / kBwdBM;
         const int64_t blk = (slot * H + head) * NCB + cb;
         const uint16_t* src = part + blk * 1024 + (int64_t)lane * 8;
-        w0[t] = *reinterpret_cast<const u32x4*>(src);
-        w1[t] = *reinterpret_cast<const u32x4*>(src + 512);
+        w0[t] = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(src));
+        w1[t] = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(src + 512));
         inv[t] = scale[blk];
       }
     }
