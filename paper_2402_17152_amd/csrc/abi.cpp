@@ -812,6 +812,7 @@ hstu_status_t attn_bwd_impl(const hstu_problem_t* p, const hstu_jagged_t* j, con
   float* dq_acc = (float*)(w + l.dq_acc);
   uint16_t* dq_part = (uint16_t*)(w + l.dq_part);
   float* dq_scale = (float*)(w + l.dq_scale);
+  const int64_t dq_slots = dq_part_slots_bound(T, p->num_seqs, N);
   int64_t* bases = (int64_t*)(w + l.bases);
   const int64_t ndq = T * H * p->d_qk;
   ja.seq_trange = (const int64_t*)(w + l.trange);
@@ -830,8 +831,8 @@ hstu_status_t attn_bwd_impl(const hstu_problem_t* p, const hstu_jagged_t* j, con
   {
     TimedScope ts("attn_bwd", s);
     HSTU_HIP(launch_attn_bwd_bf16(ja, t, p->d_qk, p->d_v, d_out, d_out_lo, dq_acc, dq_part,
-                                  dq_scale, bases, dk, dv, d_rab_pos, d_rab_time, items,
-                                  counts + 1, l.max_bwd, s),
+                                  dq_scale, dq_slots, bases, dk, dv, d_rab_pos, d_rab_time,
+                                  items, counts + 1, l.max_bwd, s),
              "attn_bwd launch");
   }
   if (split)
@@ -839,7 +840,7 @@ hstu_status_t attn_bwd_impl(const hstu_problem_t* p, const hstu_jagged_t* j, con
              "dq convert launch");
   else {
     TimedScope ts("dq_reduce", s);
-    HSTU_HIP(launch_dq_reduce_bf16(ja, p->d_qk, dq_part, dq_scale, bases, dq, s),
+    HSTU_HIP(launch_dq_reduce_bf16(ja, p->d_qk, dq_part, dq_scale, dq_slots, bases, dq, s),
              "dq reduce launch");
   }
   return ok();

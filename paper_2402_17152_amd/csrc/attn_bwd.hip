@@ -131,6 +131,8 @@ struct BwdArgs {
   uint16_t* dq_part;     // two-role kernel: f16 partial dQ blocks (see dq_step)
   float* dq_scale;       // two-role kernel: one power-of-two scale per partial block
   const int64_t* pbase;  // two-role kernel: [B+1] first partial slot of each sequence
+  int64_t dq_slots;      // two-role kernel: slots the partial buffer holds (sized for L <= N;
+                         // slots past it, only reachable with longer sequences, are skipped)
   uint16_t* dK;
   uint16_t* dV;
   float* d_rab_pos;
@@ -1452,6 +1454,7 @@ __device__ __forceinline__ void bwd_role_b(BwdSharedRS<DQK, DV>& sm, const BwdAr
     uint32_t h[8];
 #pragma unroll
     for (int k = 0; k < 8; k++) h[k] = pack_f16x2(qacc[2 * k] * sc, qacc[2 * k + 1] * sc);
+    if (slot0 + u >= A.dq_slots) return;
     uint16_t* dst = part_lane + (int64_t)u * blk_stride * 1024;
     __builtin_nontemporal_store(u32x4{h[0], h[1], h[2], h[3]}, reinterpret_cast<u32x4*>(dst));
     __builtin_nontemporal_store(u32x4{h[4], h[5], h[6], h[7]}, reinterpret_cast<u32x4*>(dst + 512));
@@ -1586,6 +1589,7 @@ __global__ __launch_bounds__(64 * NCB) void dq_reduce_kernel(JaggedArgs ja,
                                                              const float* __restrict__ scale,
                                                              const int64_t* __restrict__ rbase,
                                                              const int64_t* __restrict__ pbase,
+                                                             int64_t dq_slots,
                                                              uint16_t* __restrict__ dq) {
   constexpr int DQK = 32 * NCB;
   const int H = ja.num_heads, B = ja.num_seqs;
@@ -1627,10 +1631,10 @@ __global__ __launch_bounds__(64 * NCB) void dq_reduce_kernel(JaggedArgs ja,
     for (int t = 0; t < 4; t++) {
       const int kb = kb0 + t, j0 = kb * kBwdBN;
       const int i_end = j0 >= n_h ? min(j0 + kBwdBN, L) : L;
-      ok[t] = kb <= kb_max && i0 < i_end;
+      const int64_t slot =
+          pb + (int64_t)kb * S_b - 2 * (int64_t)kb * (kb - 1) + (i0 - j0) / kBwdBM;
+      ok[t] = kb <= kb_max && i0 < i_end && slot < dq_slots;
       if (ok[t]) {
-        const int64_t slot =
-            pb + (int64_t)kb * S_b - 2 * (int64_t)kb * (kb - 1) + (i0 - j0) / kBwdBM;
         const int64_t blk = (slot * H + head) * NCB + cb;
         const uint16_t* src = part + blk * 1024 + (int64_t)lane * 8;
         w0[t] = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(src));
@@ -1712,7 +1716,7 @@ __global__ __launch_bounds__(kBwdThreads, 1) void attn_bwd_bf16_kernel(
 template <int DQK, int DV>
 hipError_t launch_bwd(const JaggedArgs& ja, const Tensors& t, const void* d_out,
                       const void* d_out_lo, float* dq_acc, uint16_t* dq_part, float* dq_scale,
-                      const int64_t* bases, void* dk, void* dv, float* d_rab_pos,
+                      int64_t dq_slots, const int64_t* bases, void* dk, void* dv, float* d_rab_pos,
                       float* d_rab_time, const WorkItem* items, const int32_t* count,
                       int64_t max_items, hipStream_t s) {
   BwdArgs A;
@@ -1723,6 +1727,7 @@ hipError_t launch_bwd(const JaggedArgs& ja, const Tensors& t, const void* d_out,
   A.dq_acc = dq_acc;
   A.dq_part = dq_part;
   A.dq_scale = dq_scale;
+  A.dq_slots = dq_slots;
   A.pbase = bases ? bases + (ja.num_seqs + 1) : nullptr;
   A.dK = (uint16_t*)dk;
   A.dV = (uint16_t*)dv;
@@ -1744,14 +1749,15 @@ hipError_t launch_bwd(const JaggedArgs& ja, const Tensors& t, const void* d_out,
 
 hipError_t launch_attn_bwd_bf16(const JaggedArgs& ja, const Tensors& t, int dqk, int dv,
                                 const void* d_out, const void* d_out_lo, float* dq_acc,
-                                uint16_t* dq_part, float* dq_scale, const int64_t* bases,
-                                void* dk, void* dv_out, float* d_rab_pos, float* d_rab_time,
+                                uint16_t* dq_part, float* dq_scale, int64_t dq_slots,
+                                const int64_t* bases, void* dk, void* dv_out, float* d_rab_pos,
+                                float* d_rab_time,
                                 const WorkItem* items, const int32_t* count, int64_t max_items,
                                 hipStream_t s) {
 #define HSTU_BWD_CASE(A, B)                                                                  \
   if (dqk == A && dv == B)                                                                   \
-    return launch_bwd<A, B>(ja, t, d_out, d_out_lo, dq_acc, dq_part, dq_scale, bases, dk,     \
-                            dv_out, d_rab_pos, d_rab_time, items, count, max_items, s);
+    return launch_bwd<A, B>(ja, t, d_out, d_out_lo, dq_acc, dq_part, dq_scale, dq_slots, bases,\
+                            dk, dv_out, d_rab_pos, d_rab_time, items, count, max_items, s);
   HSTU_BWD_CASE(32, 32)
   HSTU_BWD_CASE(32, 64)
   HSTU_BWD_CASE(32, 128)
@@ -1766,8 +1772,8 @@ hipError_t launch_attn_bwd_bf16(const JaggedArgs& ja, const Tensors& t, int dqk,
 }
 
 hipError_t launch_dq_reduce_bf16(const JaggedArgs& ja, int dqk, const uint16_t* dq_part,
-                                 const float* dq_scale, const int64_t* bases, void* dq,
-                                 hipStream_t s) {
+                                 const float* dq_scale, int64_t dq_slots, const int64_t* bases,
+                                 void* dq, hipStream_t s) {
   // Row blocks: at most ceil(T / 32) + B; workgroups past the true count return.
   const int64_t nrb = (ja.total_tokens + kBwdBM - 1) / kBwdBM + ja.num_seqs;
   const dim3 grid((unsigned)(nrb * ja.num_heads));
@@ -1775,13 +1781,13 @@ hipError_t launch_dq_reduce_bf16(const JaggedArgs& ja, int dqk, const uint16_t* 
   const int64_t* pbase = bases + ja.num_seqs + 1;
   if (dqk == 32)
     hipLaunchKernelGGL((dq_reduce_kernel<1>), grid, dim3(64), 0, s, ja, dq_part, dq_scale, rbase,
-                       pbase, (uint16_t*)dq);
+                       pbase, dq_slots, (uint16_t*)dq);
   else if (dqk == 64)
     hipLaunchKernelGGL((dq_reduce_kernel<2>), grid, dim3(128), 0, s, ja, dq_part, dq_scale, rbase,
-                       pbase, (uint16_t*)dq);
+                       pbase, dq_slots, (uint16_t*)dq);
   else if (dqk == 128)
     hipLaunchKernelGGL((dq_reduce_kernel<4>), grid, dim3(256), 0, s, ja, dq_part, dq_scale, rbase,
-                       pbase, (uint16_t*)dq);
+                       pbase, dq_slots, (uint16_t*)dq);
   else
     return hipErrorInvalidValue;
   return hipGetLastError();

@@ -110,16 +110,18 @@ hipError_t launch_cached_self(int is_bf16, const JaggedArgs& ja, int32_t dqk, in
 // dq_acc [h][T][d_qk] with atomics (launch_dq_convert_bf16 then).
 hipError_t launch_attn_bwd_bf16(const JaggedArgs& ja, const Tensors& t, int dqk, int dv,
                                 const void* d_out, const void* d_out_lo, float* dq_acc,
-                                uint16_t* dq_part, float* dq_scale, const int64_t* bases,
-                                void* dk, void* dv_out, float* d_rab_pos, float* d_rab_time,
-                                const WorkItem* items, const int32_t* count, int64_t max_items,
-                                hipStream_t s);
+                                uint16_t* dq_part, float* dq_scale, int64_t dq_slots,
+                                const int64_t* bases, void* dk, void* dv_out, float* d_rab_pos,
+                                float* d_rab_time, const WorkItem* items, const int32_t* count,
+                                int64_t max_items, hipStream_t s);
 // dQ of the two-role backward (d_out_lo null): sums the f16 partial
 // blocks in dq_part times their scales in dq_scale (slots laid out by the
 // bases launch_prep writes) into bf16 dq [T][h][d_qk], scaled by 1/N.
+// dq_slots: the slots the buffer holds; both kernels skip slots past it,
+// which only sequences longer than N (a data error) can reach.
 hipError_t launch_dq_reduce_bf16(const JaggedArgs& ja, int dqk, const uint16_t* dq_part,
-                                 const float* dq_scale, const int64_t* bases, void* dq,
-                                 hipStream_t s);
+                                 const float* dq_scale, int64_t dq_slots, const int64_t* bases,
+                                 void* dq, hipStream_t s);
 // Partial-slot count bound of the two-role backward (32-row steps of every
 // 128-key block): sum over sequences of K S - 2 K (K - 1), K = ceil(L/128),
 // S = ceil(L/32), bounded from T, B and N alone.
