@@ -1620,15 +1620,17 @@ __global__ __launch_bounds__(64 * NCB) void dq_reduce_kernel(JaggedArgs ja,
   for (int q = 0; q < 16; q++) acc[q] = 0.0f;
   const int kb_max = i0 / kBwdBN;  // every key block starts at or before i0
   const int64_t pb = pbase[b];
-  // Four key blocks per round: their loads are all issued before the
+  // Sixteen key blocks per round (32 loads in flight per lane; four and
+  // eight ran 7 % and 2 % slower): their loads are all issued before the
   // round's sums (kept in key-block order).  The partial blocks are read
   // once, so the loads are non-temporal (as are the backward's stores).
-  for (int kb0 = 0; kb0 <= kb_max; kb0 += 4) {
-    u32x4 w0[4], w1[4];
-    float inv[4];
-    bool ok[4];
+  constexpr int KR = 16;
+  for (int kb0 = 0; kb0 <= kb_max; kb0 += KR) {
+    u32x4 w0[KR], w1[KR];
+    float inv[KR];
+    bool ok[KR];
 #pragma unroll
-    for (int t = 0; t < 4; t++) {
+    for (int t = 0; t < KR; t++) {
       const int kb = kb0 + t, j0 = kb * kBwdBN;
       const int i_end = j0 >= n_h ? min(j0 + kBwdBN, L) : L;
       const int64_t slot =
@@ -1643,7 +1645,7 @@ __global__ __launch_bounds__(64 * NCB) void dq_reduce_kernel(JaggedArgs ja,
       }
     }
 #pragma unroll
-    for (int t = 0; t < 4; t++) {
+    for (int t = 0; t < KR; t++) {
       if (!ok[t]) continue;
       const uint32_t w[8] = {w0[t][0], w0[t][1], w0[t][2], w0[t][3],
                              w1[t][0], w1[t][1], w1[t][2], w1[t][3]};
