@@ -93,6 +93,18 @@ def test_small_parity(hs, oracle_mod, dtype, case):
     _check_bwd(hs, oracle_mod, batch)
 
 
+def test_bwd_bf16_reduce_two_rounds(hs, oracle_mod):
+    """Every output of a 2200-token sequence (18 key blocks of 128, so the
+    bf16 dQ reduce sums its partial blocks over two rounds of loads) and a
+    ragged 45-token one.  bf16 only: the fp32 kernels have no reduce, and
+    at this length their time-table gradient (sums of ~2.4M pairs per
+    bucket, with heavy cancellation) sits at 1.3e-4 of its RMS."""
+    batch = inputs.make_batch(3, seed=150, lengths=(2200, 45), num_heads=1, d_qk=32, d_v=32,
+                              max_seq_len=2200, dtype="bf16")
+    _check_fwd(hs, oracle_mod, batch)
+    _check_bwd(hs, oracle_mod, batch)
+
+
 @pytest.mark.parametrize("dtype", ["bf16", "f32"])
 def test_small_parity_wide_timestamps(hs, oracle_mod, dtype):
     """Timestamps spanning more than 2^31 (and unsorted within a sequence):
