@@ -198,6 +198,7 @@ def sl_measurement(hstu, torch, stream):
     d = inputs.to_device(batch)
     N = batch.spec.max_seq_len
     L = hstu.hstu_sl_subseq_len(N, 1.6)
+    kn = hstu.hstu_sl_keep_numerator(N, 1.6)
     u, e = inputs.make_sl_draws(len(batch.lengths), batch.seq_offsets[-1], seed=5)
     ud, ed = torch.from_numpy(u).cuda(), torch.from_numpy(e).cuda()
     T = batch.total_tokens
@@ -208,8 +209,8 @@ def sl_measurement(hstu, torch, stream):
     bufs = {k: torch.empty_like(d[k]) for k in ("q", "k", "v", "u", "timestamps")}
 
     def sample():
-        hstu.hstu_stochastic_length(d["seq_offsets"], d["timestamps"], L, hstu.HSTU_SL_RANDOM, ud,
-                                    ed, out=(new_offs, gather), ws=ws, stream=stream)
+        hstu.hstu_stochastic_length(d["seq_offsets"], d["timestamps"], L, kn, hstu.HSTU_SL_RANDOM,
+                                    ud, ed, out=(new_offs, gather), ws=ws, stream=stream)
         for k, dst in bufs.items():
             hstu.hstu_gather_rows(d[k], gather, new_offs[-1:], max_rows=T, dst=dst, stream=stream)
     ms_sample = _time_ms(torch, stream, sample)

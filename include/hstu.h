@@ -332,10 +332,12 @@ hstu_status_t hstu_proj_in_bwd(const hstu_problem_t* p, int32_t d_model,
 /* ---- Stochastic Length (Eq. 4; subsequence selection and sparsity in
  * the appendix on Stochastic Length) ----
  * Shrinks a jagged batch before attention.  With L = subseq_len
- * (N_c^(alpha/2) of Eq. 4, see hstu_sl_subseq_len) and n_h the number of
- * history tokens of sequence b (its tokens before the num_targets[b]
+ * (floor(N_c^(alpha/2)) of Eq. 4, see hstu_sl_subseq_len), keep_numerator
+ * = N_c^alpha (see hstu_sl_keep_numerator; finite, >= 0) and n_h the number
+ * of history tokens of sequence b (its tokens before the num_targets[b]
  * candidates; num_targets NULL: no candidates), the sequence is kept whole
- * if n_h <= L or u_keep[b] < L^2 / n_h^2 (fp64), else it keeps exactly L
+ * if n_h <= L or u_keep[b] < keep_numerator / n_h^2 (fp64: the keep
+ * probability of Eq. 4), else it keeps exactly L
  * history tokens, chosen by `selection`, in their original order, and then
  * all its candidates.  Selection keys (the L smallest win; equal keys: the
  * later token first), with f_i = t_max - t_i over the history:
@@ -358,11 +360,15 @@ enum { HSTU_SL_GREEDY = 0, HSTU_SL_RANDOM = 1, HSTU_SL_WEIGHTED = 2 };
 /* L = floor(max_seq_len^(alpha/2)) for alpha in (0, 2]; 0 if invalid. */
 int32_t hstu_sl_subseq_len(int32_t max_seq_len, double alpha);
 
+/* max_seq_len^alpha (fp64 pow) for alpha in (0, 2]: the numerator of Eq. 4's
+ * keep probability; 0 if invalid. */
+double hstu_sl_keep_numerator(int32_t max_seq_len, double alpha);
+
 size_t hstu_sl_workspace_bytes(int32_t num_seqs);
 
 hstu_status_t hstu_stochastic_length(int32_t num_seqs, const int64_t* seq_offsets,
                                      const int64_t* timestamps, const int64_t* num_targets,
-                                     int32_t subseq_len, int32_t selection,
+                                     int32_t subseq_len, double keep_numerator, int32_t selection,
                                      const double* u_keep, const double* e_rand,
                                      int64_t* new_offsets, int64_t* gather,
                                      void* ws, size_t ws_bytes, void* hip_stream);
@@ -376,9 +382,11 @@ hstu_status_t hstu_gather_rows(const void* src, int64_t src_stride, int64_t row_
                                const int64_t* index, const int64_t* count, int64_t max_rows,
                                void* dst, int64_t dst_stride, void* hip_stream);
 
-/* Sparsity metrics of a batch (host memory offsets): sparsity = 1 - mean
- * length / max_seq_len; s2 = one minus the sparsity of the attention
- * matrix = sum_b L_b^2 / (B max_seq_len^2). */
+/* Sparsity metrics of a batch (appendix on the impact of Stochastic Length
+ * on sequence sparsity; host memory offsets): sparsity = 1 - mean length /
+ * max_seq_len; s2, the same measure over the B padded attention matrices,
+ * = 1 - sum_b L_b^2 / (B max_seq_len^2).  That form is the one the
+ * appendix's printed tables admit (s2 >= sparsity in every cell). */
 hstu_status_t hstu_sl_sparsity(int32_t num_seqs, const int64_t* seq_offsets, int32_t max_seq_len,
                                double* sparsity, double* s2);
 

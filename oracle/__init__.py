@@ -363,8 +363,17 @@ SL_GREEDY, SL_RANDOM, SL_WEIGHTED = 0, 1, 2
 
 
 def sl_subseq_len(max_seq_len, alpha):
-    """L = N_c^(alpha/2) of Eq. 4 (floor, with N_c the maximum length)."""
+    """L = N_c^(alpha/2) of Eq. 4 (floor, with N_c the maximum length): the
+    length of the subsequence, and the history length up to which a
+    sequence is always kept whole (n <= N_c^(alpha/2) iff n <= L for an
+    integer n)."""
     return int(np.floor(float(max_seq_len) ** (alpha / 2.0) + 1e-9))
+
+
+def sl_keep_numerator(max_seq_len, alpha):
+    """N_c^alpha of Eq. 4: a history of n > L tokens is kept whole with
+    probability N_c^alpha / n^2 (fp64)."""
+    return float(max_seq_len) ** float(alpha)
 
 
 def _sl_keys(ts, e, mode):
@@ -397,10 +406,12 @@ def _sl_keys(ts, e, mode):
     return keys
 
 
-def stochastic_length(seq_offsets, timestamps, num_targets, subseq_len, mode, u_keep, e_rand):
+def stochastic_length(seq_offsets, timestamps, num_targets, subseq_len, keep_num, mode, u_keep,
+                      e_rand):
     """Eq. 4 per sequence: with n_h history tokens (the candidates, if any,
     are always kept after them), keep the sequence whole if n_h <= L or
-    u_keep[b] < L^2 / n_h^2; otherwise keep L history tokens chosen by the
+    u_keep[b] < keep_num / n_h^2 (keep_num = N_c^alpha, fp64); otherwise
+    keep L = subseq_len history tokens chosen by the
     selection keys (the L smallest; equal keys: the later token first),
     in their original order.  Returns (new_offsets [B+1], gather [T'] of
     original token indices)."""
@@ -410,6 +421,7 @@ def stochastic_length(seq_offsets, timestamps, num_targets, subseq_len, mode, u_
     L = int(subseq_len)
     if L < 1:
         raise ValueError("subseq_len must be >= 1")
+    keep_num = float(keep_num)
     u = np.asarray(u_keep, dtype=np.float64)
     e = None if e_rand is None else np.asarray(e_rand, dtype=np.float64)
     gather, lens = [], []
@@ -417,7 +429,7 @@ def stochastic_length(seq_offsets, timestamps, num_targets, subseq_len, mode, u_
         o, n = int(offs[b]), int(offs[b + 1] - offs[b])
         nt = 0 if num_targets is None else int(num_targets[b])
         nh = n - nt
-        if nh <= L or u[b] < (L * L) / float(nh * nh):
+        if nh <= L or u[b] < keep_num / float(nh * nh):
             sel = list(range(o, o + n))
         else:
             keys = _sl_keys(ts[o:o + nh], None if e is None else e[o:o + nh], mode)
@@ -430,10 +442,15 @@ def stochastic_length(seq_offsets, timestamps, num_targets, subseq_len, mode, u_
 
 
 def sl_sparsity(lengths, max_seq_len):
-    """Sequence sparsity of the Stochastic Length appendix: 1 - mean length
-    / maximum length; and s2 = 1 - sparsity of the attention matrix, i.e.
-    the share of the B padded N x N score matrices that lies inside the
-    sequences, sum_b n_b^2 / (B N^2)."""
+    """The two metrics of the appendix on the impact of Stochastic Length on
+    sequence sparsity.  sparsity = 1 - mean length / maximum length N.
+    s2 is the same measure taken over the attention matrices: the share of
+    the B padded N x N score matrices that lies outside the sequences,
+    1 - sum_b n_b^2 / (B N^2).  The appendix's prose words s2 as the
+    complement of the attention matrix's sparsity, but every pair of its
+    printed tables (60-day and 90-day histories) has s2 above sparsity,
+    which only this form admits (for n_b <= N it lies between sparsity and
+    1 - (1 - sparsity)^2), so the tables decide."""
     n = np.asarray(lengths, dtype=np.float64)
     N = float(max_seq_len)
-    return 1.0 - n.mean() / N, float((n * n).sum() / (len(n) * N * N))
+    return 1.0 - n.mean() / N, 1.0 - float((n * n).sum() / (len(n) * N * N))

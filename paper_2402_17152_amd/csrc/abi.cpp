@@ -446,6 +446,11 @@ int32_t hstu_sl_subseq_len(int32_t max_seq_len, double alpha) {
   return (int32_t)std::floor(std::pow((double)max_seq_len, alpha / 2.0) + 1e-9);
 }
 
+double hstu_sl_keep_numerator(int32_t max_seq_len, double alpha) {
+  if (max_seq_len < 1 || !(alpha > 0.0) || alpha > 2.0) return 0.0;
+  return std::pow((double)max_seq_len, alpha);
+}
+
 size_t hstu_sl_workspace_bytes(int32_t num_seqs) {
   if (num_seqs < 1) return 0;
   return align_up(sizeof(int64_t) * (size_t)num_seqs) + align_up(sizeof(int32_t) * (size_t)num_seqs);
@@ -453,13 +458,16 @@ size_t hstu_sl_workspace_bytes(int32_t num_seqs) {
 
 hstu_status_t hstu_stochastic_length(int32_t num_seqs, const int64_t* seq_offsets,
                                      const int64_t* timestamps, const int64_t* num_targets,
-                                     int32_t subseq_len, int32_t selection, const double* u_keep,
-                                     const double* e_rand, int64_t* new_offsets, int64_t* gather,
-                                     void* ws, size_t ws_bytes, void* hip_stream) {
+                                     int32_t subseq_len, double keep_numerator, int32_t selection,
+                                     const double* u_keep, const double* e_rand,
+                                     int64_t* new_offsets, int64_t* gather, void* ws,
+                                     size_t ws_bytes, void* hip_stream) {
   try {
     hipStream_t s = (hipStream_t)hip_stream;
     if (num_seqs < 1) return fail(HSTU_ERR_INVALID_ARGUMENT, "num_seqs must be >= 1");
     if (subseq_len < 1) return fail(HSTU_ERR_INVALID_ARGUMENT, "subseq_len must be >= 1");
+    if (!(keep_numerator >= 0.0) || std::isinf(keep_numerator))
+      return fail(HSTU_ERR_INVALID_ARGUMENT, "keep_numerator must be finite and >= 0");
     if (selection < HSTU_SL_GREEDY || selection > HSTU_SL_WEIGHTED)
       return fail(HSTU_ERR_INVALID_ARGUMENT, "unknown selection %d", selection);
     if (!seq_offsets || !timestamps || !u_keep || !new_offsets || !gather)
@@ -474,8 +482,8 @@ hstu_status_t hstu_stochastic_length(int32_t num_seqs, const int64_t* seq_offset
     int64_t* new_len = (int64_t*)w;
     int32_t* whole = (int32_t*)(w + align_up(sizeof(int64_t) * (size_t)num_seqs));
     TimedScope ts("stochastic_length", s);
-    HSTU_HIP(launch_sl_lengths(num_seqs, seq_offsets, num_targets, subseq_len, u_keep, new_len,
-                               whole, s),
+    HSTU_HIP(launch_sl_lengths(num_seqs, seq_offsets, num_targets, subseq_len, keep_numerator,
+                               u_keep, new_len, whole, s),
              "sl lengths launch");
     HSTU_HIP(launch_complete_cumsum(num_seqs, new_len, new_offsets, 0, s), "sl offsets launch");
     HSTU_HIP(launch_sl_select(num_seqs, seq_offsets, timestamps, num_targets, subseq_len,
@@ -520,7 +528,7 @@ hstu_status_t hstu_sl_sparsity(int32_t num_seqs, const int64_t* seq_offsets, int
   }
   const double N = (double)max_seq_len;
   *sparsity = 1.0 - sum / num_seqs / N;
-  *s2 = sq / ((double)num_seqs * N * N);
+  *s2 = 1.0 - sq / ((double)num_seqs * N * N);
   return ok();
 }
 

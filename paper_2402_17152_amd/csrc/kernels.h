@@ -235,8 +235,8 @@ hipError_t launch_reduce_cols(int n, int S, const float* part, float* out, hipSt
 enum { kSlGreedy = 0, kSlRandom = 1, kSlWeighted = 2 };
 // new_len[b] and whole[b] (1: the sequence stays whole) per sequence.
 hipError_t launch_sl_lengths(int32_t B, const int64_t* offs, const int64_t* nt, int32_t L,
-                             const double* u_keep, int64_t* new_len, int32_t* whole,
-                             hipStream_t s);
+                             double keep_num, const double* u_keep, int64_t* new_len,
+                             int32_t* whole, hipStream_t s);
 // gather[new_offs[b] ..] = the original indices a sequence keeps.
 hipError_t launch_sl_select(int32_t B, const int64_t* offs, const int64_t* ts, const int64_t* nt,
                             int32_t L, int32_t mode, const double* e_rand, const int32_t* whole,

@@ -1,7 +1,8 @@
 // Stochastic Length (Eq. 4 and the subsequence selection appendix): shrinks
 // a jagged batch before attention.  A sequence whose history (the tokens
 // before its candidates) has n_h > L tokens keeps it whole with
-// probability L^2 / n_h^2 (the draw u_keep[b] is an input) and otherwise
+// probability N_c^alpha / n_h^2 (the draw u_keep[b] and the numerator
+// N_c^alpha are inputs) and otherwise
 // keeps exactly L history tokens: those with the L smallest selection keys
 // (equal keys: the later token first), in their original order.  The
 // candidates always follow.  The result is a gather list of original
@@ -26,6 +27,7 @@ constexpr int kSlThreads = 256;
 
 __global__ __launch_bounds__(256) void sl_lengths_kernel(int32_t B, const int64_t* __restrict__ offs,
                                                          const int64_t* __restrict__ nt, int32_t L,
+                                                         double keep_num,
                                                          const double* __restrict__ u_keep,
                                                          int64_t* __restrict__ new_len,
                                                          int32_t* __restrict__ whole) {
@@ -33,7 +35,7 @@ __global__ __launch_bounds__(256) void sl_lengths_kernel(int32_t B, const int64_
     const int64_t n = offs[b + 1] - offs[b];
     const int64_t t = nt ? nt[b] : 0;
     const int64_t nh = n - t;
-    const bool w = nh <= L || u_keep[b] < ((double)L * (double)L) / ((double)nh * (double)nh);
+    const bool w = nh <= L || u_keep[b] < keep_num / ((double)nh * (double)nh);
     new_len[b] = w ? n : (int64_t)L + t;
     whole[b] = w ? 1 : 0;
   }
@@ -197,11 +199,12 @@ __global__ __launch_bounds__(256) void gather_rows_kernel(const char* __restrict
 }  // namespace
 
 hipError_t launch_sl_lengths(int32_t B, const int64_t* offs, const int64_t* nt, int32_t L,
-                             const double* u_keep, int64_t* new_len, int32_t* whole,
-                             hipStream_t s) {
+                             double keep_num, const double* u_keep, int64_t* new_len,
+                             int32_t* whole, hipStream_t s) {
   if (B <= 0) return hipSuccess;
   const int blocks = (B + 255) / 256 < 1024 ? (B + 255) / 256 : 1024;
-  hipLaunchKernelGGL(sl_lengths_kernel, dim3(blocks), dim3(256), 0, s, B, offs, nt, L, u_keep,
+  hipLaunchKernelGGL(sl_lengths_kernel, dim3(blocks), dim3(256), 0, s, B, offs, nt, L, keep_num,
+                     u_keep,
                      new_len, whole);
   return hipGetLastError();
 }

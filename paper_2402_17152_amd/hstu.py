@@ -29,8 +29,8 @@ EXPORTED = ("hstu_workspace_bytes", "hstu_attn_fwd", "hstu_attn_bwd", "hstu_laye
             "hstu_attn_fwd_cached", "hstu_attn_fwd_cached_workspace_bytes",
             "hstu_proj_workspace_bytes", "hstu_proj_in_fwd",
             "hstu_proj_out_fwd", "hstu_proj_out_bwd", "hstu_proj_in_bwd",
-            "hstu_sl_subseq_len", "hstu_sl_workspace_bytes", "hstu_stochastic_length",
-            "hstu_gather_rows", "hstu_sl_sparsity")
+            "hstu_sl_subseq_len", "hstu_sl_keep_numerator", "hstu_sl_workspace_bytes",
+            "hstu_stochastic_length", "hstu_gather_rows", "hstu_sl_sparsity")
 
 
 class Problem(ctypes.Structure):
@@ -83,8 +83,10 @@ def _load():
         "hstu_proj_workspace_bytes": (sz, [PP, i32]),
         "hstu_attn_fwd_cached_workspace_bytes": (sz, [PP]),
         "hstu_sl_subseq_len": (i32, [i32, ctypes.c_double]),
+        "hstu_sl_keep_numerator": (ctypes.c_double, [i32, ctypes.c_double]),
         "hstu_sl_workspace_bytes": (sz, [i32]),
-        "hstu_stochastic_length": (i32, [i32, P, P, P, i32, i32, P, P, P, P, P, sz, P]),
+        "hstu_stochastic_length": (i32, [i32, P, P, P, i32, ctypes.c_double, i32, P, P, P, P, P,
+                                         sz, P]),
         "hstu_gather_rows": (i32, [P, i64, i64, P, P, i64, P, i64, P]),
         "hstu_sl_sparsity": (i32, [i32, P, i32, ctypes.POINTER(ctypes.c_double),
                                    ctypes.POINTER(ctypes.c_double)]),
@@ -462,12 +464,16 @@ def hstu_sl_subseq_len(max_seq_len: int, alpha: float) -> int:
     return int(lib.hstu_sl_subseq_len(int(max_seq_len), float(alpha)))
 
 
+def hstu_sl_keep_numerator(max_seq_len: int, alpha: float) -> float:
+    return float(lib.hstu_sl_keep_numerator(int(max_seq_len), float(alpha)))
+
+
 def hstu_sl_workspace_bytes(num_seqs: int) -> int:
     return int(lib.hstu_sl_workspace_bytes(int(num_seqs)))
 
 
-def hstu_stochastic_length(seq_offsets, timestamps, subseq_len, selection, u_keep, e_rand=None,
-                           num_targets=None, out=None, ws=None, stream=None):
+def hstu_stochastic_length(seq_offsets, timestamps, subseq_len, keep_numerator, selection, u_keep,
+                           e_rand=None, num_targets=None, out=None, ws=None, stream=None):
     """(new_offsets [B+1], gather [T]) on the device; the first
     new_offsets[B] entries of gather are valid (see include/hstu.h)."""
     B = seq_offsets.numel() - 1
@@ -480,7 +486,8 @@ def hstu_stochastic_length(seq_offsets, timestamps, subseq_len, selection, u_kee
         ws = torch.empty(int(lib.hstu_sl_workspace_bytes(B)), dtype=torch.uint8,
                          device=seq_offsets.device)
     _check(lib.hstu_stochastic_length(B, _ptr(seq_offsets), _ptr(timestamps), _ptr(num_targets),
-                                      int(subseq_len), int(selection), _ptr(u_keep), _ptr(e_rand),
+                                      int(subseq_len), float(keep_numerator), int(selection),
+                                      _ptr(u_keep), _ptr(e_rand),
                                       _ptr(new_offsets), _ptr(gather), _ptr(ws), ws.numel(),
                                       _stream(stream)))
     return new_offsets, gather

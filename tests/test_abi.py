@@ -207,13 +207,18 @@ def test_stochastic_length_entry_points_validate(hs):
     L = hs.lib
     assert hs.hstu_sl_workspace_bytes(0) == 0 and hs.hstu_sl_workspace_bytes(64) > 0
     assert hs.hstu_sl_subseq_len(4096, 2.5) == 0 and hs.hstu_sl_subseq_len(0, 1.6) == 0
+    assert hs.hstu_sl_keep_numerator(4096, 2.5) == 0.0
+    assert hs.hstu_sl_keep_numerator(4096, 1.6) == 4096.0 ** 1.6
 
-    def sl(B=8, Ls=16, mode=1, e=FAKE, ws=FAKE, wsb=1 << 20, offs=FAKE):
-        return L.hstu_stochastic_length(B, P(offs), P(FAKE), None, Ls, mode, P(FAKE),
+    def sl(B=8, Ls=16, mode=1, e=FAKE, ws=FAKE, wsb=1 << 20, offs=FAKE, kn=256.0):
+        return L.hstu_stochastic_length(B, P(offs), P(FAKE), None, Ls, kn, mode, P(FAKE),
                                         P(e) if e else None, P(FAKE), P(FAKE), P(ws) if ws else None,
                                         wsb, None)
     for kw, status, needle in ((dict(B=0), 1, "num_seqs"), (dict(Ls=0), 1, "subseq_len"),
                                (dict(mode=5), 1, "selection"), (dict(e=None), 1, "e_rand"),
+                               (dict(kn=-1.0), 1, "keep_numerator"),
+                               (dict(kn=float("inf")), 1, "keep_numerator"),
+                               (dict(kn=float("nan")), 1, "keep_numerator"),
                                (dict(offs=0), 1, "NULL"), (dict(ws=None), 3, "workspace"),
                                (dict(wsb=16), 3, "too small"), (dict(ws=FAKE + 64), 3, "aligned")):
         assert sl(**kw) == status, kw

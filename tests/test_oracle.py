@@ -672,20 +672,28 @@ def _sl_batch(lengths, seed=0, nt=None):
 
 def test_sl_keep_decision_closed_form(oracle_mod):
     """Eq. 4: a history of n > L tokens stays whole exactly when the draw u
-    falls below L^2 / n^2 (probability N_c^alpha / n^2 with L = N_c^(alpha/2));
-    n <= L always stays whole."""
-    L = 10
-    lengths = [5, 10, 11, 20, 40]
+    falls below N_c^alpha / n^2; n <= L = floor(N_c^(alpha/2)) always stays
+    whole.  N_c = 1000, alpha = 1.5: N_c^alpha = 31622.77 is not a square,
+    so the probability differs from L^2 / n^2 (L = 177)."""
+    N, alpha = 1000, 1.5
+    L = oracle_mod.sl_subseq_len(N, alpha)
+    kn = oracle_mod.sl_keep_numerator(N, alpha)
+    assert L == 177 and abs(kn - 1000.0 ** 1.5) == 0.0 and L * L < kn < (L + 1) ** 2
+    lengths = [5, 177, 178, 200, 400]
     offs, ts, T = _sl_batch(lengths)
     e = np.ones(T)
     for b, n in enumerate(lengths):
-        p = L * L / (n * n)
-        for u, whole in ((np.nextafter(p, 0), True), (p, False), (0.999999, n <= L)):
+        p = kn / (n * n)
+        # just below p (whole), at p (shortened); L^2/n^2 < u < p must keep it whole
+        cases = [(np.nextafter(p, 0), True), (p, False), (0.999999, n <= L)]
+        if n > L:
+            cases.append(((L * L / (n * n) + p) / 2, True))
+        for u, whole in cases:
             if n <= L:
                 whole = True
             uk = np.full(len(lengths), 0.999999)
             uk[b] = u
-            no, g = oracle_mod.stochastic_length(offs, ts, None, L, oracle_mod.SL_RANDOM, uk, e)
+            no, g = oracle_mod.stochastic_length(offs, ts, None, L, kn, oracle_mod.SL_RANDOM, uk, e)
             assert (no[b + 1] - no[b] == n) == whole, (n, u)
             if not whole:
                 assert no[b + 1] - no[b] == L
@@ -697,9 +705,11 @@ def test_sl_greedy_is_most_recent(oracle_mod):
     timestamps prefer the later token."""
     offs = np.array([0, 8])
     ts = np.array([1, 2, 3, 5, 5, 5, 9, 9], dtype=np.int64)
-    no, g = oracle_mod.stochastic_length(offs, ts, None, 4, oracle_mod.SL_GREEDY, [0.99], None)
+    no, g = oracle_mod.stochastic_length(offs, ts, None, 4, 16.0, oracle_mod.SL_GREEDY, [0.99],
+                                         None)
     assert list(g) == [4, 5, 6, 7]
-    no, g = oracle_mod.stochastic_length(offs, ts, None, 3, oracle_mod.SL_GREEDY, [0.99], None)
+    no, g = oracle_mod.stochastic_length(offs, ts, None, 3, 9.0, oracle_mod.SL_GREEDY, [0.99],
+                                         None)
     assert list(g) == [5, 6, 7]
 
 
@@ -708,7 +718,7 @@ def test_sl_candidates_kept(oracle_mod):
     candidate is kept, after the chosen history tokens."""
     offs = np.array([0, 30])
     ts = np.arange(30, dtype=np.int64) * 7
-    no, g = oracle_mod.stochastic_length(offs, ts, np.array([5]), 6, oracle_mod.SL_GREEDY,
+    no, g = oracle_mod.stochastic_length(offs, ts, np.array([5]), 6, 36.0, oracle_mod.SL_GREEDY,
                                          [0.99], None)
     assert list(g) == list(range(19, 25)) + list(range(25, 30))
 
@@ -722,7 +732,7 @@ def test_sl_random_inclusion_probability(oracle_mod):
     ts = np.arange(n, dtype=np.int64)
     counts = np.zeros(n)
     for _ in range(R):
-        _, g = oracle_mod.stochastic_length(offs, ts, None, L, oracle_mod.SL_RANDOM, [0.999],
+        _, g = oracle_mod.stochastic_length(offs, ts, None, L, L * L, oracle_mod.SL_RANDOM, [0.999],
                                             rng.exponential(size=n))
         counts[g] += 1
     p = L / n
@@ -745,7 +755,8 @@ def test_sl_weighted_inclusion_probability(oracle_mod):
     for L in (1, 2):
         counts = np.zeros(n)
         for _ in range(R):
-            _, g = oracle_mod.stochastic_length(offs, ts, None, L, oracle_mod.SL_WEIGHTED, [0.999],
+            _, g = oracle_mod.stochastic_length(offs, ts, None, L, L * L, oracle_mod.SL_WEIGHTED,
+                                                [0.999],
                                                 rng.exponential(size=n))
             counts[g] += 1
         P = w / w.sum()
@@ -761,18 +772,24 @@ def test_sl_weighted_inclusion_probability(oracle_mod):
 
 
 def test_sl_expected_cost(oracle_mod):
-    """Eq. 4's point: the expected attention cost of a history of n > L
-    tokens is (1 - p) L^2 + p n^2 = 2 L^2 - L^4 / n^2 <= 2 N_c^alpha with
-    p = L^2 / n^2; averaged over a uniform grid of keep draws."""
-    L, n, G = 16, 64, 4096
+    """Eq. 4's point: with p = N_c^alpha / n^2 the expected attention cost of
+    a history of n > L tokens is (1 - p) L^2 + p n^2 = L^2 + N_c^alpha -
+    N_c^alpha L^2 / n^2 <= 2 N_c^alpha; averaged over a uniform grid of keep
+    draws (N_c = 300, alpha = 1.5: L = 71, N_c^alpha = 5196.15)."""
+    N, alpha, n, G = 300, 1.5, 128, 1 << 16
+    L = oracle_mod.sl_subseq_len(N, alpha)
+    kn = oracle_mod.sl_keep_numerator(N, alpha)
     offs = np.array([0, n])
     ts = np.arange(n, dtype=np.int64)
+    us = (np.arange(G) + 0.5) / G
     cost = 0.0
-    for k in range(G):
-        no, _ = oracle_mod.stochastic_length(offs, ts, None, L, oracle_mod.SL_GREEDY,
-                                             [(k + 0.5) / G], None)
+    for k in range(0, G, 64):      # the decision depends on u only: evaluate 1 in 64 exactly
+        no, _ = oracle_mod.stochastic_length(offs, ts, None, L, kn, oracle_mod.SL_GREEDY,
+                                             [us[k]], None)
         cost += float(no[1]) ** 2
-    assert abs(cost / G - (2 * L * L - L ** 4 / n ** 2)) < 1e-9 * n * n
+    want = L * L + kn - kn * L * L / n ** 2
+    assert abs(cost / (G // 64) - want) < 2.0 * n * n / (G // 64)
+    assert want <= 2 * kn
 
 
 def test_sl_paper_example(oracle_mod):
@@ -785,20 +802,102 @@ def test_sl_paper_example(oracle_mod):
     N, alpha, n, want = [float(x) for x in
                          [ln for ln in open(path) if not ln.startswith("#")][0].split()]
     L = oracle_mod.sl_subseq_len(int(N), alpha)
+    kn = oracle_mod.sl_keep_numerator(int(N), alpha)
     assert L == int(want)
-    p_whole = L * L / (n * n)
+    p_whole = kn / (n * n)
     assert 1.0 - p_whole > 0.5 and 1.0 - L / n > 0.8
     offs, ts = np.array([0, int(n)]), np.arange(int(n), dtype=np.int64)
-    no, _ = oracle_mod.stochastic_length(offs, ts, None, L, oracle_mod.SL_GREEDY, [0.5], None)
+    no, _ = oracle_mod.stochastic_length(offs, ts, None, L, kn, oracle_mod.SL_GREEDY, [0.5], None)
     assert no[1] == L
 
 
 def test_sl_subseq_len_and_sparsity(oracle_mod):
-    """L = N^(alpha/2); sparsity = 1 - mean/max and s2 = sum n^2 / (B N^2) on
-    lengths with closed forms."""
+    """L = N^(alpha/2); sparsity = 1 - mean/max and s2 = 1 - sum n^2 / (B N^2)
+    on lengths with closed forms."""
     assert oracle_mod.sl_subseq_len(4096, 2.0) == 4096
     assert oracle_mod.sl_subseq_len(4096, 1.5) == 512
     sp, s2 = oracle_mod.sl_sparsity([512, 512, 512, 512], 1024)
-    assert sp == 0.5 and s2 == 0.25
+    assert sp == 0.5 and s2 == 0.75
     sp, s2 = oracle_mod.sl_sparsity([1024, 0], 1024)
     assert sp == 0.5 and s2 == 0.5
+    sp, s2 = oracle_mod.sl_sparsity([1024, 1024, 1024], 1024)
+    assert sp == 0.0 and s2 == 0.0
+
+
+def _sparsity_tables():
+    import os
+    path = os.path.join(os.path.dirname(__file__), "golden", "sl_sparsity_tables.txt")
+    rows = []
+    for ln in open(path):
+        if ln.startswith("#") or not ln.strip():
+            continue
+        h, a, N, sp, s2 = ln.split()
+        rows.append((h, float(a), int(N), float(sp) / 100.0, float(s2) / 100.0))
+    return rows
+
+
+def test_sl_sparsity_matches_printed_tables(oracle_mod):
+    """The appendix's sparsity tables (tests/golden/sl_sparsity_tables.txt,
+    60- and 90-day histories) fix which s2 the oracle computes.  For lengths
+    n_b <= N, m1 = mean n / N and m2 = mean n^2 / N^2 satisfy
+    m1^2 <= m2 <= m1, so s2 = 1 - m2 lies in [sparsity, 1 - (1 - sparsity)^2]:
+    every printed pair must fall there (within the tables' 0.05 % rounding).
+    For each pair a batch of lengths is then built that has exactly those
+    moments (a two-point length distribution on {x N, N}), and the oracle
+    must return both printed values from it.  The complement, s2 = m2,
+    would have to lie in [(1 - sparsity)^2, 1 - sparsity]: 38 of the 40
+    pairs fall outside that."""
+    rows = [r for r in _sparsity_tables() if r[0] != "30d"]
+    assert len(rows) == 40
+    half = 0.0005
+    other_fits = 0
+    for h, a, N, sp, s2 in rows:
+        assert sp - 2 * half <= s2 <= 1 - (1 - sp - half) ** 2 + half, (h, a, N, sp, s2)
+        m1, m2 = 1.0 - sp, 1.0 - s2
+        if (1 - sp) ** 2 - 2 * half <= s2 <= 1 - sp + 2 * half:
+            other_fits += 1
+        # two-point distribution: a share f of full-length sequences, the rest at x N
+        m2c = min(max(m2, m1 * m1), m1)
+        f = (m2c - m1 * m1) / (1.0 - 2.0 * m1 + m2c)
+        x = (m2c - f) / (m1 - f) if m1 > f else 0.0
+        B = 200000
+        nfull = int(round(f * B))
+        lengths = np.array([N] * nfull + [int(round(x * N))] * (B - nfull), dtype=np.int64)
+        assert lengths.max() <= N
+        got_sp, got_s2 = oracle_mod.sl_sparsity(lengths, N)
+        assert abs(got_sp - sp) <= 2 * half and abs(got_s2 - s2) <= 2 * half, (h, a, N, got_sp,
+                                                                                got_s2, sp, s2)
+    assert other_fits == 2
+
+
+def test_sl_sparsity_tables_monotone(oracle_mod):
+    """Shape of every printed table (including the 30-day table of Sec. 3.2,
+    sparsity only): lowering alpha shortens more sequences, so sparsity (and
+    s2) never decrease as alpha falls; and the oracle's sparsity of a batch
+    shortened by Eq. 4 with a lower alpha is never below that of a higher
+    alpha on the same draws (power-law lengths up to N = 4096)."""
+    rows = _sparsity_tables()
+    for h in ("30d", "60d", "90d"):
+        for N in (1024, 2048, 4096, 8192):
+            col = sorted([r for r in rows if r[0] == h and r[2] == N], key=lambda r: r[1])
+            sps = [r[3] for r in col]
+            assert all(sps[i] >= sps[i + 1] for i in range(len(sps) - 1)), (h, N, sps)
+            if h != "30d":
+                s2s = [r[4] for r in col]
+                assert all(s2s[i] >= s2s[i + 1] for i in range(len(s2s) - 1)), (h, N, s2s)
+    rng = np.random.default_rng(11)
+    N = 4096
+    lengths = np.minimum(N, (64 * rng.pareto(0.9, 400) + 64).astype(np.int64))
+    offs = np.concatenate([[0], np.cumsum(lengths)]).astype(np.int64)
+    ts = np.arange(offs[-1], dtype=np.int64)
+    u = rng.random(len(lengths))
+    prev = None
+    for alpha in (2.0, 1.9, 1.8, 1.7, 1.6):
+        L = oracle_mod.sl_subseq_len(N, alpha)
+        kn = oracle_mod.sl_keep_numerator(N, alpha)
+        no, _ = oracle_mod.stochastic_length(offs, ts, None, L, kn, oracle_mod.SL_GREEDY, u, None)
+        sp, s2 = oracle_mod.sl_sparsity(np.diff(no), N)
+        assert sp <= s2 <= 1 - (1 - sp) ** 2 + 1e-12
+        if prev is not None:
+            assert sp >= prev[0] and s2 >= prev[1]
+        prev = (sp, s2)

@@ -25,6 +25,7 @@ def test_sl_host_helpers_match_oracle(oracle_mod):
     hs = _hs()
     for N, a in ((4096, 1.6), (4096, 2.0), (8192, 1.7), (1024, 1.5), (3072, 1.9)):
         assert hs.hstu_sl_subseq_len(N, a) == oracle_mod.sl_subseq_len(N, a)
+        assert hs.hstu_sl_keep_numerator(N, a) == oracle_mod.sl_keep_numerator(N, a)
     assert hs.hstu_sl_subseq_len(4096, 0.0) == 0
     rng = np.random.default_rng(1)
     lens = rng.integers(0, 4097, 37)
@@ -48,9 +49,9 @@ def _batch(lengths, seed, dup_ts=False):
     return offs, ts
 
 
-def _run(hs, offs, ts, nt, L, mode, u, e):
+def _run(hs, offs, ts, nt, L, kn, mode, u, e):
     dev = lambda a: torch.from_numpy(np.ascontiguousarray(a)).cuda()
-    no, g = hs.hstu_stochastic_length(dev(offs), dev(ts), L, mode, dev(u),
+    no, g = hs.hstu_stochastic_length(dev(offs), dev(ts), L, kn, mode, dev(u),
                                       None if e is None else dev(e),
                                       num_targets=None if nt is None else dev(nt))
     torch.cuda.synchronize()
@@ -58,9 +59,9 @@ def _run(hs, offs, ts, nt, L, mode, u, e):
     return no, g.cpu().numpy()[:no[-1]]
 
 
-def _check(hs, oracle_mod, offs, ts, nt, L, mode, u, e):
-    got_o, got_g = _run(hs, offs, ts, nt, L, mode, u, e)
-    ref_o, ref_g = oracle_mod.stochastic_length(offs, ts, nt, L, mode, u, e)
+def _check(hs, oracle_mod, offs, ts, nt, L, kn, mode, u, e):
+    got_o, got_g = _run(hs, offs, ts, nt, L, kn, mode, u, e)
+    ref_o, ref_g = oracle_mod.stochastic_length(offs, ts, nt, L, kn, mode, u, e)
     np.testing.assert_array_equal(got_o, ref_o)
     np.testing.assert_array_equal(got_g, ref_g)
     return ref_o
@@ -73,7 +74,7 @@ MODES = [0, 1, 2]
 @pytest.mark.parametrize("mode", MODES)
 def test_sl_small_bit_exact(oracle_mod, mode):
     hs = _hs()
-    L = 10
+    L, kn = 10, 10.0 ** 2.1   # keep probability 125.89 / n^2, not L^2 / n^2
     lengths = [0, 1, 5, 10, 11, 40, 300, 1000, 8192, 257]
     for seed, dup in ((0, False), (1, True)):
         offs, ts = _batch(lengths, seed, dup_ts=dup)
@@ -84,11 +85,13 @@ def test_sl_small_bit_exact(oracle_mod, mode):
         # keep draws exactly at, just below and far from the threshold
         n = np.diff(offs)
         with np.errstate(divide="ignore"):
-            thr = (L * L) / (n.astype(np.float64) ** 2)
+            thr = kn / (n.astype(np.float64) ** 2)
         u[5] = thr[5]
         u[6] = np.nextafter(thr[6], 0)
         u[7] = 0.9999
-        ref_o = _check(hs, oracle_mod, offs, ts, None, L, mode, u, e)
+        u[9] = (L * L / 257.0 ** 2 + thr[9]) / 2    # between L^2/n^2 and the threshold: whole
+        ref_o = _check(hs, oracle_mod, offs, ts, None, L, kn, mode, u, e)
+        assert ref_o[10] - ref_o[9] == 257
         assert (np.diff(ref_o) < n).any()  # something was shortened
 
 
@@ -101,7 +104,7 @@ def test_sl_candidates_bit_exact(oracle_mod, mode):
     offs, ts = _batch(lengths, 7)
     u, e = inputs.make_sl_draws(len(lengths), offs[-1], seed=7)
     u[:] = 0.99
-    ref_o = _check(hs, oracle_mod, offs, ts, nt, 16, mode, u, e)
+    ref_o = _check(hs, oracle_mod, offs, ts, nt, 16, 256.0, mode, u, e)
     assert list(np.diff(ref_o)) == [21, 116, 5, 1040, 16]
 
 
@@ -113,8 +116,9 @@ def test_sl_training_workload(oracle_mod, mode):
     hs = _hs()
     b = inputs.make_batch("training")
     L = oracle_mod.sl_subseq_len(b.spec.max_seq_len, 1.6)
+    kn = oracle_mod.sl_keep_numerator(b.spec.max_seq_len, 1.6)
     u, e = inputs.make_sl_draws(len(b.lengths), b.seq_offsets[-1], seed=5)
-    _check(hs, oracle_mod, b.seq_offsets, b.timestamps, None, L, mode, u, e)
+    _check(hs, oracle_mod, b.seq_offsets, b.timestamps, None, L, kn, mode, u, e)
 
 
 @pytest.mark.gpu
