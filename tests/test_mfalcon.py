@@ -126,7 +126,6 @@ def test_mfalcon_small(hs, oracle_mod, case):
         assert torch.equal(o.view(torch.int16), base.view(torch.int16)), \
             f"cached outputs depend on the partition (b_m={b_m})"
     gu.assert_close("cached vs oracle", gu.to_f64(base), ref_full, 2e-2, "bf16")
-    gu.assert_close("cached vs uncached", gu.to_f64(base), full, 2e-2, "bf16")
 
 
 def test_mfalcon_cached_rejects_fp32(hs):
@@ -141,13 +140,11 @@ def test_mfalcon_cached_rejects_fp32(hs):
 
 def test_mfalcon_target_workload(hs, oracle_mod):
     """Full target workload: every b_m in (1024, 256, 16, 1) gives the same
-    cached outputs bit for bit; Algorithm 1 with b_m = 256 and the cached
-    pass both agree with the uncached target-aware forward on every
-    candidate, and with the oracle on users 0 and 11."""
+    cached outputs bit for bit; the cached pass and Algorithm 1 with
+    b_m = 256 agree with the oracle on every candidate of every user."""
     batch = inputs.make_batch("target")
     d = gu.dev_inputs(batch)
     rows = _cand_rows(batch)
-    full = gu.to_f64(gu.gpu_fwd(hs, d, batch))[rows]
     base = None
     for b_m in (1024, 256, 16, 1):
         o = mfalcon_gpu(hs, batch, d, b_m, first_uncached=False)
@@ -156,17 +153,9 @@ def test_mfalcon_target_workload(hs, oracle_mod):
         else:
             assert torch.equal(o.view(torch.int16), base.view(torch.int16)), f"b_m={b_m}"
     cached = gu.to_f64(base)
-    e = gu.assert_close("cached vs uncached", cached, full, 2e-2, "bf16")
-    print(f"\n  cached vs uncached: {e[0]:.3e} raw {e[1]:.3e}")
     alg1 = gu.to_f64(mfalcon_gpu(hs, batch, d, 256))
-    gu.assert_close("algorithm 1 vs uncached", alg1, full, 2e-2, "bf16")
-    nt = batch.num_targets
-    cstart = np.concatenate([[0], np.cumsum(nt)])
-    for b in (0, 11):
-        sub = gu.sub_batch(batch, [b])
-        ref = gu.oracle_fwd(oracle_mod, sub)[-nt[b]:]
-        got = cached[cstart[b]:cstart[b + 1]]
-        e = gu.assert_close(f"user {b} vs oracle", got, ref, 2e-2, "bf16")
-        print(f"  user {b}: err {e[0]:.3e} raw {e[1]:.3e}")
-        gu.assert_close(f"user {b} algorithm 1", alg1[cstart[b]:cstart[b + 1]], ref, 2e-2,
-                        "bf16")
+    ref = gu.oracle_fwd(oracle_mod, batch)[rows]
+    e = gu.assert_close("cached vs oracle", cached, ref, 2e-2, "bf16")
+    print(f"\n  cached: err {e[0]:.3e} raw {e[1]:.3e}")
+    e = gu.assert_close("algorithm 1 vs oracle", alg1, ref, 2e-2, "bf16")
+    print(f"  algorithm 1: err {e[0]:.3e} raw {e[1]:.3e}")
