@@ -123,6 +123,28 @@ hstu_status_t hstu_attn_fwd(const hstu_problem_t* p, const hstu_jagged_t* j,
                             void* out, void* ws, size_t ws_bytes,
                             void* hip_stream);
 
+/* hstu_attn_fwd without a workspace, for callers that cannot allocate
+ * device memory (code under stream capture, serving loops that forbid
+ * allocation).  Same arguments, result and determinism as hstu_attn_fwd
+ * minus ws / ws_bytes; the call itself allocates nothing.  The forward's
+ * scratch (work list, its length, per-sequence timestamp ranges) lives in
+ * one static device array of HSTU_NOALLOC_SCRATCH_BYTES per GPU, held from
+ * the library's first call on that GPU until the process ends; the prep
+ * launch rewrites all of it on every call, so nothing carries over between
+ * calls.  Limit: the bf16 path needs 256 + 8 (ceil(T / 128) + B) + 16 B
+ * bytes (each term rounded up to 256) within that size, about 6.6 * 10^7
+ * tokens for B = 1024; a larger problem returns HSTU_ERR_UNSUPPORTED
+ * without launching anything (the fp32 path uses no scratch).  All calls on
+ * one GPU share the array: two calls that overlap in time on that GPU (on
+ * different streams, or from different host threads without ordering)
+ * race and may return wrong results. */
+#define HSTU_NOALLOC_SCRATCH_BYTES (4u << 20)
+hstu_status_t hstu_attn_fwd_noalloc(const hstu_problem_t* p, const hstu_jagged_t* j,
+                                    const void* q, int64_t q_stride,
+                                    const void* k, int64_t k_stride,
+                                    const void* v, int64_t v_stride,
+                                    void* out, void* hip_stream);
+
 /* M-FALCON cached candidate pass (Algorithm 1, one microbatch; the
  * encoder-level cache of the appendix on M-FALCON): the attention output
  * of a microbatch of ranking candidates against the cached keys and

@@ -57,6 +57,7 @@ struct TimedScope {
   Pending p;
   hipStream_t s;
   TimedScope(const char* name, hipStream_t stream) : s(stream) {
+    if (!name) return;
     std::lock_guard<std::mutex> lk(g_tmu);
     if (!g_timing) return;
     p.name = name;
@@ -253,36 +254,98 @@ JaggedArgs make_args(const hstu_problem_t* p, const hstu_jagged_t* j) {
     if (e_ != hipSuccess) return hip_fail(e_, what); \
   } while (0)
 
-hstu_status_t attn_fwd_impl(const hstu_problem_t* p, const hstu_jagged_t* j, const Tensors& t,
-                            void* out, int out_f32, void* ws, size_t ws_bytes, hipStream_t s) {
+hstu_status_t check_fwd_args(const hstu_problem_t* p, const hstu_jagged_t* j, const Tensors& t,
+                             void* out) {
   HSTU_TRY(check_problem(p));
   HSTU_TRY(check_jagged(j));
-  const int64_t T = p->total_tokens;
   const int H = p->num_heads;
   HSTU_TRY(check_rows(p, "q", t.q, t.q_stride, (int64_t)H * p->d_qk));
   HSTU_TRY(check_rows(p, "k", t.k, t.k_stride, (int64_t)H * p->d_qk));
   HSTU_TRY(check_rows(p, "v", t.v, t.v_stride, (int64_t)H * p->d_v));
   HSTU_TRY(check_dense("out", out, 16));
-  Layout l;
-  HSTU_TRY(check_ws(p, ws, ws_bytes, &l));
-  if (T == 0) return ok();
+  return HSTU_OK;
+}
+
+// The forward's launches once its scratch is placed: the item count, the
+// work list (max_items entries) and the per-sequence timestamp ranges, all
+// written by the prep launch before the attention kernel reads them.
+hstu_status_t attn_fwd_run(const hstu_problem_t* p, const hstu_jagged_t* j, const Tensors& t,
+                           void* out, int out_f32, int32_t* counts, WorkItem* items,
+                           int64_t* trange, int64_t max_items, bool timed, hipStream_t s) {
   JaggedArgs ja = make_args(p, j);
-  char* w = (char*)ws;
   if (p->dtype == HSTU_F32) {
-    TimedScope ts("attn_fwd", s);
+    TimedScope ts(timed ? "attn_fwd" : nullptr, s);
     HSTU_HIP(launch_attn_fwd_f32(ja, t, p->d_qk, p->d_v, out, s), "attn_fwd_f32 launch");
     return ok();
   }
-  int32_t* counts = (int32_t*)(w + l.counts);
-  WorkItem* items = (WorkItem*)(w + l.fwd_items);
-  ja.seq_trange = (const int64_t*)(w + l.trange);
-  HSTU_HIP(launch_prep(ja, 0, items, counts, (int64_t*)(w + l.trange), PrepFills{}, nullptr, s),
-           "prep launch");
-  TimedScope ts("attn_fwd", s);
+  ja.seq_trange = trange;
+  HSTU_HIP(launch_prep(ja, 0, items, counts, trange, PrepFills{}, nullptr, s), "prep launch");
+  TimedScope ts(timed ? "attn_fwd" : nullptr, s);
   HSTU_HIP(launch_attn_fwd_bf16(ja, t, p->d_qk, p->d_v, out, out_f32, out_f32, items, counts,
-                                l.max_fwd, s),
+                                max_items, s),
            "attn_fwd launch");
   return ok();
+}
+
+hstu_status_t attn_fwd_impl(const hstu_problem_t* p, const hstu_jagged_t* j, const Tensors& t,
+                            void* out, int out_f32, void* ws, size_t ws_bytes, hipStream_t s) {
+  HSTU_TRY(check_fwd_args(p, j, t, out));
+  Layout l;
+  HSTU_TRY(check_ws(p, ws, ws_bytes, &l));
+  if (p->total_tokens == 0) return ok();
+  char* w = (char*)ws;
+  return attn_fwd_run(p, j, t, out, out_f32, (int32_t*)(w + l.counts),
+                      (WorkItem*)(w + l.fwd_items), (int64_t*)(w + l.trange), l.max_fwd, true, s);
+}
+
+// ---- forward without a workspace ------------------------------------------
+// hstu_attn_fwd_noalloc keeps the forward's scratch in one static device
+// array per GPU instead of a caller workspace.  Host code never passes the
+// array's name to a kernel: its device address is looked up once per
+// device with hipGetSymbolAddress and kept in g_scratch_dev.
+
+constexpr size_t kNoAllocScratch = HSTU_NOALLOC_SCRATCH_BYTES;
+static __device__ __align__(256) unsigned char scratch[kNoAllocScratch];
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_dev[kMaxDevices] = {};
+
+// Device address of the current device's scratch array, or an error.
+hstu_status_t scratch_for_current_device(char** out) {
+  int dev = -1;
+  HSTU_HIP(hipGetDevice(&dev), "hipGetDevice");
+  if (dev < 0 || dev >= kMaxDevices)
+    return fail(HSTU_ERR_UNSUPPORTED, "device index %d is above %d", dev, kMaxDevices - 1);
+  std::lock_guard<std::mutex> lk(g_scratch_mu);
+  if (!g_scratch_dev[dev]) {
+    void* ptr = nullptr;
+    HSTU_HIP(hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch)), "hipGetSymbolAddress(scratch)");
+    if (!ptr) return fail(HSTU_ERR_HIP, "hipGetSymbolAddress(scratch) returned NULL");
+    g_scratch_dev[dev] = ptr;
+  }
+  *out = (char*)g_scratch_dev[dev];
+  return HSTU_OK;
+}
+
+// Offsets of the forward's scratch inside the static array.
+struct NoAllocLayout {
+  size_t counts, items, trange, total;
+  int64_t max_items;
+};
+
+NoAllocLayout noalloc_layout(const hstu_problem_t* p) {
+  NoAllocLayout l;
+  l.max_items = max_work_items(p->total_tokens, p->num_seqs, kFwdBM);
+  size_t off = 0;
+  l.counts = off;
+  off = align_up(off + 2 * sizeof(int32_t));
+  l.items = off;
+  off = align_up(off + sizeof(WorkItem) * (size_t)l.max_items);
+  l.trange = off;
+  off = align_up(off + 2 * sizeof(int64_t) * (size_t)p->num_seqs);
+  l.total = off;
+  return l;
 }
 
 // ---- linear maps f_1 (Eq. 1) and f_2 (Eq. 3) -----------------------------
@@ -696,6 +759,30 @@ hstu_status_t hstu_attn_fwd(const hstu_problem_t* p, const hstu_jagged_t* j, con
   try {
     Tensors t{q, q_stride, k, k_stride, v, v_stride};
     return attn_fwd_impl(p, j, t, out, 0, ws, ws_bytes, (hipStream_t)hip_stream);
+  } catch (...) {
+    return fail(HSTU_ERR_INVALID_ARGUMENT, "internal error");
+  }
+}
+
+hstu_status_t hstu_attn_fwd_noalloc(const hstu_problem_t* p, const hstu_jagged_t* j,
+                                    const void* q, int64_t q_stride, const void* k,
+                                    int64_t k_stride, const void* v, int64_t v_stride, void* out,
+                                    void* hip_stream) {
+  try {
+    hipStream_t s = (hipStream_t)hip_stream;
+    Tensors t{q, q_stride, k, k_stride, v, v_stride};
+    HSTU_TRY(check_fwd_args(p, j, t, out));
+    const NoAllocLayout l = noalloc_layout(p);
+    if (p->dtype == HSTU_BF16 && l.total > kNoAllocScratch)
+      return fail(HSTU_ERR_UNSUPPORTED,
+                  "hstu_attn_fwd_noalloc: %zu bytes of scratch needed (num_seqs %d, total_tokens "
+                  "%lld), above its static %zu bytes; use hstu_attn_fwd with a workspace",
+                  l.total, p->num_seqs, (long long)p->total_tokens, kNoAllocScratch);
+    if (p->total_tokens == 0) return ok();
+    char* w = nullptr;
+    HSTU_TRY(scratch_for_current_device(&w));
+    return attn_fwd_run(p, j, t, out, 0, (int32_t*)(w + l.counts), (WorkItem*)(w + l.items),
+                        (int64_t*)(w + l.trange), l.max_items, false, s);
   } catch (...) {
     return fail(HSTU_ERR_INVALID_ARGUMENT, "internal error");
   }

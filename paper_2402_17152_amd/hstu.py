@@ -30,7 +30,8 @@ EXPORTED = ("hstu_workspace_bytes", "hstu_attn_fwd", "hstu_attn_bwd", "hstu_laye
             "hstu_proj_workspace_bytes", "hstu_proj_in_fwd",
             "hstu_proj_out_fwd", "hstu_proj_out_bwd", "hstu_proj_in_bwd",
             "hstu_sl_subseq_len", "hstu_sl_keep_numerator", "hstu_sl_workspace_bytes",
-            "hstu_stochastic_length", "hstu_gather_rows", "hstu_sl_sparsity")
+            "hstu_stochastic_length", "hstu_gather_rows", "hstu_sl_sparsity",
+            "hstu_attn_fwd_noalloc")
 
 
 class Problem(ctypes.Structure):
@@ -84,6 +85,7 @@ def _load():
         "hstu_attn_fwd_cached_workspace_bytes": (sz, [PP]),
         "hstu_sl_subseq_len": (i32, [i32, ctypes.c_double]),
         "hstu_sl_keep_numerator": (ctypes.c_double, [i32, ctypes.c_double]),
+        "hstu_attn_fwd_noalloc": (i32, [PP, PJ, P, i64, P, i64, P, i64, P, P]),
         "hstu_sl_workspace_bytes": (sz, [i32]),
         "hstu_stochastic_length": (i32, [i32, P, P, P, i32, ctypes.c_double, i32, P, P, P, P, P,
                                          sz, P]),
@@ -194,6 +196,18 @@ def hstu_attn_fwd(q, k, v, seq_offsets, timestamps, rab_pos, rab_time, max_seq_l
     _check(lib.hstu_attn_fwd(ctypes.byref(p), ctypes.byref(j), _ptr(q), _row_stride(q), _ptr(k),
                              _row_stride(k), _ptr(v), _row_stride(v), _ptr(out), _ptr(ws),
                              ws.numel(), _stream(stream)))
+    return out
+
+
+def hstu_attn_fwd_noalloc(q, k, v, seq_offsets, timestamps, rab_pos, rab_time, max_seq_len, out,
+                          num_targets=None, stream=None):
+    """hstu_attn_fwd with its scratch in the library's static device array
+    (no workspace; `out` [T, h, d_v] is required, nothing is allocated)."""
+    p = problem_for(q, v, seq_offsets, max_seq_len, rab_time)
+    j = make_jagged(seq_offsets, timestamps, rab_pos, rab_time, num_targets)
+    _check(lib.hstu_attn_fwd_noalloc(ctypes.byref(p), ctypes.byref(j), _ptr(q), _row_stride(q),
+                                     _ptr(k), _row_stride(k), _ptr(v), _row_stride(v), _ptr(out),
+                                     _stream(stream)))
     return out
 
 
