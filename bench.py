@@ -322,7 +322,7 @@ def counters_traffic(kernel: str, workload: str, src: str):
 
 
 def dq_partial_bytes(batch, block_rows=32, block_keys=128):
-    """Bytes of bf16 partial dQ blocks the two-role backward stores (and
+    """Bytes of f16 partial dQ blocks the two-role backward stores (and
     its reduce pass reads back): one 32-row x d_qk block per 32-row step of
     every 128-key block and head."""
     s = batch.spec
@@ -352,42 +352,45 @@ def dq_atomic_bytes(batch, block_keys=128):
     return rows * s.num_heads * s.d_qk * 4
 
 
-def cpu_baseline(batch, flops_full):
-    """The oracle, untuned, on the shortest sequences of the batch (one
-    OpenMP task per sequence x head, as many sequences as there are
-    threads per head), scaled to whole-workload tokens/s by FLOPs."""
-    import numpy as np
+def _cpu_model():
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
 
+
+def cpu_baseline(batch, flops_full):
+    """The oracle, untuned, over the whole workload: one forward (and, for
+    the fwd+bwd workloads, one backward with the seeded dO) on the host
+    cores, OpenMP over (sequence, head) tasks; tokens/s = T / wall time."""
     import oracle
-    from paper_2402_17152_amd import inputs
 
     threads = oracle.num_threads()
-    h = batch.spec.num_heads
-    k = max(1, min(len(batch.lengths), threads // h))
-    seqs = [int(x) for x in np.argsort(batch.lengths, kind="stable")[:k]]
-    sub = inputs.sub_batch(batch, seqs)
-    f_fwd, f_bwd = inputs.flops(sub)
     N = batch.spec.max_seq_len
-    args = (sub.seq_offsets, N, sub.timestamps, sub.rab_pos, sub.rab_time, sub.f64("q"),
-            sub.f64("k"), sub.f64("v"))
+    args = (batch.seq_offsets, N, batch.timestamps, batch.rab_pos, batch.rab_time,
+            batch.f64("q"), batch.f64("k"), batch.f64("v"))
     t0 = time.perf_counter()
-    oracle.attn_fwd(*args, num_targets=sub.num_targets)
+    oracle.attn_fwd(*args, num_targets=batch.num_targets)
     if batch.spec.backward:
-        oracle.attn_bwd(*args, sub.f64("do"), num_targets=sub.num_targets)
+        oracle.attn_bwd(*args, batch.f64("do"), num_targets=batch.num_targets)
     dt = time.perf_counter() - t0
-    f_sample = f_fwd + (f_bwd if batch.spec.backward else 0)
-    equiv_s = dt * flops_full / f_sample
+    tasks = len(batch.lengths) * batch.spec.num_heads
     return {
-        "value": batch.total_tokens / equiv_s,
+        "value": batch.total_tokens / dt,
         "unit": "tokens/s",
-        "cores": min(threads, k * h),
+        "cores": min(threads, tasks),
         "kind": "oracle",
-        "sample": (f"fp64 oracle fwd{'+bwd' if batch.spec.backward else ''} on the {k} shortest "
-                   f"sequences (lengths {[int(batch.lengths[s]) for s in seqs]}, all {h} heads): "
-                   f"{f_sample:.3e} FLOP in {dt:.2f} s = {f_sample / dt / 1e9:.2f} GFLOP/s, "
-                   f"scaled to the whole workload by FLOPs"),
-        "gflops": f_sample / dt / 1e9,
+        "sample": (f"the whole workload (T={batch.total_tokens}, {len(batch.lengths)} sequences x "
+                   f"{batch.spec.num_heads} heads): fp64 oracle fwd"
+                   f"{'+bwd' if batch.spec.backward else ''}, {flops_full:.3e} FLOP in {dt:.1f} s "
+                   f"= {flops_full / dt / 1e9:.2f} GFLOP/s on {threads} OpenMP threads "
+                   f"({_cpu_model()})"),
+        "gflops": flops_full / dt / 1e9,
         "seconds": dt,
+        "cpu_model": _cpu_model(),
     }
 
 
@@ -498,7 +501,7 @@ def main():
     if "attn_bwd" in kernels:
         kernels["attn_bwd"]["tflops"] = f_bwd / (kernels["attn_bwd"]["avg_ms"] * 1e-3) / 1e12
     if "dq_reduce" in kernels:
-        # bf16 partial blocks read, bf16 dQ written
+        # f16 partial blocks read, bf16 dQ written
         rb = dq_partial_bytes(batch) + T * spec.num_heads * spec.d_qk * 2
         kernels["dq_reduce"]["gbs"] = rb / (kernels["dq_reduce"]["avg_ms"] * 1e-3) / 1e9
     if "ln_gate" in kernels:
@@ -527,8 +530,9 @@ def main():
                 roofline["dq_atomic_bytes"] = qb
                 roofline["dq_atomic_tbs"] = qb / (kernels[dom]["avg_ms"] * 1e-3) / 1e12
             else:
-                # The two-role kernel stores them as bf16 blocks; a reduce
-                # pass (kernels.dq_reduce) reads them back.
+                # The two-role kernel stores them as f16 blocks (each with
+                # a power-of-two scale); a reduce pass (kernels.dq_reduce)
+                # reads them back.
                 roofline["dq_partial_bytes"] = dq_partial_bytes(batch)
 
     aux = None if args.no_aux else aux_measurements(hstu, torch, d, batch, stream)
