@@ -2,18 +2,24 @@
 // the L x L matrix of time buckets bkt(t_i - t_j) (notation table, entry
 // rab^{p,t}) as uint8, row-major, sequences concatenated at pair_offsets.
 //
-// HBM-write bound.  A workgroup owns 16 rows of one sequence and walks the
-// columns in slabs of 2048 whose timestamps it stages in LDS.  When the
+// HBM-write bound.  A workgroup owns 32 consecutive tokens of the batch,
+// i.e. 32 rows of one sequence (or the rows of two or more sequences that
+// meet inside the block), and walks the columns in slabs of 8192 (whole
+// rows, for sequences up to that length) whose timestamps it stages in
+// LDS.  When the
 // timestamps of its rows and of the slab lie within 2^30 of the sequence's
 // first one (always, for real event times), they are rebased to 32 bits
-// and a pair costs one v_sad_u32 and one v_ffbh_u32; otherwise the exact
-// 64-bit form runs.
-// A wave writes one row segment at a time, each lane aligned dwords (4
-// buckets) of the flat output, so a wave store covers 256 contiguous
-// bytes; only the two end dwords of a segment use byte stores.  Rows start
-// at any byte, so the slab is staged four times, shifted by 0..3 words:
-// the copy matching the row's alignment gives every lane its 4 column
-// timestamps in one aligned, bank-conflict-free 16-byte LDS read.
+// and a pair costs v_sad_u32, v_ffbh_u32 and one saturating subtract that
+// writes the bucket straight into its byte of the output dword (SDWA);
+// otherwise the exact 64-bit form runs.
+// A row segment is written as aligned 16-byte chunks, one per lane (a wave
+// store covers 1 KB), plus at most 15 bytes at each end, written one byte
+// per lane.  A chunk needs the timestamps of 16 consecutive columns: the
+// slab is staged twice, shifted by 0 and 1 words, so that the copy
+// matching the row's alignment holds them as four aligned 16-byte words
+// (or, for half of the alignments, eight 8-byte words), and each copy
+// inserts one padding word-quad every 64 entries, so that the lanes of a
+// read (64 bytes apart) spread over the LDS banks.
 #include "bias.h"
 #include "kernels.h"
 
@@ -22,64 +28,120 @@ namespace hstu {
 namespace {
 
 constexpr int kBktThreads = 256;
-constexpr int kBktRows = 16;    // rows per workgroup
-constexpr int kBktCols = 2048;  // columns staged per slab
-constexpr int kBktLd = kBktCols + 4;
+constexpr int kBktRows = 32;    // rows per workgroup
+constexpr int kBktCols = 8192;  // columns staged per slab
+// Entry y of a copy sits at y + 4 (y >> 6); y <= kBktCols.
+__device__ __forceinline__ int bkt_pidx(int y) { return y + 4 * (y >> 6); }
+constexpr int kBktLd = ((kBktCols + 2) + 4 * ((kBktCols + 2) / 64 + 1) + 3) / 4 * 4;
 
-struct BktShared {
+struct __align__(16) BktShared {
   union {
-    uint32_t t32[4][kBktLd];  // copy k holds column x at index x + k
+    uint32_t t32[2][kBktLd];  // copy s holds column x at bkt_pidx(x + s)
     int64_t t64[kBktCols];
   };
+  int64_t rowt[kBktRows];     // the workgroup's row timestamps
 };
 
-// |dt| < 2^31, so floor(log2) <= 30: the clamp matters only for B_t <= 31.
+// Leading-zero count of |ti - tj| < 2^31 (0xffffffff for 0), raised to
+// zmin = 32 - nb when CLAMP (nb <= 31), so that the saturating 31 - z
+// below is min(floor(log2 |dt|), nb - 1), and 0 for |dt| <= 1.
 template <bool CLAMP>
-__device__ __forceinline__ uint32_t bkt32(uint32_t ti, uint32_t tj, int nb) {
-  uint32_t d;
+__device__ __forceinline__ uint32_t lz32(uint32_t ti, uint32_t tj, uint32_t zmin) {
+  uint32_t d, z;
   asm("v_sad_u32 %0, %1, %2, 0" : "=v"(d) : "v"(ti), "v"(tj));
-  const int b = 31 - __clz((int)(d | 1u));
-  return (uint32_t)(CLAMP ? min(b, nb - 1) : b);
+  asm("v_ffbh_u32 %0, %1" : "=v"(z) : "v"(d));
+  if constexpr (CLAMP) z = z > zmin ? z : zmin;  // 0xffffffff stays
+  return z;
+}
+
+// Four buckets packed little-endian into one dword: byte 0 by a saturating
+// subtract, bytes 1-3 by the same subtract writing its byte in place (SDWA).
+template <bool CLAMP>
+__device__ __forceinline__ uint32_t bkt4(uint32_t ti, uint32_t a, uint32_t b, uint32_t c,
+                                         uint32_t d, uint32_t zmin, uint32_t c31) {
+  const uint32_t z0 = lz32<CLAMP>(ti, a, zmin), z1 = lz32<CLAMP>(ti, b, zmin);
+  const uint32_t z2 = lz32<CLAMP>(ti, c, zmin), z3 = lz32<CLAMP>(ti, d, zmin);
+  uint32_t r;
+  asm("v_sub_u32_e64 %0, 31, %1 clamp" : "=v"(r) : "v"(z0));
+  asm("v_sub_u32_sdwa %0, %1, %2 clamp dst_sel:BYTE_1 dst_unused:UNUSED_PRESERVE "
+      "src0_sel:DWORD src1_sel:DWORD"
+      : "+v"(r) : "v"(c31), "v"(z1));
+  asm("v_sub_u32_sdwa %0, %1, %2 clamp dst_sel:BYTE_2 dst_unused:UNUSED_PRESERVE "
+      "src0_sel:DWORD src1_sel:DWORD"
+      : "+v"(r) : "v"(c31), "v"(z2));
+  asm("v_sub_u32_sdwa %0, %1, %2 clamp dst_sel:BYTE_3 dst_unused:UNUSED_PRESERVE "
+      "src0_sel:DWORD src1_sel:DWORD"
+      : "+v"(r) : "v"(c31), "v"(z3));
+  return r;
 }
 
 template <bool CLAMP>
 __device__ __forceinline__ void row_segment32(const BktShared& sm, uint32_t ti, int nb, int64_t P,
                                               int ncols, uint8_t* __restrict__ out, int lane) {
-  // Flat bytes [P, P + ncols) hold columns 0 .. ncols-1 of the slab; dword
-  // dw covers columns 4 dw - P .. +3.  Four dwords per lane and pass, 64
-  // apart, keep every LDS read and store contiguous across the wave.
-  const int64_t first = P >> 2, last = (P + ncols - 1) >> 2;
-  const int k = (int)(P & 3);  // column 4 dw - P of copy k sits at 4 (dw - P / 4)
-  const uint32_t* tk = sm.t32[k];
-  // The two end dwords may hold bytes of neighbouring rows: byte stores.
-  if (lane < 2 && (lane == 0 || last != first)) {
-    const int64_t dw = lane ? last : first;
-    const int j0 = (int)((dw << 2) - P);
-    for (int e = 0; e < 4; e++) {
-      const int j = j0 + e;
-      if (j >= 0 && j < ncols) out[(dw << 2) + e] = (uint8_t)bkt32<CLAMP>(ti, tk[j + k], nb);
+  // Flat bytes [P, P + ncols) hold columns 0 .. ncols-1 of the slab;
+  // relative to P: the head [0, hend), nch aligned 16-byte chunks from h =
+  // (16 - P) mod 16, and the tail [tstart, ncols) (at most 15 bytes each).
+  const uint32_t zmin = CLAMP ? (uint32_t)(32 - nb) : 0u;
+  const uint32_t c31 = 31u;
+  const int64_t cfirst = (P + 15) >> 4;
+  const int h = (int)((cfirst << 4) - P);
+  const int nch = max(0, (int)(((P + ncols) >> 4) - cfirst));
+  const int hend = min(h, ncols), tstart = max(hend, h + 16 * nch);
+  uint8_t* const row = out + P;
+  // End bytes: lanes 0-15 the head, lanes 32-47 the tail (copy 0).
+  {
+    const int r = lane < 32 ? lane : tstart + (lane - 32);
+    const bool on = lane < 32 ? lane < hend : (lane < 48 && r < ncols);
+    if (on) {
+      const uint32_t z = lz32<CLAMP>(ti, sm.t32[0][bkt_pidx(r)], zmin);
+      uint32_t b;
+      asm("v_sub_u32_e64 %0, 31, %1 clamp" : "=v"(b) : "v"(z));
+      row[r] = (uint8_t)b;
     }
   }
-  // Interior dwords first+1 .. last-1, four per lane and pass; lanes past
-  // the end redo the last one (same value to the same address), so the
-  // pass has no branches and its four LDS reads are in flight together.
-  // Interior dword a (from 0) starts at column 4a + c1, c1 = 4(first+1) - P
-  // in [1, 4], and c1 + k = 4: its columns sit at tk[4a + 4 ..].
-  const int n_int = (int)(last - first - 1);
-  uint32_t* const seg = reinterpret_cast<uint32_t*>(out + ((first + 1) << 2));
-  const uint32_t* const tc = tk + 4;
-  for (int d0 = 0; d0 < n_int; d0 += 256) {
-    int a[4];
-    uint32_t v[4];
-#pragma unroll
-    for (int q = 0; q < 4; q++) {
-      a[q] = min(d0 + lane + 64 * q, n_int - 1);
-      const u32x4 tj = *reinterpret_cast<const u32x4*>(tc + 4 * a[q]);
-      v[q] = bkt32<CLAMP>(ti, tj[0], nb) | bkt32<CLAMP>(ti, tj[1], nb) << 8 |
-             bkt32<CLAMP>(ti, tj[2], nb) << 16 | bkt32<CLAMP>(ti, tj[3], nb) << 24;
+  if (lane >= nch) return;
+  // Chunk a covers columns h + 16 a .. +15, entries y .. y + 15 of copy
+  // s = P mod 2 with y = h + 16 a + s: a multiple of 4 when P mod 4 < 2
+  // (16-byte reads), else 2 mod 4 (8-byte reads).  Moving 64 chunks on
+  // adds 1024 entries, 16 whole pad periods: the offsets of the reads
+  // from the first stay fixed and the first moves by 1088.
+  const int k = (int)(P & 3), sc = k & 1;
+  const int y = h + sc + 16 * lane;
+  const int p0 = bkt_pidx(y);
+  const uint32_t* src = sm.t32[sc] + p0;
+  u32x4* dst = reinterpret_cast<u32x4*>(row + h + 16 * lane);
+  if (k < 2) {
+    const int d1 = bkt_pidx(y + 4) - p0, d2 = bkt_pidx(y + 8) - p0, d3 = bkt_pidx(y + 12) - p0;
+    for (int a = lane; a < nch; a += 64) {
+      const u32x4 t0 = *reinterpret_cast<const u32x4*>(src);
+      const u32x4 t1 = *reinterpret_cast<const u32x4*>(src + d1);
+      const u32x4 t2 = *reinterpret_cast<const u32x4*>(src + d2);
+      const u32x4 t3 = *reinterpret_cast<const u32x4*>(src + d3);
+      u32x4 v;
+      v[0] = bkt4<CLAMP>(ti, t0[0], t0[1], t0[2], t0[3], zmin, c31);
+      v[1] = bkt4<CLAMP>(ti, t1[0], t1[1], t1[2], t1[3], zmin, c31);
+      v[2] = bkt4<CLAMP>(ti, t2[0], t2[1], t2[2], t2[3], zmin, c31);
+      v[3] = bkt4<CLAMP>(ti, t3[0], t3[1], t3[2], t3[3], zmin, c31);
+      *dst = v;
+      src += 1088;
+      dst += 64;
     }
+  } else {
+    int dd[8];
 #pragma unroll
-    for (int q = 0; q < 4; q++) seg[a[q]] = v[q];
+    for (int m = 0; m < 8; m++) dd[m] = bkt_pidx(y + 2 * m) - p0;
+    for (int a = lane; a < nch; a += 64) {
+      uint2 t[8];
+#pragma unroll
+      for (int m = 0; m < 8; m++) t[m] = *reinterpret_cast<const uint2*>(src + dd[m]);
+      u32x4 v;
+#pragma unroll
+      for (int q = 0; q < 4; q++)
+        v[q] = bkt4<CLAMP>(ti, t[2 * q].x, t[2 * q].y, t[2 * q + 1].x, t[2 * q + 1].y, zmin, c31);
+      *dst = v;
+      src += 1088;
+      dst += 64;
+    }
   }
 }
 
@@ -88,74 +150,96 @@ __device__ __forceinline__ void row_segment64(const BktShared& sm, int64_t ti, i
   for (int j = lane; j < ncols; j += 64) out[P + j] = (uint8_t)time_bucket64(ti - sm.t64[j], nb);
 }
 
-__global__ __launch_bounds__(kBktThreads) void bucketize_kernel(
-    int32_t num_seqs, int32_t nb, const int64_t* __restrict__ offs, const int64_t* __restrict__ ts,
-    const int64_t* __restrict__ pair_offs, uint8_t* __restrict__ out) {
-  __shared__ BktShared sm;
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  for (int b = blockIdx.y; b < num_seqs; b += gridDim.y) {
-    const int64_t o = offs[b];
-    const int L = (int)(offs[b + 1] - o);
-    const int r0 = blockIdx.x * kBktRows;
-    if (r0 >= L) continue;  // uniform over the workgroup
-    const int rows = min(kBktRows, L - r0);
-    const int64_t* __restrict__ t = ts + o;
-    const int64_t base = pair_offs[b];
-
-    // 32-bit form: timestamps as offsets from t[0] + 2^30; it applies when
-    // every offset the workgroup touches lies in [0, 2^31), so that two of
-    // them differ by less than 2^31.  The next slab's timestamps are
-    // loaded while the current one is bucketed.
-    const int64_t t0 = t[0] - ((int64_t)1 << 30);
-    auto in32 = [](int64_t d) { return d >= 0 && d < ((int64_t)1 << 31); };
-    bool rows_ok = true;
-    if (tid < rows) rows_ok = in32(t[r0 + tid] - t0);
-    constexpr int kPer = kBktCols / kBktThreads;
-    int64_t nxt[kPer];
+// One 32-row block of a sequence: rows r0 .. r0 + rows - 1 of sequence b
+// (offset o, length L, pairs from base), every column.
+__device__ __forceinline__ void bucketize_rows(BktShared& sm, int nb, const int64_t* __restrict__ t,
+                                               int L, int64_t base, int r0, int rows,
+                                               uint8_t* __restrict__ out, int tid, int wave,
+                                               int lane) {
+  // 32-bit form: timestamps as offsets from t[0] - 2^30; it applies when
+  // every offset the workgroup touches lies in [0, 2^31), so that two of
+  // them differ by less than 2^31.  A slab's timestamps are loaded before
+  // any output of that slab is stored: loads and stores share the wave's
+  // memory counter, so a load issued after stores would wait for them.
+  const int64_t t0 = t[0] - ((int64_t)1 << 30);
+  auto in32 = [](int64_t d) { return d >= 0 && d < ((int64_t)1 << 31); };
+  bool rows_ok = true;
+  if (tid < rows) {
+    const int64_t tr = t[r0 + tid];
+    sm.rowt[tid] = tr;
+    rows_ok = in32(tr - t0);
+  }
+  constexpr int kPer = kBktCols / kBktThreads;
+  for (int c0 = 0; c0 < L; c0 += kBktCols) {
+    const int ncols = min(kBktCols, L - c0);
+    // Rebased low words, kept only if the whole workgroup passes (the
+    // 64-bit form reloads the values).
+    uint32_t cur[kPer];
+    bool ok = rows_ok;
 #pragma unroll
-    for (int e = 0; e < kPer; e++) nxt[e] = tid + e * kBktThreads < L ? t[tid + e * kBktThreads] : t0;
-    for (int c0 = 0; c0 < L; c0 += kBktCols) {
-      const int ncols = min(kBktCols, L - c0);
-      int64_t cur[kPer];
-      bool ok = rows_ok;
-#pragma unroll
-      for (int e = 0; e < kPer; e++) {
-        cur[e] = nxt[e];
-        ok = ok && in32(cur[e] - t0);
-      }
-      const bool fast = __syncthreads_and(ok);  // also: previous slab fully consumed
-      if (fast) {
-#pragma unroll
-        for (int e = 0; e < kPer; e++) {
-          const int x = tid + e * kBktThreads;
-          const uint32_t v = (uint32_t)(cur[e] - t0);
-#pragma unroll
-          for (int k = 0; k < 4; k++) sm.t32[k][x + k] = v;
-        }
-      } else {
-#pragma unroll
-        for (int e = 0; e < kPer; e++) sm.t64[tid + e * kBktThreads] = cur[e];
-      }
-      __syncthreads();
-      const int c1 = c0 + kBktCols;
+    for (int e = 0; e < kPer; e++) {
+      const int x = tid + e * kBktThreads;
+      const int64_t d = (x < ncols ? t[c0 + x] : t0) - t0;
+      ok = ok && in32(d);
+      cur[e] = (uint32_t)d;
+    }
+    const bool fast = __syncthreads_and(ok);  // also: previous slab fully consumed
+    if (fast) {
 #pragma unroll
       for (int e = 0; e < kPer; e++) {
-        const int x = c1 + tid + e * kBktThreads;
-        nxt[e] = x < L ? t[x] : t0;
+        const int x = tid + e * kBktThreads;
+        sm.t32[0][bkt_pidx(x)] = cur[e];
+        sm.t32[1][bkt_pidx(x + 1)] = cur[e];
       }
-      for (int r = wave; r < rows; r += kBktThreads / 64) {
-        const int i = r0 + r;
-        const int64_t ti = t[i];
-        const int64_t P = base + (int64_t)i * L + c0;
-        if (!fast)
-          row_segment64(sm, ti, nb, P, ncols, out, lane);
-        else if (nb <= 31)
-          row_segment32<true>(sm, (uint32_t)(ti - t0), nb, P, ncols, out, lane);
-        else
-          row_segment32<false>(sm, (uint32_t)(ti - t0), nb, P, ncols, out, lane);
+    } else {
+      for (int e = 0; e < kPer; e++) {
+        const int x = tid + e * kBktThreads;
+        sm.t64[x] = x < ncols ? t[c0 + x] : t0;
       }
     }
-    __syncthreads();  // the next sequence restages the slab
+    __syncthreads();
+    // Row set-up is wave-uniform (scalar unit).
+    for (int r = wave; r < rows; r += kBktThreads / 64) {
+      const int64_t ti = ((int64_t)__builtin_amdgcn_readfirstlane((int)(sm.rowt[r] >> 32)) << 32) |
+                         (uint32_t)__builtin_amdgcn_readfirstlane((int)sm.rowt[r]);
+      const int64_t P = base + (int64_t)(r0 + r) * L + c0;
+      if (!fast)
+        row_segment64(sm, ti, nb, P, ncols, out, lane);
+      else if (nb <= 31)
+        row_segment32<true>(sm, (uint32_t)(ti - t0), nb, P, ncols, out, lane);
+      else
+        row_segment32<false>(sm, (uint32_t)(ti - t0), nb, P, ncols, out, lane);
+    }
+    __syncthreads();  // the slab (or the row timestamps) is restaged next
+  }
+}
+
+// Workgroup g covers tokens [32 g, 32 g + 32) of the concatenated batch:
+// the rows of the sequence(s) those tokens belong to, every column.
+__global__ __launch_bounds__(kBktThreads) void bucketize_kernel(
+    int32_t num_seqs, int64_t total_tokens, int32_t nb, const int64_t* __restrict__ offs,
+    const int64_t* __restrict__ ts, const int64_t* __restrict__ pair_offs,
+    uint8_t* __restrict__ out) {
+  __shared__ BktShared sm;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  for (int64_t g = blockIdx.x; g * kBktRows < total_tokens; g += gridDim.x) {
+    int64_t R0 = g * kBktRows;
+    const int64_t R1 = min(R0 + kBktRows, total_tokens);
+    // b = the last sequence with offs[b] <= R0 (offsets are non-decreasing).
+    int lo = 0, hi = num_seqs - 1;
+    while (lo < hi) {
+      const int mid = (lo + hi + 1) >> 1;
+      if (offs[mid] <= R0) lo = mid; else hi = mid - 1;
+    }
+    for (int b = lo; b < num_seqs && R0 < R1; b++) {
+      const int64_t o = offs[b], e = offs[b + 1];
+      if (e <= R0) continue;  // empty sequence
+      const int rows = (int)(min(e, R1) - R0);
+      bucketize_rows(sm, nb, ts + o, (int)(e - o), pair_offs[b], (int)(R0 - o), rows, out, tid,
+                     wave, lane);
+      R0 += rows;
+    }
   }
 }
 
@@ -165,16 +249,11 @@ hipError_t launch_bucketize(int32_t num_seqs, int64_t total_tokens, int32_t num_
                             const int64_t* seq_offsets, const int64_t* timestamps,
                             const int64_t* pair_offsets, int64_t total_pairs, uint8_t* out,
                             hipStream_t s) {
-  if (total_pairs <= 0 || num_seqs <= 0) return hipSuccess;
-  // The longest sequence has L^2 <= total_pairs and L <= total_tokens;
-  // workgroups past a sequence's rows return at once.
-  int64_t lmax = (int64_t)sqrt((double)total_pairs);
-  while (lmax * lmax > total_pairs) lmax--;
-  while ((lmax + 1) * (lmax + 1) <= total_pairs) lmax++;
-  lmax = min(lmax, total_tokens);
-  const dim3 grid((unsigned)((lmax + kBktRows - 1) / kBktRows), (unsigned)min(num_seqs, 65535));
-  hipLaunchKernelGGL(bucketize_kernel, grid, dim3(kBktThreads), 0, s, num_seqs, num_buckets,
-                     seq_offsets, timestamps, pair_offsets, out);
+  if (total_pairs <= 0 || num_seqs <= 0 || total_tokens <= 0) return hipSuccess;
+  const int64_t blocks = (total_tokens + kBktRows - 1) / kBktRows;
+  const unsigned grid = (unsigned)min(blocks, (int64_t)1 << 30);
+  hipLaunchKernelGGL(bucketize_kernel, dim3(grid), dim3(kBktThreads), 0, s, num_seqs, total_tokens,
+                     num_buckets, seq_offsets, timestamps, pair_offsets, out);
   return hipGetLastError();
 }
 
