@@ -2,8 +2,8 @@
 // the L x L matrix of time buckets bkt(t_i - t_j) (notation table, entry
 // rab^{p,t}) as uint8, row-major, sequences concatenated at pair_offsets.
 //
-// HBM-write bound.  A workgroup owns 32 consecutive tokens of the batch,
-// i.e. 32 rows of one sequence (or the rows of two or more sequences that
+// HBM-write bound.  A workgroup owns 48 consecutive tokens of the batch,
+// i.e. 48 rows of one sequence (or the rows of two or more sequences that
 // meet inside the block), and walks the columns in slabs of 8192 (whole
 // rows, for sequences up to that length) whose timestamps it stages in
 // LDS.  When the
@@ -28,11 +28,14 @@ namespace hstu {
 namespace {
 
 constexpr int kBktThreads = 256;
-constexpr int kBktRows = 32;    // rows per workgroup
+constexpr int kBktRows = 48;    // rows per workgroup
 constexpr int kBktCols = 8192;  // columns staged per slab
-// Entry y of a copy sits at y + 4 (y >> 6); y <= kBktCols.
-__device__ __forceinline__ int bkt_pidx(int y) { return y + 4 * (y >> 6); }
-constexpr int kBktLd = ((kBktCols + 2) + 4 * ((kBktCols + 2) / 64 + 1) + 3) / 4 * 4;
+// Entry y of a copy sits at y + 4 (y >> kPadShift); y <= kBktCols.
+constexpr int kPadShift = 6;
+__device__ __forceinline__ int bkt_pidx(int y) { return y + 4 * (y >> kPadShift); }
+constexpr int kBktLd = ((kBktCols + 2) + 4 * ((kBktCols + 2) / (1 << kPadShift) + 1) + 3) / 4 * 4;
+// Entries 1024 further on (64 chunks of 16) sit this many words further.
+constexpr int kChunkStep = 1024 + 4 * (1024 >> kPadShift);
 
 struct __align__(16) BktShared {
   union {
@@ -123,7 +126,7 @@ __device__ __forceinline__ void row_segment32(const BktShared& sm, uint32_t ti, 
       v[2] = bkt4<CLAMP>(ti, t2[0], t2[1], t2[2], t2[3], zmin, c31);
       v[3] = bkt4<CLAMP>(ti, t3[0], t3[1], t3[2], t3[3], zmin, c31);
       *dst = v;
-      src += 1088;
+      src += kChunkStep;
       dst += 64;
     }
   } else {
@@ -139,7 +142,7 @@ __device__ __forceinline__ void row_segment32(const BktShared& sm, uint32_t ti, 
       for (int q = 0; q < 4; q++)
         v[q] = bkt4<CLAMP>(ti, t[2 * q].x, t[2 * q].y, t[2 * q + 1].x, t[2 * q + 1].y, zmin, c31);
       *dst = v;
-      src += 1088;
+      src += kChunkStep;
       dst += 64;
     }
   }
@@ -150,8 +153,8 @@ __device__ __forceinline__ void row_segment64(const BktShared& sm, int64_t ti, i
   for (int j = lane; j < ncols; j += 64) out[P + j] = (uint8_t)time_bucket64(ti - sm.t64[j], nb);
 }
 
-// One 32-row block of a sequence: rows r0 .. r0 + rows - 1 of sequence b
-// (offset o, length L, pairs from base), every column.
+// Rows r0 .. r0 + rows - 1 of one sequence (timestamps t, length L, pairs
+// from base), every column.
 __device__ __forceinline__ void bucketize_rows(BktShared& sm, int nb, const int64_t* __restrict__ t,
                                                int L, int64_t base, int r0, int rows,
                                                uint8_t* __restrict__ out, int tid, int wave,
@@ -214,7 +217,7 @@ __device__ __forceinline__ void bucketize_rows(BktShared& sm, int nb, const int6
   }
 }
 
-// Workgroup g covers tokens [32 g, 32 g + 32) of the concatenated batch:
+// Workgroup g covers tokens [48 g, 48 g + 48) of the concatenated batch:
 // the rows of the sequence(s) those tokens belong to, every column.
 __global__ __launch_bounds__(kBktThreads) void bucketize_kernel(
     int32_t num_seqs, int64_t total_tokens, int32_t nb, const int64_t* __restrict__ offs,
