@@ -243,7 +243,8 @@ def mfalcon_measurement(hstu, torch, stream):
     candidates, h=4, d=128, N=3072): the uncached target-aware forward over
     prefix ++ all candidates against cached passes that compute only the
     candidate rows from the prefix's cached K and V, as one microbatch of
-    1024 and as four of 256 (inputs of each microbatch gathered beforehand)."""
+    1024, four of 256 and sixteen of 64 (inputs of each microbatch gathered
+    beforehand), called one by one and replayed from a captured graph."""
     import numpy as np
     from paper_2402_17152_amd import inputs
     batch = inputs.make_batch("target")
@@ -288,15 +289,26 @@ def mfalcon_measurement(hstu, torch, stream):
     for b_m in (1024, 256, 64):
         mbs = microbatches(b_m)
 
-        def run():
+        def run(st=stream):
             for (q, k, v, co, ts, o, ws) in mbs:
                 hstu.hstu_attn_fwd_cached(q, k, v, co, ts, kc, vc, coffs, cts, d["rab_pos"],
-                                          d["rab_time"], N, out=o, ws=ws, stream=stream)
+                                          d["rab_time"], N, out=o, ws=ws, stream=st)
         ms = _time_ms(torch, stream, run)
+        # The same passes replayed from a HIP graph (captured once; each
+        # replay launches every pass's kernels without host calls in between).
+        run()
+        torch.cuda.synchronize()
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g):
+            run(st=torch.cuda.current_stream())
+        ms_graph = _time_ms(torch, stream, g.replay)
         res[f"cached_b{b_m}"] = {"ms": ms, "passes": len(mbs),
                                  "tflops": flop_cached / (ms * 1e-3) / 1e12,
                                  "candidates_per_s": cand / (ms * 1e-3),
-                                 "speedup_vs_uncached": ms_uncached / ms}
+                                 "speedup_vs_uncached": ms_uncached / ms,
+                                 "graph_ms": ms_graph,
+                                 "graph_speedup_vs_uncached": ms_uncached / ms_graph}
+        del g
     return res
 
 

@@ -45,11 +45,16 @@
  *            (offsets monotone from 0 to T, L_b <= N, 0 <= n_t <= L_b,
  *            timestamps in [0, 2^62)) are not checked by the hot calls;
  *            breaking them is undefined.  hstu_validate checks them.
- *   Precision HSTU_F32: fp32 storage and arithmetic.  HSTU_BF16: bf16
- *            storage, fp32 accumulation; the attention weights and dS are
- *            rounded to bf16 (nearest-even) before the second contraction.
- *            Bias tables and their gradients are fp32; offsets and
- *            timestamps int64.
+ *   Precision HSTU_F32: fp32 storage and arithmetic (the bias-table
+ *            gradients are summed in fp64 and stored as fp32).  Its
+ *            kernels are plain SIMT loops, one thread per (token, head),
+ *            meant for small problems and as an fp32 reference: every shape
+ *            the ABI accepts runs, but long sequences are slow (the matrix
+ *            cores serve HSTU_BF16 only).  HSTU_BF16: bf16 storage, fp32
+ *            accumulation; the attention weights and dS are rounded to
+ *            bf16 (nearest-even) before the second contraction.  Bias
+ *            tables and their gradients are fp32; offsets and timestamps
+ *            int64.
  *   Determinism  hstu_attn_fwd, hstu_layer_fwd, hstu_time_bucketize and
  *            hstu_complete_cumsum are bitwise deterministic, and so are
  *            dQ, dK and dV of hstu_attn_bwd for HSTU_BF16 (dQ is summed

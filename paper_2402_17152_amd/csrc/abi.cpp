@@ -148,6 +148,7 @@ struct Layout {
   size_t dq_part;   // f16 partial dQ blocks of hstu_attn_bwd (bf16 problems), then their
   size_t dq_scale;  // fp32 block scales; both share the space of dq_acc and dout, which
                     // that call does not use
+  size_t rab64;     // fp64 [2N-1 + B_t]: bias-gradient sums of the fp32 backward
   size_t total;
   int64_t max_fwd, max_bwd;
 };
@@ -183,6 +184,10 @@ Layout layout(const hstu_problem_t* p) {
     l.dq_scale = align_up(shared + slots * (size_t)p->d_qk * 64);
     off = std::max(off, align_up(l.dq_scale + slots * (size_t)(p->d_qk / 32) * 4));
   }
+  l.rab64 = off;
+  if (p->dtype == HSTU_F32)
+    off = align_up(off + sizeof(double) *
+                             ((size_t)(2 * p->max_seq_len - 1) + (size_t)p->num_time_buckets));
   l.total = off;
   return l;
 }
@@ -896,10 +901,19 @@ hstu_status_t attn_bwd_impl(const hstu_problem_t* p, const hstu_jagged_t* j, con
   JaggedArgs ja = make_args(p, j);
   char* w = (char*)ws;
   if (p->dtype == HSTU_F32) {
+    // Bias gradients summed in fp64 in the workspace, then stored as fp32.
+    double* rab64 = (double*)(w + l.rab64);
+    const int64_t nrab = 2 * (int64_t)N - 1 + p->num_time_buckets;
+    HSTU_HIP(launch_fill_f32((float*)rab64, 2 * nrab, 0.0f, s), "fill launch");
     TimedScope ts("attn_bwd", s);
-    HSTU_HIP(launch_attn_bwd_f32(ja, t, p->d_qk, p->d_v, d_out, dq, dk, dv, d_rab_pos,
-                                 d_rab_time, s),
+    HSTU_HIP(launch_attn_bwd_f32(ja, t, p->d_qk, p->d_v, d_out, dq, dk, dv, rab64,
+                                 rab64 + (2 * (int64_t)N - 1), s),
              "attn_bwd_f32 launch");
+    HSTU_HIP(launch_f64_to_f32_scaled(rab64, d_rab_pos, 2 * (int64_t)N - 1, 1.0 / N, s),
+             "convert launch");
+    HSTU_HIP(launch_f64_to_f32_scaled(rab64 + (2 * (int64_t)N - 1), d_rab_time,
+                                      p->num_time_buckets, 1.0 / N, s),
+             "convert launch");
     return ok();
   }
   int32_t* counts = (int32_t*)(w + l.counts);

@@ -7,7 +7,10 @@
 // thread per (token, head):
 //   forward       thread = query row i: O_i = (1/N) sum_j SiLU(s_ij) v_j;
 //   backward (a)  thread = query row i: dQ_i = (1/N) sum_j dS_ij k_j and
-//                 the bias gradients (global float atomics);
+//                 the bias gradients, summed in fp64 (one atomic per pair
+//                 for the position table; for the time table a running
+//                 sum per thread, added when the bucket changes, so that a
+//                 bucket's millions of terms do not pile up fp32 rounding);
 //   backward (b)  thread = key row j:   dK_j = (1/N) sum_i dS_ij q_i,
 //                                       dV_j = (1/N) sum_i SiLU(s_ij) dO_i.
 #include "kernels.h"
@@ -70,8 +73,8 @@ __global__ __launch_bounds__(64) void fwd_f32_kernel(JaggedArgs ja, Tensors t, f
 
 template <int DQK, int DV>
 __global__ __launch_bounds__(64) void bwd_dq_f32_kernel(JaggedArgs ja, Tensors t, const float* dO,
-                                                        float* dq, float* d_rab_pos,
-                                                        float* d_rab_time) {
+                                                        float* dq, double* rab_pos_acc,
+                                                        double* rab_time_acc) {
   const int64_t r = (int64_t)blockIdx.x * 64 + threadIdx.x;
   if (r >= ja.total_tokens) return;
   const int head = blockIdx.y, H = ja.num_heads, N = ja.max_seq_len;
@@ -87,6 +90,8 @@ __global__ __launch_bounds__(64) void bwd_dq_f32_kernel(JaggedArgs ja, Tensors t
   }
   for (int c = 0; c < DV; c++) g[c] = dog[c];
   const int64_t ti = ja.timestamps[r];
+  int run_b = -1;
+  double run = 0.0;
   for (int j = 0; j <= i; j++) {
     if (!pair_valid(i, j, w.n_h)) continue;
     const float* kj = (const float*)t.k + (w.o + j) * t.k_stride + head * DQK;
@@ -100,9 +105,16 @@ __global__ __launch_bounds__(64) void bwd_dq_f32_kernel(JaggedArgs ja, Tensors t
     const float ds = dp * (sg + s * sg * (1.0f - sg));
     for (int c = 0; c < DQK; c++) acc[c] += ds * kj[c];
     const int kpos = bias_pos(i, w.n_h) - bias_pos(j, w.n_h);
-    unsafeAtomicAdd(&d_rab_pos[(N - 1) - kpos], ds * invN);
-    unsafeAtomicAdd(&d_rab_time[time_bucket64(ti - tj, ja.num_buckets)], ds * invN);
+    unsafeAtomicAdd(&rab_pos_acc[(N - 1) - kpos], (double)ds);
+    const int b = time_bucket64(ti - tj, ja.num_buckets);
+    if (b != run_b) {
+      if (run_b >= 0) unsafeAtomicAdd(&rab_time_acc[run_b], run);
+      run_b = b;
+      run = 0.0;
+    }
+    run += (double)ds;
   }
+  if (run_b >= 0) unsafeAtomicAdd(&rab_time_acc[run_b], run);
   float* out = dq + (r * H + head) * DQK;
   for (int c = 0; c < DQK; c++) out[c] = acc[c] * invN;
 }
@@ -156,9 +168,15 @@ hipError_t fwd_case(const JaggedArgs& ja, const Tensors& t, void* out, hipStream
   return hipGetLastError();
 }
 
+__global__ __launch_bounds__(256) void f64_to_f32_kernel(const double* in, float* out, int64_t n,
+                                                        double scale) {
+  for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < n; i += (int64_t)gridDim.x * 256)
+    out[i] = (float)(in[i] * scale);
+}
+
 template <int DQK, int DV>
 hipError_t bwd_case(const JaggedArgs& ja, const Tensors& t, const void* d_out, void* dq, void* dk,
-                    void* dv, float* drp, float* drt, hipStream_t s) {
+                    void* dv, double* drp, double* drt, hipStream_t s) {
   dim3 grid((unsigned)((ja.total_tokens + 63) / 64), (unsigned)ja.num_heads);
   hipLaunchKernelGGL((bwd_dq_f32_kernel<DQK, DV>), grid, dim3(64), 0, s, ja, t,
                      (const float*)d_out, (float*)dq, drp, drt);
@@ -191,11 +209,20 @@ hipError_t launch_attn_fwd_f32(const JaggedArgs& ja, const Tensors& t, int dqk, 
   return hipErrorInvalidValue;
 }
 
+hipError_t launch_f64_to_f32_scaled(const double* in, float* out, int64_t n, double scale,
+                                    hipStream_t s) {
+  if (n <= 0) return hipSuccess;
+  const int64_t blocks = (n + 255) / 256;
+  hipLaunchKernelGGL(f64_to_f32_kernel, dim3((unsigned)(blocks < 1024 ? blocks : 1024)), dim3(256),
+                     0, s, in, out, n, scale);
+  return hipGetLastError();
+}
+
 hipError_t launch_attn_bwd_f32(const JaggedArgs& ja, const Tensors& t, int dqk, int dv,
                                const void* d_out, void* dq, void* dk, void* dv_out,
-                               float* d_rab_pos, float* d_rab_time, hipStream_t s) {
+                               double* rab_pos_acc, double* rab_time_acc, hipStream_t s) {
   if (ja.total_tokens <= 0) return hipSuccess;
-#define CALL(A, B) return bwd_case<A, B>(ja, t, d_out, dq, dk, dv_out, d_rab_pos, d_rab_time, s);
+#define CALL(A, B) return bwd_case<A, B>(ja, t, d_out, dq, dk, dv_out, rab_pos_acc, rab_time_acc, s);
   HSTU_F32_DISPATCH(CALL)
 #undef CALL
   return hipErrorInvalidValue;

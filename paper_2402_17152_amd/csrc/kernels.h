@@ -136,9 +136,14 @@ hipError_t launch_dq_convert_bf16(const float* acc, void* dq, int64_t T, int32_t
 // fp32 SIMT attention.
 hipError_t launch_attn_fwd_f32(const JaggedArgs& ja, const Tensors& t, int dqk, int dv, void* out,
                                hipStream_t s);
+// The bias gradients are added, unscaled (sums of dS), to fp64
+// accumulators that the caller zeroes and converts.
 hipError_t launch_attn_bwd_f32(const JaggedArgs& ja, const Tensors& t, int dqk, int dv,
                                const void* d_out, void* dq, void* dk, void* dv_out,
-                               float* d_rab_pos, float* d_rab_time, hipStream_t s);
+                               double* rab_pos_acc, double* rab_time_acc, hipStream_t s);
+// out[i] = (float)(in[i] * scale), i < n.
+hipError_t launch_f64_to_f32_scaled(const double* in, float* out, int64_t n, double scale,
+                                    hipStream_t s);
 
 // Matrix-core rate probe (benchmark support): `waves_per_simd` waves per
 // SIMD on every CU, each issuing iters x 8 independent bf16 32x32x16 MFMAs.

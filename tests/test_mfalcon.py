@@ -10,10 +10,11 @@ cached prefix K and V.  Checks:
 * against the oracle's own Algorithm 1 (same b_m), tau = 2e-2 RMS (bf16);
 * a candidate's cached output does not depend on the other candidates of
   its call: every partition of the candidates gives the same bits;
-* the cached pass agrees with the uncached target-aware forward over
-  prefix ++ all m candidates (the target workload: 16 users, 2048 prefix
-  tokens, 1024 candidates, h = 4, d = 128, N = 3072) for every b_m tried,
-  at the same tolerance, and with the oracle on sampled users."""
+* the cached pass on the target workload (16 users, 2048 prefix tokens,
+  1024 candidates, h = 4, d = 128, N = 3072) agrees with the oracle on
+  every candidate for every b_m tried;
+* the microbatch loop captured as a HIP graph gives, on every replay, the
+  bits of the calls made one by one."""
 import numpy as np
 import pytest
 import torch
@@ -159,3 +160,53 @@ def test_mfalcon_target_workload(hs, oracle_mod):
     print(f"\n  cached: err {e[0]:.3e} raw {e[1]:.3e}")
     e = gu.assert_close("algorithm 1 vs oracle", alg1, ref, 2e-2, "bf16")
     print(f"  algorithm 1: err {e[0]:.3e} raw {e[1]:.3e}")
+
+
+def test_mfalcon_graph_replay(hs):
+    """Sixteen cached passes of 64 candidates per user (target workload)
+    captured once as a graph and replayed three times, with eager library
+    and torch work and a synchronisation between replays: every replay
+    writes exactly the outputs of the passes called one by one."""
+    batch = inputs.make_batch("target")
+    d = gu.dev_inputs(batch)
+    offs, nt = batch.seq_offsets, batch.num_targets
+    B, N = len(nt), batch.spec.max_seq_len
+    nh = np.diff(offs) - nt
+    pre = _idx(_cat([np.arange(offs[b], offs[b] + nh[b]) for b in range(B)]))
+    kc, vc, cts = d["k"].index_select(0, pre), d["v"].index_select(0, pre), \
+        d["timestamps"].index_select(0, pre)
+    coffs = _idx(np.concatenate([[0], np.cumsum(nh)]))
+    b_m = 64
+    passes = []
+    for i in range(int(nt.max()) // b_m):
+        r = _idx(_cat([np.arange(offs[b] + nh[b] + i * b_m, offs[b] + nh[b] + (i + 1) * b_m)
+                       for b in range(B)]))
+        q, k, v = (d[x].index_select(0, r) for x in ("q", "k", "v"))
+        co = _idx(np.arange(B + 1) * b_m)
+        p = hs.problem_for(q, v, co, N, d["rab_time"])
+        passes.append((q, k, v, co, d["timestamps"].index_select(0, r), torch.empty_like(v),
+                       hs.cached_workspace(p)))
+
+    def run(stream=None):
+        for (q, k, v, co, ts, o, ws) in passes:
+            hs.hstu_attn_fwd_cached(q, k, v, co, ts, kc, vc, coffs, cts, d["rab_pos"],
+                                    d["rab_time"], N, out=o, ws=ws, stream=stream)
+
+    run()
+    torch.cuda.synchronize()
+    ref = [o.clone() for (*_, o, _) in passes]
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        run(stream=torch.cuda.current_stream())
+    q0, k0, v0, co0, ts0, _, ws0 = passes[0]
+    scratch = torch.empty_like(passes[0][5])
+    for rep in range(3):
+        for (*_, o, _) in passes:
+            o.fill_(float("nan"))
+        hs.hstu_attn_fwd_cached(q0, k0, v0, co0, ts0, kc, vc, coffs, cts, d["rab_pos"],
+                                d["rab_time"], N, out=scratch, ws=ws0)
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        for i, ((*_, o, _), r) in enumerate(zip(passes, ref)):
+            assert torch.equal(o.view(torch.int16), r.view(torch.int16)), (rep, i)
