@@ -58,10 +58,11 @@
  *   Determinism  hstu_attn_fwd, hstu_layer_fwd, hstu_time_bucketize and
  *            hstu_complete_cumsum are bitwise deterministic, and so are
  *            dQ, dK and dV of hstu_attn_bwd for HSTU_BF16 (dQ is summed
- *            from per-key-block partials in a fixed order).  The bias
- *            gradients, and in hstu_layer_bwd also dQ and the layer-norm
- *            parameter gradients, are accumulated with atomics, so their
- *            last bits may vary between runs.
+ *            from per-key-block partials in a fixed order), and of
+ *            hstu_layer_bwd for HSTU_BF16 with d_qk, d_v <= 64.  The bias
+ *            gradients, the layer-norm parameter gradients, and dQ of
+ *            hstu_layer_bwd at d_qk or d_v = 128 are accumulated with
+ *            atomics, so their last bits may vary between runs.
  */
 #ifndef HSTU_H_
 #define HSTU_H_
@@ -113,8 +114,9 @@ typedef struct {
  * every call below for the same shape; it may be reused between calls
  * on one stream but not by calls that overlap.  For HSTU_BF16 it holds
  * the backward's partial dQ blocks: about (N T / 8192 + T / 20) h d_qk
- * 64 bytes at most (bounded from T, B and N alone; 1.6 GB for T = 48118,
- * N = 8192, h = 4, d_qk = 128). */
+ * 64 bytes at most (bounded from T, B and N alone), after the layer
+ * backward's dO terms (4 T h d_v bytes): 1.7 GB for T = 48118, N = 8192,
+ * h = 4, d_qk = d_v = 128. */
 size_t hstu_workspace_bytes(const hstu_problem_t* p);
 
 /* Eq. 2 forward: out[t][a][:] = (1/N) sum_{j kept} SiLU(q.k + rab) v_j.

@@ -143,11 +143,11 @@ struct Layout {
   size_t bwd_items;
   size_t trange;    // int64 [2B]: per-sequence timestamp min / max
   size_t bases;     // int64 [2 (B + 1)]: slot tables of the partial dQ blocks
-  size_t dq_acc;    // fp32 [h][T][d_qk] (bf16 problems; hstu_layer_bwd)
   size_t dout;      // [T][h*d_v] fp32, or bf16 high then low terms: dO of hstu_layer_bwd
-  size_t dq_part;   // f16 partial dQ blocks of hstu_attn_bwd (bf16 problems), then their
-  size_t dq_scale;  // fp32 block scales; both share the space of dq_acc and dout, which
-                    // that call does not use
+  size_t dq_acc;    // fp32 [h][T][d_qk]: dQ of the single-role kernel (bf16 problems)
+  size_t dq_part;   // f16 partial dQ blocks of the two-role kernel (bf16 problems), then
+  size_t dq_scale;  // their fp32 block scales; both share the space of dq_acc, which a
+                    // call using them does not use
   size_t rab64;     // fp64 [2N-1 + B_t]: bias-gradient sums of the fp32 backward
   size_t total;
   int64_t max_fwd, max_bwd;
@@ -168,12 +168,12 @@ Layout layout(const hstu_problem_t* p) {
   off = align_up(off + 2 * sizeof(int64_t) * (size_t)p->num_seqs);
   l.bases = off;
   off = align_up(off + 2 * sizeof(int64_t) * ((size_t)p->num_seqs + 1));
+  l.dout = off;
+  off = align_up(off + 4 * (size_t)p->total_tokens * p->num_heads * p->d_v);
   const size_t shared = off;
   l.dq_acc = off;
   if (p->dtype == HSTU_BF16)
     off = align_up(off + sizeof(float) * (size_t)p->total_tokens * p->num_heads * p->d_qk);
-  l.dout = off;
-  off = align_up(off + 4 * (size_t)p->total_tokens * p->num_heads * p->d_v);
   l.dq_part = shared;
   l.dq_scale = shared;
   if (p->dtype == HSTU_BF16) {
@@ -926,16 +926,16 @@ hstu_status_t attn_bwd_impl(const hstu_problem_t* p, const hstu_jagged_t* j, con
   const int64_t ndq = T * H * p->d_qk;
   ja.seq_trange = (const int64_t*)(w + l.trange);
   // Both bias-gradient tables start at zero, and so does the fp32 dQ
-  // accumulator of the single-role (two-term dO) kernel; the two-role
-  // kernel needs the slot tables of its partial dQ blocks instead.
-  const bool split = d_out_lo != nullptr;
+  // accumulator of the single-role kernel (two-term dO at d > 64); the
+  // two-role kernel needs the slot tables of its partial dQ blocks instead.
+  const bool single = d_out_lo != nullptr && !bwd_split_two_role(p->d_qk, p->d_v);
   const PrepFills fills =
-      split ? PrepFills{{dq_acc, d_rab_pos, d_rab_time},
-                        {ndq, 2 * (int64_t)N - 1, (int64_t)p->num_time_buckets}, 3}
-            : PrepFills{{d_rab_pos, d_rab_time, nullptr},
-                        {2 * (int64_t)N - 1, (int64_t)p->num_time_buckets, 0}, 2};
+      single ? PrepFills{{dq_acc, d_rab_pos, d_rab_time},
+                         {ndq, 2 * (int64_t)N - 1, (int64_t)p->num_time_buckets}, 3}
+             : PrepFills{{d_rab_pos, d_rab_time, nullptr},
+                         {2 * (int64_t)N - 1, (int64_t)p->num_time_buckets, 0}, 2};
   HSTU_HIP(launch_prep(ja, 1, items, counts + 1, (int64_t*)(w + l.trange), fills,
-                       split ? nullptr : bases, s),
+                       single ? nullptr : bases, s),
            "prep launch");
   {
     TimedScope ts("attn_bwd", s);
@@ -944,7 +944,7 @@ hstu_status_t attn_bwd_impl(const hstu_problem_t* p, const hstu_jagged_t* j, con
                                   items, counts + 1, l.max_bwd, s),
              "attn_bwd launch");
   }
-  if (split)
+  if (single)
     HSTU_HIP(launch_dq_convert_bf16(dq_acc, dq, T, H, p->d_qk, 1.0f / (float)N, s),
              "dq convert launch");
   else {

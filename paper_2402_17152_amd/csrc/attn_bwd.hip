@@ -846,12 +846,18 @@ __device__ __forceinline__ void bwd_item(BwdShared<DQK, DV, SPLIT>& sm, const Bw
 // step orders the hand-over: A writes P and dS of step u into slot u & 1;
 // B reads them, and the Q / dO tile of step u, after the next barrier.  B
 // lags one step, so the Q / dO ring has five slots (DMA three ahead).
-template <int DQK, int DV>
+template <int DQK, int DV, bool SPLIT = false>
 struct BwdSharedRS {
   using QT = StepTile<DQK>;
   using OT = StepTile<DV>;
   static constexpr int BN = kBwdBN, BM = kBwdBM;
-  static constexpr int kSlots = 5;
+  // Q / dO ring: at step u role A reads the tiles of step u + 1 and role B
+  // those of u - 1 (and u at the next step), and LDS DMA fills kAhead steps
+  // ahead, so kAhead + 2 slots.  SPLIT also stages the low dO terms and, to
+  // fit LDS, fills two steps ahead instead of three.
+  static constexpr int kAhead = SPLIT ? 2 : 3;
+  static constexpr int kSlots = kAhead + 2;
+  static constexpr int NLO = SPLIT ? kSlots : 1, LOB = SPLIT ? OT::BYTES : 16;
   static constexpr int DST_LD = 48;   // dS^T [128 keys][32 rows] bf16 (as above)
   static constexpr int KB_LD = DQK + 16;
   static constexpr int kWinPad = 4, WIN_LD = 264;
@@ -859,6 +865,7 @@ struct BwdSharedRS {
     struct {
       __align__(16) uint8_t q[kSlots][QT::BYTES];
       __align__(16) uint8_t dO[kSlots][OT::BYTES];
+      __align__(16) uint8_t dOl[NLO][LOB];  // low terms of dO (SPLIT)
     } t;
     __align__(16) uint16_t kblk[BN * KB_LD];  // prologue only
   };
@@ -874,6 +881,9 @@ struct BwdSharedRS {
   float sTacc[64];
   static constexpr int kRing = 256;
   float sRing[4][2][kRing];
+  // SPLIT: the low bf16 terms of dS^T and P, laid out as sdST and sPA.
+  __align__(16) uint16_t sdSTl[SPLIT ? 2 : 1][SPLIT ? BN * DST_LD : 8];
+  __align__(16) u32x4 sPAl[SPLIT ? 2 : 1][4][2][SPLIT ? 64 : 1];
 };
 
 // Everything both roles compute from the item (no per-role state).
@@ -882,13 +892,14 @@ struct RsItem {
   int seq, L, n_h, j0, head, nsteps;
 };
 
-template <int DQK, int DV, bool FAST>
-__device__ __forceinline__ void bwd_role_a(BwdSharedRS<DQK, DV>& sm, const BwdArgs& A,
+template <int DQK, int DV, bool FAST, bool SPLIT>
+__device__ __forceinline__ void bwd_role_a(BwdSharedRS<DQK, DV, SPLIT>& sm, const BwdArgs& A,
                                            const RsItem& it, int64_t tbase) {
-  using Sh = BwdSharedRS<DQK, DV>;
+  using Sh = BwdSharedRS<DQK, DV, SPLIT>;
   using QT = typename Sh::QT;
   using OT = typename Sh::OT;
   constexpr int BN = Sh::BN, BM = Sh::BM, DST_LD = Sh::DST_LD, kSlots = Sh::kSlots;
+  constexpr int kAhead = Sh::kAhead;
   const JaggedArgs& ja = A.ja;
   const int H = ja.num_heads, N = ja.max_seq_len;
   const int64_t o = it.o;
@@ -905,6 +916,7 @@ __device__ __forceinline__ void bwd_role_a(BwdSharedRS<DQK, DV>& sm, const BwdAr
   const uint16_t* __restrict__ vg = (const uint16_t*)A.t.v + o * A.t.v_stride + head * DV;
   const uint16_t* __restrict__ qg = (const uint16_t*)A.t.q + o * A.t.q_stride + head * DQK;
   const uint16_t* __restrict__ dog = A.dO + (o * H + head) * DV;
+  const uint16_t* __restrict__ dogl = SPLIT ? A.dO_lo + (o * H + head) * DV : dog;
   const uint32_t kstride_b = (uint32_t)A.t.k_stride * 2u, vstride_b = (uint32_t)A.t.v_stride * 2u;
   const uint32_t qstride_b = (uint32_t)A.t.q_stride * 2u, dostride_b = (uint32_t)(H * DV) * 2u;
   const float invN = 1.0f / (float)N;
@@ -947,15 +959,19 @@ __device__ __forceinline__ void bwd_role_a(BwdSharedRS<DQK, DV>& sm, const BwdAr
   a_base(QT{}, qa);
   a_base(OT{}, oa);
 
-  // ---- staging by LDS DMA: Q, dO and the rab_pos window three steps
-  // ahead, row timestamps five.  Only role A issues DMA.  Step u needs the
-  // tiles and window of step u + 1 and (for reduce_ts(u + 3)) the row
-  // timestamps of step u + 3, all issued at step u - 2, the timestamps
-  // last; only step u - 1's operations follow them, so the wait at step
-  // u allows OPS_PER_STEP outstanding (later atomics only make it stricter).
-  constexpr int OPS_PER_STEP = QT::OPW + OT::OPW + 3 + 1;
+  // ---- staging by LDS DMA: Q and dO kAhead steps ahead (three, or two
+  // with SPLIT's low dO terms), the rab_pos window three steps ahead, row
+  // timestamps five.  Only role A issues DMA, in the order tiles, window,
+  // timestamps.  Step u needs the tiles and window of step u + 1 and (for
+  // reduce_ts(u + 3)) the row timestamps of step u + 3.  With kAhead = 3
+  // all were issued at step u - 2 and only step u - 1's operations follow
+  // them; with kAhead = 2 the tiles were the first operations of step
+  // u - 1, followed by its window and timestamps.  The wait at step u
+  // allows that many outstanding (later atomics only make it stricter).
+  constexpr int OPS_PER_STEP = kAhead == 3 ? QT::OPW + OT::OPW + 3 + 1 : 3 + 1;
   const u32x4 qrs = rsrc_words(qg, (uint32_t)(L * A.t.q_stride * 2));
   const u32x4 ors = rsrc_words(dog, (uint32_t)L * dostride_b);
+  const u32x4 orsl = rsrc_words(dogl, (uint32_t)L * dostride_b);
   const u32x4 trs = rsrc_words(ts, (uint32_t)L * 8u);
   const u32x4 prs = rsrc_words(ja.rab_pos, (uint32_t)(2 * N - 1) * 4u);
   uint32_t qoffs[QT::OPW], ooffs[OT::OPW];
@@ -981,6 +997,12 @@ __device__ __forceinline__ void bwd_role_a(BwdSharedRS<DQK, DV>& sm, const BwdAr
     for (int k = 0; k < OT::OPW; k++)
       dma_to_lds16_asm(ors, sm.ring.t.dO[slot] + 1024 * min(wave * OT::OPW + k, OT::OPS - 1),
                        ooffs[k] + (uint32_t)i0 * dostride_b);
+    if constexpr (SPLIT) {
+#pragma unroll
+      for (int k = 0; k < OT::OPW; k++)
+        dma_to_lds16_asm(orsl, sm.ring.t.dOl[slot] + 1024 * min(wave * OT::OPW + k, OT::OPS - 1),
+                         ooffs[k] + (uint32_t)i0 * dostride_b);
+    }
   };
   const int Pk = min(j0 + BN - 1, n_h);
   auto issue_win = [&](int u) {
@@ -1145,18 +1167,34 @@ __device__ __forceinline__ void bwd_role_a(BwdSharedRS<DQK, DV>& sm, const BwdAr
       if (s < DV / 16) {
         const u32x4 a = *reinterpret_cast<const u32x4*>(ob + a_off(OT{}, oa, s));
         pacc = mfma32x32x16(as_bf16x8(a), as_bf16x8(vf[s]), pacc);
+        if constexpr (SPLIT) {
+          const u32x4 al =
+              *reinterpret_cast<const u32x4*>(sm.ring.t.dOl[u % kSlots] + a_off(OT{}, oa, s));
+          pacc = mfma32x32x16(as_bf16x8(al), as_bf16x8(vf[s]), pacc);
+        }
       }
     }
   };
   // Hand-over to role B: dS^T in the dQ layout (role B reads its dK
-  // operand from it too) and P as this lane's operand registers.
-  auto store_step = [&](int u, const u32x4 (&pa)[2], const u32x4 (&da)[2]) {
+  // operand from it too) and P as this lane's operand registers; with
+  // SPLIT also their low terms (pl, dl), laid out the same way.
+  auto store_step = [&](int u, const u32x4 (&pa)[2], const u32x4 (&da)[2], const u32x4 (&pl)[2],
+                        const u32x4 (&dl)[2]) {
     uint16_t* dp = sm.sdST[u & 1] + (32 * wave + col) * DST_LD + 4 * half;
 #pragma unroll
     for (int st = 0; st < 2; st++) {
       *reinterpret_cast<uint2*>(dp + 16 * st) = uint2{da[st][0], da[st][1]};
       *reinterpret_cast<uint2*>(dp + 16 * st + 8) = uint2{da[st][2], da[st][3]};
       sm.sPA[u & 1][wave][st][lane] = pa[st];
+    }
+    if constexpr (SPLIT) {
+      uint16_t* dpl = sm.sdSTl[u & 1] + (32 * wave + col) * DST_LD + 4 * half;
+#pragma unroll
+      for (int st = 0; st < 2; st++) {
+        *reinterpret_cast<uint2*>(dpl + 16 * st) = uint2{dl[st][0], dl[st][1]};
+        *reinterpret_cast<uint2*>(dpl + 16 * st + 8) = uint2{dl[st][2], dl[st][3]};
+        sm.sPAl[u & 1][wave][st][lane] = pl[st];
+      }
     }
   };
 
@@ -1275,7 +1313,7 @@ __device__ __forceinline__ void bwd_role_a(BwdSharedRS<DQK, DV>& sm, const BwdAr
     wait_vmcnt_lgkmcnt0<OPS_PER_STEP>();
     barrier_no_fence();
     if (u >= 5 && wave == (u & 3)) ring_flush(u - 5);
-    issue_tiles(u + 3);
+    issue_tiles(u + kAhead);
     issue_win(u + 3);
     issue_ts(u + 5);
     if (u + 1 < nsteps) seed(u + 1, path_next, s_next);
@@ -1289,15 +1327,26 @@ __device__ __forceinline__ void bwd_role_a(BwdSharedRS<DQK, DV>& sm, const BwdAr
       pv[q] = p;
       dsv[q] = p_cur[q] * __builtin_fmaf(p, 1.0f - sg, sg);
     }
-    u32x4 pa[2], da[2];
+    u32x4 pa[2], da[2], pl[2], dl[2];
 #pragma unroll
     for (int st = 0; st < 2; st++) {
       pa[st] = u32x4{pack_bf16x2(pv[8 * st], pv[8 * st + 1]), pack_bf16x2(pv[8 * st + 2], pv[8 * st + 3]),
                      pack_bf16x2(pv[8 * st + 4], pv[8 * st + 5]), pack_bf16x2(pv[8 * st + 6], pv[8 * st + 7])};
       da[st] = u32x4{pack_bf16x2(dsv[8 * st], dsv[8 * st + 1]), pack_bf16x2(dsv[8 * st + 2], dsv[8 * st + 3]),
                      pack_bf16x2(dsv[8 * st + 4], dsv[8 * st + 5]), pack_bf16x2(dsv[8 * st + 6], dsv[8 * st + 7])};
+      if constexpr (SPLIT) {
+        // low terms: value - bf16(value), exact in fp32
+#pragma unroll
+        for (int e = 0; e < 4; e++) {
+          const uint32_t h = pa[st][e], g = da[st][e];
+          pl[st][e] = pack_bf16x2(pv[8 * st + 2 * e] - __uint_as_float(h << 16),
+                                  pv[8 * st + 2 * e + 1] - __uint_as_float(h & 0xffff0000u));
+          dl[st][e] = pack_bf16x2(dsv[8 * st + 2 * e] - __uint_as_float(g << 16),
+                                  dsv[8 * st + 2 * e + 1] - __uint_as_float(g & 0xffff0000u));
+        }
+      }
     }
-    store_step(u, pa, da);
+    store_step(u, pa, da, pl, dl);
     grads(u, path_cur, dsv);
     path_nn = classify(u + 2);
     reduce_ts(u + 3);
@@ -1308,7 +1357,7 @@ __device__ __forceinline__ void bwd_role_a(BwdSharedRS<DQK, DV>& sm, const BwdAr
   // Prologue: timestamps of steps 0..4, tiles and windows 0..2.
   for (int v = 0; v < 5; v++) issue_ts(v);
   for (int v = 0; v < 3; v++) {
-    issue_tiles(v);
+    if (v < kAhead) issue_tiles(v);
     issue_win(v);
   }
   wait_vmcnt_lgkmcnt0<0>();
@@ -1341,10 +1390,10 @@ __device__ __forceinline__ void bwd_role_a(BwdSharedRS<DQK, DV>& sm, const BwdAr
   }
 }
 
-template <int DQK, int DV>
-__device__ __forceinline__ void bwd_role_b(BwdSharedRS<DQK, DV>& sm, const BwdArgs& A,
+template <int DQK, int DV, bool SPLIT>
+__device__ __forceinline__ void bwd_role_b(BwdSharedRS<DQK, DV, SPLIT>& sm, const BwdArgs& A,
                                            const RsItem& it, const u32x4* kq) {
-  using Sh = BwdSharedRS<DQK, DV>;
+  using Sh = BwdSharedRS<DQK, DV, SPLIT>;
   using QT = typename Sh::QT;
   using OT = typename Sh::OT;
   constexpr int BN = Sh::BN, BM = Sh::BM, DST_LD = Sh::DST_LD, kSlots = Sh::kSlots;
@@ -1396,17 +1445,26 @@ __device__ __forceinline__ void bwd_role_b(BwdSharedRS<DQK, DV>& sm, const BwdAr
 
   // dV += P^T dO, dK += dS^T Q of step u: P as role A's operand registers,
   // dS read back from the dS^T tile in the same (accumulator-row) order.
+  // SPLIT: dV += P_hi^T dO_hi + P_lo^T dO_hi + P_hi^T dO_lo and
+  // dK += dS_hi^T Q + dS_lo^T Q.
   auto key_grads = [&](int u) {
     const uint8_t* qb = sm.ring.t.q[u % kSlots];
     const uint8_t* ob = sm.ring.t.dO[u % kSlots];
     const uint16_t* dp = sm.sdST[u & 1] + (32 * wave + col) * DST_LD + 4 * half;
-    u32x4 pa[2], da[2];
+    u32x4 pa[2], da[2], pl[2], dl[2];
 #pragma unroll
     for (int st = 0; st < 2; st++) {
       pa[st] = sm.sPA[u & 1][wave][st][lane];
       const uint2 lo = *reinterpret_cast<const uint2*>(dp + 16 * st);
       const uint2 hi = *reinterpret_cast<const uint2*>(dp + 16 * st + 8);
       da[st] = u32x4{lo.x, lo.y, hi.x, hi.y};
+      if constexpr (SPLIT) {
+        const uint16_t* dpl = sm.sdSTl[u & 1] + (32 * wave + col) * DST_LD + 4 * half;
+        pl[st] = sm.sPAl[u & 1][wave][st][lane];
+        const uint2 l2 = *reinterpret_cast<const uint2*>(dpl + 16 * st);
+        const uint2 h2 = *reinterpret_cast<const uint2*>(dpl + 16 * st + 8);
+        dl[st] = u32x4{l2.x, l2.y, h2.x, h2.y};
+      }
     }
 #pragma unroll
     for (int st = 0; st < 2; st++) {
@@ -1415,12 +1473,21 @@ __device__ __forceinline__ void bwd_role_b(BwdSharedRS<DQK, DV>& sm, const BwdAr
         const uint2 lo = lds_read_tr16((const uint16_t*)(ob + tr_off(OT{}, ot, st, 0, nb)));
         const uint2 hi = lds_read_tr16((const uint16_t*)(ob + tr_off(OT{}, ot, st, 1, nb)));
         dvacc[nb] = mfma32x32x16(as_bf16x8(pa[st]), as_bf16x8(u32x4{lo.x, lo.y, hi.x, hi.y}), dvacc[nb]);
+        if constexpr (SPLIT) {
+          dvacc[nb] = mfma32x32x16(as_bf16x8(pl[st]), as_bf16x8(u32x4{lo.x, lo.y, hi.x, hi.y}), dvacc[nb]);
+          const uint8_t* obl = sm.ring.t.dOl[u % kSlots];
+          const uint2 l2 = lds_read_tr16((const uint16_t*)(obl + tr_off(OT{}, ot, st, 0, nb)));
+          const uint2 h2 = lds_read_tr16((const uint16_t*)(obl + tr_off(OT{}, ot, st, 1, nb)));
+          dvacc[nb] = mfma32x32x16(as_bf16x8(pa[st]), as_bf16x8(u32x4{l2.x, l2.y, h2.x, h2.y}), dvacc[nb]);
+        }
       }
 #pragma unroll
       for (int nb = 0; nb < DQK / 32; nb++) {
         const uint2 lo = lds_read_tr16((const uint16_t*)(qb + tr_off(QT{}, qt, st, 0, nb)));
         const uint2 hi = lds_read_tr16((const uint16_t*)(qb + tr_off(QT{}, qt, st, 1, nb)));
         dkacc[nb] = mfma32x32x16(as_bf16x8(da[st]), as_bf16x8(u32x4{lo.x, lo.y, hi.x, hi.y}), dkacc[nb]);
+        if constexpr (SPLIT)
+          dkacc[nb] = mfma32x32x16(as_bf16x8(dl[st]), as_bf16x8(u32x4{lo.x, lo.y, hi.x, hi.y}), dkacc[nb]);
       }
     }
   };
@@ -1496,10 +1563,10 @@ __device__ __forceinline__ void bwd_role_b(BwdSharedRS<DQK, DV>& sm, const BwdAr
 
 constexpr int kRsThreads = 512;
 
-template <int DQK, int DV>
+template <int DQK, int DV, bool SPLIT>
 __global__ __launch_bounds__(kRsThreads, 1) void attn_bwd_rs_kernel(
     BwdArgs A, const WorkItem* __restrict__ items, const int32_t* __restrict__ count) {
-  using S = BwdSharedRS<DQK, DV>;
+  using S = BwdSharedRS<DQK, DV, SPLIT>;
   constexpr int BN = S::BN, KB_LD = S::KB_LD;
   __shared__ S sm;
   const JaggedArgs& ja = A.ja;
@@ -1559,11 +1626,11 @@ __global__ __launch_bounds__(kRsThreads, 1) void attn_bwd_rs_kernel(
 
   if (wave < 4) {
     if (fast)
-      bwd_role_a<DQK, DV, true>(sm, A, it, tlo);
+      bwd_role_a<DQK, DV, true, SPLIT>(sm, A, it, tlo);
     else
-      bwd_role_a<DQK, DV, false>(sm, A, it, tlo);
+      bwd_role_a<DQK, DV, false, SPLIT>(sm, A, it, tlo);
   } else {
-    bwd_role_b<DQK, DV>(sm, A, it, kq);
+    bwd_role_b<DQK, DV, SPLIT>(sm, A, it, kq);
   }
 
   __syncthreads();
@@ -1738,12 +1805,19 @@ hipError_t launch_bwd(const JaggedArgs& ja, const Tensors& t, const void* d_out,
   static_assert(sizeof(BwdShared<DQK, DV, true>) <= kLdsBytes, "LDS budget");
   static_assert(sizeof(BwdSharedRS<DQK, DV>) <= kLdsBytes, "LDS budget");
   dim3 grid((unsigned)(max_items * ja.num_heads));
-  if (d_out_lo)
-    hipLaunchKernelGGL((attn_bwd_bf16_kernel<DQK, DV, true>), grid, dim3(kBwdThreads), 0, s, A,
+  if (d_out_lo) {
+    if constexpr (bwd_split_two_role(DQK, DV)) {
+      static_assert(sizeof(BwdSharedRS<DQK, DV, true>) <= kLdsBytes, "LDS budget");
+      hipLaunchKernelGGL((attn_bwd_rs_kernel<DQK, DV, true>), grid, dim3(kRsThreads), 0, s, A,
+                         items, count);
+    } else {
+      hipLaunchKernelGGL((attn_bwd_bf16_kernel<DQK, DV, true>), grid, dim3(kBwdThreads), 0, s, A,
+                         items, count);
+    }
+  } else {
+    hipLaunchKernelGGL((attn_bwd_rs_kernel<DQK, DV, false>), grid, dim3(kRsThreads), 0, s, A,
                        items, count);
-  else
-    hipLaunchKernelGGL((attn_bwd_rs_kernel<DQK, DV>), grid, dim3(kRsThreads), 0, s, A, items,
-                       count);
+  }
   return hipGetLastError();
 }
 

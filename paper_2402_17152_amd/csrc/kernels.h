@@ -102,12 +102,17 @@ hipError_t launch_attn_fwd_bf16(const JaggedArgs& ja, const Tensors& t, int dqk,
 // key_offsets, key_chunks, chunk_stride, num_seqs, max_seq_len, rab tables).
 hipError_t launch_cached_self(int is_bf16, const JaggedArgs& ja, int32_t dqk, int32_t dv,
                               const Tensors& t, const float* o32, void* out, hipStream_t s);
+// Whether the two-term (d_out_lo) backward of these head sizes runs the
+// two-role kernel (its LDS holds the low terms for d_qk, d_v <= 64) or
+// the single-role one.
+constexpr bool bwd_split_two_role(int dqk, int dv) { return dqk <= 64 && dv <= 64; }
+
 // d_out_lo: null, or the low bf16 terms of dO (d_out holding the high
 // ones), for a dO that is the fp32 output of the layer's LayerNorm backward.
-// With d_out_lo null the two-role kernel runs and stores dQ as scaled f16
-// partial blocks in dq_part / dq_scale (slots from `bases`;
-// launch_dq_reduce_bf16 sums them); otherwise the single-role kernel adds dQ to the zeroed fp32
-// dq_acc [h][T][d_qk] with atomics (launch_dq_convert_bf16 then).
+// The two-role kernel (d_out_lo null, or bwd_split_two_role) stores dQ as
+// scaled f16 partial blocks in dq_part / dq_scale (slots from `bases`;
+// launch_dq_reduce_bf16 sums them); the single-role kernel adds dQ to the
+// zeroed fp32 dq_acc [h][T][d_qk] with atomics (launch_dq_convert_bf16 then).
 hipError_t launch_attn_bwd_bf16(const JaggedArgs& ja, const Tensors& t, int dqk, int dv,
                                 const void* d_out, const void* d_out_lo, float* dq_acc,
                                 uint16_t* dq_part, float* dq_scale, int64_t dq_slots,
