@@ -46,6 +46,8 @@ def parse():
     ap.add_argument("--no-kernel-timing", action="store_true")
     ap.add_argument("--no-aux", action="store_true",
                     help="skip the MFMA probe, bucketize and clock measurements")
+    ap.add_argument("--bucketize", action="store_true",
+                    help="only the standalone bucketize kernel on the workload's timestamps")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="only copy 256 MiB device-to-device 3 times (the reference that "
                          "scales rocprofv3 FETCH_SIZE / WRITE_SIZE to bytes), then exit")
@@ -70,6 +72,49 @@ def gpu_clock():
     return lines or None
 
 
+def bucketize_measurement(hstu, torch, d, batch, stream):
+    """The standalone bucketize kernel's write rate on the workload's
+    timestamps: warm (ten launches back to back between two events, per
+    launch) and cold (one launch after flushing the 256 MB last-level cache
+    by writing 512 MB), with the runtime's plain fill of the same buffer
+    (timed like warm) as a reachable write rate."""
+    out = {}
+    po = hstu.hstu_pair_offsets(d["seq_offsets"], stream=stream)
+    total_pairs = int(po[-1].item())
+    buckets = torch.empty(total_pairs, dtype=torch.uint8, device="cuda")
+    flush = torch.empty(512 << 20, dtype=torch.uint8, device="cuda")
+    nbytes = total_pairs + 8 * batch.total_tokens
+
+    def bucketize():
+        hstu.hstu_time_bucketize(d["seq_offsets"], d["timestamps"], d["rab_time"].numel(),
+                                 pair_offsets=po, total_pairs=total_pairs, out=buckets,
+                                 stream=stream)
+
+    def timed(fn, reps, before=None):
+        ts = []
+        for _ in range(6):
+            if before is not None:
+                before()
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record(stream)
+            for _ in range(reps):
+                fn()
+            e1.record(stream)
+            torch.cuda.synchronize()
+            ts.append(e0.elapsed_time(e1) / reps)
+        return percentile(ts[1:], 0.5)
+
+    for mode, ms in (("warm", timed(bucketize, 10)), ("cold", timed(bucketize, 1, flush.zero_))):
+        out[f"bucketize_{mode}"] = {"ms": ms, "gbs": nbytes / (ms * 1e-3) / 1e9,
+                                    "frac_hbm": nbytes / (ms * 1e-3) / 1e9 / PEAK_HBM_GBS,
+                                    "bytes": nbytes}
+    ms = timed(buckets.zero_, 10)
+    out["plain_fill_reference"] = {"ms": ms, "gbs": total_pairs / (ms * 1e-3) / 1e9,
+                                   "bytes": total_pairs}
+    del flush
+    return out
+
+
 def aux_measurements(hstu, torch, d, batch, stream):
     """Outside the timed region: the matrix-core rate of a kernel that only
     issues bf16 MFMAs (the measured ceiling the attention kernels are also
@@ -88,41 +133,7 @@ def aux_measurements(hstu, torch, d, batch, stream):
     out["mfma_probe"] = {"tflops": max(rates[1:]), "frac_of_spec": max(rates[1:]) / PEAK_BF16_TFLOPS,
                          "kernel": "bf16 v_mfma_f32_32x32x16, 8 independent chains per wave, "
                                    "2 waves per SIMD, every CU"}
-    po = hstu.hstu_pair_offsets(d["seq_offsets"], stream=stream)
-    total_pairs = int(po[-1].item())
-    buckets = torch.empty(total_pairs, dtype=torch.uint8, device="cuda")
-    flush = torch.empty(512 << 20, dtype=torch.uint8, device="cuda")
-    nbytes = total_pairs + 8 * batch.total_tokens
-    for mode in ("warm", "cold"):
-        ts = []
-        for _ in range(6):
-            if mode == "cold":
-                flush.zero_()
-            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-            e0.record(stream)
-            hstu.hstu_time_bucketize(d["seq_offsets"], d["timestamps"], d["rab_time"].numel(),
-                                     pair_offsets=po, total_pairs=total_pairs, out=buckets,
-                                     stream=stream)
-            e1.record(stream)
-            torch.cuda.synchronize()
-            ts.append(e0.elapsed_time(e1))
-        ms = percentile(ts[1:], 0.5)
-        out[f"bucketize_{mode}"] = {"ms": ms, "gbs": nbytes / (ms * 1e-3) / 1e9,
-                                    "frac_hbm": nbytes / (ms * 1e-3) / 1e9 / PEAK_HBM_GBS,
-                                    "bytes": nbytes}
-    # Write-rate reference on the same buffer: the runtime's plain fill.
-    ts = []
-    for _ in range(6):
-        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        e0.record(stream)
-        buckets.zero_()
-        e1.record(stream)
-        torch.cuda.synchronize()
-        ts.append(e0.elapsed_time(e1))
-    ms = percentile(ts[1:], 0.5)
-    out["plain_fill_reference"] = {"ms": ms, "gbs": total_pairs / (ms * 1e-3) / 1e9,
-                                   "bytes": total_pairs}
-    del flush
+    out.update(bucketize_measurement(hstu, torch, d, batch, stream))
     out["mfalcon"] = mfalcon_measurement(hstu, torch, stream)
     out["projections"] = projection_measurement(hstu, torch, stream)
     out["stochastic_length"] = sl_measurement(hstu, torch, stream)
@@ -434,6 +445,11 @@ def main():
     batch = inputs.make_batch(args.workload)
     spec = batch.spec
     d = inputs.to_device(batch)
+    if args.bucketize:
+        res = bucketize_measurement(hstu, torch, d, batch, torch.cuda.current_stream())
+        print(json.dumps({"workload": args.workload, "total_tokens": batch.total_tokens, **res}),
+              flush=True)
+        return
     T = batch.total_tokens
     N = spec.max_seq_len
     f_fwd, f_bwd = inputs.flops(batch)
