@@ -963,11 +963,12 @@ __device__ __forceinline__ void bwd_role_a(BwdSharedRS<DQK, DV, SPLIT>& sm, cons
   // with SPLIT's low dO terms), the rab_pos window three steps ahead, row
   // timestamps five.  Only role A issues DMA, in the order tiles, window,
   // timestamps.  Step u needs the tiles and window of step u + 1 and (for
-  // reduce_ts(u + 3)) the row timestamps of step u + 3.  With kAhead = 3
-  // all were issued at step u - 2 and only step u - 1's operations follow
-  // them; with kAhead = 2 the tiles were the first operations of step
-  // u - 1, followed by its window and timestamps.  The wait at step u
-  // allows that many outstanding (later atomics only make it stricter).
+  // role B's reduce_ts(u + 3), after the same barrier) the row timestamps
+  // of step u + 3.  With kAhead = 3 all were issued at step u - 2 and only
+  // step u - 1's operations follow them; with kAhead = 2 the tiles were
+  // the first operations of step u - 1, followed by its window and
+  // timestamps.  The wait at step u allows that many outstanding (later
+  // atomics only make it stricter).
   constexpr int OPS_PER_STEP = kAhead == 3 ? QT::OPW + OT::OPW + 3 + 1 : 3 + 1;
   const u32x4 qrs = rsrc_words(qg, (uint32_t)(L * A.t.q_stride * 2));
   const u32x4 ors = rsrc_words(dog, (uint32_t)L * dostride_b);
@@ -1016,16 +1017,6 @@ __device__ __forceinline__ void bwd_role_a(BwdSharedRS<DQK, DV, SPLIT>& sm, cons
   };
   auto issue_ts = [&](int u) {
     dma_to_lds4_asm(trs, sm.sT[u & 7], (uint32_t)row0(u) * 8u + 4u * (uint32_t)lane);
-  };
-  auto reduce_ts = [&](int u) {
-    if constexpr (FAST) {
-      if (wave == 0) {
-        const uint32_t v = sm.sT[u & 7][2 * (lane & 31)] - (uint32_t)tbase;
-        const uint32_t lo = wave_min_dpp(v), hi = wave_max_dpp(v);
-        sm.sTr[u & 7][lane & 31] = v;
-        if (lane < 2) sm.sRr[u & 3][lane] = lane ? hi : lo;
-      }
-    }
   };
 
   // ---- bias path of a (wave, step) tile (as in bwd_item) ----
@@ -1349,12 +1340,12 @@ __device__ __forceinline__ void bwd_role_a(BwdSharedRS<DQK, DV, SPLIT>& sm, cons
     store_step(u, pa, da, pl, dl);
     grads(u, path_cur, dsv);
     path_nn = classify(u + 2);
-    reduce_ts(u + 3);
     path_cur = path_next;
     path_next = path_nn;
   };
 
-  // Prologue: timestamps of steps 0..4, tiles and windows 0..2.
+  // Prologue: timestamps of steps 0..4, tiles and windows 0..2 (role B
+  // reduces the row timestamps of steps 0..2 between the two barriers).
   for (int v = 0; v < 5; v++) issue_ts(v);
   for (int v = 0; v < 3; v++) {
     if (v < kAhead) issue_tiles(v);
@@ -1362,8 +1353,6 @@ __device__ __forceinline__ void bwd_role_a(BwdSharedRS<DQK, DV, SPLIT>& sm, cons
   }
   wait_vmcnt_lgkmcnt0<0>();
   barrier_no_fence();  // (P1)
-  for (int v = 0; v < 3; v++) reduce_ts(v);
-  wait_vmcnt_lgkmcnt0<0>();
   barrier_no_fence();  // (P2)
   f32x16 sA, pA, sB, pB;
   path_cur = classify(0);
@@ -1392,7 +1381,8 @@ __device__ __forceinline__ void bwd_role_a(BwdSharedRS<DQK, DV, SPLIT>& sm, cons
 
 template <int DQK, int DV, bool SPLIT>
 __device__ __forceinline__ void bwd_role_b(BwdSharedRS<DQK, DV, SPLIT>& sm, const BwdArgs& A,
-                                           const RsItem& it, const u32x4* kq) {
+                                           const RsItem& it, const u32x4* kq, bool fast,
+                                           int64_t tbase) {
   using Sh = BwdSharedRS<DQK, DV, SPLIT>;
   using QT = typename Sh::QT;
   using OT = typename Sh::OT;
@@ -1528,13 +1518,27 @@ __device__ __forceinline__ void bwd_role_b(BwdSharedRS<DQK, DV, SPLIT>& sm, cons
     if (lane == 0) A.dq_scale[blk0 + (int64_t)u * blk_stride] = __uint_as_float((254u - se) << 23);
   };
 
+  // Fast path: the row timestamps of step u rebased to 32 bits, and their
+  // min / max, for role A's tile classification (one wave).  Role A's
+  // staging wait at step u covers the timestamps of step u + 3.
+  auto reduce_ts = [&](int u) {
+    if (fast && wave == 0) {
+      const uint32_t v = sm.sT[u & 7][2 * (lane & 31)] - (uint32_t)tbase;
+      const uint32_t lo = wave_min_dpp(v), hi = wave_max_dpp(v);
+      sm.sTr[u & 7][lane & 31] = v;
+      if (lane < 2) sm.sRr[u & 3][lane] = lane ? hi : lo;
+    }
+  };
   // The same barriers as role A: two in its prologue, one per step, then
   // one for the last hand-over and one before its final flushes.
   barrier_no_fence();  // (P1)
+  for (int v = 0; v < 3; v++) reduce_ts(v);
+  wait_vmcnt_lgkmcnt0<63>();
   barrier_no_fence();  // (P2)
   for (int u = 0; u < nsteps; u++) {
     wait_vmcnt_lgkmcnt0<63>();
     barrier_no_fence();
+    reduce_ts(u + 3);
     if (u >= 1) {
       key_grads(u - 1);
       if (wave < NCB) dq_step(u - 1);
@@ -1630,7 +1634,7 @@ __global__ __launch_bounds__(kRsThreads, 1) void attn_bwd_rs_kernel(
     else
       bwd_role_a<DQK, DV, false, SPLIT>(sm, A, it, tlo);
   } else {
-    bwd_role_b<DQK, DV, SPLIT>(sm, A, it, kq);
+    bwd_role_b<DQK, DV, SPLIT>(sm, A, it, kq, fast, tlo);
   }
 
   __syncthreads();
