@@ -858,7 +858,12 @@ struct BwdSharedRS {
   static constexpr int kAhead = SPLIT ? 2 : 3;
   static constexpr int kSlots = kAhead + 2;
   static constexpr int NLO = SPLIT ? kSlots : 1, LOB = SPLIT ? OT::BYTES : 16;
-  static constexpr int DST_LD = 48;   // dS^T [128 keys][32 rows] bf16 (as above)
+  // dS^T [128 keys][32 rows] bf16, pitch 72 bytes: role A's row-wise
+  // 8-byte stores and role B's row-wise dK-operand reads of 32 keys then
+  // spread over all banks (a 96-byte pitch put them on 8 of 32); the
+  // transposing reads of the dQ step take a few more conflicts than at
+  // 96 bytes (long workload: backward 1.412 -> 1.377 ms).
+  static constexpr int DST_LD = 36;
   static constexpr int KB_LD = DQK + 16;
   static constexpr int kWinPad = 4, WIN_LD = 264;
   union Ring {
