@@ -70,21 +70,29 @@ constexpr int kBwdWaves = kBwdThreads / 64;
 constexpr float kMaskedBias = -1.0e30f;
 
 // Step tile of 32 rows x D features (Q or dO), read two ways: 16-byte row
-// chunks (MFMA A operand, 8 lanes = rows 0..7 per LDS cycle) and 8-byte
-// transposing loads (B operand, 16 lanes = 4 rows x 2 chunks x 2 halves).
-// For D >= 64 the row is unpadded and chunk c of row r sits at chunk
-// c ^ swz(r), which spreads both patterns over all banks; for D = 32 rows
-// carry one pad chunk.
+// chunks (MFMA A operand, one row per lane) and 8-byte transposing loads
+// (B operand, 16 lanes = 4 rows x 2 chunks x 2 halves).  For D >= 64 the
+// row is unpadded and chunk c of row r sits at chunk c ^ swz(r); swz takes
+// 8 values, so 16 consecutive rows would meet each bank group twice: each
+// group of 8 rows therefore starts GSH bytes (half of 64 four-byte banks)
+// further on than the one before, and the 16 rows of an A-operand read
+// cover every bank once.  For D = 32 rows carry one pad chunk.
 template <int D>
 struct StepTile {
   static constexpr int CPR = D / 8;                  // data chunks per row
   static constexpr bool SWZ = D >= 64;
   static constexpr int PC = SWZ ? CPR : CPR + 1;     // chunks per row
   static constexpr int RB = PC * 16;                 // row bytes
+  static constexpr int GSH = SWZ ? 128 : 0;          // shift per group of 8 rows
   static constexpr int OPS = (32 * PC + 63) / 64;    // 1 KB DMA operations per tile
   static constexpr int OPW = (OPS + 3) / 4;          // per wave
-  static constexpr int BYTES = OPS * 1024;
+  static constexpr int BYTES = OPS * 1024 + 3 * GSH;
   __device__ static int swz(int r) { return SWZ ? 2 * (r & 3) + ((r >> 2) & 1) : 0; }
+  // Byte offset of row r, and of DMA operation o (1 KB: whole rows when
+  // SWZ, so that one operation never straddles a row group).
+  __device__ static constexpr int row_base(int r) { return r * RB + GSH * (r >> 3); }
+  __device__ static constexpr int op_base(int o) { return 1024 * o + GSH * ((o * (1024 / RB)) >> 3); }
+  static_assert(!SWZ || 1024 % RB == 0, "a DMA operation covers whole rows");
 };
 
 template <int DQK, int DV, bool SPLIT>
@@ -242,7 +250,7 @@ __device__ __forceinline__ void bwd_item(BwdShared<DQK, DV, SPLIT>& sm, const Bw
     const int sw = T::swz(col);
 #pragma unroll
     for (int k = 0; k < 4; k++)
-      ab[k] = (uint32_t)(col * T::RB + 16 * (half ^ (sw & 1)) + 32 * (k ^ (sw >> 1)));
+      ab[k] = (uint32_t)(T::row_base(col) + 16 * (half ^ (sw & 1)) + 32 * (k ^ (sw >> 1)));
   };
   auto a_off = [&](auto tile_tag, const uint32_t (&ab)[4], int s) -> uint32_t {
     using T = decltype(tile_tag);
@@ -263,7 +271,7 @@ __device__ __forceinline__ void bwd_item(BwdShared<DQK, DV, SPLIT>& sm, const Bw
   };
   auto tr_off = [&](auto tile_tag, const uint32_t (&tb)[2], int st, int hi, int nb) -> uint32_t {
     using T = decltype(tile_tag);
-    const int rows = (16 * st + 8 * hi) * T::RB;
+    const int rows = T::row_base(16 * st + 8 * hi);  // tr_row < 8: same row group
     if constexpr (T::SWZ)
       return tb[nb & 1] + (uint32_t)(rows + 64 * nb);
     else
@@ -312,16 +320,16 @@ __device__ __forceinline__ void bwd_item(BwdShared<DQK, DV, SPLIT>& sm, const Bw
     const int i0 = row0(u), slot = u & 3;
 #pragma unroll
     for (int k = 0; k < QT::OPW; k++)
-      dma_to_lds16_asm(qrs, sm.ring.t.q[slot] + 1024 * min(wave * QT::OPW + k, QT::OPS - 1),
+      dma_to_lds16_asm(qrs, sm.ring.t.q[slot] + QT::op_base(min(wave * QT::OPW + k, QT::OPS - 1)),
                    qoffs[k] + (uint32_t)i0 * qstride_b);
 #pragma unroll
     for (int k = 0; k < OT::OPW; k++)
-      dma_to_lds16_asm(ors, sm.ring.t.dO[slot] + 1024 * min(wave * OT::OPW + k, OT::OPS - 1),
+      dma_to_lds16_asm(ors, sm.ring.t.dO[slot] + OT::op_base(min(wave * OT::OPW + k, OT::OPS - 1)),
                    ooffs[k] + (uint32_t)i0 * dostride_b);
     if constexpr (SPLIT) {
 #pragma unroll
       for (int k = 0; k < OT::OPW; k++)
-        dma_to_lds16_asm(orsl, sm.ring.t.dOl[slot] + 1024 * min(wave * OT::OPW + k, OT::OPS - 1),
+        dma_to_lds16_asm(orsl, sm.ring.t.dOl[slot] + OT::op_base(min(wave * OT::OPW + k, OT::OPS - 1)),
                          ooffs[k] + (uint32_t)i0 * dostride_b);
     }
   };
@@ -951,7 +959,7 @@ __device__ __forceinline__ void bwd_role_a(BwdSharedRS<DQK, DV, SPLIT>& sm, cons
     const int sw = T::swz(col);
 #pragma unroll
     for (int k = 0; k < 4; k++)
-      ab[k] = (uint32_t)(col * T::RB + 16 * (half ^ (sw & 1)) + 32 * (k ^ (sw >> 1)));
+      ab[k] = (uint32_t)(T::row_base(col) + 16 * (half ^ (sw & 1)) + 32 * (k ^ (sw >> 1)));
   };
   auto a_off = [&](auto tile_tag, const uint32_t (&ab)[4], int s) -> uint32_t {
     using T = decltype(tile_tag);
@@ -997,16 +1005,16 @@ __device__ __forceinline__ void bwd_role_a(BwdSharedRS<DQK, DV, SPLIT>& sm, cons
     const int i0 = row0(u), slot = u % kSlots;
 #pragma unroll
     for (int k = 0; k < QT::OPW; k++)
-      dma_to_lds16_asm(qrs, sm.ring.t.q[slot] + 1024 * min(wave * QT::OPW + k, QT::OPS - 1),
+      dma_to_lds16_asm(qrs, sm.ring.t.q[slot] + QT::op_base(min(wave * QT::OPW + k, QT::OPS - 1)),
                        qoffs[k] + (uint32_t)i0 * qstride_b);
 #pragma unroll
     for (int k = 0; k < OT::OPW; k++)
-      dma_to_lds16_asm(ors, sm.ring.t.dO[slot] + 1024 * min(wave * OT::OPW + k, OT::OPS - 1),
+      dma_to_lds16_asm(ors, sm.ring.t.dO[slot] + OT::op_base(min(wave * OT::OPW + k, OT::OPS - 1)),
                        ooffs[k] + (uint32_t)i0 * dostride_b);
     if constexpr (SPLIT) {
 #pragma unroll
       for (int k = 0; k < OT::OPW; k++)
-        dma_to_lds16_asm(orsl, sm.ring.t.dOl[slot] + 1024 * min(wave * OT::OPW + k, OT::OPS - 1),
+        dma_to_lds16_asm(orsl, sm.ring.t.dOl[slot] + OT::op_base(min(wave * OT::OPW + k, OT::OPS - 1)),
                          ooffs[k] + (uint32_t)i0 * dostride_b);
     }
   };
@@ -1401,7 +1409,6 @@ __device__ __forceinline__ void bwd_role_b(BwdSharedRS<DQK, DV, SPLIT>& sm, cons
   const int col = lane & 31, half = lane >> 5;
   const int jw0 = j0 + 32 * wave;
   const float invN = 1.0f / (float)N;
-  auto row0 = [&](int u) { return j0 + BM * u; };
   // dQ: column block `wave` (waves past DQK / 32 have none) over all 128 keys.
   constexpr int NCB = DQK / 32, KSTEPS = BN / 16;
   const int tr_row = 4 * half + ((lane & 15) >> 2);
@@ -1428,7 +1435,7 @@ __device__ __forceinline__ void bwd_role_b(BwdSharedRS<DQK, DV, SPLIT>& sm, cons
   };
   auto tr_off = [&](auto tile_tag, const uint32_t (&tb)[2], int st, int hi, int nb) -> uint32_t {
     using T = decltype(tile_tag);
-    const int rows = (16 * st + 8 * hi) * T::RB;
+    const int rows = T::row_base(16 * st + 8 * hi);  // tr_row < 8: same row group
     if constexpr (T::SWZ)
       return tb[nb & 1] + (uint32_t)(rows + 64 * nb);
     else
