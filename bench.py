@@ -48,6 +48,8 @@ def parse():
                     help="skip the MFMA probe, bucketize and clock measurements")
     ap.add_argument("--bucketize", action="store_true",
                     help="only the standalone bucketize kernel on the workload's timestamps")
+    ap.add_argument("--mfalcon", action="store_true",
+                    help="only the M-FALCON cached passes on the target workload")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="only copy 256 MiB device-to-device 3 times (the reference that "
                          "scales rocprofv3 FETCH_SIZE / WRITE_SIZE to bytes), then exit")
@@ -442,6 +444,9 @@ def main():
 
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     torch.cuda.set_device(0)
+    if args.mfalcon:
+        print(json.dumps(mfalcon_measurement(hstu, torch, torch.cuda.current_stream())), flush=True)
+        return
     batch = inputs.make_batch(args.workload)
     spec = batch.spec
     d = inputs.to_device(batch)

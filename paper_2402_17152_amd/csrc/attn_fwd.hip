@@ -678,12 +678,115 @@ __global__ __launch_bounds__(256) void cached_self_kernel(JaggedArgs ja, int dqk
   }
 }
 
+// The same self term for bf16, one wave per candidate row and all its
+// heads: each lane takes 8 consecutive features (16-byte loads of q, k, v,
+// the partials and the output; rows are 16-byte aligned), the QL = DQK / 8
+// lanes of a head reduce q.k among themselves, and each head's
+// SiLU(q.k + rab) / N passes through LDS to the lanes of its output.  The
+// row's sequence comes from one load per lane and a ballot when there are
+// fewer than 64 sequences.  Per (row, head) the arithmetic is the same for
+// every partition of the candidates into passes.
+constexpr int kSelfMaxHeads = 64;
+template <int DQK, int DV>
+__global__ __launch_bounds__(256) void cached_self_rows_kernel(JaggedArgs ja, Tensors t,
+                                                               const float* __restrict__ o32,
+                                                               uint16_t* __restrict__ out) {
+  __shared__ float spn[4][kSelfMaxHeads];
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int H = ja.num_heads, N = ja.max_seq_len, B = ja.num_seqs;
+  const int64_t row = (int64_t)blockIdx.x * 4 + wave;
+  if (row >= ja.total_tokens) return;
+  int b;
+  if (B < 64) {
+    const int64_t ov = lane <= B ? ja.seq_offsets[lane] : INT64_MAX;
+    b = __popcll(__ballot(ov <= row)) - 1;  // offsets non-decreasing, offsets[B] > row
+  } else {
+    int lo = 0, hi = B - 1;
+    while (lo < hi) {
+      const int mid = (lo + hi + 1) >> 1;
+      if (ja.seq_offsets[mid] <= row) lo = mid; else hi = mid - 1;
+    }
+    b = lo;
+  }
+  const int n_h = (int)(ja.key_offsets[b + 1] - ja.key_offsets[b]);
+  const int nch = min((n_h + kCrossChunk - 1) / kCrossChunk, ja.key_chunks);
+  const float bias = ja.rab_pos[N - 1] + ja.rab_time[0];
+  const float invN = 1.0f / (float)N;
+  constexpr int QL = DQK / 8, VL = DV / 8;
+  const uint16_t* qr = (const uint16_t*)t.q + row * t.q_stride;
+  const uint16_t* kr = (const uint16_t*)t.k + row * t.k_stride;
+  const uint16_t* vr = (const uint16_t*)t.v + row * t.v_stride;
+  for (int g0 = 0; g0 < H * QL; g0 += 64) {
+    const int g = g0 + lane;
+    float part = 0.0f;
+    if (g < H * QL) {
+      const u32x4 qa = *reinterpret_cast<const u32x4*>(qr + 8 * g);
+      const u32x4 ka = *reinterpret_cast<const u32x4*>(kr + 8 * g);
+#pragma unroll
+      for (int e = 0; e < 4; e++) {
+        part = __builtin_fmaf(__uint_as_float(qa[e] << 16), __uint_as_float(ka[e] << 16), part);
+        part = __builtin_fmaf(__uint_as_float(qa[e] & 0xffff0000u),
+                              __uint_as_float(ka[e] & 0xffff0000u), part);
+      }
+    }
+#pragma unroll
+    for (int off = QL / 2; off > 0; off >>= 1) part += __shfl_xor(part, off, 64);
+    if (g < H * QL && g % QL == 0) spn[wave][g / QL] = silu(part + bias) * invN;
+  }
+  // LDS accesses of one wave complete in order; this keeps the compiler's too.
+  asm volatile("" ::: "memory");
+  for (int g0 = 0; g0 < H * VL; g0 += 64) {
+    const int g = g0 + lane;
+    if (g >= H * VL) break;
+    const float pN = spn[wave][g / VL];
+    const int64_t oi = row * H * DV + 8 * (int64_t)g;
+    float y[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+    for (int ch = 0; ch < nch; ch++) {
+      const f32x4 a = *reinterpret_cast<const f32x4*>(o32 + (int64_t)ch * ja.chunk_stride + oi);
+      const f32x4 c = *reinterpret_cast<const f32x4*>(o32 + (int64_t)ch * ja.chunk_stride + oi + 4);
+#pragma unroll
+      for (int e = 0; e < 4; e++) {
+        y[e] += a[e];
+        y[4 + e] += c[e];
+      }
+    }
+    const u32x4 va = *reinterpret_cast<const u32x4*>(vr + 8 * g);
+    u32x4 o;
+#pragma unroll
+    for (int e = 0; e < 4; e++) {
+      const float lo = y[2 * e] + pN * __uint_as_float(va[e] << 16);
+      const float hi = y[2 * e + 1] + pN * __uint_as_float(va[e] & 0xffff0000u);
+      o[e] = (uint32_t)f32_to_bf16_bits(lo) | ((uint32_t)f32_to_bf16_bits(hi) << 16);
+    }
+    *reinterpret_cast<u32x4*>(out + oi) = o;
+  }
+}
+
 }  // namespace
 
 hipError_t launch_cached_self(int is_bf16, const JaggedArgs& ja, int32_t dqk, int32_t dv,
                               const Tensors& t, const float* o32, void* out, hipStream_t s) {
+  if (ja.total_tokens <= 0) return hipSuccess;
+  if (is_bf16 && ja.num_heads <= kSelfMaxHeads) {
+    const dim3 grid((unsigned)((ja.total_tokens + 3) / 4));
+#define HSTU_SELF_CASE(A, B_)                                                              \
+  if (dqk == A && dv == B_) {                                                              \
+    hipLaunchKernelGGL((cached_self_rows_kernel<A, B_>), grid, dim3(256), 0, s, ja, t, o32, \
+                       (uint16_t*)out);                                                    \
+    return hipGetLastError();                                                              \
+  }
+    HSTU_SELF_CASE(32, 32)
+    HSTU_SELF_CASE(32, 64)
+    HSTU_SELF_CASE(32, 128)
+    HSTU_SELF_CASE(64, 32)
+    HSTU_SELF_CASE(64, 64)
+    HSTU_SELF_CASE(64, 128)
+    HSTU_SELF_CASE(128, 32)
+    HSTU_SELF_CASE(128, 64)
+    HSTU_SELF_CASE(128, 128)
+#undef HSTU_SELF_CASE
+  }
   const int64_t waves = ja.total_tokens * ja.num_heads;
-  if (waves <= 0) return hipSuccess;
   const dim3 grid((unsigned)((waves + 3) / 4));
   if (is_bf16)
     hipLaunchKernelGGL(cached_self_kernel<true>, grid, dim3(256), 0, s, ja, dqk, dv, t, o32, out);

@@ -2,6 +2,9 @@
 
   kernels <stats.csv> <title> <command> [note]
       --kernel-trace --stats CSV -> markdown table of per-kernel times.
+  by_grid <kernel_trace.csv> <name-substring,...>
+      --kernel-trace CSV -> markdown rows of median / min time per (kernel,
+      workgroups launched), for runs whose calls of one kernel differ in size.
   traffic <F.csv> <W.csv> <CF.csv> <CW.csv> <kernel-substring> <name> <workload> <source_hash>
       two --pmc runs (FETCH_SIZE, WRITE_SIZE) of a workload and the same two
       of the 256 MiB device copy (bench.py --calibrate-copy) -> the JSON
@@ -34,6 +37,22 @@ def kernels(csv_path: str, title: str, command: str, note: str = "") -> str:
     return "\n".join(out) + "\n"
 
 
+def by_grid(trace_csv: str, subs: str) -> str:
+    groups = {}
+    for r in csv.DictReader(open(trace_csv)):
+        name = short_name(r["Kernel_Name"])
+        if not any(x in name for x in subs.split(",")):
+            continue
+        wg = int(r["Grid_Size_X"]) // int(r["Workgroup_Size_X"])
+        us = (int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3
+        groups.setdefault((name, wg), []).append(us)
+    out = ["| kernel | workgroups | launches | median us | min us |", "|---|---|---|---|---|"]
+    for (name, wg), v in sorted(groups.items()):
+        v.sort()
+        out.append(f"| `{name}` | {wg} | {len(v)} | {v[len(v) // 2]:.1f} | {v[0]:.1f} |")
+    return "\n".join(out) + "\n"
+
+
 def _mean_kib(path: str, counter: str, kernel_sub: str) -> float:
     vals = [float(r["Counter_Value"]) for r in csv.DictReader(open(path))
             if r["Counter_Name"] == counter and kernel_sub in r["Kernel_Name"]]
@@ -56,4 +75,4 @@ def traffic(f_csv, w_csv, cf_csv, cw_csv, kernel_sub, name, workload, source_has
 
 if __name__ == "__main__":
     cmd, args = sys.argv[1], sys.argv[2:]
-    print({"kernels": kernels, "traffic": traffic}[cmd](*args), end="")
+    print({"kernels": kernels, "traffic": traffic, "by_grid": by_grid}[cmd](*args), end="")
