@@ -236,6 +236,60 @@ def test_fwd_bitwise_deterministic(hs):
         assert torch.equal(ba, bb)
 
 
+def _permuted(d, perm):
+    """The batch with its sequences in the order perm (new sequence i is
+    old sequence perm[i]), and for each new row its old row index."""
+    offs = d["seq_offsets"].cpu().numpy()
+    lens = np.diff(offs)
+    rows = np.concatenate([np.arange(offs[b], offs[b + 1]) for b in perm] + [np.zeros(0, np.int64)])
+    ridx = torch.from_numpy(rows.astype(np.int64)).cuda()
+    e = dict(d)
+    for name in ("q", "k", "v", "do", "timestamps"):
+        e[name] = d[name].index_select(0, ridx).contiguous()
+    e["seq_offsets"] = torch.from_numpy(
+        np.concatenate([[0], np.cumsum(lens[perm])]).astype(np.int64)).cuda()
+    if d["num_targets"] is not None:
+        e["num_targets"] = d["num_targets"][torch.from_numpy(np.asarray(perm)).cuda()].contiguous()
+    return e, ridx
+
+
+def test_batch_permutation_equivariance(hs):
+    """Sequences are independent (Sec. 3.2): permuting the sequences of a
+    batch permutes the forward output and dQ, dK, dV with them, bit for bit
+    (every row's arithmetic is fixed whatever the work list's order); the
+    bias-table gradients, summed over all sequences with atomics, agree
+    within fp32 reordering error.  A ragged batch with an empty sequence,
+    a target-aware one and the training workload, each reversed and
+    shuffled."""
+    cases = [inputs.make_batch(3, seed=51, lengths=(1, 37, 200, 129, 300, 0, 64), num_heads=2,
+                               d_qk=64, d_v=64, max_seq_len=320, dtype="bf16"),
+             inputs.make_batch(3, seed=52, lengths=(250, 190, 64), num_targets=(70, 190, 1),
+                               num_heads=2, d_qk=128, d_v=128, max_seq_len=256, dtype="bf16"),
+             inputs.make_batch("training")]
+    rng = np.random.default_rng(5)
+    for batch in cases:
+        d = gu.dev_inputs(batch)
+        N = batch.spec.max_seq_len
+        B = len(batch.lengths)
+        o = gu.gpu_fwd(hs, d, batch)
+        g = gu.gpu_bwd(hs, d, batch)
+        for perm in (np.arange(B)[::-1].copy(), rng.permutation(B)):
+            e, ridx = _permuted(d, perm)
+            op = gu.gpu_fwd(hs, e, batch)
+            gp = gu.gpu_bwd(hs, e, batch)
+            torch.cuda.synchronize()
+            back = torch.empty_like(ridx)
+            back[ridx] = torch.arange(len(ridx), device=ridx.device)
+            assert torch.equal(op.index_select(0, back), o), f"forward not equivariant, B={B}"
+            for name, x, y in zip(("dq", "dk", "dv"), gp[:3], g[:3]):
+                assert torch.equal(x.index_select(0, back), y), f"{name} not equivariant, B={B}"
+            for name, x, y in zip(("d_rab_pos", "d_rab_time"), gp[3:], g[3:]):
+                scale = float(y.abs().max()) + 1e-30
+                diff = float((x - y).abs().max())
+                assert diff <= 1e-4 * scale, (name, diff, scale)
+        print(f"\n  B={B} T={batch.total_tokens}: equivariant")
+
+
 @pytest.mark.parametrize("dtype", ["bf16", "f32"])
 def test_small_parity_clamped_buckets(hs, oracle_mod, dtype):
     """B_t = 9 time buckets with gaps of up to ~2^20 s, so most pairs have
