@@ -82,7 +82,8 @@ bool is_head_dim(int d) { return d == 32 || d == 64 || d == 128; }
 
 hstu_status_t check_problem(const hstu_problem_t* p) {
   if (!p) return fail(HSTU_ERR_INVALID_ARGUMENT, "problem is NULL");
-  if (p->num_seqs < 1) return fail(HSTU_ERR_INVALID_ARGUMENT, "num_seqs must be >= 1 (got %d)", p->num_seqs);
+  if (p->num_seqs < 1)
+    return fail(HSTU_ERR_INVALID_ARGUMENT, "num_seqs must be >= 1 (got %d)", p->num_seqs);
   if (p->total_tokens < 0) return fail(HSTU_ERR_INVALID_ARGUMENT, "total_tokens must be >= 0");
   if (p->total_tokens > (int64_t)1 << 40)
     return fail(HSTU_ERR_UNSUPPORTED, "total_tokens above 2^40 is not supported");
@@ -91,9 +92,11 @@ hstu_status_t check_problem(const hstu_problem_t* p) {
   if (p->num_heads < 1 || p->num_heads > 64)
     return fail(HSTU_ERR_UNSUPPORTED, "num_heads must be in [1, 64] (got %d)", p->num_heads);
   if (!is_head_dim(p->d_qk) || !is_head_dim(p->d_v))
-    return fail(HSTU_ERR_UNSUPPORTED, "d_qk and d_v must be 32, 64 or 128 (got %d, %d)", p->d_qk, p->d_v);
+    return fail(HSTU_ERR_UNSUPPORTED, "d_qk and d_v must be 32, 64 or 128 (got %d, %d)", p->d_qk,
+                p->d_v);
   if (p->num_time_buckets < 1 || p->num_time_buckets > 256)
-    return fail(HSTU_ERR_UNSUPPORTED, "num_time_buckets must be in [1, 256] (got %d)", p->num_time_buckets);
+    return fail(HSTU_ERR_UNSUPPORTED, "num_time_buckets must be in [1, 256] (got %d)",
+                p->num_time_buckets);
   if (p->dtype != HSTU_F32 && p->dtype != HSTU_BF16)
     return fail(HSTU_ERR_INVALID_ARGUMENT, "unknown dtype %d", (int)p->dtype);
   return HSTU_OK;
@@ -113,7 +116,8 @@ size_t elem_size(const hstu_problem_t* p) { return p->dtype == HSTU_BF16 ? 2 : 4
 hstu_status_t check_rows(const hstu_problem_t* p, const char* name, const void* ptr,
                          int64_t stride, int64_t width) {
   if (!ptr) return fail(HSTU_ERR_INVALID_ARGUMENT, "%s is NULL", name);
-  if ((uintptr_t)ptr % 16) return fail(HSTU_ERR_INVALID_ARGUMENT, "%s is not 16-byte aligned", name);
+  if ((uintptr_t)ptr % 16)
+    return fail(HSTU_ERR_INVALID_ARGUMENT, "%s is not 16-byte aligned", name);
   if (stride < width)
     return fail(HSTU_ERR_INVALID_ARGUMENT, "%s_stride %lld is smaller than a row (%lld)", name,
                 (long long)stride, (long long)width);
@@ -392,7 +396,8 @@ hstu_status_t check_mat(const char* name, const void* ptr, int64_t stride, int64
                         size_t e, int64_t rows) {
   if (!ptr && rows == 0) return HSTU_OK;
   if (!ptr) return fail(HSTU_ERR_INVALID_ARGUMENT, "%s is NULL", name);
-  if ((uintptr_t)ptr % 16) return fail(HSTU_ERR_INVALID_ARGUMENT, "%s is not 16-byte aligned", name);
+  if ((uintptr_t)ptr % 16)
+    return fail(HSTU_ERR_INVALID_ARGUMENT, "%s is not 16-byte aligned", name);
   if (stride < width)
     return fail(HSTU_ERR_INVALID_ARGUMENT, "%s_stride %lld is smaller than a row (%lld)", name,
                 (long long)stride, (long long)width);
@@ -521,7 +526,8 @@ double hstu_sl_keep_numerator(int32_t max_seq_len, double alpha) {
 
 size_t hstu_sl_workspace_bytes(int32_t num_seqs) {
   if (num_seqs < 1) return 0;
-  return align_up(sizeof(int64_t) * (size_t)num_seqs) + align_up(sizeof(int32_t) * (size_t)num_seqs);
+  return align_up(sizeof(int64_t) * (size_t)num_seqs) +
+         align_up(sizeof(int32_t) * (size_t)num_seqs);
 }
 
 hstu_status_t hstu_stochastic_length(int32_t num_seqs, const int64_t* seq_offsets,
@@ -545,7 +551,8 @@ hstu_status_t hstu_stochastic_length(int32_t num_seqs, const int64_t* seq_offset
     const size_t need = hstu_sl_workspace_bytes(num_seqs);
     if (!ws || ws_bytes < need)
       return fail(HSTU_ERR_WORKSPACE, "workspace too small: %zu < %zu bytes", ws_bytes, need);
-    if ((uintptr_t)ws % kAlign) return fail(HSTU_ERR_WORKSPACE, "workspace must be 256-byte aligned");
+    if ((uintptr_t)ws % kAlign)
+      return fail(HSTU_ERR_WORKSPACE, "workspace must be 256-byte aligned");
     char* w = (char*)ws;
     int64_t* new_len = (int64_t*)w;
     int32_t* whole = (int32_t*)(w + align_up(sizeof(int64_t) * (size_t)num_seqs));
@@ -829,7 +836,8 @@ hstu_status_t hstu_attn_fwd_cached(const hstu_problem_t* p, const hstu_jagged_t*
     }
     const CachedLayout l = cached_layout(p);
     if (!ws) return fail(HSTU_ERR_WORKSPACE, "workspace is NULL (need %zu bytes)", l.total);
-    if ((uintptr_t)ws % kAlign) return fail(HSTU_ERR_WORKSPACE, "workspace must be 256-byte aligned");
+    if ((uintptr_t)ws % kAlign)
+      return fail(HSTU_ERR_WORKSPACE, "workspace must be 256-byte aligned");
     if (ws_bytes < l.total)
       return fail(HSTU_ERR_WORKSPACE, "workspace too small: %zu < %zu bytes", ws_bytes, l.total);
     const int64_t T = p->total_tokens;
@@ -991,13 +999,15 @@ hstu_status_t hstu_layer_bwd(const hstu_problem_t* p, const hstu_jagged_t* j, co
                           : nullptr;
     HSTU_TRY(attn_bwd_check(p, j, t, dout, dq, dk, dv, d_rab_pos, d_rab_time, ws, ws_bytes, &l));
     const int64_t D = (int64_t)p->num_heads * p->d_v;
-    if (D > 4096) return fail(HSTU_ERR_UNSUPPORTED, "h*d_v must be <= 4096 (got %lld)", (long long)D);
+    if (D > 4096)
+      return fail(HSTU_ERR_UNSUPPORTED, "h*d_v must be <= 4096 (got %lld)", (long long)D);
     HSTU_TRY(check_rows(p, "u", u, u_stride, D));
     HSTU_TRY(check_dense("attn_out", attn_out, 16));
     HSTU_TRY(check_dense("d_y", d_y, 16));
     HSTU_TRY(check_dense("du", du, 16));
     if (p->total_tokens > 0 && (!ln_mean || !ln_rstd))
-      return fail(HSTU_ERR_INVALID_ARGUMENT, "ln_mean and ln_rstd (saved by hstu_layer_fwd) are required");
+      return fail(HSTU_ERR_INVALID_ARGUMENT,
+                  "ln_mean and ln_rstd (saved by hstu_layer_fwd) are required");
     if (d_ln_weight) HSTU_HIP(launch_fill_f32(d_ln_weight, D, 0.0f, s), "fill launch");
     if (d_ln_bias) HSTU_HIP(launch_fill_f32(d_ln_bias, D, 0.0f, s), "fill launch");
     if (p->total_tokens > 0) {
@@ -1024,7 +1034,8 @@ hstu_status_t hstu_layer_fwd(const hstu_problem_t* p, const hstu_jagged_t* j, co
     hipStream_t s = (hipStream_t)hip_stream;
     HSTU_TRY(check_problem(p));
     const int64_t D = (int64_t)p->num_heads * p->d_v;
-    if (D > 4096) return fail(HSTU_ERR_UNSUPPORTED, "h*d_v must be <= 4096 (got %lld)", (long long)D);
+    if (D > 4096)
+      return fail(HSTU_ERR_UNSUPPORTED, "h*d_v must be <= 4096 (got %lld)", (long long)D);
     HSTU_TRY(check_rows(p, "u", u, u_stride, D));
     HSTU_TRY(check_dense("y", y, 16));
     if (!(ln_eps >= 0.0f)) return fail(HSTU_ERR_INVALID_ARGUMENT, "ln_eps must be >= 0");
@@ -1083,7 +1094,8 @@ hstu_status_t hstu_pair_offsets(int32_t num_seqs, const int64_t* seq_offsets, in
   try {
     if (num_seqs < 1) return fail(HSTU_ERR_INVALID_ARGUMENT, "num_seqs must be >= 1");
     if (!seq_offsets || !pair_offsets) return fail(HSTU_ERR_INVALID_ARGUMENT, "NULL pointer");
-    HSTU_HIP(launch_complete_cumsum(num_seqs, seq_offsets, pair_offsets, 1, (hipStream_t)hip_stream),
+    HSTU_HIP(launch_complete_cumsum(num_seqs, seq_offsets, pair_offsets, 1,
+                                    (hipStream_t)hip_stream),
              "pair offsets launch");
     return ok();
   } catch (...) {
@@ -1102,13 +1114,16 @@ hstu_status_t hstu_validate(const hstu_problem_t* p, const hstu_jagged_t* j, voi
     HSTU_HIP(hipMemcpyAsync(offs.data(), j->seq_offsets, sizeof(int64_t) * (B + 1),
                             hipMemcpyDeviceToHost, s), "copy offsets");
     if (j->num_targets)
-      HSTU_HIP(hipMemcpyAsync(nt.data(), j->num_targets, sizeof(int64_t) * B, hipMemcpyDeviceToHost, s),
+      HSTU_HIP(hipMemcpyAsync(nt.data(), j->num_targets, sizeof(int64_t) * B,
+                              hipMemcpyDeviceToHost, s),
                "copy num_targets");
     if (T > 0)
-      HSTU_HIP(hipMemcpyAsync(ts.data(), j->timestamps, sizeof(int64_t) * T, hipMemcpyDeviceToHost, s),
+      HSTU_HIP(hipMemcpyAsync(ts.data(), j->timestamps, sizeof(int64_t) * T,
+                              hipMemcpyDeviceToHost, s),
                "copy timestamps");
     HSTU_HIP(hipStreamSynchronize(s), "synchronize");
-    if (offs[0] != 0) return fail(HSTU_ERR_DATA, "seq_offsets[0] = %lld, expected 0", (long long)offs[0]);
+    if (offs[0] != 0)
+      return fail(HSTU_ERR_DATA, "seq_offsets[0] = %lld, expected 0", (long long)offs[0]);
     if (offs[B] != T)
       return fail(HSTU_ERR_DATA, "seq_offsets[B] = %lld, expected total_tokens %lld",
                   (long long)offs[B], (long long)T);

@@ -91,7 +91,9 @@ struct StepTile {
   // Byte offset of row r, and of DMA operation o (1 KB: whole rows when
   // SWZ, so that one operation never straddles a row group).
   __device__ static constexpr int row_base(int r) { return r * RB + GSH * (r >> 3); }
-  __device__ static constexpr int op_base(int o) { return 1024 * o + GSH * ((o * (1024 / RB)) >> 3); }
+  __device__ static constexpr int op_base(int o) {
+    return 1024 * o + GSH * ((o * (1024 / RB)) >> 3);
+  }
   static_assert(!SWZ || 1024 % RB == 0, "a DMA operation covers whole rows");
 };
 
@@ -329,7 +331,8 @@ __device__ __forceinline__ void bwd_item(BwdShared<DQK, DV, SPLIT>& sm, const Bw
     if constexpr (SPLIT) {
 #pragma unroll
       for (int k = 0; k < OT::OPW; k++)
-        dma_to_lds16_asm(orsl, sm.ring.t.dOl[slot] + OT::op_base(min(wave * OT::OPW + k, OT::OPS - 1)),
+        dma_to_lds16_asm(orsl,
+                         sm.ring.t.dOl[slot] + OT::op_base(min(wave * OT::OPW + k, OT::OPS - 1)),
                          ooffs[k] + (uint32_t)i0 * dostride_b);
     }
   };
@@ -537,22 +540,27 @@ __device__ __forceinline__ void bwd_item(BwdShared<DQK, DV, SPLIT>& sm, const Bw
       for (int nb = 0; nb < DV / 32; nb++) {
         const uint2 lo = lds_read_tr16((const uint16_t*)(ob + tr_off(OT{}, ot, st, 0, nb)));
         const uint2 hi = lds_read_tr16((const uint16_t*)(ob + tr_off(OT{}, ot, st, 1, nb)));
-        dvacc[nb] = mfma32x32x16(as_bf16x8(pa[st]), as_bf16x8(u32x4{lo.x, lo.y, hi.x, hi.y}), dvacc[nb]);
+        dvacc[nb] = mfma32x32x16(as_bf16x8(pa[st]),
+                                 as_bf16x8(u32x4{lo.x, lo.y, hi.x, hi.y}), dvacc[nb]);
         if constexpr (SPLIT) {
-          dvacc[nb] = mfma32x32x16(as_bf16x8(pl[st]), as_bf16x8(u32x4{lo.x, lo.y, hi.x, hi.y}), dvacc[nb]);
+          dvacc[nb] = mfma32x32x16(as_bf16x8(pl[st]),
+                                 as_bf16x8(u32x4{lo.x, lo.y, hi.x, hi.y}), dvacc[nb]);
           const uint8_t* obl = sm.ring.t.dOl[u & 3];
           const uint2 l2 = lds_read_tr16((const uint16_t*)(obl + tr_off(OT{}, ot, st, 0, nb)));
           const uint2 h2 = lds_read_tr16((const uint16_t*)(obl + tr_off(OT{}, ot, st, 1, nb)));
-          dvacc[nb] = mfma32x32x16(as_bf16x8(pa[st]), as_bf16x8(u32x4{l2.x, l2.y, h2.x, h2.y}), dvacc[nb]);
+          dvacc[nb] = mfma32x32x16(as_bf16x8(pa[st]),
+                                 as_bf16x8(u32x4{l2.x, l2.y, h2.x, h2.y}), dvacc[nb]);
         }
       }
 #pragma unroll
       for (int nb = 0; nb < DQK / 32; nb++) {
         const uint2 lo = lds_read_tr16((const uint16_t*)(qb + tr_off(QT{}, qt, st, 0, nb)));
         const uint2 hi = lds_read_tr16((const uint16_t*)(qb + tr_off(QT{}, qt, st, 1, nb)));
-        dkacc[nb] = mfma32x32x16(as_bf16x8(da[st]), as_bf16x8(u32x4{lo.x, lo.y, hi.x, hi.y}), dkacc[nb]);
+        dkacc[nb] = mfma32x32x16(as_bf16x8(da[st]),
+                                 as_bf16x8(u32x4{lo.x, lo.y, hi.x, hi.y}), dkacc[nb]);
         if constexpr (SPLIT)
-          dkacc[nb] = mfma32x32x16(as_bf16x8(dl[st]), as_bf16x8(u32x4{lo.x, lo.y, hi.x, hi.y}), dkacc[nb]);
+          dkacc[nb] = mfma32x32x16(as_bf16x8(dl[st]),
+                                 as_bf16x8(u32x4{lo.x, lo.y, hi.x, hi.y}), dkacc[nb]);
       }
     }
   };
@@ -591,7 +599,8 @@ __device__ __forceinline__ void bwd_item(BwdShared<DQK, DV, SPLIT>& sm, const Bw
       const uint32_t vo = dq_lane + (uint32_t)((row0(u) + 8 * g) * DQK * 4);
 #pragma unroll
       for (int m = 0; m < 4; m++)
-        __builtin_amdgcn_raw_ptr_buffer_atomic_fadd_f32(qacc[4 * g + m], dqrs, vo + m * DQK * 4, 0, 0);
+        __builtin_amdgcn_raw_ptr_buffer_atomic_fadd_f32(qacc[4 * g + m], dqrs, vo + m * DQK * 4, 0,
+                                                        0);
     }
   };
 
@@ -746,10 +755,8 @@ __device__ __forceinline__ void bwd_item(BwdShared<DQK, DV, SPLIT>& sm, const Bw
     u32x4 pa[2], da[2], pl[2], dl[2];
 #pragma unroll
     for (int st = 0; st < 2; st++) {
-      pa[st] = u32x4{pack_bf16x2(pv[8 * st], pv[8 * st + 1]), pack_bf16x2(pv[8 * st + 2], pv[8 * st + 3]),
-                     pack_bf16x2(pv[8 * st + 4], pv[8 * st + 5]), pack_bf16x2(pv[8 * st + 6], pv[8 * st + 7])};
-      da[st] = u32x4{pack_bf16x2(dsv[8 * st], dsv[8 * st + 1]), pack_bf16x2(dsv[8 * st + 2], dsv[8 * st + 3]),
-                     pack_bf16x2(dsv[8 * st + 4], dsv[8 * st + 5]), pack_bf16x2(dsv[8 * st + 6], dsv[8 * st + 7])};
+      pa[st] = pack_bf16x8(pv + 8 * st);
+      da[st] = pack_bf16x8(dsv + 8 * st);
       if constexpr (SPLIT) {
         // low terms: value - bf16(value), exact in fp32
 #pragma unroll
@@ -1014,7 +1021,8 @@ __device__ __forceinline__ void bwd_role_a(BwdSharedRS<DQK, DV, SPLIT>& sm, cons
     if constexpr (SPLIT) {
 #pragma unroll
       for (int k = 0; k < OT::OPW; k++)
-        dma_to_lds16_asm(orsl, sm.ring.t.dOl[slot] + OT::op_base(min(wave * OT::OPW + k, OT::OPS - 1)),
+        dma_to_lds16_asm(orsl,
+                         sm.ring.t.dOl[slot] + OT::op_base(min(wave * OT::OPW + k, OT::OPS - 1)),
                          ooffs[k] + (uint32_t)i0 * dostride_b);
     }
   };
@@ -1239,7 +1247,8 @@ __device__ __forceinline__ void bwd_role_a(BwdSharedRS<DQK, DV, SPLIT>& sm, cons
       if (8 * (q >> 2) + (q & 3) < wrap_from) nowrap = sum;
     }
     ring_mine[(32 * u + d1_lane) & (kRing - 1)] = nowrap + carry;
-    carry = __int_as_float(__builtin_amdgcn_ds_bpermute(perm_base ^ 128, __float_as_int(sum - nowrap)));
+    carry = __int_as_float(
+        __builtin_amdgcn_ds_bpermute(perm_base ^ 128, __float_as_int(sum - nowrap)));
   };
   const int R = L - j0;
   auto ring_flush = [&](int c) {
@@ -1334,10 +1343,8 @@ __device__ __forceinline__ void bwd_role_a(BwdSharedRS<DQK, DV, SPLIT>& sm, cons
     u32x4 pa[2], da[2], pl[2], dl[2];
 #pragma unroll
     for (int st = 0; st < 2; st++) {
-      pa[st] = u32x4{pack_bf16x2(pv[8 * st], pv[8 * st + 1]), pack_bf16x2(pv[8 * st + 2], pv[8 * st + 3]),
-                     pack_bf16x2(pv[8 * st + 4], pv[8 * st + 5]), pack_bf16x2(pv[8 * st + 6], pv[8 * st + 7])};
-      da[st] = u32x4{pack_bf16x2(dsv[8 * st], dsv[8 * st + 1]), pack_bf16x2(dsv[8 * st + 2], dsv[8 * st + 3]),
-                     pack_bf16x2(dsv[8 * st + 4], dsv[8 * st + 5]), pack_bf16x2(dsv[8 * st + 6], dsv[8 * st + 7])};
+      pa[st] = pack_bf16x8(pv + 8 * st);
+      da[st] = pack_bf16x8(dsv + 8 * st);
       if constexpr (SPLIT) {
         // low terms: value - bf16(value), exact in fp32
 #pragma unroll
@@ -1474,22 +1481,27 @@ __device__ __forceinline__ void bwd_role_b(BwdSharedRS<DQK, DV, SPLIT>& sm, cons
       for (int nb = 0; nb < DV / 32; nb++) {
         const uint2 lo = lds_read_tr16((const uint16_t*)(ob + tr_off(OT{}, ot, st, 0, nb)));
         const uint2 hi = lds_read_tr16((const uint16_t*)(ob + tr_off(OT{}, ot, st, 1, nb)));
-        dvacc[nb] = mfma32x32x16(as_bf16x8(pa[st]), as_bf16x8(u32x4{lo.x, lo.y, hi.x, hi.y}), dvacc[nb]);
+        dvacc[nb] = mfma32x32x16(as_bf16x8(pa[st]),
+                                 as_bf16x8(u32x4{lo.x, lo.y, hi.x, hi.y}), dvacc[nb]);
         if constexpr (SPLIT) {
-          dvacc[nb] = mfma32x32x16(as_bf16x8(pl[st]), as_bf16x8(u32x4{lo.x, lo.y, hi.x, hi.y}), dvacc[nb]);
+          dvacc[nb] = mfma32x32x16(as_bf16x8(pl[st]),
+                                 as_bf16x8(u32x4{lo.x, lo.y, hi.x, hi.y}), dvacc[nb]);
           const uint8_t* obl = sm.ring.t.dOl[u % kSlots];
           const uint2 l2 = lds_read_tr16((const uint16_t*)(obl + tr_off(OT{}, ot, st, 0, nb)));
           const uint2 h2 = lds_read_tr16((const uint16_t*)(obl + tr_off(OT{}, ot, st, 1, nb)));
-          dvacc[nb] = mfma32x32x16(as_bf16x8(pa[st]), as_bf16x8(u32x4{l2.x, l2.y, h2.x, h2.y}), dvacc[nb]);
+          dvacc[nb] = mfma32x32x16(as_bf16x8(pa[st]),
+                                 as_bf16x8(u32x4{l2.x, l2.y, h2.x, h2.y}), dvacc[nb]);
         }
       }
 #pragma unroll
       for (int nb = 0; nb < DQK / 32; nb++) {
         const uint2 lo = lds_read_tr16((const uint16_t*)(qb + tr_off(QT{}, qt, st, 0, nb)));
         const uint2 hi = lds_read_tr16((const uint16_t*)(qb + tr_off(QT{}, qt, st, 1, nb)));
-        dkacc[nb] = mfma32x32x16(as_bf16x8(da[st]), as_bf16x8(u32x4{lo.x, lo.y, hi.x, hi.y}), dkacc[nb]);
+        dkacc[nb] = mfma32x32x16(as_bf16x8(da[st]),
+                                 as_bf16x8(u32x4{lo.x, lo.y, hi.x, hi.y}), dkacc[nb]);
         if constexpr (SPLIT)
-          dkacc[nb] = mfma32x32x16(as_bf16x8(dl[st]), as_bf16x8(u32x4{lo.x, lo.y, hi.x, hi.y}), dkacc[nb]);
+          dkacc[nb] = mfma32x32x16(as_bf16x8(dl[st]),
+                                 as_bf16x8(u32x4{lo.x, lo.y, hi.x, hi.y}), dkacc[nb]);
       }
     }
   };

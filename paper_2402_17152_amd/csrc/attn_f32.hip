@@ -222,7 +222,8 @@ hipError_t launch_attn_bwd_f32(const JaggedArgs& ja, const Tensors& t, int dqk, 
                                const void* d_out, void* dq, void* dk, void* dv_out,
                                double* rab_pos_acc, double* rab_time_acc, hipStream_t s) {
   if (ja.total_tokens <= 0) return hipSuccess;
-#define CALL(A, B) return bwd_case<A, B>(ja, t, d_out, dq, dk, dv_out, rab_pos_acc, rab_time_acc, s);
+#define CALL(A, B) \
+  return bwd_case<A, B>(ja, t, d_out, dq, dk, dv_out, rab_pos_acc, rab_time_acc, s);
   HSTU_F32_DISPATCH(CALL)
 #undef CALL
   return hipErrorInvalidValue;

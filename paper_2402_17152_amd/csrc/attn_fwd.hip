@@ -440,7 +440,8 @@ __device__ __forceinline__ void fwd_item(FwdShared<DQK, DV>& sm, const JaggedArg
         const uint2 lo = lds_read_tr16(base), hi = lds_read_tr16(base + 8 * V_LD);
         const u32x4 vb = {lo.x, lo.y, hi.x, hi.y};
         oacc[nb] = mfma32x32x16(as_bf16x8(pa[st]), as_bf16x8(vb), oacc[nb]);
-        if constexpr (SPLIT) oacc[nb] = mfma32x32x16(as_bf16x8(pa[2 + st]), as_bf16x8(vb), oacc[nb]);
+        if constexpr (SPLIT)
+          oacc[nb] = mfma32x32x16(as_bf16x8(pa[2 + st]), as_bf16x8(vb), oacc[nb]);
       }
   };
   auto activate = [&](const f32x16& acc, u32x4 (&pa)[NPA]) {
@@ -663,7 +664,8 @@ __global__ __launch_bounds__(256) void cached_self_kernel(JaggedArgs ja, int dqk
     return BF16 ? bf16_bits_to_f32(((const uint16_t*)base)[idx]) : ((const float*)base)[idx];
   };
   float part = 0.0f;
-  for (int c = lane; c < dqk; c += 64) part += ld(t.q, t.q_stride, dqk, c) * ld(t.k, t.k_stride, dqk, c);
+  for (int c = lane; c < dqk; c += 64)
+    part += ld(t.q, t.q_stride, dqk, c) * ld(t.k, t.k_stride, dqk, c);
   const float x = wave_sum_f32(part) + ja.rab_pos[N - 1] + ja.rab_time[0];
   const float pN = silu(x) / (float)N;
   for (int c = lane; c < dv; c += 64) {

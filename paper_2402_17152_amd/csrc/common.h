@@ -72,6 +72,12 @@ __device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
   return __builtin_bit_cast(uint32_t, r);
 }
 
+// Eight floats as eight bf16 (round to nearest even), low halves first.
+__device__ __forceinline__ u32x4 pack_bf16x8(const float* v) {
+  return u32x4{pack_bf16x2(v[0], v[1]), pack_bf16x2(v[2], v[3]), pack_bf16x2(v[4], v[5]),
+               pack_bf16x2(v[6], v[7])};
+}
+
 typedef _Float16 f16x2 __attribute__((ext_vector_type(2)));
 
 // Packs two floats into two f16 (round to nearest even) in one dword.

@@ -68,7 +68,8 @@ __global__ __launch_bounds__(256) void ln_gate_kernel(int64_t T, int D, const vo
                                                       const void* __restrict__ u, int64_t u_stride,
                                                       const float* __restrict__ w,
                                                       const float* __restrict__ b, float eps,
-                                                      void* __restrict__ y, float* __restrict__ mean,
+                                                      void* __restrict__ y,
+                                                      float* __restrict__ mean,
                                                       float* __restrict__ rstd) {
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int64_t t = (int64_t)blockIdx.x * 4 + wave;

@@ -70,7 +70,9 @@ __device__ void schedule_block(const JaggedArgs& ja, int mode, WorkItem* items, 
       const int nch = cross ? min(ceil_div(n_h, kCrossChunk), ja.key_chunks) : 1;
       for (int e = sub; e < nblk * nch; e += G) {
         const int x = e / nch, c = e - x * nch;
-        int w = cross ? cross_weight(n_h, c) : mode == 0 ? fwd_weight(L, n_h, x) : bwd_weight(L, n_h, x);
+        int w = cross       ? cross_weight(n_h, c)
+                : mode == 0 ? fwd_weight(L, n_h, x)
+                            : bwd_weight(L, n_h, x);
         w = min(max(w, 0), maxw);
         f(b, cross ? x * ja.key_chunks + c : x, w);
       }
@@ -179,7 +181,8 @@ int grid_for(int64_t n, int threads) {
 // Per-sequence timestamp extremes (one workgroup per sequence; eight
 // independent loads in flight per thread).  The attention kernels use them
 // to pick 32-bit rebased time arithmetic when a sequence spans < 2^31.
-__device__ void time_range_block(const JaggedArgs& ja, int b, int64_t* out, int64_t (*red)[kSchedThreads / 64]) {
+__device__ void time_range_block(const JaggedArgs& ja, int b, int64_t* out,
+                                 int64_t (*red)[kSchedThreads / 64]) {
   const int tid = threadIdx.x;
   const int64_t o = ja.seq_offsets[b];
   const int L = (int)(ja.seq_offsets[b + 1] - o);
@@ -242,7 +245,8 @@ __device__ void fill_blocks(const PrepFills& fills, int f, int nf) {
         reinterpret_cast<f32x4*>(p)[i] = z;
       done = 4 * n4;
     }
-    for (int64_t i = done + (int64_t)f * kSchedThreads + threadIdx.x; i < n; i += stride) p[i] = 0.0f;
+    for (int64_t i = done + (int64_t)f * kSchedThreads + threadIdx.x; i < n; i += stride)
+      p[i] = 0.0f;
   }
 }
 

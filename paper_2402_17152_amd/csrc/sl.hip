@@ -25,7 +25,8 @@ namespace {
 
 constexpr int kSlThreads = 256;
 
-__global__ __launch_bounds__(256) void sl_lengths_kernel(int32_t B, const int64_t* __restrict__ offs,
+__global__ __launch_bounds__(256) void sl_lengths_kernel(int32_t B,
+                                                         const int64_t* __restrict__ offs,
                                                          const int64_t* __restrict__ nt, int32_t L,
                                                          double keep_num,
                                                          const double* __restrict__ u_keep,
