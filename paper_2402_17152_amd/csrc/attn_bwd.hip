@@ -50,9 +50,9 @@
 // (its own LayerNorm backward produces it in fp32, with a dynamic range
 // across rows that a single bf16 would turn into several percent of error
 // after the cancellations of the contractions); both are staged and each
-// dO contraction runs on both.  For the same reason P and dS enter dV and
-// dK as two bf16 terms as well (hi P with both dO terms, lo P with hi dO;
-// hi and lo dS with Q); dQ keeps the single bf16 dS.
+// dO contraction runs on both.  For the same reason P and dS enter dV, dK
+// and dQ as two bf16 terms as well (hi P with both dO terms, lo P with hi
+// dO; hi and lo dS with Q and with K).
 #include <type_traits>
 
 #include "bias.h"
@@ -76,14 +76,15 @@ constexpr float kMaskedBias = -1.0e30f;
 // 8 values, so 16 consecutive rows would meet each bank group twice: each
 // group of 8 rows therefore starts GSH bytes (half of 64 four-byte banks)
 // further on than the one before, and the 16 rows of an A-operand read
-// cover every bank once.  For D = 32 rows carry one pad chunk.
-template <int D>
+// cover every bank once (GS = false leaves the groups unshifted, for a
+// kernel short of LDS).  For D = 32 rows carry one pad chunk.
+template <int D, bool GS = true>
 struct StepTile {
   static constexpr int CPR = D / 8;                  // data chunks per row
   static constexpr bool SWZ = D >= 64;
   static constexpr int PC = SWZ ? CPR : CPR + 1;     // chunks per row
   static constexpr int RB = PC * 16;                 // row bytes
-  static constexpr int GSH = SWZ ? 128 : 0;          // shift per group of 8 rows
+  static constexpr int GSH = SWZ && GS ? 128 : 0;    // shift per group of 8 rows
   static constexpr int OPS = (32 * PC + 63) / 64;    // 1 KB DMA operations per tile
   static constexpr int OPW = (OPS + 3) / 4;          // per wave
   static constexpr int BYTES = OPS * 1024 + 3 * GSH;
@@ -97,19 +98,23 @@ struct StepTile {
   static_assert(!SWZ || 1024 % RB == 0, "a DMA operation covers whole rows");
 };
 
+// The single-role kernel runs the two-term (SPLIT) backward of heads
+// larger than 64, whose staging rings nearly fill LDS: its step tiles go
+// without the row-group shift, its dS^T tiles use the 72-byte pitch and
+// its window copies a 200-float pitch (8 banks apart, as 264).
 template <int DQK, int DV, bool SPLIT>
 struct BwdShared {
-  using QT = StepTile<DQK>;
-  using OT = StepTile<DV>;
+  using QT = StepTile<DQK, false>;
+  using OT = StepTile<DV, false>;
   static constexpr int BN = kBwdBN, BM = kBwdBM;
-  // dS^T tile [128 keys][32 rows] bf16: pitch 96 bytes makes the
-  // transposing reads of the dQ step conflict free.
-  static constexpr int DST_LD = 48;
+  // dS^T tile [128 keys][32 rows] bf16, pitch 72 bytes.
+  static constexpr int DST_LD = 36;
   // The block's K, row-major, staged once per item to build the dQ
   // operand (pitch 8 dwords mod 32 banks for transposing reads).
   static constexpr int KB_LD = DQK + 16;
   static constexpr int NWIN = BM + BN;  // reversed rab_pos window (BM + BN - 1 used)
-  static constexpr int kWinPad = 4, WIN_LD = 264;
+  // Each copy is filled at kWinPad .. kWinPad + 191 (three 64-float DMAs).
+  static constexpr int kWinPad = 4, WIN_LD = 200;
   static constexpr int NLO = SPLIT ? 4 : 1, LOB = SPLIT ? OT::BYTES : 16;
   union Ring {
     struct {
@@ -121,6 +126,8 @@ struct BwdShared {
   };
   Ring ring;
   __align__(16) uint16_t sdST[2][BN * DST_LD];
+  // SPLIT: the low bf16 terms of dS^T, laid out as sdST.
+  __align__(16) uint16_t sdSTl[SPLIT ? 2 : 1][SPLIT ? BN * DST_LD : 8];
   __align__(16) float sWin[4][4][WIN_LD];  // copy c holds window[k + c] at kWinPad + k
   __align__(16) uint32_t sT[8][64];        // step row timestamps (32 int64)
   __align__(16) uint32_t sTr[8][32];       // the same rebased (fast path)
@@ -564,13 +571,22 @@ __device__ __forceinline__ void bwd_item(BwdShared<DQK, DV, SPLIT>& sm, const Bw
       }
     }
   };
-  // dS^T of step u into its LDS slot: the lane (key) writes 4 runs of 4 rows.
-  auto store_dst = [&](int u, const u32x4 (&da)[2]) {
+  // dS^T of step u into its LDS slot: the lane (key) writes 4 runs of 4
+  // rows (SPLIT: the low terms likewise).
+  auto store_dst = [&](int u, const u32x4 (&da)[2], const u32x4 (&dl)[2]) {
     uint16_t* dp = sm.sdST[u & 1] + (32 * wave + col) * DST_LD + 4 * half;
 #pragma unroll
     for (int st = 0; st < 2; st++) {
       *reinterpret_cast<uint2*>(dp + 16 * st) = uint2{da[st][0], da[st][1]};
       *reinterpret_cast<uint2*>(dp + 16 * st + 8) = uint2{da[st][2], da[st][3]};
+    }
+    if constexpr (SPLIT) {
+      uint16_t* dpl = sm.sdSTl[u & 1] + (32 * wave + col) * DST_LD + 4 * half;
+#pragma unroll
+      for (int st = 0; st < 2; st++) {
+        *reinterpret_cast<uint2*>(dpl + 16 * st) = uint2{dl[st][0], dl[st][1]};
+        *reinterpret_cast<uint2*>(dpl + 16 * st + 8) = uint2{dl[st][2], dl[st][3]};
+      }
     }
   };
   // dQ(rows of step u, the wave's 32 columns) over its keys, added to the
@@ -591,6 +607,15 @@ __device__ __forceinline__ void bwd_item(BwdShared<DQK, DV, SPLIT>& sm, const Bw
       const uint2 lo = lds_read_tr16(dp + 16 * ks * DST_LD);
       const uint2 hi = lds_read_tr16(dp + (16 * ks + 8) * DST_LD);
       qacc = mfma32x32x16(as_bf16x8(u32x4{lo.x, lo.y, hi.x, hi.y}), as_bf16x8(kq[ks]), qacc);
+    }
+    if constexpr (SPLIT) {
+      const uint16_t* dpl = sm.sdSTl[u & 1] + (kbase + tr_row) * DST_LD + tr_col;
+#pragma unroll
+      for (int ks = 0; ks < KSTEPS; ks++) {
+        const uint2 lo = lds_read_tr16(dpl + 16 * ks * DST_LD);
+        const uint2 hi = lds_read_tr16(dpl + (16 * ks + 8) * DST_LD);
+        qacc = mfma32x32x16(as_bf16x8(u32x4{lo.x, lo.y, hi.x, hi.y}), as_bf16x8(kq[ks]), qacc);
+      }
     }
   };
   auto dq_atomics = [&](int u, const f32x16& qacc) {
@@ -770,7 +795,7 @@ __device__ __forceinline__ void bwd_item(BwdShared<DQK, DV, SPLIT>& sm, const Bw
       }
     }
     key_grads(u, pa, da, pl, dl);
-    store_dst(u, da);
+    store_dst(u, da, dl);
     grads(u, path_cur, dsv);
     path_nn = classify(u + 2);
     reduce_ts(u + 3);
@@ -1523,6 +1548,15 @@ __device__ __forceinline__ void bwd_role_b(BwdSharedRS<DQK, DV, SPLIT>& sm, cons
       const uint2 lo = lds_read_tr16(dp + 16 * ks * DST_LD);
       const uint2 hi = lds_read_tr16(dp + (16 * ks + 8) * DST_LD);
       qacc = mfma32x32x16(as_bf16x8(u32x4{lo.x, lo.y, hi.x, hi.y}), as_bf16x8(kq[ks]), qacc);
+    }
+    if constexpr (SPLIT) {
+      const uint16_t* dpl = sm.sdSTl[u & 1] + tr_row * DST_LD + tr_col;
+#pragma unroll
+      for (int ks = 0; ks < KSTEPS; ks++) {
+        const uint2 lo = lds_read_tr16(dpl + 16 * ks * DST_LD);
+        const uint2 hi = lds_read_tr16(dpl + (16 * ks + 8) * DST_LD);
+        qacc = mfma32x32x16(as_bf16x8(u32x4{lo.x, lo.y, hi.x, hi.y}), as_bf16x8(kq[ks]), qacc);
+      }
     }
     // Block scale 2^(140 - e), e the biased exponent of the largest
     // magnitude (clamped so that it and its inverse are normal floats).

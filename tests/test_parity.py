@@ -94,6 +94,22 @@ def test_small_parity(hs, oracle_mod, dtype, case):
     _check_bwd(hs, oracle_mod, batch)
 
 
+HEAD_DIMS = [(a, b) for a in (32, 64, 128) for b in (32, 64, 128)]
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+@pytest.mark.parametrize("dqk,dv", HEAD_DIMS)
+def test_head_dim_pairs(hs, oracle_mod, dtype, dqk, dv):
+    """Every supported (d_qk, d_v) pair, each its own kernel instantiation:
+    a target-aware batch with ragged tails, an empty sequence, a length-1
+    one and an all-candidate one, forward and backward."""
+    batch = inputs.make_batch(3, seed=400 + dqk + dv // 8, lengths=(150, 0, 1, 97, 40),
+                              num_targets=(12, 0, 1, 0, 40), num_heads=2, d_qk=dqk, d_v=dv,
+                              max_seq_len=160, dtype=dtype)
+    _check_fwd(hs, oracle_mod, batch)
+    _check_bwd(hs, oracle_mod, batch)
+
+
 @pytest.mark.parametrize("dtype", ["bf16", "f32"])
 def test_bwd_long_sequence(hs, oracle_mod, dtype):
     """Every output of a 2200-token sequence and a ragged 45-token one.
@@ -514,6 +530,18 @@ def test_layer_bwd_small(hs, oracle_mod, dtype, affine):
     batch = inputs.make_batch(2, seed=23, lengths=(300, 0, 1, 129, 70), num_targets=(0, 0, 0, 17, 5),
                               num_heads=4, d_qk=64, d_v=64, max_seq_len=300, dtype=dtype)
     _layer_bwd_check(hs, oracle_mod, batch, affine=affine)
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+@pytest.mark.parametrize("dqk,dv", [p for p in HEAD_DIMS if p != (64, 64)])
+def test_layer_head_dim_pairs(hs, oracle_mod, dtype, dqk, dv):
+    """hstu_layer_fwd + hstu_layer_bwd for the head sizes the other layer
+    tests do not use (bf16: heads up to 64 run the two-role backward with
+    two-term operands, larger ones the single-role kernel)."""
+    batch = inputs.make_batch(2, seed=500 + dqk + dv // 8, lengths=(150, 1, 97, 40),
+                              num_targets=(12, 1, 0, 40), num_heads=2, d_qk=dqk, d_v=dv,
+                              max_seq_len=160, dtype=dtype)
+    _layer_bwd_check(hs, oracle_mod, batch)
 
 
 def test_layer_bwd_training_full(hs, oracle_mod):
