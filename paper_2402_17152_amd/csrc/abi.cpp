@@ -862,7 +862,7 @@ hstu_status_t hstu_attn_fwd_cached(const hstu_problem_t* p, const hstu_jagged_t*
                                   s),
              "attn_fwd_cached launch");
     const Tensors cand{q, q_stride, k, k_stride, v, v_stride};
-    HSTU_HIP(launch_cached_self(1, ja, p->d_qk, p->d_v, cand, o32, out, s),
+    HSTU_HIP(launch_cached_self(ja, p->d_qk, p->d_v, cand, o32, out, s),
              "cached self-term launch");
     return ok();
   } catch (...) {

@@ -634,60 +634,16 @@ hipError_t launch_fwd(const JaggedArgs& ja, const Tensors& t, void* out, int out
 
 // Self term of the cached candidate pass: the cross-mode items leave out
 // each candidate's own key (position n_h, dt = 0, so rab = rab_pos[N-1] +
-// rab_time[0]).  One wave per (row, head) finds the row's sequence, adds
-// the fp32 partials of its key chunks in chunk order, then
-// SiLU(q.k + rab) v / N, and stores the result once.
-template <bool BF16>
-__global__ __launch_bounds__(256) void cached_self_kernel(JaggedArgs ja, int dqk, int dv,
-                                                          Tensors t,
-                                                          const float* __restrict__ o32,
-                                                          void* __restrict__ out) {
-  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
-  const int H = ja.num_heads, N = ja.max_seq_len;
-  const int64_t w = (int64_t)blockIdx.x * 4 + wave;
-  if (w >= ja.total_tokens * H) return;
-  const int64_t row = w / H;
-  const int h = (int)(w - row * H);
-  // Sequence of the row: the largest b with seq_offsets[b] <= row.
-  int lo = 0, hi = ja.num_seqs - 1;
-  while (lo < hi) {
-    const int mid = (lo + hi + 1) >> 1;
-    if (ja.seq_offsets[mid] <= row)
-      lo = mid;
-    else
-      hi = mid - 1;
-  }
-  const int n_h = (int)(ja.key_offsets[lo + 1] - ja.key_offsets[lo]);
-  const int nch = min((n_h + kCrossChunk - 1) / kCrossChunk, ja.key_chunks);
-  auto ld = [&](const void* base, int64_t stride, int dim, int c) -> float {
-    const int64_t idx = row * stride + (int64_t)h * dim + c;
-    return BF16 ? bf16_bits_to_f32(((const uint16_t*)base)[idx]) : ((const float*)base)[idx];
-  };
-  float part = 0.0f;
-  for (int c = lane; c < dqk; c += 64)
-    part += ld(t.q, t.q_stride, dqk, c) * ld(t.k, t.k_stride, dqk, c);
-  const float x = wave_sum_f32(part) + ja.rab_pos[N - 1] + ja.rab_time[0];
-  const float pN = silu(x) / (float)N;
-  for (int c = lane; c < dv; c += 64) {
-    const int64_t oi = (row * H + h) * dv + c;
-    float y = 0.0f;
-    for (int ch = 0; ch < nch; ch++) y += o32[(int64_t)ch * ja.chunk_stride + oi];
-    y += pN * ld(t.v, t.v_stride, dv, c);
-    if constexpr (BF16)
-      ((uint16_t*)out)[oi] = f32_to_bf16_bits(y);
-    else
-      ((float*)out)[oi] = y;
-  }
-}
-
-// The same self term for bf16, one wave per candidate row and all its
-// heads: each lane takes 8 consecutive features (16-byte loads of q, k, v,
-// the partials and the output; rows are 16-byte aligned), the QL = DQK / 8
-// lanes of a head reduce q.k among themselves, and each head's
-// SiLU(q.k + rab) / N passes through LDS to the lanes of its output.  The
-// row's sequence comes from one load per lane and a ballot when there are
-// fewer than 64 sequences.  Per (row, head) the arithmetic is the same for
-// every partition of the candidates into passes.
+// rab_time[0]).  One wave per candidate row and all its heads adds the
+// fp32 partials of the row's key chunks in chunk order, then SiLU(q.k +
+// rab) v / N, and stores the result once (bf16).  Each lane takes 8
+// consecutive features (16-byte loads of q, k, v, the partials and the
+// output; rows are 16-byte aligned), the QL = DQK / 8 lanes of a head
+// reduce q.k among themselves, and each head's SiLU(q.k + rab) / N passes
+// through LDS to the lanes of its output.  The row's sequence comes from
+// one load per lane and a ballot when there are fewer than 64 sequences,
+// else from a binary search.  Per (row, head) the arithmetic is the same
+// for every partition of the candidates into passes.
 constexpr int kSelfMaxHeads = 64;
 template <int DQK, int DV>
 __global__ __launch_bounds__(256) void cached_self_rows_kernel(JaggedArgs ja, Tensors t,
@@ -766,35 +722,28 @@ __global__ __launch_bounds__(256) void cached_self_rows_kernel(JaggedArgs ja, Te
 
 }  // namespace
 
-hipError_t launch_cached_self(int is_bf16, const JaggedArgs& ja, int32_t dqk, int32_t dv,
-                              const Tensors& t, const float* o32, void* out, hipStream_t s) {
+hipError_t launch_cached_self(const JaggedArgs& ja, int32_t dqk, int32_t dv, const Tensors& t,
+                              const float* o32, void* out, hipStream_t s) {
   if (ja.total_tokens <= 0) return hipSuccess;
-  if (is_bf16 && ja.num_heads <= kSelfMaxHeads) {
-    const dim3 grid((unsigned)((ja.total_tokens + 3) / 4));
+  if (ja.num_heads > kSelfMaxHeads) return hipErrorInvalidValue;
+  const dim3 grid((unsigned)((ja.total_tokens + 3) / 4));
 #define HSTU_SELF_CASE(A, B_)                                                              \
   if (dqk == A && dv == B_) {                                                              \
     hipLaunchKernelGGL((cached_self_rows_kernel<A, B_>), grid, dim3(256), 0, s, ja, t, o32, \
                        (uint16_t*)out);                                                    \
     return hipGetLastError();                                                              \
   }
-    HSTU_SELF_CASE(32, 32)
-    HSTU_SELF_CASE(32, 64)
-    HSTU_SELF_CASE(32, 128)
-    HSTU_SELF_CASE(64, 32)
-    HSTU_SELF_CASE(64, 64)
-    HSTU_SELF_CASE(64, 128)
-    HSTU_SELF_CASE(128, 32)
-    HSTU_SELF_CASE(128, 64)
-    HSTU_SELF_CASE(128, 128)
+  HSTU_SELF_CASE(32, 32)
+  HSTU_SELF_CASE(32, 64)
+  HSTU_SELF_CASE(32, 128)
+  HSTU_SELF_CASE(64, 32)
+  HSTU_SELF_CASE(64, 64)
+  HSTU_SELF_CASE(64, 128)
+  HSTU_SELF_CASE(128, 32)
+  HSTU_SELF_CASE(128, 64)
+  HSTU_SELF_CASE(128, 128)
 #undef HSTU_SELF_CASE
-  }
-  const int64_t waves = ja.total_tokens * ja.num_heads;
-  const dim3 grid((unsigned)((waves + 3) / 4));
-  if (is_bf16)
-    hipLaunchKernelGGL(cached_self_kernel<true>, grid, dim3(256), 0, s, ja, dqk, dv, t, o32, out);
-  else
-    hipLaunchKernelGGL(cached_self_kernel<false>, grid, dim3(256), 0, s, ja, dqk, dv, t, o32, out);
-  return hipGetLastError();
+  return hipErrorInvalidValue;
 }
 
 hipError_t launch_attn_fwd_bf16(const JaggedArgs& ja, const Tensors& t, int dqk, int dv, void* out,

@@ -98,10 +98,11 @@ hipError_t launch_attn_fwd_bf16(const JaggedArgs& ja, const Tensors& t, int dqk,
 // The self term of the cached candidate pass: out = (sum over the row's
 // key chunks, in order, of the fp32 partials at o32 + c * ja.chunk_stride)
 // + SiLU(q.k + rab_pos[N-1] + rab_time[0]) v / N per (row, head), in bf16
-// or fp32.  ja: the cross-mode arguments (seq_offsets of the candidates,
-// key_offsets, key_chunks, chunk_stride, num_seqs, max_seq_len, rab tables).
-hipError_t launch_cached_self(int is_bf16, const JaggedArgs& ja, int32_t dqk, int32_t dv,
-                              const Tensors& t, const float* o32, void* out, hipStream_t s);
+// (at most 64 heads).  ja: the cross-mode arguments (seq_offsets of the
+// candidates, key_offsets, key_chunks, chunk_stride, num_seqs, max_seq_len,
+// rab tables).
+hipError_t launch_cached_self(const JaggedArgs& ja, int32_t dqk, int32_t dv, const Tensors& t,
+                              const float* o32, void* out, hipStream_t s);
 // Whether the two-term (d_out_lo) backward of these head sizes runs the
 // two-role kernel (its LDS holds the low terms for d_qk, d_v <= 64) or
 // the single-role one.

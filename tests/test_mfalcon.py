@@ -103,9 +103,25 @@ SMALL = [
 ]
 
 
-@pytest.mark.parametrize("case", range(len(SMALL)))
+# Shapes for the launch variants of the cached pass: 70 users (the self
+# term's sequence lookup by binary search instead of a ballot), 64 heads
+# (the most the ABI takes: every lane of the self term's head loop busy),
+# prefixes of two and three 512-key chunks with ragged ends, and the
+# remaining head sizes.
+SHAPES = [
+    (tuple(int(x) for x in np.random.default_rng(5).integers(0, 40, 70)),
+     tuple(int(x) for x in np.random.default_rng(6).integers(0, 7, 70)), 1, 32, 64, 64),
+    ((20, 5, 0), (3, 4, 2), 64, 32, 32, 32),
+    ((1100, 530), (7, 20), 1, 64, 32, 1200),
+    ((600, 90), (33, 3), 2, 128, 32, 700),
+    ((70, 513), (40, 9), 1, 128, 64, 600),
+    ((45, 200), (12, 30), 2, 64, 128, 256),
+]
+
+
+@pytest.mark.parametrize("case", range(len(SMALL) + len(SHAPES)))
 def test_mfalcon_small(hs, oracle_mod, case):
-    nh, nt, h, dqk, dv, N = SMALL[case]
+    nh, nt, h, dqk, dv, N = (SMALL + SHAPES)[case]
     nh, nt = np.array(nh), np.array(nt)
     batch = inputs.make_batch("target", seed=100 + case, lengths=nh + nt, num_targets=nt,
                               num_heads=h, d_qk=dqk, d_v=dv, max_seq_len=N)
@@ -115,7 +131,7 @@ def test_mfalcon_small(hs, oracle_mod, case):
     ref_full = gu.oracle_fwd(oracle_mod, batch)[_cand_rows(batch)]
     gu.assert_close("uncached", full, ref_full, 2e-2, "bf16")
     cached = {}
-    for b_m in (1, 5, 12, 37, int(nt.max())):
+    for b_m in sorted({1, 5, 12, 37, int(nt.max())}):
         ref = oracle_mod.mfalcon_fwd(batch.seq_offsets, nt, b_m, N, batch.timestamps,
                                      batch.rab_pos, batch.rab_time, *f64)
         got = gu.to_f64(mfalcon_gpu(hs, batch, d, b_m))
