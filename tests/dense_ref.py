@@ -1,8 +1,9 @@
-"""Dense per-sequence brute force in NumPy (fp64), used only to pin the
-oracle.  It is written in matrix form, independently of the oracle's
-loops: an explicit L x L mask built the way Algorithm 1 builds it
-(lower-triangular matrix, then candidate rows/columns cleared off the
-diagonal), the full score matrix, and the backward as matrix products."""
+"""Dense per-sequence brute force in NumPy (fp64), used to pin the oracle
+and, with `rnd`, to emulate the rounding of the matrix-core operands.  It
+is written in matrix form, independently of the oracle's loops: an
+explicit L x L mask built the way Algorithm 1 builds it (lower-triangular
+matrix, then candidate rows/columns cleared off the diagonal), the full
+score matrix, and the backward as matrix products."""
 import numpy as np
 
 
@@ -42,9 +43,15 @@ def dsilu(x):
     return s * (1.0 + x * (1.0 - s))
 
 
-def seq_dense(q, k, v, ts, rab_pos, rab_time, N, n_t, d_out=None):
+def _exact(x):
+    return x
+
+
+def seq_dense(q, k, v, ts, rab_pos, rab_time, N, n_t, d_out=None, rnd=_exact):
     """One sequence, all heads.  q,k: [L,h,dqk]; v,d_out: [L,h,dv].
-    Returns O [L,h,dv] and, if d_out is given, the gradients."""
+    Returns O [L,h,dv] and, if d_out is given, the gradients.  `rnd` is
+    applied to SiLU(S) and to dP SiLU'(S) (both before the 1/N) where they
+    enter the products with V, dO, K and Q."""
     L, H, _ = q.shape
     M = mask_alg1(L, n_t)
     bias = rab_pos[position_index(L, n_t, N)] + rab_time[bucket_matrix(ts, len(rab_time))]
@@ -56,14 +63,16 @@ def seq_dense(q, k, v, ts, rab_pos, rab_time, N, n_t, d_out=None):
     for a in range(H):
         S = q[:, a, :] @ k[:, a, :].T + bias
         A = np.where(M, silu(S) / N, 0.0)
-        O[:, a, :] = A @ v[:, a, :]
+        Ar = np.where(M, rnd(silu(S)), 0.0) / N
+        O[:, a, :] = Ar @ v[:, a, :]
         if d_out is not None:
             G = d_out[:, a, :]
             dA = G @ v[:, a, :].T
             dS = np.where(M, dA * dsilu(S) / N, 0.0)
-            dv[:, a, :] = A.T @ G
-            dq[:, a, :] = dS @ k[:, a, :]
-            dk[:, a, :] = dS.T @ q[:, a, :]
+            dSr = np.where(M, rnd(dA * dsilu(S)), 0.0) / N
+            dv[:, a, :] = Ar.T @ G
+            dq[:, a, :] = dSr @ k[:, a, :]
+            dk[:, a, :] = dSr.T @ q[:, a, :]
             np.add.at(drp, position_index(L, n_t, N)[M], dS[M])
             np.add.at(drt, bucket_matrix(ts, len(rab_time))[M], dS[M])
     if d_out is not None:
@@ -71,7 +80,8 @@ def seq_dense(q, k, v, ts, rab_pos, rab_time, N, n_t, d_out=None):
     return O, grads
 
 
-def jagged_dense(batch_offsets, ts, rab_pos, rab_time, N, q, k, v, num_targets=None, d_out=None):
+def jagged_dense(batch_offsets, ts, rab_pos, rab_time, N, q, k, v, num_targets=None, d_out=None,
+                 rnd=_exact):
     B = len(batch_offsets) - 1
     O = np.zeros((q.shape[0], q.shape[1], v.shape[2]))
     tot = None
@@ -81,7 +91,7 @@ def jagged_dense(batch_offsets, ts, rab_pos, rab_time, N, q, k, v, num_targets=N
             continue
         nt = 0 if num_targets is None else int(num_targets[b])
         o, g = seq_dense(q[s:e], k[s:e], v[s:e], ts[s:e], rab_pos, rab_time, N, nt,
-                         None if d_out is None else d_out[s:e])
+                         None if d_out is None else d_out[s:e], rnd)
         O[s:e] = o
         if g is not None:
             if tot is None:
