@@ -338,6 +338,101 @@ def _permuted(d, perm):
     return e, ridx
 
 
+def test_attention_graph_replay(hs):
+    """hstu_attn_fwd then hstu_attn_bwd captured once as a graph and
+    replayed three times, with eager library and torch work on other
+    buffers and a synchronisation between replays: every replay writes the
+    eager results (O, dQ, dK, dV bitwise; the bias gradients, summed with
+    atomics in varying order, to 1e-5 of their largest magnitude).  No memset node is
+    recorded: the calls clear their buffers with kernels."""
+    batch = inputs.make_batch(3, seed=77, lengths=(700, 0, 1, 300, 129), num_heads=2, d_qk=64,
+                              d_v=128, max_seq_len=768, dtype="bf16",
+                              num_targets=(50, 0, 1, 0, 129))
+    d = gu.dev_inputs(batch)
+    N = batch.spec.max_seq_len
+    p = hs.problem_for(d["q"], d["v"], d["seq_offsets"], N, d["rab_time"])
+    ws = hs.workspace(p)
+    out = torch.empty_like(d["v"])
+    grads = (torch.empty_like(d["q"]), torch.empty_like(d["k"]), torch.empty_like(d["v"]),
+             torch.empty_like(d["rab_pos"]), torch.empty_like(d["rab_time"]))
+
+    def run(stream=None):
+        hs.hstu_attn_fwd(d["q"], d["k"], d["v"], d["seq_offsets"], d["timestamps"], d["rab_pos"],
+                         d["rab_time"], N, num_targets=d["num_targets"], out=out, ws=ws,
+                         stream=stream)
+        hs.hstu_attn_bwd(d["q"], d["k"], d["v"], d["do"], d["seq_offsets"], d["timestamps"],
+                         d["rab_pos"], d["rab_time"], N, num_targets=d["num_targets"],
+                         grads=grads, ws=ws, stream=stream)
+
+    run()
+    torch.cuda.synchronize()
+    ref = [out.clone()] + [x.clone() for x in grads]
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        run(stream=torch.cuda.current_stream())
+    for rep in range(3):
+        for x in [out, *grads]:
+            x.fill_(float("nan"))
+        other = gu.gpu_bwd(hs, d, batch)  # eager work with its own buffers
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        for i, (x, r) in enumerate(zip([out, *grads[:3]], ref[:4])):
+            assert torch.equal(x.view(torch.int16), r.view(torch.int16)), (rep, i)
+        for x, r in zip(grads[3:], ref[4:]):
+            assert torch.isfinite(x).all(), rep
+            assert (x - r).abs().max().item() <= 1e-5 * r.abs().max().item(), rep
+        del other
+
+
+def test_layer_graph_replay(hs):
+    """hstu_layer_fwd then hstu_layer_bwd (two-term path, affine LayerNorm)
+    captured once and replayed three times between eager calls: Y, the
+    saved statistics and dQ, dK, dV, dU bitwise equal to the eager call;
+    the parameter and bias-table gradients (summed with atomics in varying
+    order) to 1e-5 of their largest magnitude."""
+    batch = inputs.make_batch(2, seed=78, lengths=(300, 0, 1, 129, 70), num_heads=4, d_qk=64,
+                              d_v=64, max_seq_len=300, dtype="bf16", num_targets=(0, 0, 0, 17, 5))
+    d = gu.dev_inputs(batch)
+    N, D = 300, 4 * 64
+    w, b = _ln_params(D, 5)
+    wt, bb = torch.from_numpy(w).cuda(), torch.from_numpy(b).cuda()
+    dy = d["do"].reshape(-1, D)
+    p = hs.problem_for(d["q"], d["v"], d["seq_offsets"], N, d["rab_time"])
+    ws = hs.workspace(p)
+
+    def run(stream=None):
+        f = hs.hstu_layer_fwd(d["q"], d["k"], d["v"], d["u"], d["seq_offsets"], d["timestamps"],
+                              d["rab_pos"], d["rab_time"], N, num_targets=d["num_targets"],
+                              ln_weight=wt, ln_bias=bb, ws=ws, stream=stream)
+        ao, y, mu, rs = f
+        g = hs.hstu_layer_bwd(d["q"], d["k"], d["v"], d["u"], ao, mu, rs, dy, d["seq_offsets"],
+                              d["timestamps"], d["rab_pos"], d["rab_time"], N,
+                              num_targets=d["num_targets"], ln_weight=wt, ln_bias=bb, ws=ws,
+                              stream=stream)
+        return [y, mu, rs, *g]
+
+    ref = [x.clone() for x in run()]
+    torch.cuda.synchronize()
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        res = run(stream=torch.cuda.current_stream())
+    for rep in range(3):
+        for x in res:
+            x.fill_(float("nan"))
+        run()  # eager calls on their own outputs (same workspace, same stream)
+        torch.cuda.synchronize()
+        graph.replay()
+        torch.cuda.synchronize()
+        for i, (x, r) in enumerate(zip(res, ref)):
+            if i < 7:  # y, mean, rstd, dq, dk, dv, du
+                assert torch.equal(x.view(torch.int16) if x.dtype == torch.bfloat16 else x,
+                                   r.view(torch.int16) if r.dtype == torch.bfloat16 else r), (rep, i)
+            else:
+                assert torch.isfinite(x).all(), (rep, i)
+                assert (x - r).abs().max().item() <= 1e-5 * r.abs().max().item(), (rep, i)
+
+
 def test_batch_permutation_equivariance(hs):
     """Sequences are independent (Sec. 3.2): permuting the sequences of a
     batch permutes the forward output and dQ, dK, dV with them, bit for bit
