@@ -531,7 +531,7 @@ def test_validate_data_errors(hs):
 
 def test_bucketize_bit_exact(hs, oracle_mod):
     """Standalone bucketisation equals the oracle byte for byte, including
-    empty sequences, length 1, the clamp (B_t = 9), a ragged total, rows
+    empty sequences, length 1, the clamps (B_t = 9 and 1; 256), a ragged total, rows
     past one 4096-column slab and spans beyond 2^31 (the 64-bit path)."""
     rng = np.random.default_rng(9)
     lens = np.array([0, 1, 17, 300, 0, 45, 1024, 3, 5000, 4100], dtype=np.int64)
@@ -544,7 +544,7 @@ def test_bucketize_bit_exact(hs, oracle_mod):
     ts[offs[6]:offs[7]] = rng.permutation(ts[offs[6]:offs[7]])   # unsorted sequence
     # two column slabs on the 64-bit path (span ~ 2^41)
     ts[offs[9]:offs[10]] = (1 << 50) + np.cumsum(rng.integers(0, 1 << 30, int(lens[9])))
-    for nb in (128, 9):
+    for nb in (128, 9, 1, 256):
         po_ref, bk_ref = oracle_mod.time_bucketize(offs, ts, nb)
         so = torch.from_numpy(offs).cuda()
         po = hs.hstu_pair_offsets(so)
