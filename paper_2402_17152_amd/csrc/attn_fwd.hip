@@ -1,7 +1,7 @@
 // Fused jagged pointwise-attention forward, bf16 MFMA (gfx950).
 //
 // Computes Eq. 2 of the paper, O = (1/N) SiLU(Q K^T + rab^{p,t}) V, over a
-// jagged batch without padding (Sec. 3.2, "fully raggified" attention),
+// jagged batch without padding (Sec. 3.2),
 // with the relative bias built on chip from the position table and the
 // time-bucket table (notation table, rab^{p,t}; kernel appendix: bias
 // construction fused into the attention kernel).  Pointwise aggregation

@@ -1,8 +1,8 @@
 // Jagged tile scheduler and small utility kernels.
 //
 // The scheduler turns the jagged batch into a list of (sequence, block)
-// work items for the attention kernels -- the "fully raggified" grouped
-// computation of the paper (Sec. 3.2; appendix on the fused kernels):
+// work items for the attention kernels -- the grouped computation over
+// unpadded sequences of the paper (Sec. 3.2; appendix on the fused kernels):
 // no padding, causally empty tiles never become work.  Items are written
 // longest-first (counting sort by tile count) so that the hardware
 // dispatcher, which hands out workgroups in index order, starts the

@@ -140,7 +140,7 @@ def test_matches_dense_brute_force(oracle_mod, case):
 
 
 def test_jagged_equals_padded_masked(oracle_mod):
-    """Fully raggified attention (Sec. 3.2; kernel appendix) equals the
+    """Attention over the unpadded jagged batch (Sec. 3.2; kernel appendix) equals the
     padded computation with padding keys masked: pad every sequence to N,
     run dense attention with a key-padding mask, compare valid rows."""
     c = _small(lengths=(7, 13, 1, 20), N=24)
