@@ -179,6 +179,38 @@ def test_bf16_edge_is_the_operand_rounding(hs, oracle_mod):
         assert c_gpu <= 1.05 * c_emu + 1e-4, (name, c_gpu, c_emu)
 
 
+def _scaled(batch, names, factor):
+    """The batch with tensors `names` multiplied by a power of two (exact in
+    both storage types, away from overflow)."""
+    import dataclasses
+    store = dict(batch.store)
+    for n in names:
+        a = store[n]
+        if a.dtype == np.uint16:  # bf16 bits: add log2(factor) to the exponent of non-zeros
+            e = int(np.log2(factor))
+            assert 2 ** e == factor
+            nz = (a & 0x7F80) != 0
+            store[n] = np.where(nz, a + np.uint16(e << 7), a).astype(np.uint16)
+        else:
+            store[n] = (a * np.float32(factor)).astype(a.dtype)
+    return dataclasses.replace(batch, store=store)
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+def test_large_scores(hs, oracle_mod, dtype):
+    """Q and K scaled by 8 (scores 64 times larger, up to hundreds): SiLU
+    deep in both saturated ranges (exp2 overflowing to inf for large
+    negative scores, underflowing for large positive ones) and outputs
+    with a wide dynamic range, forward and backward."""
+    batch = inputs.make_batch(3, seed=71, lengths=(200, 1, 77, 130), num_heads=2, d_qk=64, d_v=32,
+                              max_seq_len=256, dtype=dtype, num_targets=(20, 0, 0, 130))
+    batch = _scaled(batch, ("q", "k"), 8)
+    s = batch.f64("q")[:200, 0] @ batch.f64("k")[:200, 0].T
+    assert np.abs(s).max() > 100.0
+    _check_fwd(hs, oracle_mod, batch)
+    _check_bwd(hs, oracle_mod, batch)
+
+
 @pytest.mark.parametrize("dtype", ["bf16", "f32"])
 def test_bwd_long_sequence(hs, oracle_mod, dtype):
     """Every output of a 2200-token sequence and a ragged 45-token one.
