@@ -41,6 +41,17 @@ def _check_fwd(hs, oracle, batch):
     return e
 
 
+# The bias-table gradients of a bf16 problem are fp32 sums of an fp32 dS
+# (built from exact products of the bf16 inputs), so they sit far inside
+# the bf16 bar (1e-6 to 1.1e-4 of their RMS over the suite); a tighter bar
+# for them catches a misrouted diagonal or bucket that 2e-2 would not.
+TAU_BIAS_GRAD_BF16 = 1e-3
+
+
+def _tau_bias(batch):
+    return min(gu.tol(batch), TAU_BIAS_GRAD_BF16)
+
+
 def _check_bwd(hs, oracle, batch):
     d = gu.dev_inputs(batch)
     got = gu.gpu_bwd(hs, d, batch)
@@ -49,7 +60,8 @@ def _check_bwd(hs, oracle, batch):
     errs = {}
     for name, g, r in zip(("dq", "dk", "dv", "d_rab_pos", "d_rab_time"), got, ref):
         store = "f32" if name.startswith("d_rab") else batch.spec.dtype
-        errs[name] = gu.assert_close(name, gu.to_f64(g), r, gu.tol(batch), store)
+        tau = _tau_bias(batch) if name.startswith("d_rab") else gu.tol(batch)
+        errs[name] = gu.assert_close(name, gu.to_f64(g), r, tau, store)
         print(f"  {name} err {errs[name][0]:.3e} raw {errs[name][1]:.3e}")
     return errs
 
@@ -292,7 +304,10 @@ def _full(hs, oracle_mod, batch, backward):
         return
     r = _oracle_cached("bwd", oracle_mod, batch, gu.oracle_bwd)
     for name, gi, ri in zip(("dq", "dk", "dv", "d_rab_pos", "d_rab_time"), got, r):
-        e = gu.assert_close(name, gi, ri, tau, "f32" if name.startswith("d_rab") else st)
+        if name.startswith("d_rab"):
+            e = gu.assert_close(name, gi, ri, _tau_bias(batch), "f32")
+        else:
+            e = gu.assert_close(name, gi, ri, tau, st)
         print(f"  {name} err {e[0]:.3e} raw {e[1]:.3e}")
     # exact zeros: offsets j > i and buckets no pair reaches
     N = batch.spec.max_seq_len
@@ -713,7 +728,7 @@ def _layer_bwd_check(hs, oracle_mod, batch, seqs=None, affine=True):
     gs = got if seqs is None else gpu(sub)
     for name, gi, ri in zip(("d_ln_weight", "d_ln_bias", "d_rab_pos", "d_rab_time"),
                             gs[4:], ref[4:]):
-        e = gu.assert_close(name, gi, ri, tau)
+        e = gu.assert_close(name, gi, ri, _tau_bias(batch))
         print(f"  {name} err {e[0]:.3e} raw {e[1]:.3e}")
 
 
