@@ -56,6 +56,11 @@ SMALL = [
     (1000, 128, 2, 64, 32),
     (257, 256, 4, 32, 64),
     (1, 64, 1, 32, 64),
+    # 128-wide heads, widths that are not multiples of the 128 / 256 tiles
+    (513, 384, 3, 128, 64),
+    (130, 192, 1, 128, 128),
+    # a longer contraction (f_1 over D = 1024, f_2 over h d_v = 512)
+    (700, 1024, 8, 64, 64),
 ]
 
 
