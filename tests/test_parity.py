@@ -480,6 +480,43 @@ def test_layer_graph_replay(hs):
                 assert (x - r).abs().max().item() <= 1e-5 * r.abs().max().item(), (rep, i)
 
 
+def test_concurrent_streams(hs):
+    """Two batches on two streams at once (each call with its own
+    workspace and outputs): every result equals the same call made alone."""
+    b1 = inputs.make_batch(3, seed=81, lengths=(700, 33, 0, 258), num_heads=2, d_qk=128, d_v=64,
+                           max_seq_len=768, dtype="bf16", num_targets=(0, 5, 0, 30))
+    b2 = inputs.make_batch(3, seed=82, lengths=(129, 1024, 64), num_heads=3, d_qk=64, d_v=128,
+                           max_seq_len=1024, dtype="bf16")
+    ds = [gu.dev_inputs(b) for b in (b1, b2)]
+
+    def call(d, b, stream):
+        N = b.spec.max_seq_len
+        p = hs.problem_for(d["q"], d["v"], d["seq_offsets"], N, d["rab_time"])
+        ws = hs.workspace(p)
+        o = hs.hstu_attn_fwd(d["q"], d["k"], d["v"], d["seq_offsets"], d["timestamps"],
+                             d["rab_pos"], d["rab_time"], N, num_targets=d["num_targets"],
+                             ws=ws, stream=stream)
+        g = hs.hstu_attn_bwd(d["q"], d["k"], d["v"], d["do"], d["seq_offsets"], d["timestamps"],
+                             d["rab_pos"], d["rab_time"], N, num_targets=d["num_targets"],
+                             ws=ws, stream=stream)
+        return [o, *g]
+
+    alone = [call(d, b, torch.cuda.current_stream()) for d, b in zip(ds, (b1, b2))]
+    torch.cuda.synchronize()
+    streams = [torch.cuda.Stream(), torch.cuda.Stream()]
+    for rep in range(2):
+        together = []
+        for d, b, st in zip(ds, (b1, b2), streams):
+            with torch.cuda.stream(st):
+                together.append(call(d, b, st))
+        torch.cuda.synchronize()
+        for a, t in zip(alone, together):
+            for i, (x, y) in enumerate(zip(a[:4], t[:4])):
+                assert torch.equal(x.view(torch.int16), y.view(torch.int16)), (rep, i)
+            for x, y in zip(a[4:], t[4:]):
+                assert (x - y).abs().max().item() <= 1e-5 * x.abs().max().item(), rep
+
+
 def test_batch_permutation_equivariance(hs):
     """Sequences are independent (Sec. 3.2): permuting the sequences of a
     batch permutes the forward output and dQ, dK, dV with them, bit for bit
