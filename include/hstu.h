@@ -51,10 +51,12 @@
  *            meant for small problems and as an fp32 reference: every shape
  *            the ABI accepts runs, but long sequences are slow (the matrix
  *            cores serve HSTU_BF16 only).  HSTU_BF16: bf16 storage, fp32
- *            accumulation; the attention weights and dS are rounded to
- *            bf16 (nearest-even) before the second contraction.  Bias
- *            tables and their gradients are fp32; offsets and timestamps
- *            int64.
+ *            accumulation; in hstu_attn_fwd / hstu_attn_bwd the attention
+ *            weights and dS are rounded to bf16 (nearest-even) where they
+ *            enter the matrix cores; hstu_layer_fwd / hstu_layer_bwd carry
+ *            them, and the layer's dO, as two bf16 terms (hi + lo, about
+ *            2^-17 relative instead of 2^-9).  Bias tables and their
+ *            gradients are fp32; offsets and timestamps int64.
  *   Determinism  hstu_attn_fwd, hstu_layer_fwd, hstu_time_bucketize and
  *            hstu_complete_cumsum are bitwise deterministic, and so are
  *            dQ, dK and dV of hstu_attn_bwd for HSTU_BF16 (dQ is summed
@@ -227,8 +229,10 @@ hstu_status_t hstu_layer_fwd(const hstu_problem_t* p, const hstu_jagged_t* j,
 
 /* Backward of the whole layer (Eq. 2 and Eq. 3) from dY, the gradient of
  * Y = LayerNorm(attn_out) (.) U: du = LN(attn_out) (.) dY, the layer-norm
- * backward to dO = d attn_out (into the workspace, in the problem's
- * dtype), then hstu_attn_bwd with that dO.  attn_out (fp32), ln_weight,
+ * backward to dO = d attn_out (into the workspace: two bf16 terms for
+ * HSTU_BF16, fp32 for HSTU_F32), then the attention backward of
+ * hstu_attn_bwd with that dO (for HSTU_BF16 with P and dS as two bf16
+ * terms in every contraction).  attn_out (fp32), ln_weight,
  * ln_bias, ln_mean and ln_rstd are the output, parameters and saved
  * statistics of the hstu_layer_fwd call (ln_mean, ln_rstd required;
  * weight / bias NULL for the identity affine).  d_y, du: dense [T][h*d_v]
