@@ -42,7 +42,9 @@
 //        of 32 diagonals is complete once the rows have moved past it and
 //        is then summed over the rings, added to the table in HBM and
 //        cleared.  Masked pairs carry dS = 0, so every tile takes this
-//        path; candidate rows (all at position n_h) add straight to HBM.
+//        path; candidate rows (all at position n_h) put every pair of a
+//        key on one entry, which each lane sums in an LDS word of its own
+//        and adds to HBM once per item.
 // Tiles whose bucket is not fixed by the timestamp extremes (near the
 // diagonal, ragged, 64-bit timestamps) sum dS bucket by bucket over the
 // tile's bucket range.
@@ -137,6 +139,7 @@ struct BwdShared {
   // Position-gradient rings, one per (wave, half): diagonal k at k % 256.
   static constexpr int kRing = 256;
   float sRing[kBwdWaves][2][kRing];
+  float sCand[kBwdWaves][64];  // per lane: dS of candidate rows at its key
 };
 
 struct BwdArgs {
@@ -661,6 +664,12 @@ __device__ __forceinline__ void bwd_item(BwdShared<DQK, DV, SPLIT>& sm, const Bw
   float* const ring_mine = sm.sRing[wave][half];
   const int d1_lane = 4 * half - col - 32 * wave;  // D1 = 32 u + d1_lane
   float carry = 0.0f;  // partner's crossing sum of the previous step
+  // Candidate rows all sit at position n_h, so every candidate pair of the
+  // lane's key j lands on one position entry, (N-1) - (n_h - p(j)): the
+  // lane sums them over the item in its own LDS word (a register would
+  // stay live through every step) and adds them once at its end.
+  float* const cand_sum = &sm.sCand[wave][lane];
+  *cand_sum = 0.0f;
   auto pos_step = [&](int u, const float (&ds)[16]) {
     float sum = 0.0f, wsum = 0.0f;
 #pragma unroll
@@ -695,16 +704,16 @@ __device__ __forceinline__ void bwd_item(BwdShared<DQK, DV, SPLIT>& sm, const Bw
   auto grads = [&](int u, const Path& pth, const float (&ds)[16]) {
     const int i0 = row0(u);
     if (i0 + BM - 1 >= n_h && i0 < L) {
-      // Candidate rows: position n_h for every one; straight to HBM, and
-      // out of the diagonal sums.
-      float dh[16];
+      // Candidate rows: into the lane's candidate sum, out of the
+      // diagonal sums.
+      float dh[16], cs = 0.0f;
 #pragma unroll
       for (int q = 0; q < 16; q++) {
         const int i = i0 + 8 * (q >> 2) + 4 * half + (q & 3);
         dh[q] = i < n_h ? ds[q] : 0.0f;
-        if (i >= n_h && i < L && key_ok && pair_valid(i, my_j, n_h))
-          unsafeAtomicAdd(&A.d_rab_pos[(N - 1) - (n_h - pj)], ds[q] * invN);
+        if (i >= n_h && i < L && key_ok && pair_valid(i, my_j, n_h)) cs += ds[q];
       }
+      *cand_sum += cs;
       pos_step(u, dh);
     } else {
       pos_step(u, ds);
@@ -837,6 +846,8 @@ __device__ __forceinline__ void bwd_item(BwdShared<DQK, DV, SPLIT>& sm, const Bw
   }
   time_flush(0);
   time_flush(1);
+  if (const float cv = *cand_sum; cv != 0.0f)
+    unsafeAtomicAdd(&A.d_rab_pos[(N - 1) - (n_h - pj)], cv * invN);
   // The last crossing sums belong to D1 of step nsteps; then the chunks
   // not flushed inside the loop, max(0, nsteps - 5) .. nsteps.
   ring_mine[(32 * nsteps + d1_lane) & (kRing - 1)] = carry;
@@ -926,6 +937,7 @@ struct BwdSharedRS {
   float sTacc[64];
   static constexpr int kRing = 256;
   float sRing[4][2][kRing];
+  float sCand[4][64];  // per role-A lane: dS of candidate rows at its key
   // SPLIT: the low bf16 terms of dS^T and P, laid out as sdST and sPA.
   __align__(16) uint16_t sdSTl[SPLIT ? 2 : 1][SPLIT ? BN * DST_LD : 8];
   __align__(16) u32x4 sPAl[SPLIT ? 2 : 1][4][2][SPLIT ? 64 : 1];
@@ -1262,6 +1274,12 @@ __device__ __forceinline__ void bwd_role_a(BwdSharedRS<DQK, DV, SPLIT>& sm, cons
   float* const ring_mine = sm.sRing[wave][half];
   const int d1_lane = 4 * half - col - 32 * wave;  // D1 = 32 u + d1_lane
   float carry = 0.0f;  // partner's crossing sum of the previous step
+  // Candidate rows all sit at position n_h, so every candidate pair of the
+  // lane's key j lands on one position entry, (N-1) - (n_h - p(j)): the
+  // lane sums them over the item in its own LDS word (a register would
+  // stay live through every step) and adds them once at its end.
+  float* const cand_sum = &sm.sCand[wave][lane];
+  *cand_sum = 0.0f;
   auto pos_step = [&](int u, const float (&ds)[16]) {
     float sum = 0.0f, nowrap = 0.0f;
 #pragma unroll
@@ -1293,14 +1311,14 @@ __device__ __forceinline__ void bwd_role_a(BwdSharedRS<DQK, DV, SPLIT>& sm, cons
   auto grads = [&](int u, const Path& pth, const float (&ds)[16]) {
     const int i0 = row0(u);
     if (i0 + BM - 1 >= n_h && i0 < L) {
-      float dh[16];
+      float dh[16], cs = 0.0f;
 #pragma unroll
       for (int q = 0; q < 16; q++) {
         const int i = i0 + 8 * (q >> 2) + 4 * half + (q & 3);
         dh[q] = i < n_h ? ds[q] : 0.0f;
-        if (i >= n_h && i < L && key_ok && pair_valid(i, my_j, n_h))
-          unsafeAtomicAdd(&A.d_rab_pos[(N - 1) - (n_h - pj)], ds[q] * invN);
+        if (i >= n_h && i < L && key_ok && pair_valid(i, my_j, n_h)) cs += ds[q];
       }
+      *cand_sum += cs;
       pos_step(u, dh);
     } else {
       pos_step(u, ds);
@@ -1415,6 +1433,8 @@ __device__ __forceinline__ void bwd_role_a(BwdSharedRS<DQK, DV, SPLIT>& sm, cons
   barrier_no_fence();  // (L)
   time_flush(0);
   time_flush(1);
+  if (const float cv = *cand_sum; cv != 0.0f)
+    unsafeAtomicAdd(&A.d_rab_pos[(N - 1) - (n_h - pj)], cv * invN);
   ring_mine[(32 * nsteps + d1_lane) & (kRing - 1)] = carry;
   wait_vmcnt_lgkmcnt0<0>();
   barrier_no_fence();  // (E)

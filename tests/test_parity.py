@@ -335,9 +335,10 @@ def test_workload_long_full(hs, oracle_mod):
 
 
 def test_workload_target_full(hs, oracle_mod):
-    """bf16 target-aware workload (16 x (2048 + 1024), h=4, d=128, N=3072),
-    forward over the whole batch."""
-    _full(hs, oracle_mod, inputs.make_batch("target"), backward=False)
+    """bf16 target-aware workload (16 x (2048 + 1024), h=4, d=128, N=3072):
+    forward and backward over the whole batch; every candidate row puts
+    its pairs with one key on one position entry, summed over 1024 rows."""
+    _full(hs, oracle_mod, inputs.make_batch("target"), backward=True)
 
 
 def test_fwd_bitwise_deterministic(hs):
