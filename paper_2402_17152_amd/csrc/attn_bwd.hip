@@ -949,10 +949,16 @@ struct RsItem {
   int seq, L, n_h, j0, head, nsteps;
 };
 
-template <int DQK, int DV, bool FAST, bool SPLIT>
+// TGT: the batch may hold candidate rows (num_targets given); without
+// them the candidate paths below are compiled out.  CF: candidate rows
+// against history keys are full tiles (key-only position term, one-bucket
+// time paths); the two-term instance leaves them on the general path,
+// which timed faster there on batches without candidates.
+template <int DQK, int DV, bool FAST, bool SPLIT, bool TGT>
 __device__ __forceinline__ void bwd_role_a(BwdSharedRS<DQK, DV, SPLIT>& sm, const BwdArgs& A,
                                            const RsItem& it, int64_t tbase) {
   using Sh = BwdSharedRS<DQK, DV, SPLIT>;
+  constexpr bool CF = TGT && !SPLIT;
   using QT = typename Sh::QT;
   using OT = typename Sh::OT;
   constexpr int BN = Sh::BN, BM = Sh::BM, DST_LD = Sh::DST_LD, kSlots = Sh::kSlots;
@@ -1087,8 +1093,11 @@ __device__ __forceinline__ void bwd_role_a(BwdSharedRS<DQK, DV, SPLIT>& sm, cons
     __device__ int slot_far() const { return (code >> 8) & 63; }
     __device__ uint32_t thr() const { return 1u << ((code >> 14) & 31); }
   };
+  // Full tile: every pair valid, either history rows after all of the
+  // wave's keys, or candidate rows against history keys only.
   auto full_tile = [&](int i0) {
-    return (jw0 + 31 <= i0) && (i0 + BM - 1 < L) && (i0 + BM - 1 < n_h);
+    return (i0 + BM - 1 < L) &&
+           ((jw0 + 31 <= i0 && i0 + BM - 1 < n_h) || (CF && i0 >= n_h && jw0 + 31 < n_h));
   };
   auto classify = [&](int u) -> Path {
     Path r{kGeneral, 0.0f, 0.0f};
@@ -1166,16 +1175,27 @@ __device__ __forceinline__ void bwd_role_a(BwdSharedRS<DQK, DV, SPLIT>& sm, cons
       }
     }
   };
+  // Candidate rows all sit at position n_h: their position term depends
+  // on the key alone.
+  auto full_win = [&](int u, float (&w)[16]) {
+    if (CF && row0(u) >= n_h) {
+      const float wc = sm.sWin[u & 3][0][Sh::kWinPad + Pk - pj];
+#pragma unroll
+      for (int q = 0; q < 16; q++) w[q] = wc;
+    } else {
+      win_reads(u, w);
+    }
+  };
   auto seed = [&](int u, const Path& pth, f32x16& acc) {
     if (pth.kind() == kUniform) {
       float w[16];
-      win_reads(u, w);
+      full_win(u, w);
 #pragma unroll
       for (int q = 0; q < 16; q++) acc[q] = w[q] + pth.cb;
     } else if (pth.kind() == kTwo) {
       float w[16];
       uint32_t ti[16];
-      win_reads(u, w);
+      full_win(u, w);
       row_ts(u, ti);
       const uint32_t lim = tjr + pth.thr();
 #pragma unroll
@@ -1279,7 +1299,7 @@ __device__ __forceinline__ void bwd_role_a(BwdSharedRS<DQK, DV, SPLIT>& sm, cons
   // lane sums them over the item in its own LDS word (a register would
   // stay live through every step) and adds them once at its end.
   float* const cand_sum = &sm.sCand[wave][lane];
-  *cand_sum = 0.0f;
+  if constexpr (TGT) *cand_sum = 0.0f;
   auto pos_step = [&](int u, const float (&ds)[16]) {
     float sum = 0.0f, nowrap = 0.0f;
 #pragma unroll
@@ -1310,7 +1330,7 @@ __device__ __forceinline__ void bwd_role_a(BwdSharedRS<DQK, DV, SPLIT>& sm, cons
   };
   auto grads = [&](int u, const Path& pth, const float (&ds)[16]) {
     const int i0 = row0(u);
-    if (i0 + BM - 1 >= n_h && i0 < L) {
+    if (TGT && i0 + BM - 1 >= n_h && i0 < L) {
       float dh[16], cs = 0.0f;
 #pragma unroll
       for (int q = 0; q < 16; q++) {
@@ -1319,7 +1339,13 @@ __device__ __forceinline__ void bwd_role_a(BwdSharedRS<DQK, DV, SPLIT>& sm, cons
         if (i >= n_h && i < L && key_ok && pair_valid(i, my_j, n_h)) cs += ds[q];
       }
       *cand_sum += cs;
-      pos_step(u, dh);
+      if (CF && i0 >= n_h) {
+        // no history row: the step's diagonal sums are all zero
+        ring_mine[(32 * u + d1_lane) & (kRing - 1)] = carry;
+        carry = 0.0f;
+      } else {
+        pos_step(u, dh);
+      }
     } else {
       pos_step(u, ds);
     }
@@ -1433,8 +1459,10 @@ __device__ __forceinline__ void bwd_role_a(BwdSharedRS<DQK, DV, SPLIT>& sm, cons
   barrier_no_fence();  // (L)
   time_flush(0);
   time_flush(1);
-  if (const float cv = *cand_sum; cv != 0.0f)
-    unsafeAtomicAdd(&A.d_rab_pos[(N - 1) - (n_h - pj)], cv * invN);
+  if constexpr (TGT) {
+    if (const float cv = *cand_sum; cv != 0.0f)
+      unsafeAtomicAdd(&A.d_rab_pos[(N - 1) - (n_h - pj)], cv * invN);
+  }
   ring_mine[(32 * nsteps + d1_lane) & (kRing - 1)] = carry;
   wait_vmcnt_lgkmcnt0<0>();
   barrier_no_fence();  // (E)
@@ -1645,7 +1673,7 @@ __device__ __forceinline__ void bwd_role_b(BwdSharedRS<DQK, DV, SPLIT>& sm, cons
 
 constexpr int kRsThreads = 512;
 
-template <int DQK, int DV, bool SPLIT>
+template <int DQK, int DV, bool SPLIT, bool TGT>
 __global__ __launch_bounds__(kRsThreads, 1) void attn_bwd_rs_kernel(
     BwdArgs A, const WorkItem* __restrict__ items, const int32_t* __restrict__ count) {
   using S = BwdSharedRS<DQK, DV, SPLIT>;
@@ -1708,9 +1736,9 @@ __global__ __launch_bounds__(kRsThreads, 1) void attn_bwd_rs_kernel(
 
   if (wave < 4) {
     if (fast)
-      bwd_role_a<DQK, DV, true, SPLIT>(sm, A, it, tlo);
+      bwd_role_a<DQK, DV, true, SPLIT, TGT>(sm, A, it, tlo);
     else
-      bwd_role_a<DQK, DV, false, SPLIT>(sm, A, it, tlo);
+      bwd_role_a<DQK, DV, false, SPLIT, TGT>(sm, A, it, tlo);
   } else {
     bwd_role_b<DQK, DV, SPLIT>(sm, A, it, kq, fast, tlo);
   }
@@ -1890,15 +1918,21 @@ hipError_t launch_bwd(const JaggedArgs& ja, const Tensors& t, const void* d_out,
   if (d_out_lo) {
     if constexpr (bwd_split_two_role(DQK, DV)) {
       static_assert(sizeof(BwdSharedRS<DQK, DV, true>) <= kLdsBytes, "LDS budget");
-      hipLaunchKernelGGL((attn_bwd_rs_kernel<DQK, DV, true>), grid, dim3(kRsThreads), 0, s, A,
-                         items, count);
+      // (One instance for the two-term form: without its candidate paths
+      // it timed slower.)
+      hipLaunchKernelGGL((attn_bwd_rs_kernel<DQK, DV, true, true>), grid, dim3(kRsThreads), 0,
+                         s, A, items, count);
     } else {
       hipLaunchKernelGGL((attn_bwd_bf16_kernel<DQK, DV, true>), grid, dim3(kBwdThreads), 0, s, A,
                          items, count);
     }
   } else {
-    hipLaunchKernelGGL((attn_bwd_rs_kernel<DQK, DV, false>), grid, dim3(kRsThreads), 0, s, A,
-                       items, count);
+    if (ja.num_targets)
+      hipLaunchKernelGGL((attn_bwd_rs_kernel<DQK, DV, false, true>), grid, dim3(kRsThreads), 0, s,
+                         A, items, count);
+    else
+      hipLaunchKernelGGL((attn_bwd_rs_kernel<DQK, DV, false, false>), grid, dim3(kRsThreads), 0, s,
+                         A, items, count);
   }
   return hipGetLastError();
 }

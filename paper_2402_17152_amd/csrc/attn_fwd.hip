@@ -96,8 +96,10 @@ __device__ __forceinline__ float silu(float x) {
 // spread and would magnify a bf16 P).
 // Row i of the item is global row orow + i, key j global key okey + j;
 // keys at or past key_lim do not exist (cross mode: the cached prefix has
-// n_h keys).
-template <int DQK, int DV, bool FAST, bool SPLIT>
+// n_h keys).  TGT: self mode with candidate rows, whose blocks may visit
+// candidate key tiles after the history tiles; otherwise step u's tile is
+// kt0 + u.
+template <int DQK, int DV, bool FAST, bool SPLIT, bool TGT>
 __device__ __forceinline__ void fwd_item(FwdShared<DQK, DV>& sm, const JaggedArgs& ja,
                                          const Tensors& t, void* __restrict__ out, int out_f32,
                                          int64_t orow, int64_t okey, int L, int n_h, int key_lim,
@@ -154,7 +156,12 @@ __device__ __forceinline__ void fwd_item(FwdShared<DQK, DV>& sm, const JaggedArg
   const int nA = max(0, min(kt1, kend) - kt0);
   const int bstart = max(nh_blk, i0 / BN);
   const int n = nA + max(0, kend - bstart);
-  auto kb_of = [&](int u) { return u < nA ? kt0 + u : bstart + (u - nA); };
+  auto kb_of = [&](int u) {
+    if constexpr (TGT)
+      return u < nA ? kt0 + u : bstart + (u - nA);
+    else
+      return kt0 + u;
+  };
   auto pos_base_of = [&](int j0) { return (N - 1) + min(j0, n_h) - R; };
 
   const int tr_row = 4 * (lane >> 5) + ((lane & 15) >> 2);
@@ -558,7 +565,7 @@ __device__ __forceinline__ void fwd_item(FwdShared<DQK, DV>& sm, const JaggedArg
   }
 }
 
-template <int DQK, int DV, bool SPLIT>
+template <int DQK, int DV, bool SPLIT, bool TGT>
 __global__ __launch_bounds__(256, 2) void attn_fwd_bf16_kernel(JaggedArgs ja, Tensors t,
                                                                void* __restrict__ out, int out_f32,
                                                                const WorkItem* __restrict__ items,
@@ -610,11 +617,11 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_bf16_kernel(JaggedArgs ja, Te
     sm.sTab[x] = (fast && x == 31) ? ja.rab_time[0] : ja.rab_time[min(63 - x, NB - 1)];
   __syncthreads();
   if (fast) {
-    fwd_item<DQK, DV, true, SPLIT>(sm, ja, t, outp, out_f32, orow, okey, L, n_h, key_lim, kt0, kt1,
-                                   i0, head, tlo);
+    fwd_item<DQK, DV, true, SPLIT, TGT>(sm, ja, t, outp, out_f32, orow, okey, L, n_h, key_lim, kt0,
+                                        kt1, i0, head, tlo);
   } else {
-    fwd_item<DQK, DV, false, SPLIT>(sm, ja, t, outp, out_f32, orow, okey, L, n_h, key_lim, kt0, kt1,
-                                    i0, head, tlo);
+    fwd_item<DQK, DV, false, SPLIT, TGT>(sm, ja, t, outp, out_f32, orow, okey, L, n_h, key_lim, kt0,
+                                         kt1, i0, head, tlo);
   }
 }
 
@@ -623,12 +630,24 @@ hipError_t launch_fwd(const JaggedArgs& ja, const Tensors& t, void* out, int out
                       const WorkItem* items, const int32_t* count, int64_t max_items,
                       hipStream_t s) {
   dim3 grid((unsigned)(max_items * ja.num_heads));
-  if (split)
-    hipLaunchKernelGGL((attn_fwd_bf16_kernel<DQK, DV, true>), grid, dim3(256), 0, s, ja, t, out,
-                       out_f32, items, count);
-  else
-    hipLaunchKernelGGL((attn_fwd_bf16_kernel<DQK, DV, false>), grid, dim3(256), 0, s, ja, t, out,
-                       out_f32, items, count);
+  // Candidate key tiles exist only for self attention with targets (cross
+  // mode's keys are the cached prefix alone).
+  const bool tgt = ja.num_targets && !ja.key_offsets;
+#define HSTU_LAUNCH_FWD(SP, TG)                                                                  \
+  hipLaunchKernelGGL((attn_fwd_bf16_kernel<DQK, DV, SP, TG>), grid, dim3(256), 0, s, ja, t, out, \
+                     out_f32, items, count)
+  if (split) {
+    if (tgt)
+      HSTU_LAUNCH_FWD(true, true);
+    else
+      HSTU_LAUNCH_FWD(true, false);
+  } else {
+    if (tgt)
+      HSTU_LAUNCH_FWD(false, true);
+    else
+      HSTU_LAUNCH_FWD(false, false);
+  }
+#undef HSTU_LAUNCH_FWD
   return hipGetLastError();
 }
 
