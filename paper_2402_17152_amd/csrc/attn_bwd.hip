@@ -55,6 +55,7 @@
 // dO contraction runs on both.  For the same reason P and dS enter dV, dK
 // and dQ as two bf16 terms as well (hi P with both dO terms, lo P with hi
 // dO; hi and lo dS with Q and with K).
+#include <algorithm>
 #include <type_traits>
 
 #include "bias.h"
@@ -1673,17 +1674,16 @@ __device__ __forceinline__ void bwd_role_b(BwdSharedRS<DQK, DV, SPLIT>& sm, cons
 
 constexpr int kRsThreads = 512;
 
-template <int DQK, int DV, bool SPLIT, bool TGT>
-__global__ __launch_bounds__(kRsThreads, 1) void attn_bwd_rs_kernel(
-    BwdArgs A, const WorkItem* __restrict__ items, const int32_t* __restrict__ count) {
+// One work item (a 128-key block of one sequence and head) of the
+// two-role backward.  FAST: the sequence's timestamps span less than 2^31
+// and are rebased to 32 bits; the 64-bit path is a kernel of its own, so
+// that the code the common case runs does not carry it.
+template <int DQK, int DV, bool SPLIT, bool TGT, bool FAST>
+__device__ __forceinline__ void rs_item(BwdSharedRS<DQK, DV, SPLIT>& sm, const BwdArgs& A,
+                                        const WorkItem wi, const int head) {
   using S = BwdSharedRS<DQK, DV, SPLIT>;
   constexpr int BN = S::BN, KB_LD = S::KB_LD;
-  __shared__ S sm;
   const JaggedArgs& ja = A.ja;
-  const int item = (int)(blockIdx.x / (unsigned)ja.num_heads);
-  const int head = (int)blockIdx.x - item * ja.num_heads;
-  if (item >= *count) return;
-  const WorkItem wi = items[item];
   const int N = ja.max_seq_len, NB = ja.num_buckets;
   RsItem it;
   it.o = ja.seq_offsets[wi.seq];
@@ -1696,8 +1696,8 @@ __global__ __launch_bounds__(kRsThreads, 1) void attn_bwd_rs_kernel(
   const int i_end = it.j0 >= it.n_h ? min(it.j0 + BN, it.L) : it.L;
   it.nsteps = (i_end - it.j0 + S::BM - 1) / S::BM;
   const int tid = threadIdx.x;
-  const int64_t tlo = ja.seq_trange[2 * wi.seq], thi = ja.seq_trange[2 * wi.seq + 1];
-  const bool fast = thi - tlo < ((int64_t)1 << 31);
+  const int64_t tlo = ja.seq_trange[2 * wi.seq];
+  constexpr bool fast = FAST;
   for (int x = tid; x < 64; x += kRsThreads) {
     sm.sTab[x] = (fast && x == 31) ? ja.rab_time[0] : ja.rab_time[min(63 - x, NB - 1)];
     sm.sTacc[x] = 0.0f;
@@ -1734,14 +1734,10 @@ __global__ __launch_bounds__(kRsThreads, 1) void attn_bwd_rs_kernel(
     __syncthreads();  // the ring may be overwritten from here on
   }
 
-  if (wave < 4) {
-    if (fast)
-      bwd_role_a<DQK, DV, true, SPLIT, TGT>(sm, A, it, tlo);
-    else
-      bwd_role_a<DQK, DV, false, SPLIT, TGT>(sm, A, it, tlo);
-  } else {
-    bwd_role_b<DQK, DV, SPLIT>(sm, A, it, kq, fast, tlo);
-  }
+  if (wave < 4)
+    bwd_role_a<DQK, DV, FAST, SPLIT, TGT>(sm, A, it, tlo);
+  else
+    bwd_role_b<DQK, DV, SPLIT>(sm, A, it, kq, FAST, tlo);
 
   __syncthreads();
   const float invN = 1.0f / (float)N;
@@ -1749,6 +1745,46 @@ __global__ __launch_bounds__(kRsThreads, 1) void attn_bwd_rs_kernel(
     const float v = sm.sTacc[tid];
     const int b = (fast && tid == 31) ? 0 : min(63 - tid, NB - 1);
     if (v != 0.0f) unsafeAtomicAdd(&A.d_rab_time[b], v * invN);
+  }
+}
+
+__device__ __forceinline__ bool seq_fast(const JaggedArgs& ja, int seq) {
+  return ja.seq_trange[2 * seq + 1] - ja.seq_trange[2 * seq] < ((int64_t)1 << 31);
+}
+
+// The items of sequences on the 32-bit timestamp path, one per workgroup
+// (the others return at once).
+template <int DQK, int DV, bool SPLIT, bool TGT>
+__global__ __launch_bounds__(kRsThreads, 1) void attn_bwd_rs_kernel(
+    BwdArgs A, const WorkItem* __restrict__ items, const int32_t* __restrict__ count) {
+  __shared__ BwdSharedRS<DQK, DV, SPLIT> sm;
+  const int H = A.ja.num_heads;
+  const int item = (int)(blockIdx.x / (unsigned)H);
+  const int head = (int)blockIdx.x - item * H;
+  if (item >= *count) return;
+  const WorkItem wi = items[item];
+  if (!seq_fast(A.ja, wi.seq)) return;
+  rs_item<DQK, DV, SPLIT, TGT, true>(sm, A, wi, head);
+}
+
+// The items of sequences whose timestamps span 2^31 or more, in a
+// grid-stride loop over the work list; when there is no such sequence
+// (the check reads every sequence's range once) the launch ends at once.
+template <int DQK, int DV, bool SPLIT, bool TGT>
+__global__ __launch_bounds__(kRsThreads, 1) void attn_bwd_rs_wide_kernel(
+    BwdArgs A, const WorkItem* __restrict__ items, const int32_t* __restrict__ count) {
+  __shared__ BwdSharedRS<DQK, DV, SPLIT> sm;
+  const JaggedArgs& ja = A.ja;
+  int wide = 0;
+  for (int b = (int)threadIdx.x; b < ja.num_seqs; b += kRsThreads) wide |= !seq_fast(ja, b);
+  if (!__syncthreads_or(wide)) return;
+  const int H = ja.num_heads;
+  const int total = *count * H;
+  for (int w = (int)blockIdx.x; w < total; w += (int)gridDim.x) {
+    const WorkItem wi = items[w / H];
+    if (seq_fast(ja, wi.seq)) continue;
+    __syncthreads();  // the previous item's last LDS reads are done
+    rs_item<DQK, DV, SPLIT, TGT, false>(sm, A, wi, w - (w / H) * H);
   }
 }
 
@@ -1915,6 +1951,14 @@ hipError_t launch_bwd(const JaggedArgs& ja, const Tensors& t, const void* d_out,
   static_assert(sizeof(BwdShared<DQK, DV, true>) <= kLdsBytes, "LDS budget");
   static_assert(sizeof(BwdSharedRS<DQK, DV>) <= kLdsBytes, "LDS budget");
   dim3 grid((unsigned)(max_items * ja.num_heads));
+  // The two-role kernel runs as two launches: the items on the 32-bit
+  // timestamp path, then those of sequences spanning 2^31 or more, by at
+  // most one workgroup per CU, each of which first reads every sequence's
+  // range (fewer workgroups for many sequences, so that this check stays
+  // within ~256 K ranges read in all) and ends when none is that wide.
+  int64_t nwide = std::min<int64_t>(max_items * ja.num_heads, 256);
+  nwide = std::max<int64_t>(1, std::min<int64_t>(nwide, 262144 / std::max(1, ja.num_seqs)));
+  const dim3 wide_grid((unsigned)nwide);
   if (d_out_lo) {
     if constexpr (bwd_split_two_role(DQK, DV)) {
       static_assert(sizeof(BwdSharedRS<DQK, DV, true>) <= kLdsBytes, "LDS budget");
@@ -1922,17 +1966,24 @@ hipError_t launch_bwd(const JaggedArgs& ja, const Tensors& t, const void* d_out,
       // it timed slower.)
       hipLaunchKernelGGL((attn_bwd_rs_kernel<DQK, DV, true, true>), grid, dim3(kRsThreads), 0,
                          s, A, items, count);
+      hipLaunchKernelGGL((attn_bwd_rs_wide_kernel<DQK, DV, true, true>), wide_grid,
+                         dim3(kRsThreads), 0, s, A, items, count);
     } else {
       hipLaunchKernelGGL((attn_bwd_bf16_kernel<DQK, DV, true>), grid, dim3(kBwdThreads), 0, s, A,
                          items, count);
     }
   } else {
-    if (ja.num_targets)
+    if (ja.num_targets) {
       hipLaunchKernelGGL((attn_bwd_rs_kernel<DQK, DV, false, true>), grid, dim3(kRsThreads), 0, s,
                          A, items, count);
-    else
+      hipLaunchKernelGGL((attn_bwd_rs_wide_kernel<DQK, DV, false, true>), wide_grid,
+                         dim3(kRsThreads), 0, s, A, items, count);
+    } else {
       hipLaunchKernelGGL((attn_bwd_rs_kernel<DQK, DV, false, false>), grid, dim3(kRsThreads), 0, s,
                          A, items, count);
+      hipLaunchKernelGGL((attn_bwd_rs_wide_kernel<DQK, DV, false, false>), wide_grid,
+                         dim3(kRsThreads), 0, s, A, items, count);
+    }
   }
   return hipGetLastError();
 }
