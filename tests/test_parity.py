@@ -251,6 +251,31 @@ def test_small_parity_wide_timestamps(hs, oracle_mod, dtype):
     _check_bwd(hs, oracle_mod, batch)
 
 
+def _mixed_wide_timestamps(lengths, wide, seed):
+    """Timestamps of a batch where the sequences in `wide` span more than
+    2^31 (random, unsorted) and the others follow the workload's gaps."""
+    rng = np.random.default_rng(seed)
+    offs = np.concatenate([[0], np.cumsum(lengths)])
+    ts = 1_700_000_000 + np.cumsum(rng.integers(0, 1200, size=int(offs[-1])))
+    for b in wide:
+        ts[offs[b]:offs[b + 1]] = rng.integers(0, 1 << 60, size=lengths[b])
+    return ts.astype(np.int64)
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+@pytest.mark.parametrize("targets", [None, (20, 0, 30, 0, 5)])
+def test_mixed_wide_timestamps(hs, oracle_mod, dtype, targets):
+    """One batch with sequences on both timestamp paths: the 32-bit ones
+    go to the main backward kernel and the wide ones to its second launch,
+    whose results meet in the same dQ, dK, dV and bias tables."""
+    lengths = (200, 77, 130, 150, 33)
+    ts = _mixed_wide_timestamps(lengths, wide=(0, 2), seed=19)
+    batch = inputs.make_batch(3, seed=32, lengths=lengths, num_heads=2, d_qk=64, d_v=64,
+                              max_seq_len=256, dtype=dtype, timestamps=ts, num_targets=targets)
+    _check_fwd(hs, oracle_mod, batch)
+    _check_bwd(hs, oracle_mod, batch)
+
+
 def test_workload_tiny_full(hs, oracle_mod):
     """fp32 tiny workload (B=4, h=2, d=32, N=128): every output in full."""
     batch = inputs.make_batch("tiny")
@@ -790,6 +815,19 @@ def test_layer_head_dim_pairs(hs, oracle_mod, dtype, dqk, dv):
     batch = inputs.make_batch(2, seed=500 + dqk + dv // 8, lengths=(150, 1, 97, 40),
                               num_targets=(12, 1, 0, 40), num_heads=2, d_qk=dqk, d_v=dv,
                               max_seq_len=160, dtype=dtype)
+    _layer_bwd_check(hs, oracle_mod, batch)
+
+
+@pytest.mark.parametrize("dqk,dv", [(64, 64), (128, 128)])
+def test_layer_mixed_wide_timestamps(hs, oracle_mod, dqk, dv):
+    """hstu_layer_bwd (two-term operands) on a batch mixing sequences on
+    both timestamp paths, with candidates: the two-role instance and its
+    second launch at d <= 64, the single-role kernel at d = 128."""
+    lengths = (150, 97, 40, 120)
+    ts = _mixed_wide_timestamps(lengths, wide=(1, 3), seed=23)
+    batch = inputs.make_batch(2, seed=600 + dqk, lengths=lengths, num_targets=(12, 0, 40, 7),
+                              num_heads=2, d_qk=dqk, d_v=dv, max_seq_len=160, dtype="bf16",
+                              timestamps=ts)
     _layer_bwd_check(hs, oracle_mod, batch)
 
 
