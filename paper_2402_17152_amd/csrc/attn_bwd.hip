@@ -46,8 +46,10 @@
 //        key on one entry, which each lane sums in an LDS word of its own
 //        and adds to HBM once per item.
 // Tiles whose bucket is not fixed by the timestamp extremes (near the
-// diagonal, ragged, 64-bit timestamps) sum dS bucket by bucket over the
-// tile's bucket range.
+// diagonal, ragged, 64-bit timestamps): each lane walks its 16 pairs in
+// row order and adds every run of equal bucket to the LDS table with one
+// float atomic (sweeping the tile's bucket range with a wave reduction per
+// bucket cost several times a one-bucket step).
 // SPLIT (the layer's backward): dO arrives as two bf16 terms, hi + lo
 // (its own LayerNorm backward produces it in fp32, with a dynamic range
 // across rows that a single bf16 would turn into several percent of error
@@ -737,25 +739,21 @@ __device__ __forceinline__ void bwd_item(BwdShared<DQK, DV, SPLIT>& sm, const Bw
       }
     } else {
       // Bucket by bucket over the slots of the tile's valid pairs.
+      // Several buckets: a lane's 16 pairs (rows in order, its one key)
+      // form runs of equal slot, each added once to the LDS table (masked
+      // pairs carry dS = 0 and may sit in any run).
       int sl[16];
       pair_slots(u, sl);
-      uint32_t lo = 64, hi = 0;
+      float run = ds[0];
 #pragma unroll
-      for (int q = 0; q < 16; q++) {
-        const int i = i0 + 8 * (q >> 2) + 4 * half + (q & 3);
-        if (!(key_ok && i < L && pair_valid(i, my_j, n_h))) sl[q] = 64;
-        lo = min(lo, (uint32_t)sl[q]);
-        hi = sl[q] < 64 ? max(hi, (uint32_t)sl[q]) : hi;
+      for (int q = 1; q < 16; q++) {
+        if (sl[q] != sl[q - 1]) {
+          atomicAdd(&sm.sTacc[sl[q - 1]], run);
+          run = 0.0f;
+        }
+        run += ds[q];
       }
-      lo = wave_min_dpp(lo);
-      hi = wave_max_dpp(hi);
-      for (int b = (int)lo; b <= (int)hi; b++) {
-        float acc = 0.0f;
-#pragma unroll
-        for (int q = 0; q < 16; q++) acc += sl[q] == b ? ds[q] : 0.0f;
-        acc = wave_sum_dpp(acc);
-        if (lane == 0 && acc != 0.0f) atomicAdd(&sm.sTacc[b], acc);
-      }
+      atomicAdd(&sm.sTacc[sl[15]], run);
     }
   };
 
@@ -1367,25 +1365,21 @@ __device__ __forceinline__ void bwd_role_a(BwdSharedRS<DQK, DV, SPLIT>& sm, cons
         time_add(0, pth.slot(), tot);
       }
     } else {
+      // Several buckets: a lane's 16 pairs (rows in order, its one key)
+      // form runs of equal slot, each added once to the LDS table (masked
+      // pairs carry dS = 0 and may sit in any run).
       int sl[16];
       pair_slots(u, sl);
-      uint32_t lo = 64, hi = 0;
+      float run = ds[0];
 #pragma unroll
-      for (int q = 0; q < 16; q++) {
-        const int i = i0 + 8 * (q >> 2) + 4 * half + (q & 3);
-        if (!(key_ok && i < L && pair_valid(i, my_j, n_h))) sl[q] = 64;
-        lo = min(lo, (uint32_t)sl[q]);
-        hi = sl[q] < 64 ? max(hi, (uint32_t)sl[q]) : hi;
+      for (int q = 1; q < 16; q++) {
+        if (sl[q] != sl[q - 1]) {
+          atomicAdd(&sm.sTacc[sl[q - 1]], run);
+          run = 0.0f;
+        }
+        run += ds[q];
       }
-      lo = wave_min_dpp(lo);
-      hi = wave_max_dpp(hi);
-      for (int b = (int)lo; b <= (int)hi; b++) {
-        float acc = 0.0f;
-#pragma unroll
-        for (int q = 0; q < 16; q++) acc += sl[q] == b ? ds[q] : 0.0f;
-        acc = wave_sum_dpp(acc);
-        if (lane == 0 && acc != 0.0f) atomicAdd(&sm.sTacc[b], acc);
-      }
+      atomicAdd(&sm.sTacc[sl[15]], run);
     }
   };
 
