@@ -106,6 +106,11 @@ __device__ __forceinline__ void fwd_item(FwdShared<DQK, DV>& sm, const JaggedArg
                                          int kt0, int kt1, int i0, int head, int64_t tbase) {
   using Sh = FwdShared<DQK, DV>;
   constexpr int BM = Sh::BM, BN = Sh::BN, K_LD = Sh::K_LD, V_LD = Sh::V_LD;
+  // Masked tiles with history keys read the window as full tiles do; the
+  // instances that run three workgroups per CU (d_qk, d_v <= 64) keep
+  // reading it entry by entry, as the other form costs them registers past
+  // that occupancy.
+  constexpr bool kMaskedWindowReads = DQK > 64 || DV > 64;
   constexpr int KCH = BN * DQK / 8, VCH = BN * DV / 8;
   constexpr int KPT = (KCH + 255) / 256, VPT = (VCH + 255) / 256;
   static_assert(BN == 32 && BM == 128, "4 waves x 32 rows, 32-key tiles");
@@ -407,7 +412,7 @@ __device__ __forceinline__ void fwd_item(FwdShared<DQK, DV>& sm, const JaggedArg
       time_terms(u, tv);
 #pragma unroll
       for (int q = 0; q < 16; q++) acc[q] = wv[q] + tv[q];
-    } else {
+    } else if constexpr (!kMaskedWindowReads) {
       // Masked, ragged or candidate pairs: invalid pairs read window entry 0.
       const int pb = min(j0, n_h);
       bool ok[16];
@@ -420,6 +425,36 @@ __device__ __forceinline__ void fwd_item(FwdShared<DQK, DV>& sm, const JaggedArg
       }
 #pragma unroll
       for (int q = 0; q < 16; q++) wv[q] = sm.sWin[ks][0][Sh::kWinPad + x[q]];
+      time_terms(u, tv);
+#pragma unroll
+      for (int q = 0; q < 16; q++) acc[q] = ok[q] ? wv[q] + tv[q] : kMaskedBias;
+    } else {
+      // The same with history keys (position = index) by the window reads
+      // of full tiles (they stay inside the window for every lane, valid
+      // or not); candidate keys (all at position n_h) entry by entry.
+      bool ok[16];
+#pragma unroll
+      for (int q = 0; q < 16; q++) {
+        const int j = j0 + 8 * (q >> 2) + 4 * half + (q & 3);
+        ok[q] = row_ok && j < key_lim && pair_valid(my_i, j, n_h);
+      }
+      if (!TGT || j0 + BN - 1 < n_h) {
+        const int c = a_win & 3;
+        const float* wp = &sm.sWin[ks][c][Sh::kWinPad + a_win - c];
+#pragma unroll
+        for (int g = 0; g < 4; g++) {
+          const f32x4 w = *reinterpret_cast<const f32x4*>(wp + 8 * g);
+#pragma unroll
+          for (int m = 0; m < 4; m++) wv[4 * g + m] = w[m];
+        }
+      } else {
+        const int pb = min(j0, n_h);
+#pragma unroll
+        for (int q = 0; q < 16; q++) {
+          const int j = j0 + 8 * (q >> 2) + 4 * half + (q & 3);
+          wv[q] = sm.sWin[ks][0][Sh::kWinPad + (ok[q] ? bias_pos(j, n_h) - pb + R - pi : 0)];
+        }
+      }
       time_terms(u, tv);
 #pragma unroll
       for (int q = 0; q < 16; q++) acc[q] = ok[q] ? wv[q] + tv[q] : kMaskedBias;
