@@ -958,6 +958,9 @@ __device__ __forceinline__ void bwd_role_a(BwdSharedRS<DQK, DV, SPLIT>& sm, cons
                                            const RsItem& it, int64_t tbase) {
   using Sh = BwdSharedRS<DQK, DV, SPLIT>;
   constexpr bool CF = TGT && !SPLIT;
+  // Masked tiles of history rows read the position window as full tiles
+  // do, where registers allow: at d_qk or d_v = 128 the other form spills.
+  constexpr bool kMaskedWindowReads = DQK <= 64 && DV <= 64;
   using QT = typename Sh::QT;
   using OT = typename Sh::OT;
   constexpr int BN = Sh::BN, BM = Sh::BM, DST_LD = Sh::DST_LD, kSlots = Sh::kSlots;
@@ -1199,6 +1202,21 @@ __device__ __forceinline__ void bwd_role_a(BwdSharedRS<DQK, DV, SPLIT>& sm, cons
       const uint32_t lim = tjr + pth.thr();
 #pragma unroll
       for (int q = 0; q < 16; q++) acc[q] = w[q] + (ti[q] >= lim ? pth.cb_far : pth.cb);
+    } else if (kMaskedWindowReads && (!TGT || row0(u) + BM - 1 < n_h)) {
+      // Masked or ragged pairs of history rows (position = index): the
+      // window reads of full tiles, then the mask.
+      const int i0 = row0(u);
+      int sl[16];
+      pair_slots(u, sl);
+      float w[16], tv[16];
+      win_reads(u, w);
+#pragma unroll
+      for (int q = 0; q < 16; q++) tv[q] = sm.sTab[sl[q]];
+#pragma unroll
+      for (int q = 0; q < 16; q++) {
+        const int i = i0 + 8 * (q >> 2) + 4 * half + (q & 3);
+        acc[q] = key_ok && i < L && pair_valid(i, my_j, n_h) ? w[q] + tv[q] : kMaskedBias;
+      }
     } else {
       const int i0 = row0(u), pi0 = min(i0, n_h);
       int sl[16];
